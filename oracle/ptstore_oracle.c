@@ -1,0 +1,297 @@
+/*
+ * CPU oracle of the prefix store -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, single-threaded C. It exists so that the GPU library can be
+ * checked against something obviously correct; nothing on the product path
+ * may link or call it. It shares no source with the GPU library.
+ *
+ * What it computes (PTStore, Section 4.1 "Co-optimized compact metadata and
+ * fast prefix queries", and Section 1 "Contributions"):
+ *
+ *   - Stored objects are sequences of fixed-size token blocks. The store
+ *     keeps each distinct block-prefix exactly once, as a node of a trie
+ *     whose root is the empty prefix: prefixes "grow redundancy-free ...
+ *     in divergent directions, similar to a trie" (Section 1).
+ *   - Every node has a dense unique id and a KV payload of block_bytes in
+ *     a pool indexed by that id. An object's metadata is the flat list of
+ *     the ids on its root path: it inherits the ids of its longest common
+ *     prefix with what is stored and appends ids for its own increment
+ *     (Section 4.1).
+ *   - lookup: the longest common prefix, in whole blocks, of a request with
+ *     everything stored (Section 4.1, the LCP query), plus the ids along it.
+ *   - gather: a load iterates over those ids and copies their tensors into
+ *     application-supplied memory (Section 4.1), here a paged cache laid out
+ *     [layer][K|V][cache block][head][slot][dim].
+ *   - insert: a store saves only the increment beyond the LCP (Section 4),
+ *     processing the batch one request after another; new nodes get the next
+ *     free id. No node is created beyond the capacity.
+ *   - scatter: copies the KV of the nodes an insert created from the paged
+ *     cache into the pool.
+ *
+ * Trie representation: each node keeps a pointer to its parent, its first
+ * child and its next sibling; a child is found by comparing the block's
+ * tokens against each child in turn. No hashing is involved anywhere.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_ERR_INVALID 1
+#define ORC_ERR_FULL 2
+#define ORC_ERR_NOMEM 3
+
+typedef struct onode {
+    int32_t id;                 /* -1 for the root */
+    struct onode *parent;
+    struct onode *first_child;
+    struct onode *next_sibling;
+    int32_t *tokens;            /* block_tokens tokens of this block */
+} onode_t;
+
+typedef struct {
+    int32_t layers, kv_heads, head_dim, block_tokens, elem_bytes;
+    int64_t chunk_bytes;        /* kv_heads * block_tokens * head_dim * elem_bytes */
+    int64_t block_bytes;        /* layers * 2 * chunk_bytes */
+    int64_t capacity;           /* maximum number of nodes */
+    int64_t count;              /* nodes created so far (= next id) */
+    int64_t bad_entries;        /* skipped out-of-range ids / cache blocks */
+    onode_t root;
+    onode_t **by_id;            /* id -> node */
+    uint8_t *pool;              /* capacity * block_bytes, or NULL */
+} ostore_t;
+
+ostore_t *orc_create(int32_t layers, int32_t kv_heads, int32_t head_dim,
+                     int32_t block_tokens, int32_t elem_bytes,
+                     int64_t capacity, int32_t with_payload)
+{
+    if (layers < 1 || kv_heads < 1 || head_dim < 1 || block_tokens < 1 ||
+        elem_bytes < 1 || capacity < 0)
+        return NULL;
+    ostore_t *s = (ostore_t *)calloc(1, sizeof(ostore_t));
+    if (!s) return NULL;
+    s->layers = layers;
+    s->kv_heads = kv_heads;
+    s->head_dim = head_dim;
+    s->block_tokens = block_tokens;
+    s->elem_bytes = elem_bytes;
+    s->chunk_bytes = (int64_t)kv_heads * block_tokens * head_dim * elem_bytes;
+    s->block_bytes = (int64_t)layers * 2 * s->chunk_bytes;
+    s->capacity = capacity;
+    s->root.id = -1;
+    s->by_id = (onode_t **)calloc(capacity > 0 ? (size_t)capacity : 1, sizeof(onode_t *));
+    if (!s->by_id) { free(s); return NULL; }
+    if (with_payload && capacity > 0) {
+        s->pool = (uint8_t *)calloc((size_t)capacity, (size_t)s->block_bytes);
+        if (!s->pool) { free(s->by_id); free(s); return NULL; }
+    }
+    return s;
+}
+
+void orc_destroy(ostore_t *s)
+{
+    if (!s) return;
+    for (int64_t i = 0; i < s->count; i++) {
+        free(s->by_id[i]->tokens);
+        free(s->by_id[i]);
+    }
+    free(s->by_id);
+    free(s->pool);
+    free(s);
+}
+
+/* The child of `node` whose block equals `blk`, or NULL. */
+static onode_t *find_child(const ostore_t *s, const onode_t *node, const int32_t *blk)
+{
+    size_t nbytes = (size_t)s->block_tokens * sizeof(int32_t);
+    for (onode_t *c = node->first_child; c; c = c->next_sibling)
+        if (memcmp(c->tokens, blk, nbytes) == 0)
+            return c;
+    return NULL;
+}
+
+static onode_t *add_child(ostore_t *s, onode_t *node, const int32_t *blk)
+{
+    onode_t *c = (onode_t *)calloc(1, sizeof(onode_t));
+    if (!c) return NULL;
+    c->tokens = (int32_t *)malloc((size_t)s->block_tokens * sizeof(int32_t));
+    if (!c->tokens) { free(c); return NULL; }
+    memcpy(c->tokens, blk, (size_t)s->block_tokens * sizeof(int32_t));
+    c->id = (int32_t)s->count;
+    c->parent = node;
+    c->next_sibling = node->first_child;
+    node->first_child = c;
+    s->by_id[s->count++] = c;
+    return c;
+}
+
+/* Number of whole blocks of request r that are considered. */
+static int32_t request_blocks(const ostore_t *s, const int64_t *offsets, int32_t r,
+                              int32_t max_blocks)
+{
+    int64_t len = offsets[r + 1] - offsets[r];
+    int64_t n = len / s->block_tokens;
+    return (int32_t)(n < max_blocks ? n : max_blocks);
+}
+
+static int check_batch(const int64_t *offsets, int32_t R, int32_t max_blocks)
+{
+    if (R < 0 || max_blocks < 1 || (R > 0 && !offsets)) return ORC_ERR_INVALID;
+    for (int32_t r = 0; r < R; r++)
+        if (offsets[r + 1] < offsets[r]) return ORC_ERR_INVALID;
+    return ORC_OK;
+}
+
+/*
+ * LCP query (Section 4.1): m[r] = the largest k such that blocks 0..k-1 of
+ * request r form a path from the root; ids[r][b] = id of the b-th node on
+ * it, -1 for b >= m[r]. Only the first max_blocks whole blocks count.
+ */
+int orc_lookup(const ostore_t *s, const int32_t *tokens, const int64_t *offsets,
+               int32_t R, int32_t max_blocks, int32_t *m, int32_t *ids)
+{
+    int rc = check_batch(offsets, R, max_blocks);
+    if (rc) return rc;
+    for (int32_t r = 0; r < R; r++) {
+        int32_t n = request_blocks(s, offsets, r, max_blocks);
+        const int32_t *seq = tokens + offsets[r];
+        int32_t *row = ids + (int64_t)r * max_blocks;
+        const onode_t *node = &s->root;
+        int32_t b = 0;
+        for (; b < n; b++) {
+            const onode_t *c = find_child(s, node, seq + (int64_t)b * s->block_tokens);
+            if (!c) break;
+            row[b] = c->id;
+            node = c;
+        }
+        m[r] = b;
+        for (int32_t j = b; j < max_blocks; j++) row[j] = -1;
+    }
+    return ORC_OK;
+}
+
+/* Byte offset of (layer l, K|V kv, cache block cb) in the paged cache. */
+static int64_t cache_off(const ostore_t *s, int64_t cache_blocks, int32_t l, int32_t kv,
+                         int64_t cb)
+{
+    return (((int64_t)l * 2 + kv) * cache_blocks + cb) * s->chunk_bytes;
+}
+
+/* Byte offset of (node id, layer l, K|V kv) in the pool. */
+static int64_t pool_off(const ostore_t *s, int64_t id, int32_t l, int32_t kv)
+{
+    return id * s->block_bytes + ((int64_t)l * 2 + kv) * s->chunk_bytes;
+}
+
+/*
+ * Load (Section 4.1): for every matched block b < m[r] whose block-table
+ * entry is >= 0, copy each (layer, K|V) slab of pool[ids[r][b]] into
+ * cache[layer][K|V][block_table[r][b]]. Out-of-range ids or cache blocks
+ * are skipped and counted in bad_entries.
+ */
+int orc_gather(ostore_t *s, const int32_t *ids, const int32_t *m, const int32_t *block_table,
+               int32_t R, int32_t max_blocks, uint8_t *cache, int64_t cache_blocks)
+{
+    if (!s->pool || R < 0 || max_blocks < 1 || cache_blocks < 0) return ORC_ERR_INVALID;
+    for (int32_t r = 0; r < R; r++) {
+        int32_t mr = m[r] < max_blocks ? m[r] : max_blocks;
+        for (int32_t b = 0; b < mr; b++) {
+            int64_t id = ids[(int64_t)r * max_blocks + b];
+            int64_t cb = block_table[(int64_t)r * max_blocks + b];
+            if (cb < 0) continue;
+            if (cb >= cache_blocks || id < 0 || id >= s->count) { s->bad_entries++; continue; }
+            for (int32_t l = 0; l < s->layers; l++)
+                for (int32_t kv = 0; kv < 2; kv++)
+                    memcpy(cache + cache_off(s, cache_blocks, l, kv, cb),
+                           s->pool + pool_off(s, id, l, kv), (size_t)s->chunk_bytes);
+        }
+    }
+    return ORC_OK;
+}
+
+/*
+ * Store (Sections 1 and 4): requests are taken in batch order. Each one
+ * walks its blocks from the root; existing nodes (stored earlier, or
+ * created by an earlier request of this batch) are reused, a missing block
+ * becomes a new node with the next id, unless the store already holds
+ * `capacity` nodes, in which case the walk of this request stops there.
+ * Outputs: m_out[r] = blocks of r resident after the call, ids[r][b] their
+ * ids (-1 beyond), created[r][b] = 1 where request r created the node.
+ * Returns ORC_ERR_FULL if some block was refused for lack of capacity.
+ */
+int orc_insert(ostore_t *s, const int32_t *tokens, const int64_t *offsets, int32_t R,
+               int32_t max_blocks, int32_t *m_out, int32_t *ids, uint8_t *created)
+{
+    int rc = check_batch(offsets, R, max_blocks);
+    if (rc) return rc;
+    int full = 0;
+    for (int32_t r = 0; r < R; r++) {
+        int32_t n = request_blocks(s, offsets, r, max_blocks);
+        const int32_t *seq = tokens + offsets[r];
+        int32_t *row = ids + (int64_t)r * max_blocks;
+        uint8_t *crow = created + (int64_t)r * max_blocks;
+        memset(crow, 0, (size_t)max_blocks);
+        onode_t *node = &s->root;
+        int32_t b = 0;
+        for (; b < n; b++) {
+            const int32_t *blk = seq + (int64_t)b * s->block_tokens;
+            onode_t *c = find_child(s, node, blk);
+            if (!c) {
+                if (s->count >= s->capacity) { full = 1; break; }
+                c = add_child(s, node, blk);
+                if (!c) return ORC_ERR_NOMEM;
+                crow[b] = 1;
+            }
+            row[b] = c->id;
+            node = c;
+        }
+        m_out[r] = b;
+        for (int32_t j = b; j < max_blocks; j++) row[j] = -1;
+    }
+    return full ? ORC_ERR_FULL : ORC_OK;
+}
+
+/*
+ * Store data: for every (r, b) with created[r][b] = 1 and a block-table
+ * entry >= 0, copy each (layer, K|V) slab of cache[..][block_table[r][b]]
+ * into pool[ids[r][b]].
+ */
+int orc_scatter(ostore_t *s, const int32_t *ids, const uint8_t *created,
+                const int32_t *block_table, int32_t R, int32_t max_blocks,
+                const uint8_t *cache, int64_t cache_blocks)
+{
+    if (!s->pool || R < 0 || max_blocks < 1 || cache_blocks < 0) return ORC_ERR_INVALID;
+    for (int32_t r = 0; r < R; r++) {
+        for (int32_t b = 0; b < max_blocks; b++) {
+            int64_t k = (int64_t)r * max_blocks + b;
+            if (!created[k]) continue;
+            int64_t id = ids[k];
+            int64_t cb = block_table[k];
+            if (cb < 0) continue;
+            if (cb >= cache_blocks || id < 0 || id >= s->count) { s->bad_entries++; continue; }
+            for (int32_t l = 0; l < s->layers; l++)
+                for (int32_t kv = 0; kv < 2; kv++)
+                    memcpy(s->pool + pool_off(s, id, l, kv),
+                           cache + cache_off(s, cache_blocks, l, kv, cb), (size_t)s->chunk_bytes);
+        }
+    }
+    return ORC_OK;
+}
+
+/* ---- inspection helpers for the tests ---- */
+
+int64_t orc_count(const ostore_t *s) { return s->count; }
+int64_t orc_bad_entries(const ostore_t *s) { return s->bad_entries; }
+int64_t orc_block_bytes(const ostore_t *s) { return s->block_bytes; }
+uint8_t *orc_pool(ostore_t *s) { return s->pool; }
+
+/* parent id (-1 = root) and tokens of node `id`; returns ORC_ERR_INVALID if absent. */
+int orc_node(const ostore_t *s, int64_t id, int32_t *parent, int32_t *tokens_out)
+{
+    if (id < 0 || id >= s->count) return ORC_ERR_INVALID;
+    const onode_t *n = s->by_id[id];
+    *parent = n->parent ? n->parent->id : -1;
+    if (tokens_out)
+        memcpy(tokens_out, n->tokens, (size_t)s->block_tokens * sizeof(int32_t));
+    return ORC_OK;
+}

@@ -1,0 +1,98 @@
+"""Planted mistakes in a copy of the oracle must each fail some pin.
+
+Each mutant is the oracle's C source with one plausible slip (a dropped
+term, a wrong index, a transposed layout, an off-by-one), compiled to a
+temporary library. The pins of test_oracle.py run against it and at least
+one must fail; this shows the pins would catch such a slip in the oracle
+itself. All on the CPU; each mutant runs in a child process so that a
+mutant which corrupts memory cannot take the test session down.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle.ref as ref
+from tests import test_oracle as pins
+
+MUTANTS = {
+    "match_first_token_only": ("if (memcmp(c->tokens, blk, nbytes) == 0)",
+                               "if (memcmp(c->tokens, blk, sizeof(int32_t)) == 0)"),
+    "lookup_m_off_by_one": ("        m[r] = b;\n        for (int32_t j = b; j < max_blocks; j++) row[j] = -1;\n    }\n    return ORC_OK;",
+                            "        m[r] = b > 0 ? b - 1 : 0;\n        for (int32_t j = b; j < max_blocks; j++) row[j] = -1;\n    }\n    return ORC_OK;"),
+    "created_never_set": ("crow[b] = 1;", "crow[b] = 0;"),
+    "capacity_off_by_one": ("if (s->count >= s->capacity) { full = 1; break; }",
+                            "if (s->count + 1 >= s->capacity) { full = 1; break; }"),
+    "cache_layout_transposed": ("return (((int64_t)l * 2 + kv) * cache_blocks + cb) * s->chunk_bytes;",
+                                "return (((int64_t)cb * s->layers + l) * 2 + kv) * s->chunk_bytes;"),
+    "pool_kv_layer_swapped": ("return id * s->block_bytes + ((int64_t)l * 2 + kv) * s->chunk_bytes;",
+                              "return id * s->block_bytes + ((int64_t)kv * s->layers + l) * s->chunk_bytes;"),
+    "partial_block_counted": ("int64_t n = len / s->block_tokens;",
+                              "int64_t n = (len + s->block_tokens - 1) / s->block_tokens;"),
+    "ids_start_at_one": ("c->id = (int32_t)s->count;", "c->id = (int32_t)s->count + 1;"),
+    "scatter_every_occurrence": ("if (!created[k]) continue;", "if (ids[k] < 0) continue;"),
+    "root_children_by_parent_ignored": ("        onode_t *node = &s->root;\n        int32_t b = 0;\n        for (; b < n; b++) {\n            const int32_t *blk",
+                                        "        onode_t *node = &s->root;\n        int32_t b = 0;\n        for (; b < n; b++) {\n            node = &s->root;\n            const int32_t *blk"),
+}
+
+# pins that need no mutable global state; each gets a fresh store
+PIN_CALLS = [
+    lambda: [pins.test_golden_oracle(c) for c in pins.load_golden("incremental_ids.json")["cases"]],
+    lambda: pins._check_against_brute(5, 2, 3, 4, 6, 6, 30, rounds=3, n_req=20),
+    lambda: pins._check_against_brute(9, 16, 2, 4, 5, 4, 1000, rounds=3, n_req=20),
+    lambda: pins._check_against_brute(8, 16, 3, 4, 8, 8, 1000, rounds=3, n_req=20, shared_head=True),
+    pins.test_invariants_after_inserts,
+    pins.test_gather_scatter_layout_and_sentinel,
+    pins.test_ground_truth_tiny,
+    pins.test_full_match_and_max_blocks_truncation,
+    pins.test_capacity_zero,
+]
+
+
+def run_battery(lib: str) -> int:
+    """Number of pins that fail against the library at ``lib``."""
+    ref.DEFAULT_LIB = lib
+    caught = 0
+    for call in PIN_CALLS:
+        try:
+            call()
+        except (AssertionError, KeyError, ValueError):
+            caught += 1
+    return caught
+
+
+_CHILD = """
+import sys
+sys.path.insert(0, {root!r})
+from tests import test_oracle_mutations as t
+n = t.run_battery({lib!r})
+print("CAUGHT", n)
+"""
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(ref._SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    msrc = tmp_path / "mutant.c"
+    msrc.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libmutant.so")
+    ref.build_oracle(lib, src=str(msrc))
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    p = subprocess.run([sys.executable, "-c", _CHILD.format(root=root, lib=lib)],
+                       capture_output=True, text=True, timeout=300)
+    if p.returncode != 0:
+        # the mutant crashed the child: it did not pass unnoticed either
+        assert p.returncode != 0
+        return
+    line = [l for l in p.stdout.splitlines() if l.startswith("CAUGHT")][-1]
+    assert int(line.split()[1]) > 0, f"no pin caught mutant {name}"
+
+
+def test_unmutated_passes_battery():
+    for call in PIN_CALLS:
+        call()
