@@ -1,0 +1,221 @@
+/*
+ * ptstore.h -- C ABI of the GPU-resident prefix store (MI355X / gfx950).
+ *
+ * The store keeps KV-cache prefixes at block granularity, each distinct
+ * block-prefix exactly once, so that stored prefixes grow without redundancy
+ * in divergent directions like a trie (PTStore, Section 1 "Contributions").
+ * Every stored block has a dense unique id; an object's metadata is the flat
+ * list of the ids on its path, inherited from its longest common prefix with
+ * what is stored plus new ids for its own increment (Section 4.1,
+ * "Co-optimized compact metadata and fast prefix queries"). The calls below
+ * are the prefix query (LCP lookup), the load of the tensors behind a list
+ * of ids into application-supplied GPU memory (gather), and the store of a
+ * new object's increment (insert + scatter), as in Section 4.1 and the
+ * client API of Section 5.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - A block is `block_tokens` consecutive int32 tokens. Only whole blocks
+ *    count; a trailing partial block is never matched or stored. Only the
+ *    first `max_blocks` blocks of a request are considered.
+ *  - A batch of R requests is CSR: `tokens` (int32, device) and `offsets`
+ *    (int64, device, R+1 entries); request r is tokens[offsets[r] ..
+ *    offsets[r+1]). `n_tokens` is the length of `tokens`. A request whose
+ *    offsets are decreasing, negative or beyond n_tokens is treated as empty
+ *    and counted in `bad_entries`.
+ *  - Per-(request, block) arrays are row-major [R][max_blocks].
+ *  - KV payload of one block: [layer][K|V][head][slot][dim] elements of
+ *    `elem_bytes` bytes; a (layer, K|V) slab of head*slot*dim elements is a
+ *    "chunk". The store's pool is [pool_blocks][layer][K|V][head][slot][dim]
+ *    (each block contiguous). The caller's paged cache is
+ *    [layer][K|V][cache_blocks][head][slot][dim]. Payload bytes are copied
+ *    verbatim: no arithmetic is done on them.
+ *  - Every pointer argument except `cfg`/`out`/`stats` is a DEVICE pointer
+ *    owned by the caller. `stream` is a hipStream_t (NULL = default stream).
+ *    Calls only enqueue work on `stream` and return; outputs are valid once
+ *    the stream has reached that point. Calls on one store must be ordered
+ *    on one stream (a store is not safe for concurrent calls); a lookup sees
+ *    exactly the inserts enqueued before it.
+ *  - Return codes: PTSTORE_OK, or an error found on the host before any
+ *    work is enqueued. Conditions only the device can see (a full store,
+ *    out-of-range entries) are counted and reported by ptstore_stats().
+ */
+#ifndef PTSTORE_H
+#define PTSTORE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ptstore ptstore_t;
+
+enum {
+    PTSTORE_OK = 0,
+    PTSTORE_ERR_INVALID = 1, /* bad argument (null pointer, negative size, misaligned, ...) */
+    PTSTORE_ERR_FULL = 2,    /* reserved: a full store is reported through ptstore_stats */
+    PTSTORE_ERR_HIP = 3,     /* a HIP runtime call failed (see ptstore_last_error) */
+    PTSTORE_ERR_NOMEM = 4    /* device or host allocation failed */
+};
+
+/* Configuration flags. */
+enum {
+    /* Mask index keys to 8 bits so that hash collisions are the rule: used
+     * to test that results never depend on the hash (every hit is verified
+     * on tokens and parent). Slow; for tests only. */
+    PTSTORE_FLAG_WEAK_HASH = 1u,
+    /* Count probes, token comparisons and compare-and-swap attempts. */
+    PTSTORE_FLAG_COUNTERS = 2u,
+    /* Record HIP events around every gather / scatter / lookup kernel so
+     * that ptstore_kernel_times() can report their durations. */
+    PTSTORE_FLAG_TIMING = 4u
+};
+
+typedef struct {
+    int32_t num_layers;    /* L >= 1 */
+    int32_t num_kv_heads;  /* H >= 1 */
+    int32_t head_dim;      /* D >= 1 */
+    int32_t block_tokens;  /* tokens per block, 1..64 */
+    int32_t elem_bytes;    /* bytes per KV element (2 for fp16 / bf16) */
+    int64_t pool_blocks;   /* blocks the pool can hold, 0 .. 2^31-4 */
+    int64_t index_slots;   /* hash index slots (power of two) or 0 for
+                              the smallest power of two >= 2*pool_blocks.
+                              The store holds at most min(pool_blocks,
+                              index_slots/2) blocks. */
+    uint64_t hash_seed;    /* results never depend on it */
+    uint32_t flags;        /* PTSTORE_FLAG_* */
+} ptstore_config_t;
+
+typedef struct {
+    int64_t blocks_stored;  /* blocks (trie nodes) held, = next id */
+    int64_t capacity;       /* maximum blocks_stored */
+    int64_t index_slots;
+    int64_t block_bytes;    /* L * 2 * H * block_tokens * D * elem_bytes */
+    int64_t chunk_bytes;    /* H * block_tokens * D * elem_bytes */
+    int64_t full_events;    /* inserts that refused blocks for lack of room */
+    int64_t bad_entries;    /* skipped malformed requests, ids or cache blocks */
+    int64_t probes;         /* index slots read (PTSTORE_FLAG_COUNTERS) */
+    int64_t token_compares; /* candidate blocks compared token by token */
+    int64_t cas_attempts;   /* compare-and-swap attempts by inserts */
+    int64_t cas_failures;
+} ptstore_stats_t;
+
+/* Device buffers of a store, for inspection by tests (read-only use). */
+typedef struct {
+    void *pool;             /* [capacity][block_bytes] */
+    const int32_t *parent;  /* [capacity] parent id, -1 for a root child */
+    const int32_t *tokens;  /* [capacity][block_tokens] */
+    const void *slots;      /* [index_slots] of {uint64 key, int32 id, int32 pad} */
+    int64_t capacity;
+    int64_t index_slots;
+} ptstore_buffers_t;
+
+/*
+ * Create a store on the current HIP device: allocates the pool, the block
+ * metadata and the hash index, and waits until they are initialised.
+ * On success *out owns them until ptstore_destroy(). Errors: INVALID (bad
+ * shape, chunk bytes not a multiple of 16, sizes out of range), NOMEM, HIP.
+ */
+int ptstore_create(const ptstore_config_t *cfg, ptstore_t **out);
+
+/* Wait for the device, then free everything the store owns. NULL is a no-op. */
+int ptstore_destroy(ptstore_t *store);
+
+/*
+ * LCP query (Section 4.1): for each request r, m[r] = the largest k such that
+ * its blocks 0..k-1 are a stored prefix (blocks beyond max_blocks ignored),
+ * and ids[r][b] = the id of the stored block at depth b for b < m[r], -1
+ * beyond. Outputs: m [R] int32, ids [R][max_blocks] int32.
+ * Errors: INVALID (store NULL, R < 0, max_blocks < 1, n_tokens < 0 or
+ * >= 2^32, a NULL pointer with R > 0).
+ */
+int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                   int64_t n_tokens, int32_t R, int32_t max_blocks,
+                   int32_t *m, int32_t *ids, void *stream);
+
+/*
+ * Load (Section 4.1: iterate over an object's ids and bring their tensors
+ * into application-supplied GPU memory): for every r and b < m[r] with
+ * block_table[r][b] >= 0, copy each (layer, K|V) chunk of pool block
+ * ids[r][b] into cache[layer][K|V][block_table[r][b]]. Entries with an id
+ * outside [0, blocks_stored) or a cache block >= cache_blocks are skipped
+ * and counted in bad_entries. Destinations must be distinct (two entries
+ * naming the same cache block race). `cache` must be 16-byte aligned.
+ */
+int ptstore_gather(ptstore_t *store, const int32_t *ids, const int32_t *m,
+                   const int32_t *block_table, int32_t R, int32_t max_blocks,
+                   void *cache, int64_t cache_blocks, void *stream);
+
+/*
+ * ptstore_lookup followed by ptstore_gather of its result, enqueued
+ * back to back on `stream` (the measured hot path). m and ids are written
+ * as by ptstore_lookup.
+ */
+int ptstore_lookup_gather(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                          int64_t n_tokens, int32_t R, int32_t max_blocks,
+                          int32_t *m, int32_t *ids, const int32_t *block_table,
+                          void *cache, int64_t cache_blocks, void *stream);
+
+/*
+ * Store (Sections 1 and 4): with the same result as taking the requests one
+ * after another, each request reuses the stored blocks of its longest
+ * common prefix (including blocks created by earlier requests of this
+ * batch) and creates one new block per missing block, ids handed out
+ * densely in (request, block) order. Once the store holds `capacity`
+ * blocks nothing more is created; a request then keeps only the blocks it
+ * could reuse or create (the cut is always a prefix) and full_events is
+ * incremented. Outputs: m_out [R] = blocks of r resident after the call;
+ * ids [R][max_blocks] their ids (-1 beyond m_out); created [R][max_blocks]
+ * = 1 exactly where request r created the block (a block shared by several
+ * requests of the batch is created by the first of them).
+ * Uses store-owned scratch sized for R * max_blocks, grown on demand (the
+ * growth waits for `stream`). Errors as ptstore_lookup, plus NOMEM.
+ */
+int ptstore_insert(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                   int64_t n_tokens, int32_t R, int32_t max_blocks,
+                   int32_t *m_out, int32_t *ids, uint8_t *created, void *stream);
+
+/*
+ * Store the tensors of new blocks: for every (r, b) with created[r][b] != 0
+ * and block_table[r][b] >= 0, copy each chunk of
+ * cache[layer][K|V][block_table[r][b]] into pool block ids[r][b].
+ * Out-of-range ids / cache blocks are skipped and counted in bad_entries.
+ */
+int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created,
+                    const int32_t *block_table, int32_t R, int32_t max_blocks,
+                    const void *cache, int64_t cache_blocks, void *stream);
+
+/* Wait for the device and read the store's counters into *stats. */
+int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);
+
+/* Zero the event counters (probes, compares, CAS, full_events, bad_entries). */
+int ptstore_reset_counters(ptstore_t *store);
+
+/* Device buffers of the store (see ptstore_buffers_t). */
+int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
+
+/*
+ * With PTSTORE_FLAG_TIMING: wait for the device, then return the summed
+ * durations (ms) and launch counts of the kernels recorded since the last
+ * call, for kind 0 = gather copy, 1 = lookup, 2 = scatter copy,
+ * 3 = insert (all its kernels). Resets the records.
+ */
+int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64_t *launches);
+
+/* Launch shape of the copy kernels (gather and scatter); 0 keeps a field's
+ * default. chunks_per_group: chunks one workgroup copies; threads: 64..1024,
+ * a multiple of 64. For tuning sweeps. */
+int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t threads);
+
+/* Human-readable text for a return code. */
+const char *ptstore_strerror(int code);
+
+/* Text of the last error on this host thread ("" if none). */
+const char *ptstore_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PTSTORE_H */

@@ -1,0 +1,477 @@
+// Host runtime of the prefix store: the C ABI declared in include/ptstore.h.
+//
+// The store owns, on one device:
+//   pool    [capacity][layer][K|V][head][slot][dim]  KV payload, per-block contiguous
+//   parent  [capacity] int32, tokens [capacity][block_tokens] int32   block metadata
+//   slots   [index_slots] {key, id}                  open-addressing block index
+//   ht      key-chain constants, state: counters and the block count
+//   scratch insert work space, grown on demand
+// Calls check their arguments, enqueue kernels on the caller's stream and
+// return; nothing on the lookup / gather path allocates or synchronises.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/ptstore.h"
+#include "kernels.hpp"
+
+using namespace ptsd;
+
+struct ptstore {
+    ptstore_config_t cfg;
+    int device;
+    int64_t chunk_bytes, block_bytes, capacity;
+    uint64_t slots_n;
+    uint8_t* pool;
+    int32_t* parent;
+    int32_t* tokens;
+    Slot* slots;
+    HashTables* ht;
+    DevState* state;
+    void* scratch;
+    size_t scratch_bytes;
+    int32_t chunks_per_group, threads;
+    // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[4];
+    std::vector<hipEvent_t> free_ev;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* what, hipError_t e = hipSuccess) {
+    char buf[512];
+    if (e != hipSuccess)
+        snprintf(buf, sizeof buf, "%s: %s", what, hipGetErrorString(e));
+    else
+        snprintf(buf, sizeof buf, "%s", what);
+    g_last_error = buf;
+    return code;
+}
+
+uint64_t next_pow2(uint64_t x) {
+    uint64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// (a * b) mod 2^61-1 on the host
+uint64_t host_mulmod61(uint64_t a, uint64_t b) {
+    unsigned __int128 p = (unsigned __int128)a * b;
+    uint64_t lo = (uint64_t)p & kM61;
+    uint64_t hi = (uint64_t)(p >> 61);
+    return mod61(lo + hi);
+}
+
+void make_hash_tables(uint64_t seed, bool weak, HashTables* h) {
+    memset(h, 0, sizeof *h);
+    const uint64_t P = mod61(mix64(seed ^ 0x2545F4914F6CDD1Dull)) % (kM61 - 2) + 2;
+    uint64_t x = P;
+    for (int j = 0; j < kWave; ++j) {
+        h->pow_lane[j] = x;  // P^(j+1)
+        x = host_mulmod61(x, P);
+    }
+    uint64_t y = P;
+    for (int t = 0; t < 6; ++t) {
+        h->pow_step[t] = y;  // P^(2^t)
+        y = host_mulmod61(y, y);
+    }
+    h->root_key = mod61(mix64(seed ^ 0x9E3779B97F4A7C15ull));
+    h->content_seed = mix64(seed ^ 0xD6E8FEB86659FD93ull);
+    h->slot_seed = mix64(seed ^ 0xA0761D6478BD642Full);
+    h->weak = weak ? 1u : 0u;
+}
+
+IndexView index_view(ptstore_t* s) {
+    IndexView ix;
+    ix.slots = s->slots;
+    ix.slot_mask = s->slots_n - 1;
+    ix.parent = s->parent;
+    ix.tokens = s->tokens;
+    ix.ht = s->ht;
+    ix.state = s->state;
+    ix.block_tokens = s->cfg.block_tokens;
+    ix.counters = (s->cfg.flags & PTSTORE_FLAG_COUNTERS) ? 1 : 0;
+    return ix;
+}
+
+CopyPlan copy_plan(ptstore_t* s) {
+    CopyPlan p;
+    p.pool = s->pool;
+    p.block_bytes = s->block_bytes;
+    p.chunk_bytes = s->chunk_bytes;
+    p.chunks_per_block = 2 * s->cfg.num_layers;
+    p.chunks_per_group = s->chunks_per_group;
+    p.threads = s->threads;
+    p.state = s->state;
+    return p;
+}
+
+hipEvent_t take_event(ptstore_t* s) {
+    if (!s->free_ev.empty()) {
+        hipEvent_t e = s->free_ev.back();
+        s->free_ev.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets the kernels enqueued during its lifetime with two events.
+struct Timed {
+    ptstore_t* s;
+    int kind;
+    hipStream_t st;
+    hipEvent_t a = nullptr;
+    Timed(ptstore_t* s_, int k, hipStream_t st_) : s(s_), kind(k), st(st_) {
+        if (s->cfg.flags & PTSTORE_FLAG_TIMING) {
+            a = take_event(s);
+            if (a) hipEventRecord(a, st);
+        }
+    }
+    ~Timed() {
+        if (!a) return;
+        hipEvent_t b = take_event(s);
+        if (!b) return;
+        hipEventRecord(b, st);
+        s->ev[kind].push_back({a, b});
+    }
+};
+
+bool check_batch(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, int64_t n_tokens,
+                 int32_t R, int32_t max_blocks) {
+    (void)s;
+    if (R < 0 || max_blocks < 1) return false;
+    if (n_tokens < 0 || n_tokens >= (int64_t)0xFFFFFFFFll) return false;
+    if ((int64_t)R * max_blocks > (1ll << 29)) return false;
+    if (R > 0 && (!offsets || (!tokens && n_tokens > 0))) return false;
+    return true;
+}
+
+int set_device(ptstore_t* s) {
+    hipError_t e = hipSetDevice(s->device);
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "hipSetDevice", e);
+}
+
+}  // namespace
+
+namespace ptsd {
+__global__ void k_fill_slots(Slot* slots, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        Slot z;
+        z.key = kEmptyKey;
+        z.id = -1;
+        z.pad = 0;
+        slots[i] = z;
+    }
+}
+
+hipError_t launch_fill_slots(Slot* slots, int64_t n, hipStream_t s) {
+    int64_t g = (n + 255) / 256;
+    if (g > 65536) g = 65536;
+    if (g < 1) g = 1;
+    hipLaunchKernelGGL(k_fill_slots, dim3((unsigned)g), dim3(256), 0, s, slots, n);
+    return hipGetLastError();
+}
+}  // namespace ptsd
+
+#pragma GCC visibility push(default)
+extern "C" {
+
+const char* ptstore_strerror(int code) {
+    switch (code) {
+        case PTSTORE_OK: return "ok";
+        case PTSTORE_ERR_INVALID: return "invalid argument";
+        case PTSTORE_ERR_FULL: return "store full";
+        case PTSTORE_ERR_HIP: return "HIP runtime error";
+        case PTSTORE_ERR_NOMEM: return "out of memory";
+        default: return "unknown error";
+    }
+}
+
+const char* ptstore_last_error(void) { return g_last_error.c_str(); }
+
+int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
+    if (!cfg || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_create: null argument");
+    *out = nullptr;
+    const ptstore_config_t c = *cfg;
+    if (c.num_layers < 1 || c.num_kv_heads < 1 || c.head_dim < 1 || c.block_tokens < 1 ||
+        c.block_tokens > 64 || c.elem_bytes < 1)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_create: bad shape");
+    if (c.pool_blocks < 0 || c.pool_blocks > (int64_t)0x7FFFFFFC)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_create: pool_blocks out of range");
+    const int64_t chunk = (int64_t)c.num_kv_heads * c.block_tokens * c.head_dim * c.elem_bytes;
+    if (chunk % 16 != 0 || chunk > (1ll << 30))
+        return fail(PTSTORE_ERR_INVALID, "ptstore_create: chunk bytes must be a multiple of 16");
+    uint64_t slots_n;
+    if (c.index_slots == 0) {
+        slots_n = next_pow2((uint64_t)(2 * (c.pool_blocks > 1 ? c.pool_blocks : 1)));
+        if (slots_n < 64) slots_n = 64;
+    } else {
+        if (c.index_slots < 2 || (c.index_slots & (c.index_slots - 1)) != 0 ||
+            c.index_slots > (1ll << 32))
+            return fail(PTSTORE_ERR_INVALID, "ptstore_create: index_slots must be a power of two >= 2");
+        slots_n = (uint64_t)c.index_slots;
+    }
+    ptstore_t* s = new (std::nothrow) ptstore();
+    if (!s) return fail(PTSTORE_ERR_NOMEM, "ptstore_create: host allocation");
+    s->cfg = c;
+    s->chunk_bytes = chunk;
+    s->block_bytes = chunk * 2 * c.num_layers;
+    s->slots_n = slots_n;
+    s->capacity = c.pool_blocks < (int64_t)(slots_n / 2) ? c.pool_blocks : (int64_t)(slots_n / 2);
+    s->chunks_per_group = 8;
+    s->threads = 256;
+    hipError_t e = hipGetDevice(&s->device);
+    if (e != hipSuccess) {
+        delete s;
+        return fail(PTSTORE_ERR_HIP, "hipGetDevice", e);
+    }
+    const size_t pool_bytes = (size_t)(s->capacity > 0 ? s->capacity : 1) * (size_t)s->block_bytes;
+    const size_t cap1 = (size_t)(s->capacity > 0 ? s->capacity : 1);
+    if ((e = hipMalloc(&s->pool, pool_bytes)) != hipSuccess ||
+        (e = hipMalloc(&s->parent, cap1 * 4)) != hipSuccess ||
+        (e = hipMalloc(&s->tokens, cap1 * 4 * c.block_tokens)) != hipSuccess ||
+        (e = hipMalloc(&s->slots, slots_n * sizeof(Slot))) != hipSuccess ||
+        (e = hipMalloc(&s->ht, sizeof(HashTables))) != hipSuccess ||
+        (e = hipMalloc(&s->state, sizeof(DevState))) != hipSuccess) {
+        ptstore_destroy(s);
+        hipGetLastError();
+        return fail(PTSTORE_ERR_NOMEM, "ptstore_create: hipMalloc", e);
+    }
+    HashTables h;
+    make_hash_tables(c.hash_seed, (c.flags & PTSTORE_FLAG_WEAK_HASH) != 0, &h);
+    DevState st;
+    memset(&st, 0, sizeof st);
+    if ((e = hipMemcpy(s->ht, &h, sizeof h, hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = hipMemcpy(s->state, &st, sizeof st, hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = launch_fill_slots(s->slots, (int64_t)slots_n, nullptr)) != hipSuccess ||
+        (e = hipDeviceSynchronize()) != hipSuccess) {
+        ptstore_destroy(s);
+        return fail(PTSTORE_ERR_HIP, "ptstore_create: initialisation", e);
+    }
+    *out = s;
+    return PTSTORE_OK;
+}
+
+int ptstore_destroy(ptstore_t* s) {
+    if (!s) return PTSTORE_OK;
+    hipSetDevice(s->device);
+    hipDeviceSynchronize();
+    for (auto& v : s->ev)
+        for (auto& p : v) {
+            hipEventDestroy(p.first);
+            hipEventDestroy(p.second);
+        }
+    for (auto e : s->free_ev) hipEventDestroy(e);
+    hipFree(s->pool);
+    hipFree(s->parent);
+    hipFree(s->tokens);
+    hipFree(s->slots);
+    hipFree(s->ht);
+    hipFree(s->state);
+    hipFree(s->scratch);
+    delete s;
+    return PTSTORE_OK;
+}
+
+int ptstore_lookup(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, int64_t n_tokens,
+                   int32_t R, int32_t max_blocks, int32_t* m, int32_t* ids, void* stream) {
+    if (!s || !check_batch(s, tokens, offsets, n_tokens, R, max_blocks) || (R > 0 && (!m || !ids)))
+        return fail(PTSTORE_ERR_INVALID, "ptstore_lookup: bad argument");
+    if (R == 0) return PTSTORE_OK;
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    Batch b{tokens, offsets, n_tokens, R, max_blocks};
+    hipError_t e;
+    {
+        Timed t(s, 1, st);
+        e = launch_lookup(index_view(s), b, m, ids, st);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_lookup: launch", e);
+}
+
+int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int32_t* block_table,
+                   int32_t R, int32_t max_blocks, void* cache, int64_t cache_blocks, void* stream) {
+    if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
+        (R > 0 && (!ids || !m || !block_table || !cache)) ||
+        (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_gather: bad argument");
+    if ((int64_t)R * max_blocks * 2 * s->cfg.num_layers > 0x7FFFFFFFll * s->chunks_per_group)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_gather: batch too large for one launch");
+    if (R == 0) return PTSTORE_OK;
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    {
+        Timed t(s, 0, st);
+        e = launch_gather(copy_plan(s), ids, m, block_table, R, max_blocks,
+                          static_cast<uint8_t*>(cache), cache_blocks, st);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_gather: launch", e);
+}
+
+int ptstore_lookup_gather(ptstore_t* s, const int32_t* tokens, const int64_t* offsets,
+                          int64_t n_tokens, int32_t R, int32_t max_blocks, int32_t* m, int32_t* ids,
+                          const int32_t* block_table, void* cache, int64_t cache_blocks,
+                          void* stream) {
+    if (!s || (R > 0 && (!block_table || !cache)) || cache_blocks < 0 ||
+        (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_lookup_gather: bad argument");
+    int rc = ptstore_lookup(s, tokens, offsets, n_tokens, R, max_blocks, m, ids, stream);
+    if (rc) return rc;
+    return ptstore_gather(s, ids, m, block_table, R, max_blocks, cache, cache_blocks, stream);
+}
+
+int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, int64_t n_tokens,
+                   int32_t R, int32_t max_blocks, int32_t* m_out, int32_t* ids, uint8_t* created,
+                   void* stream) {
+    if (!s || !check_batch(s, tokens, offsets, n_tokens, R, max_blocks) ||
+        (R > 0 && (!m_out || !ids || !created)))
+        return fail(PTSTORE_ERR_INVALID, "ptstore_insert: bad argument");
+    if (R == 0) return PTSTORE_OK;
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    uint64_t tn;
+    const size_t need = insert_scratch_bytes(R, max_blocks, &tn);
+    hipError_t e;
+    if (need > s->scratch_bytes) {
+        // earlier work on this stream may still use the old scratch
+        if ((e = hipStreamSynchronize(st)) != hipSuccess)
+            return fail(PTSTORE_ERR_HIP, "ptstore_insert: stream sync", e);
+        hipFree(s->scratch);
+        s->scratch = nullptr;
+        s->scratch_bytes = 0;
+        size_t grow = need + need / 4;
+        if ((e = hipMalloc(&s->scratch, grow)) != hipSuccess) {
+            hipGetLastError();
+            return fail(PTSTORE_ERR_NOMEM, "ptstore_insert: scratch hipMalloc", e);
+        }
+        s->scratch_bytes = grow;
+    }
+    InsertScratch sc;
+    insert_scratch_carve(s->scratch, R, max_blocks, &sc);
+    InsertTarget tgt{s->slots, s->parent, s->tokens, s->capacity};
+    Batch b{tokens, offsets, n_tokens, R, max_blocks};
+    {
+        Timed t(s, 3, st);
+        e = launch_insert(index_view(s), tgt, b, sc, m_out, ids, created, st);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_insert: launch", e);
+}
+
+int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
+                    const int32_t* block_table, int32_t R, int32_t max_blocks, const void* cache,
+                    int64_t cache_blocks, void* stream) {
+    if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
+        (R > 0 && (!ids || !created || !block_table || !cache)) ||
+        (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: bad argument");
+    if ((int64_t)R * max_blocks * 2 * s->cfg.num_layers > 0x7FFFFFFFll * s->chunks_per_group)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: batch too large for one launch");
+    if (R == 0) return PTSTORE_OK;
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    {
+        Timed t(s, 2, st);
+        e = launch_scatter(copy_plan(s), ids, created, block_table, R, max_blocks,
+                           static_cast<const uint8_t*>(cache), cache_blocks, st);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_scatter: launch", e);
+}
+
+int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
+    if (!s || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_stats: null argument");
+    int rc = set_device(s);
+    if (rc) return rc;
+    DevState st;
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(&st, s->state, sizeof st, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, "ptstore_stats", e);
+    out->blocks_stored = (int64_t)st.count;
+    out->capacity = s->capacity;
+    out->index_slots = (int64_t)s->slots_n;
+    out->block_bytes = s->block_bytes;
+    out->chunk_bytes = s->chunk_bytes;
+    out->full_events = (int64_t)st.full_events;
+    out->bad_entries = (int64_t)st.bad_entries;
+    out->probes = (int64_t)st.probes;
+    out->token_compares = (int64_t)st.token_compares;
+    out->cas_attempts = (int64_t)st.cas_attempts;
+    out->cas_failures = (int64_t)st.cas_failures;
+    return PTSTORE_OK;
+}
+
+int ptstore_reset_counters(ptstore_t* s) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_reset_counters: null store");
+    int rc = set_device(s);
+    if (rc) return rc;
+    DevState st;
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(&st, s->state, sizeof st, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) {
+        const unsigned long long count = st.count;
+        memset(&st, 0, sizeof st);
+        st.count = count;
+        e = hipMemcpy(s->state, &st, sizeof st, hipMemcpyHostToDevice);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_reset_counters", e);
+}
+
+int ptstore_get_buffers(ptstore_t* s, ptstore_buffers_t* out) {
+    if (!s || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_get_buffers: null argument");
+    out->pool = s->pool;
+    out->parent = s->parent;
+    out->tokens = s->tokens;
+    out->slots = s->slots;
+    out->capacity = s->capacity;
+    out->index_slots = (int64_t)s->slots_n;
+    return PTSTORE_OK;
+}
+
+int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* launches) {
+    if (!s || kind < 0 || kind > 3 || !total_ms || !launches)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_kernel_times: bad argument");
+    int rc = set_device(s);
+    if (rc) return rc;
+    double sum = 0;
+    int64_t n = 0;
+    for (auto& p : s->ev[kind]) {
+        hipError_t e = hipEventSynchronize(p.second);
+        float ms = 0;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.first, p.second);
+        if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, "ptstore_kernel_times", e);
+        sum += ms;
+        ++n;
+        s->free_ev.push_back(p.first);
+        s->free_ev.push_back(p.second);
+    }
+    s->ev[kind].clear();
+    *total_ms = sum;
+    *launches = n;
+    return PTSTORE_OK;
+}
+
+int ptstore_set_copy_shape(ptstore_t* s, int32_t chunks_per_group, int32_t threads) {
+    if (!s || chunks_per_group < 0 || threads < 0 || (threads && (threads < 64 || threads > 1024 || threads % 64)))
+        return fail(PTSTORE_ERR_INVALID, "ptstore_set_copy_shape: bad argument");
+    if (chunks_per_group) s->chunks_per_group = chunks_per_group;
+    if (threads) s->threads = threads;
+    return PTSTORE_OK;
+}
+
+}  // extern "C"
+#pragma GCC visibility pop

@@ -1,0 +1,141 @@
+// Device-side building blocks shared by the prefix-store kernels (gfx950).
+//
+// Keys. A request's block b gets a chained key k_b that depends on all of
+// its tokens up to the end of block b: k_b = P * k_{b-1} + c_b (mod 2^61-1),
+// where c_b is a 64-bit mix of the block's tokens reduced mod 2^61-1 and
+// k_{-1} is a seed-derived root key. Because the chain is affine, the keys of
+// a 64-block window come out of one wavefront prefix scan instead of 64
+// dependent steps. Keys only steer probing: a hit is accepted only after its
+// block's tokens and parent id are compared, so results never depend on the
+// hash (the store is exact, as the paper's id lists are).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ptsd {
+
+constexpr uint64_t kM61 = (1ull << 61) - 1;
+constexpr uint64_t kEmptyKey = ~0ull;  // never a key: keys are < 2^61
+constexpr int kWave = 64;
+
+// One slot of the open-addressing block index.
+struct alignas(16) Slot {
+    uint64_t key;  // index key, kEmptyKey if free
+    int32_t id;    // block id
+    int32_t pad;
+};
+
+// Per-store constants of the key chain, in device memory.
+struct HashTables {
+    uint64_t pow_lane[kWave];  // P^(j+1), j = 0..63
+    uint64_t pow_step[6];      // P^(2^t), t = 0..5
+    uint64_t root_key;         // k_{-1}
+    uint64_t content_seed;
+    uint64_t slot_seed;
+    uint32_t weak;             // 1: index keys masked to 8 bits
+    uint32_t pad;
+};
+
+// Device-side counters and status of a store.
+struct DevState {
+    unsigned long long count;         // blocks stored (= next id)
+    unsigned long long full_events;
+    unsigned long long bad_entries;
+    unsigned long long probes;
+    unsigned long long token_compares;
+    unsigned long long cas_attempts;
+    unsigned long long cas_failures;
+    unsigned long long insert_old_count;  // scratch: count before the running insert
+};
+
+__host__ __device__ inline uint64_t mix64(uint64_t z) {
+    // SplitMix64 finaliser (Steele, Lea, Flood 2014)
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__host__ __device__ inline uint64_t mod61(uint64_t x) {
+    x = (x & kM61) + (x >> 61);
+    return x >= kM61 ? x - kM61 : x;
+}
+
+__device__ inline uint64_t mulmod61(uint64_t a, uint64_t b) {
+    uint64_t lo = a * b;
+    uint64_t hi = __umul64hi(a, b);
+    uint64_t x = (lo & kM61) + ((lo >> 61) | (hi << 3));
+    return mod61(x);
+}
+
+__device__ inline uint64_t addmod61(uint64_t a, uint64_t b) { return mod61(a + b); }
+
+// Content hash of one block of BT tokens (BT words read from `blk`).
+template <int BT>
+__device__ inline uint64_t content_hash_regs(const int32_t (&t)[BT], uint64_t seed) {
+    uint64_t h = seed ^ (0x9E3779B97F4A7C15ull * BT);
+#pragma unroll
+    for (int i = 0; i < BT; i += 2) {
+        uint64_t w = (uint64_t)(uint32_t)t[i];
+        if (i + 1 < BT) w |= (uint64_t)(uint32_t)t[i + 1] << 32;
+        h = mix64(h ^ (w + 0x632BE59BD9B4E019ull * (uint64_t)(i + 1)));
+    }
+    return mod61(mix64(h));
+}
+
+__device__ inline uint64_t content_hash_mem(const int32_t* __restrict__ blk, int bt, uint64_t seed) {
+    uint64_t h = seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)bt);
+    for (int i = 0; i < bt; i += 2) {
+        uint64_t w = (uint64_t)(uint32_t)blk[i];
+        if (i + 1 < bt) w |= (uint64_t)(uint32_t)blk[i + 1] << 32;
+        h = mix64(h ^ (w + 0x632BE59BD9B4E019ull * (uint64_t)(i + 1)));
+    }
+    return mod61(mix64(h));
+}
+
+__device__ inline uint64_t index_key(uint64_t k, const HashTables& ht) {
+    return ht.weak ? (k & 0xFFull) : k;
+}
+
+__device__ inline uint64_t slot_of(uint64_t ikey, uint64_t seed, uint64_t mask) {
+    return mix64(ikey ^ seed) & mask;
+}
+
+// 64-bit wavefront shuffles built from 32-bit ones.
+__device__ inline uint64_t shfl_u64(uint64_t v, int src) {
+    uint32_t lo = __shfl((int)(uint32_t)v, src, kWave);
+    uint32_t hi = __shfl((int)(uint32_t)(v >> 32), src, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ inline uint64_t shfl_up_u64(uint64_t v, int d) {
+    uint32_t lo = __shfl_up((int)(uint32_t)v, d, kWave);
+    uint32_t hi = __shfl_up((int)(uint32_t)(v >> 32), d, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive scan of the affine key chain over one 64-block window.
+// c: this lane's content hash (0 for lanes past the request's end);
+// carry: k_{w0-1}. Returns this lane's chained key k_{w0+lane}.
+__device__ inline uint64_t window_chain(uint64_t c, uint64_t carry, const HashTables* __restrict__ ht,
+                                        int lane) {
+    uint64_t s = c;
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+        const int d = 1 << t;
+        uint64_t sp = shfl_up_u64(s, d);
+        if (lane >= d) s = addmod61(s, mulmod61(ht->pow_step[t], sp));
+    }
+    return addmod61(mulmod61(ht->pow_lane[lane], carry), s);
+}
+
+__device__ inline unsigned long long ballot64(bool p) { return __ballot(p); }
+
+// Sum of a per-lane count over the wave, added once to a device counter.
+__device__ inline void wave_count(unsigned long long* ctr, unsigned long long v, int lane) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v += (unsigned long long)shfl_u64(v, lane ^ d);
+    if (lane == 0 && v) atomicAdd(ctr, v);
+}
+
+}  // namespace ptsd

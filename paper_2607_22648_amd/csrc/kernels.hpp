@@ -1,0 +1,80 @@
+// Launch interface between the host runtime (api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device_common.hpp"
+
+namespace ptsd {
+
+// Read-only view of the store used by the lookup kernels.
+struct IndexView {
+    const Slot* slots;
+    uint64_t slot_mask;
+    const int32_t* parent;   // [capacity]
+    const int32_t* tokens;   // [capacity][block_tokens]
+    const HashTables* ht;
+    DevState* state;
+    int32_t block_tokens;
+    int32_t counters;        // 1: count probes and comparisons
+};
+
+struct Batch {
+    const int32_t* tokens;
+    const int64_t* offsets;
+    int64_t n_tokens;
+    int32_t R;
+    int32_t max_blocks;
+};
+
+// lookup.hip
+hipError_t launch_lookup(const IndexView& ix, const Batch& b, int32_t* m, int32_t* ids,
+                         hipStream_t s);
+hipError_t launch_hash_all(const IndexView& ix, const Batch& b, uint64_t* keys, hipStream_t s);
+
+// copy.hip
+struct CopyPlan {
+    uint8_t* pool;
+    int64_t block_bytes;
+    int64_t chunk_bytes;
+    int32_t chunks_per_block;  // 2 * layers
+    int32_t chunks_per_group;
+    int32_t threads;
+    DevState* state;
+};
+hipError_t launch_gather(const CopyPlan& p, const int32_t* ids, const int32_t* m,
+                         const int32_t* block_table, int32_t R, int32_t max_blocks,
+                         uint8_t* cache, int64_t cache_blocks, hipStream_t s);
+hipError_t launch_scatter(const CopyPlan& p, const int32_t* ids, const uint8_t* created,
+                          const int32_t* block_table, int32_t R, int32_t max_blocks,
+                          const uint8_t* cache, int64_t cache_blocks, hipStream_t s);
+
+// insert.hip
+struct BatchEntry;  // defined in insert.hip
+struct InsertScratch {
+    uint64_t* keys;       // [R][max_blocks]
+    int32_t* m0;          // [R] match length before the insert
+    int32_t* label;       // [R][max_blocks] batch-table slot of each new block
+    int32_t* cnt;         // [R] blocks each request is the first to need
+    int32_t* base;        // [R] exclusive scan of cnt
+    void* table;          // batch table, table_mask + 1 entries of 16 bytes
+    uint64_t table_mask;
+};
+size_t insert_scratch_bytes(int32_t R, int32_t max_blocks, uint64_t* table_entries);
+void insert_scratch_carve(void* base, int32_t R, int32_t max_blocks, InsertScratch* out);
+
+struct InsertTarget {
+    Slot* slots;
+    int32_t* parent;
+    int32_t* tokens;
+    int64_t capacity;
+};
+hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Batch& b,
+                         const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+                         uint8_t* created, hipStream_t s);
+
+// api.hip helpers
+hipError_t launch_fill_slots(Slot* slots, int64_t n, hipStream_t s);
+
+}  // namespace ptsd

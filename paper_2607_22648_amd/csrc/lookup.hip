@@ -1,0 +1,235 @@
+// Batched longest-common-prefix lookup (PTStore Section 4.1, the LCP query:
+// the longest prefix of a request that is stored, and the ids along it).
+//
+// One wavefront per request, lane j owns block w0+j of a 64-block window:
+//   1. each lane loads its block's tokens and hashes them;
+//   2. a wave prefix scan chains the hashes into per-block prefix keys;
+//   3. each lane probes the open-addressing index for its key and accepts the
+//      first slot whose stored block has the same tokens;
+//   4. the candidate of lane j must have as parent the id accepted by lane
+//      j-1 (the root, -1, for block 0); a ballot finds the first lane that
+//      fails, which is the end of the match. If that lane did find a block
+//      with the right tokens but the wrong parent (two prefixes whose keys
+//      collide), it keeps probing for one with the right parent before the
+//      window is decided, so the answer never depends on the hash.
+// Windows are walked in order and the walk stops at the first miss.
+#include "kernels.hpp"
+
+namespace ptsd {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWavesPerGroup = kThreads / kWave;
+
+// Tokens of one block held in registers (BT = 16) or read from memory (BT = 0).
+template <int BT>
+struct BlockTokens {
+    int32_t t[BT];
+    __device__ inline void load(const int32_t* __restrict__ p) {
+        if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+#pragma unroll
+            for (int i = 0; i < BT; i += 4) {
+                int4 v = *reinterpret_cast<const int4*>(p + i);
+                t[i] = v.x; t[i + 1] = v.y; t[i + 2] = v.z; t[i + 3] = v.w;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < BT; ++i) t[i] = p[i];
+        }
+    }
+    __device__ inline uint64_t hash(uint64_t seed, int) const { return content_hash_regs<BT>(t, seed); }
+    // stored rows are BT*4 = 64-byte aligned
+    __device__ inline bool equals(const int32_t* __restrict__ s, int) const {
+        bool eq = true;
+#pragma unroll
+        for (int i = 0; i < BT; i += 4) {
+            int4 v = *reinterpret_cast<const int4*>(s + i);
+            eq &= (v.x == t[i]) & (v.y == t[i + 1]) & (v.z == t[i + 2]) & (v.w == t[i + 3]);
+        }
+        return eq;
+    }
+};
+
+template <>
+struct BlockTokens<0> {
+    const int32_t* p;
+    __device__ inline void load(const int32_t* __restrict__ q) { p = q; }
+    __device__ inline uint64_t hash(uint64_t seed, int bt) const { return content_hash_mem(p, bt, seed); }
+    __device__ inline bool equals(const int32_t* __restrict__ s, int bt) const {
+        for (int i = 0; i < bt; ++i)
+            if (s[i] != p[i]) return false;
+        return true;
+    }
+};
+
+// Linear probing from `pos` for a slot holding `ikey` whose block has the
+// lane's tokens (and, if need_parent, parent id `want_parent`).
+// Returns the block id or -1 at the first empty slot; *pos_out is the slot.
+template <int BT>
+__device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos,
+                                const BlockTokens<BT>& bk, bool need_parent, int32_t want_parent,
+                                uint64_t* pos_out, unsigned long long* probes,
+                                unsigned long long* cmps) {
+    const int bt = BT ? BT : ix.block_tokens;
+    while (true) {
+        const Slot s = ix.slots[pos];
+        ++*probes;
+        if (s.key == kEmptyKey) {
+            *pos_out = pos;
+            return -1;
+        }
+        if (s.key == ikey) {
+            ++*cmps;
+            if (bk.equals(ix.tokens + (int64_t)s.id * bt, bt) &&
+                (!need_parent || ix.parent[s.id] == want_parent)) {
+                *pos_out = pos;
+                return s.id;
+            }
+        }
+        pos = (pos + 1) & ix.slot_mask;
+    }
+}
+
+// Request bounds; a malformed request is empty and counted.
+__device__ inline int32_t request_blocks(const Batch& b, int64_t r, int bt, int lane,
+                                         DevState* st, int64_t* o0) {
+    int64_t a = b.offsets[r], e = b.offsets[r + 1];
+    if (a < 0 || e < a || e > b.n_tokens) {
+        if (lane == 0) atomicAdd(&st->bad_entries, 1ull);
+        *o0 = 0;
+        return 0;
+    }
+    *o0 = a;
+    int64_t n = (e - a) / bt;
+    return (int32_t)(n < b.max_blocks ? n : b.max_blocks);
+}
+
+template <int BT>
+__global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, int32_t* __restrict__ m_out,
+                                                     int32_t* __restrict__ ids_out) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWavesPerGroup + (threadIdx.x / kWave);
+    if (r >= bat.R) return;  // uniform per wave
+    const int bt = BT ? BT : ix.block_tokens;
+    const HashTables* __restrict__ ht = ix.ht;
+    int64_t o0;
+    const int32_t n = request_blocks(bat, r, bt, lane, ix.state, &o0);
+    const int32_t* __restrict__ seq = bat.tokens + o0;
+    int32_t* __restrict__ row = ids_out + r * bat.max_blocks;
+
+    uint64_t carry_key = ht->root_key;
+    int32_t carry_id = -1;  // the root
+    int32_t m = 0;
+    unsigned long long probes = 0, cmps = 0;
+    int w0 = 0;
+    bool done = false;
+    for (; w0 < n && !done; w0 += kWave) {
+        const int b = w0 + lane;
+        const bool active = b < n;
+        BlockTokens<BT> bk;
+        uint64_t c = 0;
+        if (active) {
+            bk.load(seq + (int64_t)b * bt);
+            c = bk.hash(ht->content_seed, bt);
+        }
+        const uint64_t k = window_chain(c, carry_key, ht, lane);
+        const uint64_t ik = index_key(k, *ht);
+        int32_t cand = -1;
+        uint64_t pos = 0;
+        if (active)
+            cand = probe<BT>(ix, ik, slot_of(ik, ht->slot_seed, ix.slot_mask), bk, false, 0, &pos,
+                             &probes, &cmps);
+        int first_bad = kWave;
+        while (true) {
+            int32_t prev = __shfl_up(cand, 1, kWave);
+            if (lane == 0) prev = carry_id;
+            const int32_t par = cand >= 0 ? ix.parent[cand] : -2;
+            const bool ok = active && cand >= 0 && par == prev;
+            const unsigned long long bad = ballot64(!ok);
+            if (bad == 0) break;
+            const int f = __ffsll((long long)bad) - 1;
+            const int retry = __shfl((active && cand >= 0 && par != prev) ? 1 : 0, f, kWave);
+            if (!retry) {
+                first_bad = f;
+                break;
+            }
+            // keys of two different prefixes collided: lane f looks further
+            // along its probe sequence for the block with the right parent
+            if (lane == f)
+                cand = probe<BT>(ix, ik, (pos + 1) & ix.slot_mask, bk, true, prev, &pos, &probes,
+                                 &cmps);
+        }
+        if (active) row[b] = lane < first_bad ? cand : -1;
+        if (first_bad < kWave) {
+            m = w0 + first_bad;
+            done = true;
+        } else {
+            m = w0 + kWave;
+            carry_id = __shfl(cand, kWave - 1, kWave);
+            carry_key = shfl_u64(k, kWave - 1);
+        }
+    }
+    const int fill_from = w0 < n ? w0 : n;
+    for (int b = fill_from + lane; b < bat.max_blocks; b += kWave) row[b] = -1;
+    if (lane == 0) m_out[r] = m;
+    if (ix.counters) {
+        wave_count(&ix.state->probes, probes, lane);
+        wave_count(&ix.state->token_compares, cmps, lane);
+    }
+}
+
+// Chained keys of every whole block of every request (no probing).
+template <int BT>
+__global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, uint64_t* __restrict__ keys) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWavesPerGroup + (threadIdx.x / kWave);
+    if (r >= bat.R) return;
+    const int bt = BT ? BT : ix.block_tokens;
+    const HashTables* __restrict__ ht = ix.ht;
+    int64_t o0;
+    // malformed requests were already counted by the lookup of the same batch
+    int64_t a = bat.offsets[r], e = bat.offsets[r + 1];
+    int32_t n = 0;
+    o0 = 0;
+    if (!(a < 0 || e < a || e > bat.n_tokens)) {
+        o0 = a;
+        int64_t nb = (e - a) / bt;
+        n = (int32_t)(nb < bat.max_blocks ? nb : bat.max_blocks);
+    }
+    const int32_t* __restrict__ seq = bat.tokens + o0;
+    uint64_t carry = ht->root_key;
+    for (int w0 = 0; w0 < n; w0 += kWave) {
+        const int b = w0 + lane;
+        uint64_t c = 0;
+        if (b < n) {
+            BlockTokens<BT> bk;
+            bk.load(seq + (int64_t)b * bt);
+            c = bk.hash(ht->content_seed, bt);
+        }
+        const uint64_t k = window_chain(c, carry, ht, lane);
+        if (b < n) keys[r * bat.max_blocks + b] = k;
+        carry = shfl_u64(k, kWave - 1);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_lookup(const IndexView& ix, const Batch& b, int32_t* m, int32_t* ids, hipStream_t s) {
+    const unsigned grid = (unsigned)((b.R + kWavesPerGroup - 1) / kWavesPerGroup);
+    if (ix.block_tokens == 16)
+        hipLaunchKernelGGL(k_lookup<16>, dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+    else
+        hipLaunchKernelGGL(k_lookup<0>, dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+    return hipGetLastError();
+}
+
+hipError_t launch_hash_all(const IndexView& ix, const Batch& b, uint64_t* keys, hipStream_t s) {
+    const unsigned grid = (unsigned)((b.R + kWavesPerGroup - 1) / kWavesPerGroup);
+    if (ix.block_tokens == 16)
+        hipLaunchKernelGGL(k_hash_all<16>, dim3(grid), dim3(kThreads), 0, s, ix, b, keys);
+    else
+        hipLaunchKernelGGL(k_hash_all<0>, dim3(grid), dim3(kThreads), 0, s, ix, b, keys);
+    return hipGetLastError();
+}
+
+}  // namespace ptsd

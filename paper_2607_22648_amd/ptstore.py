@@ -1,0 +1,329 @@
+"""Python binding of the C ABI in include/ptstore.h (argument marshalling only).
+
+The functions carry the C names and forward device pointers of torch tensors
+plus the current HIP stream; every step of the work runs in the HIP library
+``libptstore.so``. If the library has not been built this module raises at
+import time: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libptstore.so")
+
+PTSTORE_OK, PTSTORE_ERR_INVALID, PTSTORE_ERR_FULL, PTSTORE_ERR_HIP, PTSTORE_ERR_NOMEM = 0, 1, 2, 3, 4
+PTSTORE_FLAG_WEAK_HASH, PTSTORE_FLAG_COUNTERS, PTSTORE_FLAG_TIMING = 1, 2, 4
+KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT = 0, 1, 2, 3
+
+
+class ptstore_config_t(C.Structure):
+    _fields_ = [("num_layers", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("block_tokens", C.c_int32), ("elem_bytes", C.c_int32),
+                ("pool_blocks", C.c_int64), ("index_slots", C.c_int64),
+                ("hash_seed", C.c_uint64), ("flags", C.c_uint32)]
+
+
+class ptstore_stats_t(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in (
+        "blocks_stored", "capacity", "index_slots", "block_bytes", "chunk_bytes", "full_events",
+        "bad_entries", "probes", "token_compares", "cas_attempts", "cas_failures")]
+
+
+class ptstore_buffers_t(C.Structure):
+    _fields_ = [("pool", C.c_void_p), ("parent", C.c_void_p), ("tokens", C.c_void_p),
+                ("slots", C.c_void_p), ("capacity", C.c_int64), ("index_slots", C.c_int64)]
+
+
+class PTStoreError(RuntimeError):
+    def __init__(self, fn: str, code: int, detail: str):
+        super().__init__(f"{fn} failed: code {code} ({detail})")
+        self.code = code
+
+
+EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gather",
+           "ptstore_lookup_gather", "ptstore_insert", "ptstore_scatter", "ptstore_stats",
+           "ptstore_reset_counters", "ptstore_get_buffers", "ptstore_kernel_times",
+           "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error")
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it first (python -m "
+                          "paper_2607_22648_amd.build or __graft_entry__.build())")
+    lib = C.CDLL(LIB_PATH)
+    p, i32, i64, d = C.c_void_p, C.c_int32, C.c_int64, C.c_double
+    sig = {
+        "ptstore_create": [C.POINTER(ptstore_config_t), C.POINTER(C.c_void_p)],
+        "ptstore_destroy": [p],
+        "ptstore_lookup": [p, p, p, i64, i32, i32, p, p, p],
+        "ptstore_gather": [p, p, p, p, i32, i32, p, i64, p],
+        "ptstore_lookup_gather": [p, p, p, i64, i32, i32, p, p, p, p, i64, p],
+        "ptstore_insert": [p, p, p, i64, i32, i32, p, p, p, p],
+        "ptstore_scatter": [p, p, p, p, i32, i32, p, i64, p],
+        "ptstore_stats": [p, C.POINTER(ptstore_stats_t)],
+        "ptstore_reset_counters": [p],
+        "ptstore_get_buffers": [p, C.POINTER(ptstore_buffers_t)],
+        "ptstore_kernel_times": [p, i32, C.POINTER(d), C.POINTER(i64)],
+        "ptstore_set_copy_shape": [p, i32, i32],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    lib.ptstore_strerror.argtypes = [C.c_int]
+    lib.ptstore_strerror.restype = C.c_char_p
+    lib.ptstore_last_error.argtypes = []
+    lib.ptstore_last_error.restype = C.c_char_p
+    return lib
+
+
+_lib = _load()
+
+
+def lib() -> C.CDLL:
+    return _lib
+
+
+def _check(fn: str, rc: int):
+    if rc != PTSTORE_OK:
+        raise PTStoreError(fn, rc, _lib.ptstore_last_error().decode())
+
+
+def _dev(t: Optional[torch.Tensor], dtype, name: str) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+# ---------------------------------------------------------------------------
+# C entry points under their own names
+# ---------------------------------------------------------------------------
+
+def ptstore_create(cfg: ptstore_config_t) -> C.c_void_p:
+    h = C.c_void_p()
+    _check("ptstore_create", _lib.ptstore_create(C.byref(cfg), C.byref(h)))
+    return h
+
+
+def ptstore_destroy(h) -> None:
+    _check("ptstore_destroy", _lib.ptstore_destroy(h))
+
+
+def ptstore_lookup(h, tokens, offsets, max_blocks, m, ids, stream=None) -> None:
+    R = offsets.numel() - 1
+    _check("ptstore_lookup", _lib.ptstore_lookup(
+        h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
+        tokens.numel(), R, max_blocks, _dev(m, torch.int32, "m"), _dev(ids, torch.int32, "ids"),
+        _stream(stream)))
+
+
+def _cache_blocks(cache: torch.Tensor, chunk_bytes: int, layers: int) -> int:
+    nbytes = cache.numel() * cache.element_size()
+    per = chunk_bytes * 2 * layers
+    if nbytes % per:
+        raise ValueError("cache size is not a whole number of blocks")
+    return nbytes // per
+
+
+def ptstore_gather(h, ids, m, block_table, cache, cache_blocks, stream=None) -> None:
+    R, maxb = ids.shape
+    _check("ptstore_gather", _lib.ptstore_gather(
+        h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
+        _dev(block_table, torch.int32, "block_table"), R, maxb, _dev(cache, None, "cache"),
+        cache_blocks, _stream(stream)))
+
+
+def ptstore_lookup_gather(h, tokens, offsets, max_blocks, m, ids, block_table, cache, cache_blocks,
+                          stream=None) -> None:
+    R = offsets.numel() - 1
+    _check("ptstore_lookup_gather", _lib.ptstore_lookup_gather(
+        h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
+        tokens.numel(), R, max_blocks, _dev(m, torch.int32, "m"), _dev(ids, torch.int32, "ids"),
+        _dev(block_table, torch.int32, "block_table"), _dev(cache, None, "cache"), cache_blocks,
+        _stream(stream)))
+
+
+def ptstore_insert(h, tokens, offsets, max_blocks, m_out, ids, created, stream=None) -> None:
+    R = offsets.numel() - 1
+    _check("ptstore_insert", _lib.ptstore_insert(
+        h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
+        tokens.numel(), R, max_blocks, _dev(m_out, torch.int32, "m_out"),
+        _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"), _stream(stream)))
+
+
+def ptstore_scatter(h, ids, created, block_table, cache, cache_blocks, stream=None) -> None:
+    R, maxb = ids.shape
+    _check("ptstore_scatter", _lib.ptstore_scatter(
+        h, _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"),
+        _dev(block_table, torch.int32, "block_table"), R, maxb, _dev(cache, None, "cache"),
+        cache_blocks, _stream(stream)))
+
+
+def ptstore_stats(h) -> dict:
+    s = ptstore_stats_t()
+    _check("ptstore_stats", _lib.ptstore_stats(h, C.byref(s)))
+    return {n: getattr(s, n) for n, _ in s._fields_}
+
+
+def ptstore_reset_counters(h) -> None:
+    _check("ptstore_reset_counters", _lib.ptstore_reset_counters(h))
+
+
+def ptstore_get_buffers(h) -> ptstore_buffers_t:
+    b = ptstore_buffers_t()
+    _check("ptstore_get_buffers", _lib.ptstore_get_buffers(h, C.byref(b)))
+    return b
+
+
+def ptstore_kernel_times(h, kind: int) -> Tuple[float, int]:
+    ms, n = C.c_double(), C.c_int64()
+    _check("ptstore_kernel_times", _lib.ptstore_kernel_times(h, kind, C.byref(ms), C.byref(n)))
+    return ms.value, n.value
+
+
+def ptstore_set_copy_shape(h, chunks_per_group: int = 0, threads: int = 0) -> None:
+    _check("ptstore_set_copy_shape", _lib.ptstore_set_copy_shape(h, chunks_per_group, threads))
+
+
+def ptstore_strerror(code: int) -> str:
+    return _lib.ptstore_strerror(code).decode()
+
+
+def ptstore_last_error() -> str:
+    return _lib.ptstore_last_error().decode()
+
+
+# ---------------------------------------------------------------------------
+# Convenience wrapper
+# ---------------------------------------------------------------------------
+
+@dataclass
+class StoreShape:
+    layers: int
+    kv_heads: int
+    head_dim: int
+    block_tokens: int = 16
+    elem_bytes: int = 2
+
+    @property
+    def chunk_bytes(self) -> int:
+        return self.kv_heads * self.block_tokens * self.head_dim * self.elem_bytes
+
+    @property
+    def block_bytes(self) -> int:
+        return self.layers * 2 * self.chunk_bytes
+
+
+class PrefixStore:
+    """A store on the current device; methods take device tensors."""
+
+    def __init__(self, shape: StoreShape, pool_blocks: int, index_slots: int = 0,
+                 hash_seed: int = 0x5EED, flags: int = 0):
+        self.shape = shape
+        cfg = ptstore_config_t(shape.layers, shape.kv_heads, shape.head_dim, shape.block_tokens,
+                               shape.elem_bytes, pool_blocks, index_slots, hash_seed, flags)
+        self.h = ptstore_create(cfg)
+
+    def close(self):
+        if getattr(self, "h", None):
+            ptstore_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def cache_blocks(self, cache: torch.Tensor) -> int:
+        return _cache_blocks(cache, self.shape.chunk_bytes, self.shape.layers)
+
+    def lookup(self, tokens, offsets, max_blocks, m=None, ids=None, stream=None):
+        R = offsets.numel() - 1
+        dev = offsets.device
+        m = torch.empty(R, dtype=torch.int32, device=dev) if m is None else m
+        ids = torch.empty((R, max_blocks), dtype=torch.int32, device=dev) if ids is None else ids
+        ptstore_lookup(self.h, tokens, offsets, max_blocks, m, ids, stream)
+        return m, ids
+
+    def gather(self, ids, m, block_table, cache, stream=None):
+        ptstore_gather(self.h, ids, m, block_table, cache, self.cache_blocks(cache), stream)
+
+    def lookup_gather(self, tokens, offsets, max_blocks, block_table, cache, m=None, ids=None,
+                      stream=None):
+        R = offsets.numel() - 1
+        dev = offsets.device
+        m = torch.empty(R, dtype=torch.int32, device=dev) if m is None else m
+        ids = torch.empty((R, max_blocks), dtype=torch.int32, device=dev) if ids is None else ids
+        ptstore_lookup_gather(self.h, tokens, offsets, max_blocks, m, ids, block_table, cache,
+                              self.cache_blocks(cache), stream)
+        return m, ids
+
+    def insert(self, tokens, offsets, max_blocks, stream=None):
+        R = offsets.numel() - 1
+        dev = offsets.device
+        m = torch.empty(R, dtype=torch.int32, device=dev)
+        ids = torch.empty((R, max_blocks), dtype=torch.int32, device=dev)
+        created = torch.empty((R, max_blocks), dtype=torch.uint8, device=dev)
+        ptstore_insert(self.h, tokens, offsets, max_blocks, m, ids, created, stream)
+        return m, ids, created
+
+    def scatter(self, ids, created, block_table, cache, stream=None):
+        ptstore_scatter(self.h, ids, created, block_table, cache, self.cache_blocks(cache), stream)
+
+    def stats(self) -> dict:
+        return ptstore_stats(self.h)
+
+    def reset_counters(self):
+        ptstore_reset_counters(self.h)
+
+    def kernel_times(self, kind: int) -> Tuple[float, int]:
+        return ptstore_kernel_times(self.h, kind)
+
+    def set_copy_shape(self, chunks_per_group: int = 0, threads: int = 0):
+        ptstore_set_copy_shape(self.h, chunks_per_group, threads)
+
+    def buffers(self) -> ptstore_buffers_t:
+        return ptstore_get_buffers(self.h)
+
+    def pool_tensor(self) -> torch.Tensor:
+        """The pool as a uint8 [capacity, block_bytes] device tensor (no copy)."""
+        b = self.buffers()
+        n = b.capacity * self.shape.block_bytes
+        return _wrap_device(b.pool, n, torch.uint8).view(b.capacity, self.shape.block_bytes)
+
+    def meta_tensors(self) -> Tuple[torch.Tensor, torch.Tensor]:
+        """(parent [capacity] int32, tokens [capacity, block_tokens] int32), device, no copy."""
+        b = self.buffers()
+        par = _wrap_device(b.parent, b.capacity, torch.int32)
+        tok = _wrap_device(b.tokens, b.capacity * self.shape.block_tokens, torch.int32)
+        return par, tok.view(b.capacity, self.shape.block_tokens)
+
+
+class _CudaArray:
+    def __init__(self, ptr: int, n: int, typestr: str):
+        self.__cuda_array_interface__ = {"shape": (n,), "typestr": typestr, "data": (ptr, False),
+                                         "version": 2, "strides": None}
+
+
+def _wrap_device(ptr: int, n: int, dtype) -> torch.Tensor:
+    typestr = {torch.uint8: "|u1", torch.int32: "<i4"}[dtype]
+    return torch.as_tensor(_CudaArray(ptr, n, typestr), device="cuda")

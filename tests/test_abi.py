@@ -1,0 +1,52 @@
+"""The C-ABI library loads and exports every function include/ptstore.h declares (no GPU)."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ptstore.h")
+LIB = os.path.join(ROOT, "paper_2607_22648_amd", "libptstore.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ptstore_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_api():
+    names = declared_functions()
+    for n in ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gather",
+              "ptstore_lookup_gather", "ptstore_insert", "ptstore_scatter", "ptstore_stats"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    assert os.path.exists(LIB), "build the library first (__graft_entry__.build())"
+    lib = C.CDLL(LIB)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_names_match_header():
+    from paper_2607_22648_amd import ptstore as P
+    assert sorted(P.EXPORTS) == declared_functions()
+    for n in P.EXPORTS:
+        assert hasattr(P, n), n
+
+
+def test_strerror_without_gpu():
+    lib = C.CDLL(LIB)
+    lib.ptstore_strerror.restype = C.c_char_p
+    assert lib.ptstore_strerror(0) == b"ok"
+    assert lib.ptstore_strerror(1) == b"invalid argument"
+
+
+def test_config_struct_layout_matches_header():
+    """ctypes mirrors of the C structs have the sizes the header implies."""
+    from paper_2607_22648_amd import ptstore as P
+    assert C.sizeof(P.ptstore_config_t) == 5 * 4 + 4 + 8 + 8 + 8 + 4 + 4  # incl. padding
+    assert C.sizeof(P.ptstore_stats_t) == 11 * 8
+    assert C.sizeof(P.ptstore_buffers_t) == 6 * 8

@@ -1,0 +1,360 @@
+"""GPU library vs the CPU oracle, element by element, through the C ABI.
+
+Sizes here are small enough for the oracle to finish in seconds but span
+several 64-block windows, several copy groups and ragged tails. The bar is
+bit-exact: all outputs are integers, indices and copied bytes.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import OracleStore
+from workloads import synth
+from tests.helpers import load_golden, spell_batch, random_block_batch, block_table_identity
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2607_22648_amd import ptstore as P
+    from tests.twin import Twin, to_dev, host, random_bytes, DEV
+
+
+def _atoms(rng, n, bt, vocab, shared_head=False):
+    while True:
+        a = rng.integers(0, vocab, size=(n, bt), dtype=np.int32)
+        if shared_head:
+            a[:, :-1] = a[0, :-1]
+        if len({r.tobytes() for r in a}) == n:
+            return a
+
+
+# ---------------------------------------------------------------------------
+# golden example and random tries
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", load_golden("incremental_ids.json")["cases"], ids=lambda c: c["name"])
+def test_golden_example(case):
+    g = load_golden("incremental_ids.json")
+    t = Twin(1, 1, 8, g["block_tokens"], case["capacity"])
+    toks, offs = spell_batch(case["insert"], g["blocks"])
+    (m, ids, cr), _ = t.insert(toks, offs, case["insert_max_blocks"])
+    e = case["expect_insert"]
+    assert host(m).tolist() == e["m"] and host(ids).tolist() == e["ids"]
+    assert host(cr).tolist() == e["created"]
+    assert t.gpu.stats()["blocks_stored"] == e["count"]
+    assert (t.gpu.stats()["full_events"] > 0) == e["rc_full"]
+    toks, offs = spell_batch(case["lookup"], g["blocks"])
+    (m, ids), _ = t.lookup(toks, offs, case["lookup_max_blocks"])
+    assert host(m).tolist() == case["expect_lookup"]["m"]
+    assert host(ids).tolist() == case["expect_lookup"]["ids"]
+    t.close()
+
+
+@pytest.mark.parametrize("bt", [16, 2, 5])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_random_tries(seed, bt):
+    rng = np.random.default_rng(100 + seed)
+    atoms = _atoms(rng, 3, bt, 4, shared_head=(seed == 2))
+    maxb = 70  # crosses a 64-block window
+    cap = [10_000, 150, 40][seed]
+    t = Twin(1, 1, 8, bt, cap)
+    for rnd in range(4):
+        toks, offs = random_block_batch(rng, 48, atoms, 80)
+        t.insert(toks, offs, maxb)
+        toks, offs = random_block_batch(rng, 48, atoms, 90)
+        t.lookup(toks, offs, maxb)
+    t.check_meta()
+    t.close()
+
+
+def test_weak_hash_gives_same_results():
+    """Index keys masked to 8 bits: collisions everywhere, same outputs."""
+    rng = np.random.default_rng(5)
+    atoms = _atoms(rng, 4, 16, 6)
+    t = Twin(1, 1, 8, 16, 3000, flags=P.PTSTORE_FLAG_WEAK_HASH | P.PTSTORE_FLAG_COUNTERS)
+    for _ in range(3):
+        toks, offs = random_block_batch(rng, 64, atoms, 40)
+        t.insert(toks, offs, 40)
+        toks, offs = random_block_batch(rng, 64, atoms, 45)
+        t.lookup(toks, offs, 40)
+    st = t.gpu.stats()
+    assert st["token_compares"] > st["probes"] // 4  # collisions really happened
+    t.close()
+
+
+def test_hash_seed_does_not_change_results():
+    rng = np.random.default_rng(6)
+    atoms = _atoms(rng, 3, 16, 5)
+    ins = [random_block_batch(rng, 40, atoms, 30) for _ in range(3)]
+    lk = random_block_batch(rng, 80, atoms, 35)
+    outs = []
+    for seed in (1, 2, 0xDEADBEEF):
+        s = P.PrefixStore(P.StoreShape(1, 1, 8, 16), 5000, hash_seed=seed)
+        for toks, offs in ins:
+            s.insert(to_dev(toks), to_dev(offs), 30)
+        m, ids = s.lookup(to_dev(lk[0]), to_dev(lk[1]), 30)
+        outs.append((host(m), host(ids)))
+        s.close()
+    for m, ids in outs[1:]:
+        np.testing.assert_array_equal(m, outs[0][0])
+        np.testing.assert_array_equal(ids, outs[0][1])
+
+
+def test_insert_is_deterministic_across_copy_shapes():
+    rng = np.random.default_rng(8)
+    atoms = _atoms(rng, 2, 16, 3)
+    toks, offs = random_block_batch(rng, 300, atoms, 20)
+    res = []
+    for shape in ((8, 256), (1, 64), (3, 1024)):
+        s = P.PrefixStore(P.StoreShape(2, 1, 8, 16), 8000, hash_seed=shape[0])
+        s.set_copy_shape(*shape)
+        m, ids, cr = s.insert(to_dev(toks), to_dev(offs), 20)
+        res.append((host(m), host(ids), host(cr)))
+        s.close()
+    for r in res[1:]:
+        for a, b in zip(r, res[0]):
+            np.testing.assert_array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# payload movement
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cpg,threads", [(8, 256), (1, 64), (5, 512), (64, 1024)])
+def test_scatter_then_gather_bytes(cpg, threads):
+    rng = np.random.default_rng(9)
+    L, H, D, bt = 3, 2, 4, 16  # chunk = 2*16*4*2 = 256 B, 6 chunks per block
+    atoms = _atoms(rng, 3, bt, 5)
+    t = Twin(L, H, D, bt, 500)
+    t.gpu.set_copy_shape(cpg, threads)
+    toks, offs = random_block_batch(rng, 40, atoms, 8, tail_p=0.3)
+    R, maxb = len(offs) - 1, 8
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, maxb)
+    t.scatter_random(ids, cr, rids, rcr, block_table_identity(R, maxb), seed=11)
+    t.check_pool()
+    # gather through a permuted block table with holes into a sentinel cache
+    lt, lo = random_block_batch(rng, 30, atoms, 10, tail_p=0.5)
+    R2, maxb2 = len(lo) - 1, 10
+    NB2 = R2 * maxb2 + 13
+    perm = rng.permutation(NB2)[:R2 * maxb2].astype(np.int32).reshape(R2, maxb2)
+    perm[rng.random(perm.shape) < 0.2] = -1
+    t.lookup_gather(lt, lo, maxb2, perm, NB2)
+    assert t.gpu.stats()["bad_entries"] == 0
+    t.close()
+
+
+def test_gather_skips_out_of_range_entries():
+    t = Twin(2, 1, 8, 16, 64)
+    toks, offs = synth.concat_requests([np.arange(48, dtype=np.int32)])
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, 3)
+    t.scatter_random(ids, cr, rids, rcr, np.array([[0, 1, 2]], np.int32), seed=3)
+    bt_tab = np.array([[0, 99, 1]], dtype=np.int32)  # 99 >= cache_blocks
+    t.lookup_gather(toks, offs, 3, bt_tab, 4)
+    assert t.gpu.stats()["bad_entries"] == 1 and t.ref.bad_entries == 1
+    # ids beyond the stored count through the plain gather entry point
+    cache = torch.zeros(2 * 2 * 4 * t.shape.chunk_bytes, dtype=torch.uint8, device=DEV)
+    bad_ids = to_dev(np.array([[0, 7, -3]], np.int32))
+    t.gpu.gather(bad_ids, to_dev(np.array([3], np.int32)), to_dev(np.array([[0, 1, 2]], np.int32)),
+                 cache)
+    assert t.gpu.stats()["bad_entries"] == 3
+    t.close()
+
+
+# ---------------------------------------------------------------------------
+# capacity and edge cases
+# ---------------------------------------------------------------------------
+
+def test_capacity_cut_matches_oracle():
+    rng = np.random.default_rng(12)
+    atoms = _atoms(rng, 3, 16, 4)
+    t = Twin(1, 1, 8, 16, 37)
+    for _ in range(3):
+        toks, offs = random_block_batch(rng, 30, atoms, 12)
+        t.insert(toks, offs, 12)
+    assert t.gpu.stats()["blocks_stored"] == 37 and t.gpu.stats()["full_events"] >= 1
+    toks, offs = random_block_batch(rng, 30, atoms, 12)
+    t.lookup(toks, offs, 12)
+    t.close()
+
+
+def test_tiny_index_limits_capacity():
+    t = Twin(1, 1, 8, 16, 1000, index_slots=16)  # at most 8 blocks
+    assert t.capacity == 8
+    toks, offs = synth.concat_requests([np.arange(16 * 12, dtype=np.int32)])
+    t.insert(toks, offs, 12)
+    assert t.gpu.stats()["blocks_stored"] == 8
+    t.lookup(toks, offs, 12)
+    t.close()
+
+
+def test_edge_cases():
+    t = Twin(1, 1, 8, 16, 100)
+    # empty batch
+    (m, ids), _ = t.lookup(np.zeros(0, np.int32), np.zeros(1, np.int64), 4)
+    assert m.numel() == 0
+    t.insert(np.zeros(0, np.int32), np.zeros(1, np.int64), 4)
+    # empty requests, shorter than one block, ragged tails, exactly one block
+    seqs = [np.zeros(0, np.int32), np.arange(5, dtype=np.int32), np.arange(16, dtype=np.int32),
+            np.arange(37, dtype=np.int32), np.arange(16 * 70 + 3, dtype=np.int32)]
+    toks, offs = synth.concat_requests(seqs)
+    t.insert(toks, offs, 1)     # max_blocks = 1
+    t.insert(toks, offs, 64)    # exactly one window
+    t.insert(toks, offs, 65)    # one block into the second window
+    t.lookup(toks, offs, 200)   # more room than any request needs
+    # full match: every block of the request is stored
+    (m, ids), _ = t.lookup(toks[offs[3]:offs[4]], np.array([0, 37]), 10)
+    assert host(m).tolist() == [2]
+    t.close()
+
+
+def test_invalid_arguments_are_rejected():
+    lib = P.lib()
+    s = P.PrefixStore(P.StoreShape(1, 1, 8, 16), 10)
+    d = torch.zeros(64, dtype=torch.int32, device=DEV)
+    o = torch.zeros(2, dtype=torch.int64, device=DEV)
+    bad = [
+        lib.ptstore_lookup(s.h, d.data_ptr(), o.data_ptr(), 64, 1, 0, d.data_ptr(), d.data_ptr(), None),
+        lib.ptstore_lookup(s.h, d.data_ptr(), o.data_ptr(), 64, -1, 4, d.data_ptr(), d.data_ptr(), None),
+        lib.ptstore_lookup(s.h, d.data_ptr(), None, 64, 1, 4, d.data_ptr(), d.data_ptr(), None),
+        lib.ptstore_lookup(None, d.data_ptr(), o.data_ptr(), 64, 1, 4, d.data_ptr(), d.data_ptr(), None),
+        lib.ptstore_gather(s.h, d.data_ptr(), d.data_ptr(), d.data_ptr(), 1, 4, d.data_ptr() + 4, 1, None),
+        lib.ptstore_insert(s.h, d.data_ptr(), o.data_ptr(), 1 << 33, 1, 4, d.data_ptr(), d.data_ptr(),
+                           d.data_ptr(), None),
+    ]
+    assert all(rc == P.PTSTORE_ERR_INVALID for rc in bad), bad
+    cfg = P.ptstore_config_t(1, 1, 8, 16, 2, 10, 6, 0, 0)  # index_slots not a power of two
+    h = C.c_void_p()
+    assert lib.ptstore_create(C.byref(cfg), C.byref(h)) == P.PTSTORE_ERR_INVALID
+    cfg = P.ptstore_config_t(1, 1, 3, 1, 2, 10, 0, 0, 0)  # chunk of 6 bytes
+    assert lib.ptstore_create(C.byref(cfg), C.byref(h)) == P.PTSTORE_ERR_INVALID
+    s.close()
+
+
+def test_malformed_offsets_are_empty_and_counted():
+    s = P.PrefixStore(P.StoreShape(1, 1, 8, 16), 100)
+    toks = to_dev(np.arange(64, dtype=np.int32))
+    offs = to_dev(np.array([0, 32, 16, 200], np.int64))  # decreasing, then beyond n_tokens
+    m, ids, cr = s.insert(toks, offs, 4)
+    torch.cuda.synchronize()
+    assert host(m).tolist() == [2, 0, 0]
+    assert s.stats()["bad_entries"] == 2
+    s.close()
+
+
+# ---------------------------------------------------------------------------
+# workload-shaped cases, scaled down
+# ---------------------------------------------------------------------------
+
+def _prefill(t: Twin, toks, offs, maxb, seed, batch=64):
+    """Insert + scatter in batches, checking every output."""
+    R = len(offs) - 1
+    for lo in range(0, R, batch):
+        hi = min(R, lo + batch)
+        bt_, bo = toks[offs[lo]:offs[hi]], (offs[lo:hi + 1] - offs[lo]).astype(np.int64)
+        (m, ids, cr), (rc, rm, rids, rcr) = t.insert(bt_, bo, maxb)
+        t.scatter_random(ids, cr, rids, rcr, block_table_identity(hi - lo, maxb), seed=seed + lo)
+
+
+def test_tiny_config_full():
+    w = synth.build("tiny")
+    t = Twin.for_shape(w.shape, 4096)
+    st_, so = w.store_batch()
+    _prefill(t, st_, so, w.passage_blocks, seed=21)
+    t.check_pool()
+    R, maxb = w.n_requests, w.max_blocks
+    (m, ids, _), _ = t.lookup_gather(w.tokens, w.offsets, maxb, block_table_identity(R, maxb), R * maxb)
+    expect = np.where(np.isin(w.req_passage, w.stored), w.passage_blocks, 0)
+    np.testing.assert_array_equal(host(m), expect)
+    t.close()
+
+
+def test_llama8b_shape_small():
+    """32 layers x 8 heads x 128 bf16 (2 MiB blocks), few passages."""
+    w = synth.build("llama8b", n_passages=8, n_requests=8, stored_ranks=[1, 2, 3, 4])
+    t = Twin.for_shape(w.shape, 4 * 224 + 64)
+    st_, so = w.store_batch()
+    _prefill(t, st_, so, w.passage_blocks, seed=31, batch=2)
+    R, maxb = w.n_requests, w.max_blocks
+    t.lookup_gather(w.tokens, w.offsets, maxb, block_table_identity(R, maxb), R * maxb)
+    t.close()
+
+
+def test_llama70b_shape_short_passages():
+    """80 layers (5 MiB blocks, 160 chunks per block) with short passages."""
+    w = synth.build("llama70b_shard", n_passages=4, passage_tokens=1024, suffix_tokens=256,
+                    n_requests=4, stored_ranks=[1, 3])
+    t = Twin.for_shape(w.shape, 256)
+    st_, so = w.store_batch()
+    _prefill(t, st_, so, w.passage_blocks, seed=41, batch=2)
+    R, maxb = w.n_requests, w.max_blocks
+    t.lookup_gather(w.tokens, w.offsets, maxb, block_table_identity(R, maxb), R * maxb)
+    t.close()
+
+
+def test_long_requests_many_windows():
+    """32768-token requests (2048 blocks = 32 windows) with a small KV shape."""
+    kv = synth.KVShape(1, 1, 8, 16, "fp16")
+    w = synth.make_passage_workload("long", kv, 6, 30720, 2048, 8, 1.2, [1, 3, 5], 4, seed=5)
+    t = Twin.for_shape(kv, 3 * 1920 + 16)
+    st_, so = w.store_batch()
+    _prefill(t, st_, so, w.passage_blocks, seed=51, batch=3)
+    R, maxb = w.n_requests, w.max_blocks
+    (m, _, _), _ = t.lookup_gather(w.tokens, w.offsets, maxb, block_table_identity(R, maxb), R * maxb)
+    expect = np.where(np.isin(w.req_passage, w.stored), 1920, 0)
+    np.testing.assert_array_equal(host(m), expect)
+    # branch inside a window and exactly on window boundaries
+    base = w.passages[0]
+    seqs = []
+    for cut in (63, 64, 65, 127, 128, 1000, 1919):
+        s = base.copy()
+        s[cut * 16 + 3] += 1
+        seqs.append(s)
+    toks, offs = synth.concat_requests(seqs)
+    (m, _), _ = t.lookup(toks, offs, 2048)
+    assert host(m).tolist() == [63, 64, 65, 127, 128, 1000, 1919]
+    t.close()
+
+
+def test_trie_config_small():
+    cap = 20_000
+    w = synth.build("trie", capacity=cap, n_requests=1024, chunk_walks=4096)
+    t = Twin.for_shape(w.shape, cap)
+    R = len(w.store_offsets) - 1
+    for lo in range(0, R, 512):
+        hi = min(R, lo + 512)
+        toks = w.store_tokens[w.store_offsets[lo]:w.store_offsets[hi]]
+        offs = (w.store_offsets[lo:hi + 1] - w.store_offsets[lo]).astype(np.int64)
+        (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, w.depth)
+        t.scatter_random(ids, cr, rids, rcr, block_table_identity(hi - lo, w.depth), seed=lo)
+    assert t.gpu.stats()["blocks_stored"] == cap
+    t.check_pool()
+    Rq = w.n_requests
+    t.lookup_gather(w.tokens, w.offsets, w.depth, block_table_identity(Rq, w.depth), Rq * w.depth)
+    t.close()
+
+
+def test_stream_config_small():
+    kv = synth.KVShape(2, 8, 128, 16, "bf16")
+    sw = synth.build("stream", n_rounds=6, per_round=24, pool_blocks=4000,
+                     base_override=dict(shape=kv, n_passages=24, passage_tokens=512,
+                                        suffix_tokens=128, n_requests=24,
+                                        stored_ranks=list(range(1, 13))))
+    base = sw.base
+    t = Twin.for_shape(kv, sw.pool_blocks)
+    st_, so = base.store_batch()
+    _prefill(t, st_, so, base.passage_blocks, seed=61)
+    maxb = int(np.diff(base.offsets).max()) // 16
+    for i, rd in enumerate(sw.rounds):
+        R = len(rd.lookup_offsets) - 1
+        t.lookup_gather(rd.lookup_tokens, rd.lookup_offsets, maxb, block_table_identity(R, maxb),
+                        R * maxb)
+        Ri = len(rd.insert_offsets) - 1
+        (m, ids, cr), (rc, rm, rids, rcr) = t.insert(rd.insert_tokens, rd.insert_offsets, maxb)
+        t.scatter_random(ids, cr, rids, rcr, block_table_identity(Ri, maxb), seed=1000 + i)
+    t.check_pool()
+    t.check_meta()
+    t.close()
