@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama8b", choices=["llama8b", "tiny"])
-    ap.add_argument("--cpu-sample", type=int, default=32,
+    ap.add_argument("--cpu-sample", type=int, default=256,
                     help="requests of the workload the CPU oracle is timed on (0: skip)")
     ap.add_argument("--copy-shape", default="", help="chunks_per_group,threads of the copy kernels")
     ap.add_argument("--seed", type=int, default=1234)
@@ -56,6 +56,19 @@ def parse():
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def recorded_traffic(config: str):
+    """HBM bytes per gather launch from the committed rocprofv3 counter record,
+    or None if there is none for this workload or the copy kernel changed since."""
+    from paper_2607_22648_amd.profile_summary import copy_source_sha
+    path = os.path.join(ROOT, "profiles", f"gather_{config}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("copy_hip_sha256") != copy_source_sha():
+        return None
+    return rec["traffic_bytes_per_launch"]
 
 
 def prefill(store, w, dev, torch, batch_passages: int):
@@ -96,35 +109,43 @@ def prefill(store, w, dev, torch, batch_passages: int):
             "blocks": int(store.stats()["blocks_stored"])}
 
 
-def cpu_baseline(w, sample: int, seed: int):
-    """Time the CPU oracle (1 thread) on the first `sample` requests."""
+def cpu_baseline(w, sample: int):
+    """Time the CPU oracle (1 thread) on the first `sample` requests, sub-batched as on the GPU."""
     from oracle import OracleStore
-    sh = w.shape
-    toks, offs = w.request_slice(0, sample)
-    # the oracle store holds the stored passages these requests reference
-    need = [p for p in w.stored if p in set(int(x) for x in w.req_passage[:sample])]
-    o = OracleStore.for_shape(sh, capacity=max(1, len(need) * w.passage_blocks))
     from workloads.synth import concat_requests
+    sh = w.shape
+    sample = min(sample, w.n_requests)
+    # the oracle store holds the stored passages these requests reference
+    used = set(int(x) for x in w.req_passage[:sample])
+    need = [p for p in w.stored if int(p) in used]
+    o = OracleStore.for_shape(sh, capacity=max(1, len(need) * w.passage_blocks))
     if need:
         st, so = concat_requests([w.passages[p] for p in need])
         o.insert(st, so, w.passage_blocks)
-        o.pool()[:] = 0x5A  # resident payload (content is irrelevant to the timing)
+        o.pool()[:] = 0x5A  # resident payload (its content does not change the work)
     maxb = w.max_blocks
-    R = sample
-    cache_blocks = R * maxb
+    subs = [(lo, min(hi, sample)) for lo, hi in w.sub_batches() if lo < sample]
+    max_R = max(hi - lo for lo, hi in subs)
+    cache_blocks = max_R * maxb
     cache = np.empty(sh.layers * 2 * cache_blocks * sh.chunk_bytes, dtype=np.uint8)
     cache[:] = 0xA5
-    bt = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
-    t0 = time.perf_counter()
-    m, ids = o.lookup(toks, offs, maxb)
-    o.gather(ids, m, bt, cache, cache_blocks)
-    dt = time.perf_counter() - t0
-    moved = int(m.sum()) * 2 * sh.block_bytes
+    moved = 0
+    dt = 0.0
+    for lo, hi in subs:
+        toks, offs = w.request_slice(lo, hi)
+        R = hi - lo
+        bt = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
+        t0 = time.perf_counter()
+        m, ids = o.lookup(toks, offs, maxb)
+        o.gather(ids, m, bt, cache, cache_blocks)
+        dt += time.perf_counter() - t0
+        moved += int(m.sum()) * 2 * sh.block_bytes
     o.close()
-    return {"value": round(R / dt, 3), "unit": "requests/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {R} of {w.n_requests} requests ({int(m.sum())} matched blocks, "
-                      f"{moved / 1e9:.1f} GB moved); oracle store holds the {len(need)} stored "
-                      f"passages they reference",
+    what = "all" if sample == w.n_requests else f"the first {sample} of"
+    return {"value": round(sample / dt, 3), "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": f"{what} {w.n_requests} requests in sub-batches of {w.sub_batch} "
+                      f"({moved / 1e9:.1f} GB moved); the oracle store holds the {len(need)} "
+                      f"stored passages they reference",
             "seconds": round(dt, 3), "GBps": round(moved / dt / 1e9, 2),
             "host_cpus": os.cpu_count()}
 
@@ -224,7 +245,7 @@ def main():
     cpu = None
     if args.cpu_sample:
         log("timing the CPU oracle ...")
-        cpu = cpu_baseline(w, min(args.cpu_sample, w.n_requests), args.seed)
+        cpu = cpu_baseline(w, args.cpu_sample)
         log(f"cpu baseline: {cpu}")
 
     out = {
@@ -252,7 +273,8 @@ def main():
         "matched_blocks_per_step": matched,
         "roofline": {"bound": "hbm", "kernel": "k_copy<gather>",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": recorded_traffic(args.config),
                      "avg_launch_ms": round(gather_avg_ms, 4), "launches": g_n,
                      "bytes_per_launch": int(gather_bytes_launch)},
         "lookup_kernel_avg_ms": round(l_ms / max(l_n, 1), 4),

@@ -18,6 +18,7 @@ SOURCES = ["api.hip", "lookup.hip", "copy.hip", "insert.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
+    "-I" + os.path.join(os.path.dirname(HERE), "include"),
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
     "-Wall", "-Wno-unused-function",
     # never emit packed fp32 VALU ops

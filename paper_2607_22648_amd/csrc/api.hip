@@ -12,12 +12,11 @@
 
 #include <cstdio>
 #include <cstring>
-#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
 
-#include "../../include/ptstore.h"
+#include "ptstore.h"
 #include "kernels.hpp"
 
 using namespace ptsd;
@@ -133,14 +132,14 @@ struct Timed {
     Timed(ptstore_t* s_, int k, hipStream_t st_) : s(s_), kind(k), st(st_) {
         if (s->cfg.flags & PTSTORE_FLAG_TIMING) {
             a = take_event(s);
-            if (a) hipEventRecord(a, st);
+            if (a) (void)hipEventRecord(a, st);
         }
     }
     ~Timed() {
         if (!a) return;
         hipEvent_t b = take_event(s);
         if (!b) return;
-        hipEventRecord(b, st);
+        (void)hipEventRecord(b, st);
         s->ev[kind].push_back({a, b});
     }
 };
@@ -228,8 +227,10 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     s->block_bytes = chunk * 2 * c.num_layers;
     s->slots_n = slots_n;
     s->capacity = c.pool_blocks < (int64_t)(slots_n / 2) ? c.pool_blocks : (int64_t)(slots_n / 2);
-    s->chunks_per_group = 8;
-    s->threads = 256;
+    // one 32 KiB-class chunk per 1024-thread workgroup: the shape whose
+    // bandwidth held up best whatever the physical placement of pool and cache
+    s->chunks_per_group = 1;
+    s->threads = 1024;
     hipError_t e = hipGetDevice(&s->device);
     if (e != hipSuccess) {
         delete s;
@@ -244,7 +245,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         (e = hipMalloc(&s->ht, sizeof(HashTables))) != hipSuccess ||
         (e = hipMalloc(&s->state, sizeof(DevState))) != hipSuccess) {
         ptstore_destroy(s);
-        hipGetLastError();
+        (void)hipGetLastError();
         return fail(PTSTORE_ERR_NOMEM, "ptstore_create: hipMalloc", e);
     }
     HashTables h;
@@ -264,21 +265,21 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
 
 int ptstore_destroy(ptstore_t* s) {
     if (!s) return PTSTORE_OK;
-    hipSetDevice(s->device);
-    hipDeviceSynchronize();
+    (void)hipSetDevice(s->device);
+    (void)hipDeviceSynchronize();
     for (auto& v : s->ev)
         for (auto& p : v) {
-            hipEventDestroy(p.first);
-            hipEventDestroy(p.second);
+            (void)hipEventDestroy(p.first);
+            (void)hipEventDestroy(p.second);
         }
-    for (auto e : s->free_ev) hipEventDestroy(e);
-    hipFree(s->pool);
-    hipFree(s->parent);
-    hipFree(s->tokens);
-    hipFree(s->slots);
-    hipFree(s->ht);
-    hipFree(s->state);
-    hipFree(s->scratch);
+    for (auto e : s->free_ev) (void)hipEventDestroy(e);
+    (void)hipFree(s->pool);
+    (void)hipFree(s->parent);
+    (void)hipFree(s->tokens);
+    (void)hipFree(s->slots);
+    (void)hipFree(s->ht);
+    (void)hipFree(s->state);
+    (void)hipFree(s->scratch);
     delete s;
     return PTSTORE_OK;
 }
@@ -350,12 +351,12 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
         // earlier work on this stream may still use the old scratch
         if ((e = hipStreamSynchronize(st)) != hipSuccess)
             return fail(PTSTORE_ERR_HIP, "ptstore_insert: stream sync", e);
-        hipFree(s->scratch);
+        (void)hipFree(s->scratch);
         s->scratch = nullptr;
         s->scratch_bytes = 0;
         size_t grow = need + need / 4;
         if ((e = hipMalloc(&s->scratch, grow)) != hipSuccess) {
-            hipGetLastError();
+            (void)hipGetLastError();
             return fail(PTSTORE_ERR_NOMEM, "ptstore_insert: scratch hipMalloc", e);
         }
         s->scratch_bytes = grow;

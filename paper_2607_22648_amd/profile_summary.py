@@ -1,0 +1,148 @@
+"""Summarise rocprofv3 output of bench.py into short text notes under profiles/.
+
+Inputs (directories written by rocprofv3 ``--output-format csv``):
+  --trace DIR   a ``--kernel-trace --stats`` run (uses *_kernel_stats.csv)
+  --fetch DIR   a ``--pmc FETCH_SIZE`` run (uses *_counter_collection.csv)
+  --write DIR   a ``--pmc WRITE_SIZE`` run
+  --bench FILE  the JSON line bench.py printed in the counter runs
+
+HBM traffic of a kernel = FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+scaled by the factor that maps the same counter onto the known byte count of
+a plain device-to-device copy in the same run (the 8 GiB copy bench.py does
+for its copy ceiling, a ``__amd_rocclr_copyBuffer`` dispatch). The record
+carries the SHA-256 of the copy kernel's source; bench.py reports the traffic
+only while that source is unchanged.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+from collections import defaultdict
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+COPY_SRC = os.path.join(HERE, "csrc", "copy.hip")
+GATHER = "k_copy<true>"
+SCATTER = "k_copy<false>"
+PLAIN_COPY = "__amd_rocclr_copyBuffer"
+PLAIN_COPY_BYTES = 8 << 30  # bench.py's copy-ceiling tensor
+
+
+def copy_source_sha() -> str:
+    return hashlib.sha256(open(COPY_SRC, "rb").read()).hexdigest()
+
+
+def _one(pattern: str) -> str:
+    hits = glob.glob(pattern)
+    if not hits:
+        raise FileNotFoundError(pattern)
+    return hits[0]
+
+
+def kernel_stats(trace_dir: str):
+    rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "*kernel_stats.csv")))))
+    return [(r["Name"], int(r["Calls"]), float(r["AverageNs"]) / 1e6, float(r["Percentage"]))
+            for r in rows]
+
+
+def counter_per_dispatch(pmc_dir: str, counter: str):
+    """{kernel short name: [value per dispatch]} for the gather, scatter and plain copy."""
+    out = defaultdict(list)
+    for r in csv.DictReader(open(_one(os.path.join(pmc_dir, "*counter_collection.csv")))):
+        if r["Counter_Name"] != counter:
+            continue
+        name = r["Kernel_Name"]
+        for key in (GATHER, SCATTER, PLAIN_COPY):
+            if key in name:
+                out[key].append(float(r["Counter_Value"]))
+    return out
+
+
+def plain_copy_value(vals):
+    """The 8 GiB copy dispatches (the largest plain-copy dispatches of the run)."""
+    top = max(vals)
+    return [v for v in vals if v > 0.9 * top]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--bench", required=True, help="bench.py JSON line of a counter run")
+    ap.add_argument("--trace-bench", default=None, help="bench.py JSON line of the trace run")
+    ap.add_argument("--out", default=os.path.join(os.path.dirname(HERE), "profiles"))
+    ap.add_argument("--name", default="gather_llama8b")
+    ap.add_argument("--cmd", required=True, help="the command that produced the inputs")
+    a = ap.parse_args()
+
+    bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
+    algo = bench["roofline"]["bytes_per_launch"]
+    fetch = counter_per_dispatch(a.fetch, "FETCH_SIZE")
+    write = counter_per_dispatch(a.write, "WRITE_SIZE")
+    pf = plain_copy_value(fetch[PLAIN_COPY])
+    pw = plain_copy_value(write[PLAIN_COPY])
+    known_kib = PLAIN_COPY_BYTES / 1024
+    f_factor = known_kib / (sum(pf) / len(pf))
+    w_factor = known_kib / (sum(pw) / len(pw))
+    g_fetch = sum(fetch[GATHER]) / len(fetch[GATHER])
+    g_write = sum(write[GATHER]) / len(write[GATHER])
+    traffic = (g_fetch * f_factor + g_write * w_factor) * 1024
+    stats = kernel_stats(a.trace)
+
+    os.makedirs(a.out, exist_ok=True)
+    rec = {
+        "kernel": GATHER,
+        "workload": bench["config"]["workload"],
+        "copy_hip_sha256": copy_source_sha(),
+        "fetch_kib_per_dispatch": round(g_fetch, 1),
+        "write_kib_per_dispatch": round(g_write, 1),
+        "fetch_factor": round(f_factor, 4),
+        "write_factor": round(w_factor, 4),
+        "traffic_bytes_per_launch": int(traffic),
+        "algorithmic_bytes_per_launch": int(algo),
+        "traffic_over_algorithmic": round(traffic / algo, 4),
+        "dispatches": len(fetch[GATHER]),
+    }
+    with open(os.path.join(a.out, f"{a.name}_traffic.json"), "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+
+    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the GPU box):", "",
+             "```", a.cmd.strip(), "```", "",
+             "| kernel | calls | avg ms | % of GPU time |", "|---|---|---|---|"]
+    for name, calls, avg, pct in stats[:12]:
+        short = name if len(name) < 70 else name[:67] + "..."
+        lines.append(f"| `{short}` | {calls} | {avg:.4f} | {pct:.2f} |")
+    g = [s for s in stats if GATHER in s[0]]
+    if g:
+        lines += ["", f"Gather kernel average over {g[0][1]} dispatches: **{g[0][2]:.4f} ms**."]
+    if a.trace_bench:
+        tb = json.loads(open(a.trace_bench).read().strip().splitlines()[-1])["roofline"]
+        lines += [f"bench.py's own HIP-event average in the same run: **{tb['avg_launch_ms']:.4f} ms** "
+                  f"over {tb['launches']} timed launches ({tb['achieved']:.1f} GB/s, "
+                  f"{100 * tb['frac']:.1f}% of 8 TB/s)."]
+    with open(os.path.join(a.out, f"{a.name}_kernel_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    lines = [f"# HBM traffic: {a.name}", "", "Commands (repository root, GPU box):", "", "```",
+             a.cmd.strip(), "```", "",
+             "| quantity | value |", "|---|---|",
+             f"| gather FETCH_SIZE per dispatch | {g_fetch:,.0f} KiB ({len(fetch[GATHER])} dispatches) |",
+             f"| gather WRITE_SIZE per dispatch | {g_write:,.0f} KiB |",
+             f"| plain 8 GiB copy FETCH_SIZE | {sum(pf) / len(pf):,.0f} KiB -> factor {f_factor:.4f} |",
+             f"| plain 8 GiB copy WRITE_SIZE | {sum(pw) / len(pw):,.0f} KiB -> factor {w_factor:.4f} |",
+             f"| traffic per gather launch (scaled) | {traffic / 1e9:.3f} GB |",
+             f"| algorithmic bytes per launch | {algo / 1e9:.3f} GB |",
+             f"| traffic / algorithmic | {traffic / algo:.4f} |",
+             "", f"Copy kernel source SHA-256: `{rec['copy_hip_sha256']}`."]
+    with open(os.path.join(a.out, f"{a.name}_hbm_counters.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()
