@@ -307,8 +307,6 @@ int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int
         (R > 0 && (!ids || !m || !block_table || !cache)) ||
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather: bad argument");
-    if ((int64_t)R * max_blocks * 2 * s->cfg.num_layers > 0x7FFFFFFFll * s->chunks_per_group)
-        return fail(PTSTORE_ERR_INVALID, "ptstore_gather: batch too large for one launch");
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
     if (rc) return rc;
@@ -379,8 +377,6 @@ int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
         (R > 0 && (!ids || !created || !block_table || !cache)) ||
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
         return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: bad argument");
-    if ((int64_t)R * max_blocks * 2 * s->cfg.num_layers > 0x7FFFFFFFll * s->chunks_per_group)
-        return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: batch too large for one launch");
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
     if (rc) return rc;

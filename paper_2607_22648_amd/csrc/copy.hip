@@ -56,12 +56,13 @@ struct CopyArgs {
     int32_t chunks_per_block;
     int32_t chunks_per_group;
     int32_t groups;            // ceil(chunks_per_block / chunks_per_group)
+    int64_t units;             // R * max_blocks * groups
     DevState* state;
 };
 
+// One unit: group g of the chunks of block b of request r.
 template <bool GATHER>
-__global__ __launch_bounds__(1024) void k_copy(CopyArgs a) {
-    const int64_t unit = blockIdx.x;
+__device__ inline void copy_unit(const CopyArgs& a, int64_t unit) {
     const int64_t rb = unit / a.groups;
     const int g = (int)(unit - rb * a.groups);
     const int64_t r = rb / a.max_blocks;
@@ -91,6 +92,13 @@ __global__ __launch_bounds__(1024) void k_copy(CopyArgs a) {
     }
 }
 
+// Units are visited grid-stride: the grid is capped so that it never exceeds
+// the launch limit on total work-items, and is usually one unit per group.
+template <bool GATHER>
+__global__ __launch_bounds__(1024) void k_copy(CopyArgs a) {
+    for (int64_t unit = blockIdx.x; unit < a.units; unit += gridDim.x) copy_unit<GATHER>(a, unit);
+}
+
 CopyArgs make_args(const CopyPlan& p, int32_t max_blocks, int64_t cache_blocks) {
     CopyArgs a{};
     a.pool = p.pool;
@@ -105,14 +113,15 @@ CopyArgs make_args(const CopyPlan& p, int32_t max_blocks, int64_t cache_blocks) 
     return a;
 }
 
-hipError_t launch(const CopyArgs& a, bool gather, int32_t R, int threads, hipStream_t s) {
-    const int64_t units = (int64_t)R * a.max_blocks * a.groups;
-    if (units == 0) return hipSuccess;
-    if (units > 0x7FFFFFFFll) return hipErrorInvalidValue;
+hipError_t launch(CopyArgs a, bool gather, int32_t R, int threads, hipStream_t s) {
+    a.units = (int64_t)R * a.max_blocks * a.groups;
+    if (a.units == 0) return hipSuccess;
+    const int64_t max_groups = (1ll << 31) / threads;
+    const unsigned grid = (unsigned)(a.units < max_groups ? a.units : max_groups);
     if (gather)
-        hipLaunchKernelGGL(k_copy<true>, dim3((unsigned)units), dim3(threads), 0, s, a);
+        hipLaunchKernelGGL(k_copy<true>, dim3(grid), dim3(threads), 0, s, a);
     else
-        hipLaunchKernelGGL(k_copy<false>, dim3((unsigned)units), dim3(threads), 0, s, a);
+        hipLaunchKernelGGL(k_copy<false>, dim3(grid), dim3(threads), 0, s, a);
     return hipGetLastError();
 }
 

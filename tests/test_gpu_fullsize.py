@@ -1,0 +1,251 @@
+"""Parity at the workloads' full sizes, in the launch configuration bench.py times.
+
+At these sizes the oracle runs without payload (its trie alone), so:
+- m, ids and created are compared with the oracle for every request, exactly;
+- every gathered block is compared with pool[id] on the device (a property
+  that holds at any size), and every cache block the gather must not touch
+  still holds the sentinel;
+- pool blocks whose input bytes were recorded when they were scattered are
+  compared byte for byte through the gather (sampled outputs).
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import OracleStore
+from workloads import synth
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+if torch.cuda.is_available():
+    from paper_2607_22648_amd import ptstore as P
+    from tests.twin import to_dev, host, DEV
+
+SENTINEL = 0xA5
+
+
+def _shape(kv):
+    return P.StoreShape(kv.layers, kv.kv_heads, kv.head_dim, kv.block_tokens, kv.elem_bytes)
+
+
+def _free(*objs):
+    for o in objs:
+        if hasattr(o, "close"):
+            o.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+class Recorder:
+    """Input bytes of sampled blocks at the moment they are scattered."""
+
+    def __init__(self, kv, want: int, seed: int):
+        self.kv, self.want = kv, want
+        self.rng = np.random.default_rng(seed)
+        self.bytes = {}
+
+    def take(self, cache: torch.Tensor, nb_cache: int, ids: np.ndarray, created: np.ndarray,
+             bt: np.ndarray, k: int):
+        cand = np.argwhere((created != 0) & (bt >= 0))
+        if len(cand) == 0 or len(self.bytes) >= self.want:
+            return
+        cv = cache.view(self.kv.layers, 2, nb_cache, self.kv.chunk_bytes)
+        for r, b in cand[self.rng.choice(len(cand), size=min(k, len(cand)), replace=False)]:
+            self.bytes[int(ids[r, b])] = host(cv[:, :, int(bt[r, b])])
+
+
+def insert_scatter(store, ref, kv, toks, offs, maxb, seed, rec: Recorder = None, k=4,
+                   compact=False):
+    """Insert on both sides (outputs compared), scatter seeded random KV on the GPU.
+
+    With compact=True only created blocks get a cache slot (block table -1 elsewhere)."""
+    m, ids, cr = store.insert(to_dev(toks), to_dev(offs), maxb)
+    rc, rm, rids, rcr = ref.insert(toks, offs, maxb)
+    ids_h, cr_h = host(ids), host(cr)
+    np.testing.assert_array_equal(host(m), rm)
+    np.testing.assert_array_equal(ids_h, rids)
+    np.testing.assert_array_equal(cr_h, rcr)
+    R = len(offs) - 1
+    if compact:
+        flat = cr_h.reshape(-1).astype(np.int64)
+        bt = np.where(flat != 0, np.cumsum(flat) - 1, -1).astype(np.int32).reshape(R, maxb)
+        nb_cache = max(1, int(flat.sum()))
+    else:
+        bt = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
+        nb_cache = R * maxb
+    cache = torch.empty(kv.layers * 2 * nb_cache * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    cache.random_(0, 256, generator=g)
+    store.scatter(ids, cr, to_dev(bt), cache)
+    if rec is not None:
+        rec.take(cache, nb_cache, ids_h, cr_h, bt, k)
+    torch.cuda.synchronize()
+    del cache
+    return ids_h, cr_h
+
+
+def check_gather(store, kv, cache, m_h, ids_h, bt_h, rec: Recorder = None, chunk=128):
+    """Every gathered block == pool[id]; untouched blocks keep the sentinel; recorded bytes."""
+    cap = store.stats()["capacity"]
+    nb_cache = cache.numel() // (kv.layers * 2 * kv.chunk_bytes)
+    cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
+    pv = store.pool_tensor().view(cap, kv.layers, 2, kv.chunk_bytes)
+    R, maxb = ids_h.shape
+    hit = (np.arange(maxb)[None, :] < m_h[:, None]) & (bt_h >= 0)
+    sel_ids = to_dev(ids_h[hit].astype(np.int64))
+    sel_bt = to_dev(bt_h[hit].astype(np.int64))
+    for s in range(0, sel_ids.numel(), chunk):
+        a = cv[:, :, sel_bt[s:s + chunk]]
+        b = pv[sel_ids[s:s + chunk]].permute(1, 2, 0, 3)
+        assert torch.equal(a, b), f"gathered blocks {s}..{s + chunk} differ from the pool"
+    untouched = np.ones(nb_cache, dtype=bool)
+    untouched[bt_h[hit]] = False
+    un = to_dev(np.flatnonzero(untouched))
+    for s in range(0, un.numel(), chunk):
+        assert bool((cv[:, :, un[s:s + chunk]] == SENTINEL).all()), "gather wrote outside its blocks"
+    if rec is not None:
+        seen = 0
+        for (r, b) in np.argwhere(hit):
+            i = int(ids_h[r, b])
+            if i in rec.bytes:
+                np.testing.assert_array_equal(host(cv[:, :, int(bt_h[r, b])]), rec.bytes[i])
+                seen += 1
+        return seen
+    return 0
+
+
+def lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec=None):
+    R = len(offs) - 1
+    bt_h = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
+    cache.fill_(SENTINEL)
+    m, ids = store.lookup_gather(to_dev(toks), to_dev(offs), maxb, to_dev(bt_h), cache)
+    rm, rids = ref.lookup(toks, offs, maxb)
+    m_h, ids_h = host(m), host(ids)
+    np.testing.assert_array_equal(m_h, rm)
+    np.testing.assert_array_equal(ids_h, rids)
+    seen = check_gather(store, kv, cache, m_h, ids_h, bt_h, rec)
+    return m_h, seen
+
+
+def _passage_store(w, capacity, batch, rec):
+    kv = w.shape
+    store = P.PrefixStore(_shape(kv), capacity)
+    ref = OracleStore.for_shape(kv, capacity, with_payload=False)
+    st, so = w.store_batch()
+    Rs = len(so) - 1
+    for lo in range(0, Rs, batch):
+        hi = min(Rs, lo + batch)
+        insert_scatter(store, ref, kv, st[so[lo]:so[hi]], (so[lo:hi + 1] - so[lo]).astype(np.int64),
+                       w.passage_blocks, seed=lo, rec=rec, k=8)
+    assert store.stats()["blocks_stored"] == ref.count == len(w.stored) * w.passage_blocks
+    return store, ref
+
+
+def test_llama8b_full():
+    w = synth.build("llama8b")
+    kv = w.shape
+    rec = Recorder(kv, 64, 1)
+    store, ref = _passage_store(w, len(w.stored) * w.passage_blocks, 32, rec)
+    maxb = w.max_blocks
+    cache = torch.empty(kv.layers * 2 * w.sub_batch * maxb * kv.chunk_bytes, dtype=torch.uint8,
+                        device=DEV)
+    seen = 0
+    for lo, hi in w.sub_batches():
+        toks, offs = w.request_slice(lo, hi)
+        m_h, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
+        seen += s
+        expect = np.where(np.isin(w.req_passage[lo:hi], w.stored), w.passage_blocks, 0)
+        np.testing.assert_array_equal(m_h, expect)
+    assert seen > 0
+    del cache
+    _free(store, ref)
+
+
+def test_llama70b_shard_full():
+    w = synth.build("llama70b_shard")
+    kv = w.shape
+    rec = Recorder(kv, 32, 2)
+    store, ref = _passage_store(w, len(w.stored) * w.passage_blocks, 2, rec)
+    maxb = w.max_blocks
+    cache = torch.empty(kv.layers * 2 * w.sub_batch * maxb * kv.chunk_bytes, dtype=torch.uint8,
+                        device=DEV)
+    seen = 0
+    for lo, hi in w.sub_batches():
+        toks, offs = w.request_slice(lo, hi)
+        m_h, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
+        seen += s
+        expect = np.where(np.isin(w.req_passage[lo:hi], w.stored), w.passage_blocks, 0)
+        np.testing.assert_array_equal(m_h, expect)
+    assert seen > 0
+    del cache
+    _free(store, ref)
+
+
+def test_trie_full():
+    w = synth.build("trie")
+    kv = w.shape
+    store = P.PrefixStore(_shape(kv), w.capacity, flags=P.PTSTORE_FLAG_COUNTERS)
+    ref = OracleStore.for_shape(kv, w.capacity, with_payload=False)
+    rec = Recorder(kv, 256, 3)
+    W = len(w.store_offsets) - 1
+    batch = 32768
+    for lo in range(0, W, batch):
+        hi = min(W, lo + batch)
+        toks = w.store_tokens[w.store_offsets[lo]:w.store_offsets[hi]]
+        offs = (w.store_offsets[lo:hi + 1] - w.store_offsets[lo]).astype(np.int64)
+        insert_scatter(store, ref, kv, toks, offs, w.depth, seed=lo, rec=rec, k=16, compact=True)
+    st = store.stats()
+    assert st["blocks_stored"] == ref.count == w.capacity and st["full_events"] >= 1
+    R = w.n_requests
+    cache = torch.empty(kv.layers * 2 * R * w.depth * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
+    m_h, seen = lookup_gather_checked(store, ref, kv, w.tokens, w.offsets, w.depth, cache, rec)
+    assert seen > 0 and m_h.mean() > 60
+    del cache
+    _free(store, ref)
+
+
+def test_stream_full():
+    sw = synth.build("stream")
+    base = sw.base
+    kv = base.shape
+    rec = Recorder(kv, 64, 4)
+    store, ref = _passage_store(base, sw.pool_blocks, 32, rec)
+    maxb = base.max_blocks
+    per = len(sw.rounds[0].lookup_offsets) - 1
+    cache = torch.empty(kv.layers * 2 * per * maxb * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
+    nb_cache = per * maxb
+    g = torch.Generator(device=DEV)
+    seen = 0
+    for i, rd in enumerate(sw.rounds):
+        _, s = lookup_gather_checked(store, ref, kv, rd.lookup_tokens, rd.lookup_offsets, maxb,
+                                     cache, rec)
+        seen += s
+        # inserts: KV of the new blocks is fresh in the cache, then scattered
+        Ri = len(rd.insert_offsets) - 1
+        bt_h = np.arange(Ri * maxb, dtype=np.int32).reshape(Ri, maxb)
+        g.manual_seed(10_000 + i)
+        cache.random_(0, 256, generator=g)
+        m, ids, cr = store.insert(to_dev(rd.insert_tokens), to_dev(rd.insert_offsets), maxb)
+        rc, rm, rids, rcr = ref.insert(rd.insert_tokens, rd.insert_offsets, maxb)
+        ids_h, cr_h = host(ids), host(cr)
+        np.testing.assert_array_equal(host(m), rm)
+        np.testing.assert_array_equal(ids_h, rids)
+        np.testing.assert_array_equal(cr_h, rcr)
+        store.scatter(ids, cr, to_dev(bt_h), cache)
+        # every created block now holds its cache block's bytes
+        made = np.argwhere(cr_h != 0)
+        if len(made):
+            cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
+            pv = store.pool_tensor().view(-1, kv.layers, 2, kv.chunk_bytes)
+            sel_ids = to_dev(ids_h[cr_h != 0].astype(np.int64))
+            sel_bt = to_dev(bt_h[cr_h != 0].astype(np.int64))
+            assert torch.equal(cv[:, :, sel_bt], pv[sel_ids].permute(1, 2, 0, 3))
+            rec.take(cache, nb_cache, ids_h, cr_h, bt_h, 1)
+    assert store.stats()["blocks_stored"] == ref.count
+    assert ref.count > len(base.stored) * base.passage_blocks
+    assert seen > 0
+    del cache
+    _free(store, ref)

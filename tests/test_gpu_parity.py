@@ -358,3 +358,18 @@ def test_stream_config_small():
     t.check_pool()
     t.check_meta()
     t.close()
+
+
+def test_copy_grid_beyond_launch_limit():
+    """More (request, block, chunk) units than one launch may hold: the copy
+    kernels walk them grid-stride (20,000 requests x 64 blocks x 2 chunks)."""
+    rng = np.random.default_rng(13)
+    R, maxb = 20_000, 64
+    toks = rng.integers(0, 32000, size=R * maxb * 16, dtype=np.int32)
+    offs = np.arange(R + 1, dtype=np.int64) * (maxb * 16)
+    t = Twin(1, 1, 8, 16, R * maxb)
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, maxb)
+    t.scatter_random(ids, cr, rids, rcr, block_table_identity(R, maxb), seed=17)
+    t.check_pool()
+    t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
+    t.close()

@@ -16,6 +16,7 @@ from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
+import pandas as pd
 
 VOCAB = 32000
 
@@ -196,13 +197,12 @@ class TrieWorkload:
         return self.depth
 
 
-def _trie_walks(root: np.uint64, n: int, depth: int, branch_p: float, fanout: int,
-                block_tokens: int, rng: np.random.Generator):
+def _trie_paths(root: np.uint64, n: int, depth: int, branch_p: float, fanout: int,
+                rng: np.random.Generator) -> np.ndarray:
+    """[n, depth] path hashes of n random walks from the root."""
     h = np.full(n, root, dtype=np.uint64)
     paths = np.empty((n, depth), dtype=np.uint64)
-    toks = np.empty((n, depth, block_tokens), dtype=np.int32)
     thresh = np.uint64(int(branch_p * 2.0 ** 64) & _M64)
-    tj = (np.arange(1, block_tokens + 1, dtype=np.uint64) * np.uint64(0xD1B54A32D192ED03))
     for lvl in range(depth):
         u = _splitmix64(h ^ np.uint64(0xA0761D6478BD642F))
         nchild = np.where(u < thresh, fanout, 1).astype(np.int64)
@@ -210,9 +210,21 @@ def _trie_walks(root: np.uint64, n: int, depth: int, branch_p: float, fanout: in
         with np.errstate(over="ignore"):
             h = _splitmix64(h * np.uint64(0x100000001B3) + pick.astype(np.uint64) + np.uint64(1))
         paths[:, lvl] = h
-        t = _splitmix64(h[:, None] ^ tj[None, :])
-        toks[:, lvl, :] = (t % np.uint64(VOCAB)).astype(np.int32)
-    return paths, toks.reshape(n, depth * block_tokens)
+    return paths
+
+
+def _node_tokens(h: np.ndarray, block_tokens: int) -> np.ndarray:
+    """The block of tokens a tree node carries, a function of its path hash."""
+    tj = np.arange(1, block_tokens + 1, dtype=np.uint64) * np.uint64(0xD1B54A32D192ED03)
+    t = _splitmix64(h.reshape(-1)[:, None] ^ tj[None, :])
+    return (t % np.uint64(VOCAB)).astype(np.int32)
+
+
+def _walk_tokens(paths: np.ndarray, block_tokens: int) -> np.ndarray:
+    """Tokens of walks, [n * depth * block_tokens], computed once per distinct node."""
+    codes, uniq = pd.factorize(paths.reshape(-1))
+    table = _node_tokens(np.asarray(uniq, dtype=np.uint64), block_tokens)
+    return table[codes].reshape(-1)
 
 
 def make_trie_workload(
@@ -228,28 +240,28 @@ def make_trie_workload(
     """Draw store walks until they visit at least ``capacity`` distinct nodes."""
     rng = np.random.default_rng(seed)
     root = np.uint64(int(rng.integers(0, 2**63)))
-    path_chunks, tok_chunks = [], []
-    seen = np.zeros(0, dtype=np.uint64)
-    while seen.size < capacity:
-        p, t = _trie_walks(root, chunk_walks, depth, branch_p, fanout, shape.block_tokens, rng)
-        path_chunks.append(p)
-        tok_chunks.append(t)
-        seen = np.unique(np.concatenate([seen, p.ravel()]))
-    paths = np.concatenate(path_chunks)
-    toks = np.concatenate(tok_chunks)
+    chunks = []
+    seen = pd.Index(np.zeros(0, dtype=np.uint64))
+    distinct = 0
+    while distinct < capacity:
+        p = _trie_paths(root, chunk_walks, depth, branch_p, fanout, rng)
+        chunks.append(p)
+        seen = seen.append(pd.Index(pd.unique(p.reshape(-1)))).unique()
+        distinct = len(seen)
+    paths = np.concatenate(chunks)
     # keep only the walks needed to reach `capacity` distinct nodes in walk order
-    flat = paths.ravel()
-    _, first = np.unique(flat, return_index=True)
-    new_per_walk = np.bincount(first // depth, minlength=paths.shape[0])
-    cum = np.cumsum(new_per_walk)
-    W = int(np.searchsorted(cum, capacity) + 1)
-    paths, toks = paths[:W], toks[:W]
-    store_offsets = np.arange(W + 1, dtype=np.int64) * (depth * shape.block_tokens)
-    rp, rt = _trie_walks(root, n_requests, depth, branch_p, fanout, shape.block_tokens, rng)
-    offsets = np.arange(n_requests + 1, dtype=np.int64) * (depth * shape.block_tokens)
-    return TrieWorkload(shape, depth, branch_p, fanout, capacity,
-                        toks.reshape(-1), store_offsets, paths,
-                        rt.reshape(-1), offsets, rp, seed)
+    first = ~pd.Index(paths.reshape(-1)).duplicated(keep="first")
+    new_per_walk = first.reshape(paths.shape).sum(axis=1)
+    W = int(np.searchsorted(np.cumsum(new_per_walk), capacity) + 1)
+    paths = paths[:W]
+    bt = shape.block_tokens
+    store_tokens = _walk_tokens(paths, bt)
+    store_offsets = np.arange(W + 1, dtype=np.int64) * (depth * bt)
+    rp = _trie_paths(root, n_requests, depth, branch_p, fanout, rng)
+    tokens = _walk_tokens(rp, bt)
+    offsets = np.arange(n_requests + 1, dtype=np.int64) * (depth * bt)
+    return TrieWorkload(shape, depth, branch_p, fanout, capacity, store_tokens, store_offsets,
+                        paths, tokens, offsets, rp, seed)
 
 
 # ---------------------------------------------------------------------------
