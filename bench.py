@@ -46,10 +46,13 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="llama8b", choices=["llama8b", "tiny"])
-    ap.add_argument("--cpu-sample", type=int, default=256,
-                    help="requests of the workload the CPU oracle is timed on (0: skip)")
-    ap.add_argument("--copy-shape", default="", help="chunks_per_group,threads of the copy kernels")
+    ap.add_argument("--config", default="llama8b",
+                    choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream"])
+    ap.add_argument("--cpu-sample", type=int, default=-1,
+                    help="requests the CPU oracle is timed on (0: skip; -1: the whole batch, "
+                         "8 requests for the 70B-shaped shard)")
+    ap.add_argument("--copy-shape", default="",
+                    help="chunks_per_group,threads[,grid] of the copy kernels")
     ap.add_argument("--seed", type=int, default=1234)
     return ap.parse_args()
 
@@ -150,31 +153,67 @@ def cpu_baseline(w, sample: int):
             "host_cpus": os.cpu_count()}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding of "
-                                   "the store is a design, not code (--gpus 1)"}))
-        sys.exit(2)
-    import torch
-    from paper_2607_22648_amd import ptstore as P
-    from workloads import synth
+def d2d_ceiling(torch, dev) -> float:
+    """GB/s of a plain device-to-device copy of 8 GiB through torch (read + write)."""
+    a = torch.empty(8 << 30, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = 2 * a.numel() * 5 / (e0.elapsed_time(e1) * 1e6)
+    del a, b
+    torch.cuda.empty_cache()
+    return round(gbps, 1)
 
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    t0 = time.time()
+
+def base_line(args, value, unit, ms_per_step, config):
+    return {"metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+            "data": "synthetic", "config": config}
+
+
+def roofline(kernel, bytes_per_launch, avg_ms, launches, traffic):
+    achieved = bytes_per_launch / (avg_ms * 1e6)
+    return {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic, "avg_launch_ms": round(avg_ms, 4), "launches": launches,
+            "bytes_per_launch": int(bytes_per_launch)}
+
+
+WORKLOAD_TEXT = {
+    "tiny": "tiny fp16 KV (2 x 8 x 128), 64 req x 1024 tok (768-tok Zipf-1.0 passage of 32 + 256 "
+            "fresh), store = top-16 passages",
+    "llama8b": "llama8b-shaped KV, 256 req x 4096 tok (3584-tok Zipf-1.1 passage of 512 + 512 "
+               "fresh), store = top-256 passages",
+    "llama70b_shard": "llama70b-shaped KV (80 x 8 x 128 bf16), 64 req x 32768 tok (30720-tok "
+                      "Zipf-1.2 passage of 64 + 2048 fresh), one GPU's shard = odd ranks 1..31 "
+                      "(16 passages)",
+    "trie": "divergent trie, 8192 walks of a 64-level tree (4 children at p=0.1), 1M stored "
+            "blocks, 1 x 8 x 128 fp16 KV",
+    "stream": "llama8b-shaped store, rounds of 128 lookups+gathers and 128 dedup inserts + "
+              "scatter, 160 GB pool",
+}
+
+
+def run_passage(args, torch, P, synth, dev):
     w = synth.build(args.config, seed=args.seed)
     log(f"workload {args.config}: {w.n_requests} requests, max_blocks {w.max_blocks}, "
-        f"{len(w.stored)} stored passages, generated in {time.time() - t0:.1f}s")
+        f"{len(w.stored)} stored passages")
     sh = w.shape
     shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
     pool_blocks = len(w.stored) * w.passage_blocks
     store = P.PrefixStore(shape, pool_blocks, flags=P.PTSTORE_FLAG_TIMING)
     if args.copy_shape:
-        cpg, thr = (int(x) for x in args.copy_shape.split(","))
-        store.set_copy_shape(cpg, thr)
+        store.set_copy_shape(*(int(x) for x in args.copy_shape.split(",")))
     t0 = time.time()
-    pre = prefill(store, w, dev, torch, batch_passages=32 if sh.layers > 2 else 64)
+    batch = max(1, (16 << 30) // (w.passage_blocks * sh.block_bytes))
+    pre = prefill(store, w, dev, torch, batch_passages=min(64, batch))
     log(f"prefill: {pre} ({time.time() - t0:.1f}s)")
 
     # requests resident in HBM, one paged cache shared by the sub-batches
@@ -219,71 +258,239 @@ def main():
     l_ms, l_n = store.kernel_times(P.KIND_LOOKUP)
 
     ms_per_step = elapsed * 1e3 / args.steps
-    req_per_s = w.n_requests * args.steps / elapsed
     gather_bytes_step = matched * 2 * sh.block_bytes
     lookup_bytes_step = blocks_examined * LOOKUP_BYTES_PER_BLOCK
     step_GBps = (gather_bytes_step + lookup_bytes_step) / (ms_per_step * 1e6)
-    gather_avg_ms = g_ms / max(g_n, 1)
-    gather_bytes_launch = gather_bytes_step / len(subs)
-    achieved = gather_bytes_launch / (gather_avg_ms * 1e6)
-
-    # copy ceiling: a plain device-to-device copy of 8 GiB through torch
-    a = torch.empty(8 << 30, dtype=torch.uint8, device=dev)
-    b = torch.empty_like(a)
-    b.copy_(a)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(5):
-        b.copy_(a)
-    e1.record()
-    torch.cuda.synchronize()
-    d2d = 2 * a.numel() * 5 / (e0.elapsed_time(e1) * 1e6)
-    del a, b
-
     st = store.stats()
+    del cache
+    store.close()
+    torch.cuda.empty_cache()
+    d2d = d2d_ceiling(torch, dev)
     cpu = None
     if args.cpu_sample:
+        n = args.cpu_sample if args.cpu_sample > 0 else (8 if sh.layers > 32 else w.n_requests)
         log("timing the CPU oracle ...")
-        cpu = cpu_baseline(w, args.cpu_sample)
+        cpu = cpu_baseline(w, n)
         log(f"cpu baseline: {cpu}")
-
-    out = {
-        "metric": METRIC,
-        "value": round(req_per_s, 2),
-        "unit": "requests/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 3),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "u8",
-        "data": "synthetic",
-        "config": {"workload": "llama8b-shaped KV, 256 req x 4096 tok (3584-tok Zipf-1.1 passage "
-                               "of 512 + 512 fresh), store = top-256 passages"
-                   if args.config == "llama8b" else args.config,
-                   "layers": sh.layers, "kv_heads": sh.kv_heads, "head_dim": sh.head_dim,
-                   "block_tokens": sh.block_tokens, "kv_dtype": sh.dtype,
-                   "requests": w.n_requests, "sub_batches": len(subs), "sub_batch": w.sub_batch,
-                   "stored_blocks": st["blocks_stored"], "block_bytes": sh.block_bytes},
+    out = base_line(args, w.n_requests * args.steps / elapsed, "requests/s", ms_per_step, {
+        "workload": WORKLOAD_TEXT[args.config],
+        "layers": sh.layers, "kv_heads": sh.kv_heads, "head_dim": sh.head_dim,
+        "block_tokens": sh.block_tokens, "kv_dtype": sh.dtype,
+        "requests": w.n_requests, "sub_batches": len(subs), "sub_batch": w.sub_batch,
+        "stored_blocks": st["blocks_stored"], "block_bytes": sh.block_bytes})
+    out.update({
         "hbm_GBps": round(step_GBps, 1),
         "hbm_frac": round(step_GBps / HBM_PEAK_GBPS, 4),
         "matched_blocks_per_step": matched,
-        "roofline": {"bound": "hbm", "kernel": "k_copy<gather>",
-                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": recorded_traffic(args.config),
-                     "avg_launch_ms": round(gather_avg_ms, 4), "launches": g_n,
-                     "bytes_per_launch": int(gather_bytes_launch)},
+        "roofline": roofline("k_copy_pairs<true> (gather)", gather_bytes_step / len(subs), g_ms / max(g_n, 1),
+                             g_n, recorded_traffic(args.config)),
         "lookup_kernel_avg_ms": round(l_ms / max(l_n, 1), 4),
-        "d2d_copy_GBps": round(d2d, 1),
+        "d2d_copy_GBps": d2d,
         "prefill": pre,
         "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+    })
+    return out
+
+
+def run_trie(args, torch, P, synth, dev):
+    t0 = time.time()
+    w = synth.build("trie", seed=args.seed)
+    log(f"trie workload: {len(w.store_offsets) - 1} store walks, {w.n_requests} requests "
+        f"({time.time() - t0:.1f}s)")
+    sh = w.shape
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    store = P.PrefixStore(shape, w.capacity, flags=P.PTSTORE_FLAG_TIMING | P.PTSTORE_FLAG_COUNTERS)
+    W = len(w.store_offsets) - 1
+    g = torch.Generator(device=dev)
+    created_total = 0
+    for lo in range(0, W, 32768):
+        hi = min(W, lo + 32768)
+        toks = torch.from_numpy(w.store_tokens[w.store_offsets[lo]:w.store_offsets[hi]]).to(dev)
+        offs = torch.from_numpy((w.store_offsets[lo:hi + 1] - w.store_offsets[lo])
+                                .astype(np.int64)).to(dev)
+        m, ids, cr = store.insert(toks, offs, w.depth)
+        flat = cr.view(-1).to(torch.int64)
+        n_new = int(flat.sum().item())
+        created_total += n_new
+        if n_new == 0:
+            continue
+        bt = torch.where(flat != 0, torch.cumsum(flat, 0) - 1, -1).to(torch.int32).view_as(cr)
+        cache = torch.empty(sh.layers * 2 * n_new * sh.chunk_bytes, dtype=torch.uint8, device=dev)
+        g.manual_seed(lo)
+        cache.random_(0, 256, generator=g)
+        store.scatter(ids, cr, bt, cache)
+        del cache
+    torch.cuda.synchronize()
+    ins_ms, ins_n = store.kernel_times(P.KIND_INSERT)
+    sc_ms, sc_n = store.kernel_times(P.KIND_SCATTER)
+    torch.cuda.empty_cache()
+    R = w.n_requests
+    toks = torch.from_numpy(w.tokens).to(dev)
+    offs = torch.from_numpy(w.offsets).to(dev)
+    m = torch.empty(R, dtype=torch.int32, device=dev)
+    ids = torch.empty((R, w.depth), dtype=torch.int32, device=dev)
+    bt = torch.arange(R * w.depth, dtype=torch.int32, device=dev).view(R, w.depth)
+    cache = torch.full((sh.layers * 2 * R * w.depth * sh.chunk_bytes,), 0xA5, dtype=torch.uint8,
+                       device=dev)
+    # lookup only (the probe-bound headline of this workload)
+    for _ in range(args.warmup):
+        store.lookup(toks, offs, w.depth, m=m, ids=ids)
+    torch.cuda.synchronize()
+    store.kernel_times(P.KIND_LOOKUP)
+    store.reset_counters()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        store.lookup(toks, offs, w.depth, m=m, ids=ids)
+    torch.cuda.synchronize()
+    lk_elapsed = time.perf_counter() - t0
+    lk_ms, lk_n = store.kernel_times(P.KIND_LOOKUP)
+    stt = store.stats()
+    probes = stt["probes"] / args.steps
+    compares = stt["token_compares"] / args.steps
+    matched = int(m.sum().item())
+    # fused lookup + gather
+    for _ in range(args.warmup):
+        store.lookup_gather(toks, offs, w.depth, bt, cache, m=m, ids=ids)
+    torch.cuda.synchronize()
+    store.kernel_times(P.KIND_GATHER)
+    store.kernel_times(P.KIND_LOOKUP)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        store.lookup_gather(toks, offs, w.depth, bt, cache, m=m, ids=ids)
+    torch.cuda.synchronize()
+    fu_elapsed = time.perf_counter() - t0
+    g_ms, g_n = store.kernel_times(P.KIND_GATHER)
     store.close()
+    del cache
+    torch.cuda.empty_cache()
+    cpu = None
+    if args.cpu_sample:
+        from oracle import OracleStore
+        o = OracleStore.for_shape(sh, w.capacity, with_payload=False)
+        o.insert(w.store_tokens, w.store_offsets, w.depth)
+        reps, t_cpu = 0, 0.0
+        while t_cpu < 2.0:
+            t1 = time.perf_counter()
+            o.lookup(w.tokens, w.offsets, w.depth)
+            t_cpu += time.perf_counter() - t1
+            reps += 1
+        o.close()
+        cpu = {"value": round(R * reps / t_cpu, 1), "unit": "lookups/s", "cores": 1,
+               "kind": "oracle", "sample": f"lookup only (pointer trie, no payload) of all {R} "
+                                           f"walks, {reps} repetitions", "seconds": round(t_cpu, 3)}
+    lk_avg = lk_ms / max(lk_n, 1)
+    out = base_line(args, R * args.steps / fu_elapsed, "requests/s", fu_elapsed * 1e3 / args.steps, {
+        "workload": WORKLOAD_TEXT["trie"], "requests": R, "depth": w.depth,
+        "stored_blocks": int(stt["blocks_stored"]), "block_bytes": sh.block_bytes})
+    out.update({
+        "lookup_only": {"lookups_per_s": round(R * args.steps / lk_elapsed, 1),
+                        "kernel_avg_ms": round(lk_avg, 4),
+                        "lookups_per_s_kernel": round(R / (lk_avg / 1e3), 1),
+                        "probes_per_call": int(probes), "token_compares_per_call": int(compares),
+                        "probes_per_s_kernel": round(probes / (lk_avg / 1e3), 1),
+                        "blocks_examined": int(R * w.depth),
+                        "algorithmic_GBps": round(R * w.depth * LOOKUP_BYTES_PER_BLOCK
+                                                  / (lk_avg * 1e6), 1)},
+        "matched_blocks": matched,
+        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
+                             g_n, recorded_traffic("trie")),
+        "prefill": {"insert_ms": round(ins_ms, 3), "insert_calls": ins_n,
+                    "scatter_ms": round(sc_ms, 3), "blocks": created_total},
+        "cpu_baseline": cpu,
+    })
+    return out
+
+
+def run_stream(args, torch, P, synth, dev):
+    sw = synth.build("stream", seed=args.seed)
+    base = sw.base
+    sh = base.shape
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    store = P.PrefixStore(shape, sw.pool_blocks, flags=P.PTSTORE_FLAG_TIMING)
+    pre = prefill(store, base, dev, torch, batch_passages=32)
+    maxb = base.max_blocks
+    per = len(sw.rounds[0].lookup_offsets) - 1
+    cache = torch.full((sh.layers * 2 * per * maxb * sh.chunk_bytes,), 0xA5, dtype=torch.uint8,
+                       device=dev)
+    bt = torch.arange(per * maxb, dtype=torch.int32, device=dev).view(per, maxb)
+    m = torch.empty(per, dtype=torch.int32, device=dev)
+    ids = torch.empty((per, maxb), dtype=torch.int32, device=dev)
+    rounds = [(torch.from_numpy(r.lookup_tokens).to(dev), torch.from_numpy(r.lookup_offsets).to(dev),
+               torch.from_numpy(r.insert_tokens).to(dev), torch.from_numpy(r.insert_offsets).to(dev))
+              for r in sw.rounds]
+    n_timed = min(args.steps, len(rounds) - args.warmup)
+    stats = {"matched": 0, "created": 0}
+
+    def one_round(i, count):
+        lt, lo, it, io = rounds[i]
+        store.lookup_gather(lt, lo, maxb, bt, cache, m=m, ids=ids)
+        im, iids, icr = store.insert(it, io, maxb)
+        store.scatter(iids, icr, bt[:io.numel() - 1], cache)
+        if count:
+            return m, icr
+        return None
+
+    for i in range(args.warmup):
+        one_round(i, False)
+    torch.cuda.synchronize()
+    for k in (P.KIND_GATHER, P.KIND_LOOKUP, P.KIND_INSERT, P.KIND_SCATTER):
+        store.kernel_times(k)
+    blocks0 = store.stats()["blocks_stored"]
+    keep = []
+    t0 = time.perf_counter()
+    for i in range(args.warmup, args.warmup + n_timed):
+        mm, cr = one_round(i, True)
+        keep.append((mm.sum(), cr.to(torch.int64).sum()))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    matched = int(sum(int(a.item()) for a, _ in keep))
+    created = int(sum(int(b.item()) for _, b in keep))
+    t = {k: store.kernel_times(v) for k, v in (("gather", P.KIND_GATHER), ("lookup", P.KIND_LOOKUP),
+                                               ("insert", P.KIND_INSERT), ("scatter", P.KIND_SCATTER))}
+    st = store.stats()
+    store.close()
+    del cache
+    torch.cuda.empty_cache()
+    g_ms, g_n = t["gather"]
+    ms_round = elapsed * 1e3 / n_timed
+    out = base_line(args, per * n_timed / elapsed, "requests/s", ms_round, {
+        "workload": WORKLOAD_TEXT["stream"], "lookups_per_round": per, "inserts_per_round": per,
+        "timed_rounds": n_timed, "pool_blocks": sw.pool_blocks, "block_bytes": sh.block_bytes})
+    out["steps"] = n_timed
+    out.update({
+        "inserts_per_s": round(per * n_timed / elapsed, 2),
+        "matched_blocks": matched, "created_blocks": created,
+        "blocks_stored": {"before": blocks0, "after": st["blocks_stored"]},
+        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
+                             g_ms / max(g_n, 1), g_n, recorded_traffic("stream")),
+        "kernel_ms_per_round": {k: round(v[0] / n_timed, 4) for k, v in t.items()},
+        "scatter_GBps": round(created * 2 * sh.block_bytes / (t["scatter"][0] * 1e6), 1)
+        if t["scatter"][0] else None,
+        "prefill": pre,
+        "cpu_baseline": None,
+    })
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding of "
+                                   "the store is a design, not code (--gpus 1)"}))
+        sys.exit(2)
+    import torch
+    from paper_2607_22648_amd import ptstore as P
+    from workloads import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.config == "trie":
+        out = run_trie(args, torch, P, synth, dev)
+    elif args.config == "stream":
+        out = run_stream(args, torch, P, synth, dev)
+    else:
+        out = run_passage(args, torch, P, synth, dev)
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

@@ -142,6 +142,9 @@ int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * outside [0, blocks_stored) or a cache block >= cache_blocks are skipped
  * and counted in bad_entries. Destinations must be distinct (two entries
  * naming the same cache block race). `cache` must be 16-byte aligned.
+ * The call first builds a dense list of the blocks to copy in store-owned
+ * scratch of 8 bytes per (request, block), grown on demand (growing waits
+ * for `stream`), then copies only those blocks.
  */
 int ptstore_gather(ptstore_t *store, const int32_t *ids, const int32_t *m,
                    const int32_t *block_table, int32_t R, int32_t max_blocks,
@@ -198,15 +201,20 @@ int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
 /*
  * With PTSTORE_FLAG_TIMING: wait for the device, then return the summed
  * durations (ms) and launch counts of the kernels recorded since the last
- * call, for kind 0 = gather copy, 1 = lookup, 2 = scatter copy,
- * 3 = insert (all its kernels). Resets the records.
+ * call, for kind 0 = gather copy kernel, 1 = lookup, 2 = scatter copy
+ * kernel, 3 = insert (all its kernels), 4 = descriptor-list build of gather
+ * and scatter. Resets the records of that kind.
  */
 int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64_t *launches);
 
 /* Launch shape of the copy kernels (gather and scatter); 0 keeps a field's
- * default. chunks_per_group: chunks one workgroup copies; threads: 64..1024,
- * a multiple of 64. For tuning sweeps. */
-int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t threads);
+ * current value. chunks_per_group: (layer, K|V) chunks one unit moves;
+ * threads: workgroup size, 64..1024, a multiple of 64; grid: workgroups of
+ * the copy kernels (by default a gather launches one per possible unit and
+ * a scatter four times what every compute unit holds). For tuning sweeps;
+ * results never depend on it. */
+int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t threads,
+                           int32_t grid);
 
 /* Human-readable text for a return code. */
 const char *ptstore_strerror(int code);

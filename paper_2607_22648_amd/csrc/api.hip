@@ -5,7 +5,9 @@
 //   parent  [capacity] int32, tokens [capacity][block_tokens] int32   block metadata
 //   slots   [index_slots] {key, id}                  open-addressing block index
 //   ht      key-chain constants, state: counters and the block count
-//   scratch insert work space, grown on demand
+//   scratch insert work space; copy_scratch gather/scatter descriptor lists
+//           (both grown on demand, so the hot path allocates only when a
+//           batch is larger than every earlier one)
 // Calls check their arguments, enqueue kernels on the caller's stream and
 // return; nothing on the lookup / gather path allocates or synchronises.
 #include <hip/hip_runtime.h>
@@ -34,9 +36,12 @@ struct ptstore {
     DevState* state;
     void* scratch;
     size_t scratch_bytes;
-    int32_t chunks_per_group, threads;
+    void* copy_scratch;
+    size_t copy_scratch_bytes;
+    int32_t chunks_per_group, threads, grid;
+    int32_t cus;  // compute units of the device
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[4];
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[5];
     std::vector<hipEvent_t> free_ev;
 };
 
@@ -108,6 +113,9 @@ CopyPlan copy_plan(ptstore_t* s) {
     p.chunks_per_block = 2 * s->cfg.num_layers;
     p.chunks_per_group = s->chunks_per_group;
     p.threads = s->threads;
+    p.grid = s->grid;
+    // a looping copy: every compute unit holds its full share, four times over
+    p.loop_grid = s->cus * (2048 / s->threads) * 4;
     p.state = s->state;
     return p;
 }
@@ -157,6 +165,24 @@ bool check_batch(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, in
 int set_device(ptstore_t* s) {
     hipError_t e = hipSetDevice(s->device);
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "hipSetDevice", e);
+}
+
+// Make *buf hold at least `need` bytes. Growing waits for `st` first, since
+// work already enqueued on it may still read the old buffer.
+int ensure_scratch(void** buf, size_t* have, size_t need, hipStream_t st, const char* who) {
+    if (need <= *have) return PTSTORE_OK;
+    hipError_t e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, who, e);
+    (void)hipFree(*buf);
+    *buf = nullptr;
+    *have = 0;
+    const size_t grow = need + need / 4;
+    if ((e = hipMalloc(buf, grow)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(PTSTORE_ERR_NOMEM, who, e);
+    }
+    *have = grow;
+    return PTSTORE_OK;
 }
 
 }  // namespace
@@ -231,10 +257,13 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     // bandwidth held up best whatever the physical placement of pool and cache
     s->chunks_per_group = 1;
     s->threads = 1024;
+    s->grid = 0;
     hipError_t e = hipGetDevice(&s->device);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&s->cus, hipDeviceAttributeMultiprocessorCount, s->device);
     if (e != hipSuccess) {
         delete s;
-        return fail(PTSTORE_ERR_HIP, "hipGetDevice", e);
+        return fail(PTSTORE_ERR_HIP, "ptstore_create: device query", e);
     }
     const size_t pool_bytes = (size_t)(s->capacity > 0 ? s->capacity : 1) * (size_t)s->block_bytes;
     const size_t cap1 = (size_t)(s->capacity > 0 ? s->capacity : 1);
@@ -280,6 +309,7 @@ int ptstore_destroy(ptstore_t* s) {
     (void)hipFree(s->ht);
     (void)hipFree(s->state);
     (void)hipFree(s->scratch);
+    (void)hipFree(s->copy_scratch);
     delete s;
     return PTSTORE_OK;
 }
@@ -311,11 +341,21 @@ int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int
     int rc = set_device(s);
     if (rc) return rc;
     hipStream_t st = (hipStream_t)stream;
+    rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes, copy_scratch_bytes(R, max_blocks),
+                        st, "ptstore_gather: scratch");
+    if (rc) return rc;
+    CopyScratch sc;
+    copy_scratch_carve(s->copy_scratch, R, max_blocks, &sc);
+    const CopyPlan plan = copy_plan(s);
     hipError_t e;
     {
+        Timed t(s, 4, st);
+        e = launch_gather_select(plan, sc, ids, m, block_table, R, max_blocks, cache_blocks, st);
+    }
+    if (e == hipSuccess) {
         Timed t(s, 0, st);
-        e = launch_gather(copy_plan(s), ids, m, block_table, R, max_blocks,
-                          static_cast<uint8_t*>(cache), cache_blocks, st);
+        e = launch_gather_copy(plan, sc, static_cast<uint8_t*>(cache), cache_blocks, R, max_blocks,
+                               st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_gather: launch", e);
 }
@@ -345,20 +385,8 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     uint64_t tn;
     const size_t need = insert_scratch_bytes(R, max_blocks, &tn);
     hipError_t e;
-    if (need > s->scratch_bytes) {
-        // earlier work on this stream may still use the old scratch
-        if ((e = hipStreamSynchronize(st)) != hipSuccess)
-            return fail(PTSTORE_ERR_HIP, "ptstore_insert: stream sync", e);
-        (void)hipFree(s->scratch);
-        s->scratch = nullptr;
-        s->scratch_bytes = 0;
-        size_t grow = need + need / 4;
-        if ((e = hipMalloc(&s->scratch, grow)) != hipSuccess) {
-            (void)hipGetLastError();
-            return fail(PTSTORE_ERR_NOMEM, "ptstore_insert: scratch hipMalloc", e);
-        }
-        s->scratch_bytes = grow;
-    }
+    int rc2 = ensure_scratch(&s->scratch, &s->scratch_bytes, need, st, "ptstore_insert: scratch");
+    if (rc2) return rc2;
     InsertScratch sc;
     insert_scratch_carve(s->scratch, R, max_blocks, &sc);
     InsertTarget tgt{s->slots, s->parent, s->tokens, s->capacity};
@@ -381,11 +409,21 @@ int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
     int rc = set_device(s);
     if (rc) return rc;
     hipStream_t st = (hipStream_t)stream;
+    rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes, copy_scratch_bytes(R, max_blocks),
+                        st, "ptstore_scatter: scratch");
+    if (rc) return rc;
+    CopyScratch sc;
+    copy_scratch_carve(s->copy_scratch, R, max_blocks, &sc);
+    const CopyPlan plan = copy_plan(s);
     hipError_t e;
     {
+        Timed t(s, 4, st);
+        e = launch_scatter_select(plan, sc, ids, created, block_table, R, max_blocks, cache_blocks, st);
+    }
+    if (e == hipSuccess) {
         Timed t(s, 2, st);
-        e = launch_scatter(copy_plan(s), ids, created, block_table, R, max_blocks,
-                           static_cast<const uint8_t*>(cache), cache_blocks, st);
+        e = launch_scatter_copy(plan, sc, static_cast<const uint8_t*>(cache), cache_blocks, R,
+                                max_blocks, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_scatter: launch", e);
 }
@@ -440,7 +478,7 @@ int ptstore_get_buffers(ptstore_t* s, ptstore_buffers_t* out) {
 }
 
 int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* launches) {
-    if (!s || kind < 0 || kind > 3 || !total_ms || !launches)
+    if (!s || kind < 0 || kind > 4 || !total_ms || !launches)
         return fail(PTSTORE_ERR_INVALID, "ptstore_kernel_times: bad argument");
     int rc = set_device(s);
     if (rc) return rc;
@@ -462,11 +500,13 @@ int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* 
     return PTSTORE_OK;
 }
 
-int ptstore_set_copy_shape(ptstore_t* s, int32_t chunks_per_group, int32_t threads) {
-    if (!s || chunks_per_group < 0 || threads < 0 || (threads && (threads < 64 || threads > 1024 || threads % 64)))
+int ptstore_set_copy_shape(ptstore_t* s, int32_t chunks_per_group, int32_t threads, int32_t grid) {
+    if (!s || chunks_per_group < 0 || threads < 0 || grid < 0 ||
+        (threads && (threads < 64 || threads > 1024 || threads % 64)))
         return fail(PTSTORE_ERR_INVALID, "ptstore_set_copy_shape: bad argument");
     if (chunks_per_group) s->chunks_per_group = chunks_per_group;
     if (threads) s->threads = threads;
+    if (grid) s->grid = grid;
     return PTSTORE_OK;
 }
 

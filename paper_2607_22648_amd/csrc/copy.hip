@@ -7,15 +7,22 @@
 //   pool  [id][layer][K|V][head][slot][dim]        chunk c at id*block + c*chunk
 //   cache [layer][K|V][cache block][head][slot][dim] chunk c at (c*NB + cb)*chunk
 //
-// The work is flattened over (request, block, group of chunks) units so that
-// requests with very different match lengths balance across the GPU; a unit
-// whose block is not copied exits at once. Threads move 16-byte vectors with
-// non-temporal loads and stores (the stream is touched once). The default
-// launch gives each 1024-thread workgroup one chunk (two vectors per thread
-// for a 32 KiB chunk): measured on MI355X it kept ~6.2-6.6 TB/s whatever the
-// physical placement of pool and cache, where fatter workgroups (8 chunks,
-// 256 threads, an 8-deep unrolled stripe per thread) swung between 5.5 and
-// 6.6 TB/s. Pure HBM streaming: no LDS, no MFMA.
+// A call runs in two parts, like the paper's bulk transfer of a list of
+// (offset, size) segments in one request (Section 4.1, RDMA-aware
+// consolidation):
+//   select  count the blocks each request must move (wave per request), scan
+//           the counts, then write a dense descriptor list of (id, cache
+//           block) pairs, compacted with a wave ballot. Entries with an id or
+//           cache block out of range are dropped here and counted.
+//   copy    workgroups walk (descriptor, group of chunks) units; the number
+//           of units is read on the device, so no host round trip separates
+//           the parts. Threads move 16-byte vectors with non-temporal loads
+//           and stores (the stream is touched once).
+// Only blocks that are really copied cost work, however sparse they are in
+// the [request][block] arrays (a few created blocks per insert, half the
+// requests missing the store). The default copy shape gives each
+// 1024-thread workgroup one chunk per unit (two vectors per thread for a
+// 32 KiB chunk). Pure HBM streaming: no LDS, no MFMA.
 #include "kernels.hpp"
 
 namespace ptsd {
@@ -24,6 +31,8 @@ namespace {
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 constexpr int kUnroll = 8;
+constexpr int kSelThreads = 256;
+constexpr int kSelWaves = kSelThreads / kWave;
 
 __device__ inline v4u ld_nt(const v4u* p) { return __builtin_nontemporal_load(p); }
 __device__ inline void st_nt(v4u* p, v4u v) { __builtin_nontemporal_store(v, p); }
@@ -42,111 +51,231 @@ __device__ inline void copy_span(const v4u* __restrict__ src, v4u* __restrict__ 
     for (; i < n16; i += nt) st_nt(dst + i, ld_nt(src + i));
 }
 
+struct SelectArgs {
+    const int32_t* ids;
+    const int32_t* m;          // gather: blocks b < m[r] are moved
+    const uint8_t* created;    // scatter: blocks with created != 0 are moved
+    const int32_t* block_table;
+    int32_t R;
+    int32_t max_blocks;
+    int64_t cache_blocks;
+    DevState* state;
+    CopyScratch sc;
+};
+
+// Should (r, b) be moved? Sets *bad for an entry out of range.
+template <bool GATHER>
+__device__ inline bool selected(const SelectArgs& a, int64_t rb, unsigned long long count,
+                                Pair* out, bool* bad) {
+    *bad = false;
+    if (!GATHER && !a.created[rb]) return false;
+    const int32_t cb = a.block_table[rb];
+    if (cb < 0) return false;
+    const int32_t id = a.ids[rb];
+    if ((int64_t)cb >= a.cache_blocks || id < 0 || (unsigned long long)id >= count) {
+        *bad = true;
+        return false;
+    }
+    out->id = id;
+    out->cb = cb;
+    return true;
+}
+
+template <bool GATHER>
+__device__ inline int32_t row_len(const SelectArgs& a, int64_t r) {
+    if (!GATHER) return a.max_blocks;
+    const int32_t mr = a.m[r];
+    return mr < 0 ? 0 : (mr < a.max_blocks ? mr : a.max_blocks);
+}
+
+__device__ inline unsigned long long lanes_below(int lane) {
+    return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(kSelThreads) void k_select_count(SelectArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
+    if (r >= a.R) return;
+    const int32_t n = row_len<GATHER>(a, r);
+    const unsigned long long count = a.state->count;
+    int32_t cnt = 0, bad = 0;
+    for (int32_t b0 = 0; b0 < n; b0 += kWave) {
+        const int32_t b = b0 + lane;
+        Pair p;
+        bool isbad = false;
+        const bool sel = b < n && selected<GATHER>(a, r * a.max_blocks + b, count, &p, &isbad);
+        cnt += __popcll(ballot64(sel));
+        bad += __popcll(ballot64(isbad));
+    }
+    if (lane == 0) {
+        a.sc.row_cnt[r] = cnt;
+        if (bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
+    }
+}
+
+// One workgroup: exclusive scan of row_cnt into row_base, total into *total.
+__global__ __launch_bounds__(1024) void k_select_scan(SelectArgs a) {
+    __shared__ long long part[1024];
+    const int R = a.R;
+    const int t = threadIdx.x, nt = blockDim.x;
+    const int per = (R + nt - 1) / nt;
+    const int lo = min(R, t * per), hi = min(R, lo + per);
+    long long s = 0;
+    for (int i = lo; i < hi; ++i) s += a.sc.row_cnt[i];
+    part[t] = s;
+    __syncthreads();
+    for (int d = 1; d < nt; d <<= 1) {
+        long long v = t >= d ? part[t - d] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    long long run = part[t] - s;
+    for (int i = lo; i < hi; ++i) {
+        a.sc.row_base[i] = run;
+        run += a.sc.row_cnt[i];
+    }
+    if (t == nt - 1) *a.sc.total = (unsigned long long)part[nt - 1];
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
+    if (r >= a.R) return;
+    const int32_t n = row_len<GATHER>(a, r);
+    const unsigned long long count = a.state->count;
+    int64_t pos = a.sc.row_base[r];
+    for (int32_t b0 = 0; b0 < n; b0 += kWave) {
+        const int32_t b = b0 + lane;
+        Pair p;
+        bool isbad = false;
+        const bool sel = b < n && selected<GATHER>(a, r * a.max_blocks + b, count, &p, &isbad);
+        const unsigned long long mask = ballot64(sel);
+        if (sel) a.sc.pairs[pos + __popcll(mask & lanes_below(lane))] = p;
+        pos += __popcll(mask);
+    }
+}
+
 struct CopyArgs {
     uint8_t* pool;
     uint8_t* cache;
-    const int32_t* ids;
-    const int32_t* m;          // gather: blocks b < m[r] are copied
-    const uint8_t* created;    // scatter: blocks with created != 0 are copied
-    const int32_t* block_table;
+    const Pair* pairs;
+    const unsigned long long* total;
     int64_t block_bytes;
     int64_t chunk_bytes;
     int64_t cache_blocks;
-    int32_t max_blocks;
     int32_t chunks_per_block;
     int32_t chunks_per_group;
     int32_t groups;            // ceil(chunks_per_block / chunks_per_group)
-    int64_t units;             // R * max_blocks * groups
-    DevState* state;
 };
 
-// One unit: group g of the chunks of block b of request r.
+// The (descriptor, chunk group) units are visited grid-stride. The host
+// picks the grid: a gather launches one workgroup per possible unit, so the
+// dense front of the list runs in hardware dispatch order (neighbouring
+// workgroups copy neighbouring chunks, the few workgroups past the end exit
+// at once); a scatter, whose created blocks are sparse, launches a few
+// workgroups per compute unit that loop.
 template <bool GATHER>
-__device__ inline void copy_unit(const CopyArgs& a, int64_t unit) {
-    const int64_t rb = unit / a.groups;
-    const int g = (int)(unit - rb * a.groups);
-    const int64_t r = rb / a.max_blocks;
-    const int b = (int)(rb - r * a.max_blocks);
-    if (GATHER) {
-        if (b >= a.m[r]) return;
-    } else {
-        if (!a.created[rb]) return;
-    }
-    const int64_t id = a.ids[rb];
-    const int64_t cb = a.block_table[rb];
-    if (cb < 0) return;
-    if (cb >= a.cache_blocks || id < 0 || id >= (int64_t)a.state->count) {
-        if (threadIdx.x == 0 && g == 0) atomicAdd(&a.state->bad_entries, 1ull);
-        return;
-    }
-    const int c0 = g * a.chunks_per_group;
-    const int c1 = min(c0 + a.chunks_per_group, a.chunks_per_block);
+__global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
+    const unsigned long long units = *a.total * (unsigned long long)a.groups;
     const int n16 = (int)(a.chunk_bytes >> 4);
-    for (int c = c0; c < c1; ++c) {
-        uint8_t* p = a.pool + id * a.block_bytes + (int64_t)c * a.chunk_bytes;
-        uint8_t* q = a.cache + ((int64_t)c * a.cache_blocks + cb) * a.chunk_bytes;
-        if (GATHER)
-            copy_span(reinterpret_cast<const v4u*>(p), reinterpret_cast<v4u*>(q), n16);
-        else
-            copy_span(reinterpret_cast<const v4u*>(q), reinterpret_cast<v4u*>(p), n16);
+    for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
+        const unsigned long long d = unit / (unsigned)a.groups;
+        const int g = (int)(unit - d * (unsigned)a.groups);
+        const Pair p = a.pairs[d];
+        const int c0 = g * a.chunks_per_group;
+        const int c1 = min(c0 + a.chunks_per_group, a.chunks_per_block);
+        for (int c = c0; c < c1; ++c) {
+            uint8_t* src = a.pool + (int64_t)p.id * a.block_bytes + (int64_t)c * a.chunk_bytes;
+            uint8_t* dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
+            if (GATHER)
+                copy_span(reinterpret_cast<const v4u*>(src), reinterpret_cast<v4u*>(dst), n16);
+            else
+                copy_span(reinterpret_cast<const v4u*>(dst), reinterpret_cast<v4u*>(src), n16);
+        }
     }
 }
 
-// Units are visited grid-stride: the grid is capped so that it never exceeds
-// the launch limit on total work-items, and is usually one unit per group.
 template <bool GATHER>
-__global__ __launch_bounds__(1024) void k_copy(CopyArgs a) {
-    for (int64_t unit = blockIdx.x; unit < a.units; unit += gridDim.x) copy_unit<GATHER>(a, unit);
+hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, const int32_t* m,
+                  const uint8_t* created, const int32_t* bt, int32_t R, int32_t max_blocks,
+                  int64_t cache_blocks, hipStream_t s) {
+    SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc};
+    const unsigned grid = (unsigned)((R + kSelWaves - 1) / kSelWaves);
+    hipLaunchKernelGGL(k_select_count<GATHER>, dim3(grid), dim3(kSelThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_select_scan, dim3(1), dim3(1024), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_select_fill<GATHER>, dim3(grid), dim3(kSelThreads), 0, s, a);
+    return hipGetLastError();
 }
 
-CopyArgs make_args(const CopyPlan& p, int32_t max_blocks, int64_t cache_blocks) {
+template <bool GATHER>
+hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_t cache_blocks,
+                int32_t R, int32_t max_blocks, hipStream_t s) {
     CopyArgs a{};
     a.pool = p.pool;
+    a.cache = cache;
+    a.pairs = sc.pairs;
+    a.total = sc.total;
     a.block_bytes = p.block_bytes;
     a.chunk_bytes = p.chunk_bytes;
     a.cache_blocks = cache_blocks;
-    a.max_blocks = max_blocks;
     a.chunks_per_block = p.chunks_per_block;
     a.chunks_per_group = p.chunks_per_group;
     a.groups = (p.chunks_per_block + p.chunks_per_group - 1) / p.chunks_per_group;
-    a.state = p.state;
-    return a;
-}
-
-hipError_t launch(CopyArgs a, bool gather, int32_t R, int threads, hipStream_t s) {
-    a.units = (int64_t)R * a.max_blocks * a.groups;
-    if (a.units == 0) return hipSuccess;
-    const int64_t max_groups = (1ll << 31) / threads;
-    const unsigned grid = (unsigned)(a.units < max_groups ? a.units : max_groups);
-    if (gather)
-        hipLaunchKernelGGL(k_copy<true>, dim3(grid), dim3(threads), 0, s, a);
-    else
-        hipLaunchKernelGGL(k_copy<false>, dim3(grid), dim3(threads), 0, s, a);
+    const int64_t bound = (int64_t)R * max_blocks * a.groups;  // units if every entry moves
+    const int64_t cap = (1ll << 31) / p.threads;                 // launch limit on work-items
+    int64_t grid = p.grid ? p.grid : (GATHER ? bound : (int64_t)p.loop_grid);
+    if (grid > bound) grid = bound;
+    if (grid > cap) grid = cap;
+    if (grid < 1) return hipSuccess;
+    hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_gather(const CopyPlan& p, const int32_t* ids, const int32_t* m,
-                         const int32_t* block_table, int32_t R, int32_t max_blocks,
-                         uint8_t* cache, int64_t cache_blocks, hipStream_t s) {
-    CopyArgs a = make_args(p, max_blocks, cache_blocks);
-    a.cache = cache;
-    a.ids = ids;
-    a.m = m;
-    a.block_table = block_table;
-    return launch(a, true, R, p.threads, s);
+size_t copy_scratch_bytes(int32_t R, int32_t max_blocks) {
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    return up((size_t)R * max_blocks * sizeof(Pair)) + up((size_t)R * 4) + up((size_t)R * 8) + 256;
 }
 
-hipError_t launch_scatter(const CopyPlan& p, const int32_t* ids, const uint8_t* created,
-                          const int32_t* block_table, int32_t R, int32_t max_blocks,
-                          const uint8_t* cache, int64_t cache_blocks, hipStream_t s) {
-    CopyArgs a = make_args(p, max_blocks, cache_blocks);
-    a.cache = const_cast<uint8_t*>(cache);
-    a.ids = ids;
-    a.created = created;
-    a.block_table = block_table;
-    return launch(a, false, R, p.threads, s);
+void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* out) {
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    uint8_t* q = static_cast<uint8_t*>(base);
+    out->pairs = reinterpret_cast<Pair*>(q);
+    q += up((size_t)R * max_blocks * sizeof(Pair));
+    out->row_cnt = reinterpret_cast<int32_t*>(q);
+    q += up((size_t)R * 4);
+    out->row_base = reinterpret_cast<int64_t*>(q);
+    q += up((size_t)R * 8);
+    out->total = reinterpret_cast<unsigned long long*>(q);
+}
+
+hipError_t launch_gather_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,
+                                const int32_t* m, const int32_t* block_table, int32_t R,
+                                int32_t max_blocks, int64_t cache_blocks, hipStream_t s) {
+    return select<true>(p, sc, ids, m, nullptr, block_table, R, max_blocks, cache_blocks, s);
+}
+
+hipError_t launch_scatter_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,
+                                 const uint8_t* created, const int32_t* block_table, int32_t R,
+                                 int32_t max_blocks, int64_t cache_blocks, hipStream_t s) {
+    return select<false>(p, sc, ids, nullptr, created, block_table, R, max_blocks, cache_blocks, s);
+}
+
+hipError_t launch_gather_copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache,
+                              int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s) {
+    return copy<true>(p, sc, cache, cache_blocks, R, max_blocks, s);
+}
+
+hipError_t launch_scatter_copy(const CopyPlan& p, const CopyScratch& sc, const uint8_t* cache,
+                               int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s) {
+    return copy<false>(p, sc, const_cast<uint8_t*>(cache), cache_blocks, R, max_blocks, s);
 }
 
 }  // namespace ptsd

@@ -39,16 +39,39 @@ struct CopyPlan {
     int64_t block_bytes;
     int64_t chunk_bytes;
     int32_t chunks_per_block;  // 2 * layers
-    int32_t chunks_per_group;
-    int32_t threads;
+    int32_t chunks_per_group;  // chunks one copy unit moves
+    int32_t threads;           // workgroup size of the copy kernel
+    int32_t grid;              // workgroups of the copy kernel, 0 = chosen per call
+    int32_t loop_grid;         // workgroups of a looping (sparse) copy
     DevState* state;
 };
-hipError_t launch_gather(const CopyPlan& p, const int32_t* ids, const int32_t* m,
-                         const int32_t* block_table, int32_t R, int32_t max_blocks,
-                         uint8_t* cache, int64_t cache_blocks, hipStream_t s);
-hipError_t launch_scatter(const CopyPlan& p, const int32_t* ids, const uint8_t* created,
-                          const int32_t* block_table, int32_t R, int32_t max_blocks,
-                          const uint8_t* cache, int64_t cache_blocks, hipStream_t s);
+
+// One block to move: pool block id <-> cache block cb.
+struct Pair {
+    int32_t id;
+    int32_t cb;
+};
+
+// Descriptor list of one gather / scatter call.
+struct CopyScratch {
+    Pair* pairs;               // [R * max_blocks] (dense prefix of *total entries)
+    int32_t* row_cnt;          // [R]
+    int64_t* row_base;         // [R]
+    unsigned long long* total; // number of pairs
+};
+size_t copy_scratch_bytes(int32_t R, int32_t max_blocks);
+void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* out);
+
+hipError_t launch_gather_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,
+                                const int32_t* m, const int32_t* block_table, int32_t R,
+                                int32_t max_blocks, int64_t cache_blocks, hipStream_t s);
+hipError_t launch_scatter_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,
+                                 const uint8_t* created, const int32_t* block_table, int32_t R,
+                                 int32_t max_blocks, int64_t cache_blocks, hipStream_t s);
+hipError_t launch_gather_copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache,
+                              int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s);
+hipError_t launch_scatter_copy(const CopyPlan& p, const CopyScratch& sc, const uint8_t* cache,
+                               int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s);
 
 // insert.hip
 struct BatchEntry;  // defined in insert.hip

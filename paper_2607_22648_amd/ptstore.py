@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libptstore.so")
 
 PTSTORE_OK, PTSTORE_ERR_INVALID, PTSTORE_ERR_FULL, PTSTORE_ERR_HIP, PTSTORE_ERR_NOMEM = 0, 1, 2, 3, 4
 PTSTORE_FLAG_WEAK_HASH, PTSTORE_FLAG_COUNTERS, PTSTORE_FLAG_TIMING = 1, 2, 4
-KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT = 0, 1, 2, 3
+KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT, KIND_SELECT = 0, 1, 2, 3, 4
 
 
 class ptstore_config_t(C.Structure):
@@ -70,7 +70,7 @@ def _load() -> C.CDLL:
         "ptstore_reset_counters": [p],
         "ptstore_get_buffers": [p, C.POINTER(ptstore_buffers_t)],
         "ptstore_kernel_times": [p, i32, C.POINTER(d), C.POINTER(i64)],
-        "ptstore_set_copy_shape": [p, i32, i32],
+        "ptstore_set_copy_shape": [p, i32, i32, i32],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -199,8 +199,9 @@ def ptstore_kernel_times(h, kind: int) -> Tuple[float, int]:
     return ms.value, n.value
 
 
-def ptstore_set_copy_shape(h, chunks_per_group: int = 0, threads: int = 0) -> None:
-    _check("ptstore_set_copy_shape", _lib.ptstore_set_copy_shape(h, chunks_per_group, threads))
+def ptstore_set_copy_shape(h, chunks_per_group: int = 0, threads: int = 0, grid: int = 0) -> None:
+    _check("ptstore_set_copy_shape", _lib.ptstore_set_copy_shape(h, chunks_per_group, threads,
+                                                                  grid))
 
 
 def ptstore_strerror(code: int) -> str:
@@ -298,8 +299,8 @@ class PrefixStore:
     def kernel_times(self, kind: int) -> Tuple[float, int]:
         return ptstore_kernel_times(self.h, kind)
 
-    def set_copy_shape(self, chunks_per_group: int = 0, threads: int = 0):
-        ptstore_set_copy_shape(self.h, chunks_per_group, threads)
+    def set_copy_shape(self, chunks_per_group: int = 0, threads: int = 0, grid: int = 0):
+        ptstore_set_copy_shape(self.h, chunks_per_group, threads, grid)
 
     def buffers(self) -> ptstore_buffers_t:
         return ptstore_get_buffers(self.h)

@@ -124,13 +124,14 @@ def test_insert_is_deterministic_across_copy_shapes():
 # payload movement
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("cpg,threads", [(8, 256), (1, 64), (5, 512), (64, 1024)])
-def test_scatter_then_gather_bytes(cpg, threads):
+@pytest.mark.parametrize("cpg,threads,grid", [(8, 256, 0), (1, 64, 0), (5, 512, 7), (64, 1024, 0),
+                                             (1, 1024, 1), (2, 128, 3000)])
+def test_scatter_then_gather_bytes(cpg, threads, grid):
     rng = np.random.default_rng(9)
     L, H, D, bt = 3, 2, 4, 16  # chunk = 2*16*4*2 = 256 B, 6 chunks per block
     atoms = _atoms(rng, 3, bt, 5)
     t = Twin(L, H, D, bt, 500)
-    t.gpu.set_copy_shape(cpg, threads)
+    t.gpu.set_copy_shape(cpg, threads, grid)
     toks, offs = random_block_batch(rng, 40, atoms, 8, tail_p=0.3)
     R, maxb = len(offs) - 1, 8
     (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, maxb)
