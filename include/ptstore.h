@@ -106,7 +106,7 @@ typedef struct {
     void *pool;             /* [capacity][block_bytes] */
     const int32_t *parent;  /* [capacity] parent id, -1 for a root child */
     const int32_t *tokens;  /* [capacity][block_tokens] */
-    const void *slots;      /* [index_slots] of {uint64 key, int32 id, int32 pad} */
+    const void *slots;      /* [index_slots] of {uint64 key, int32 id, int32 parent} */
     int64_t capacity;
     int64_t index_slots;
 } ptstore_buffers_t;

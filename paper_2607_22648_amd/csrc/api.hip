@@ -194,7 +194,7 @@ __global__ void k_fill_slots(Slot* slots, int64_t n) {
         Slot z;
         z.key = kEmptyKey;
         z.id = -1;
-        z.pad = 0;
+        z.parent = -1;
         slots[i] = z;
     }
 }
@@ -443,8 +443,13 @@ int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     out->chunk_bytes = s->chunk_bytes;
     out->full_events = (int64_t)st.full_events;
     out->bad_entries = (int64_t)st.bad_entries;
-    out->probes = (int64_t)st.probes;
-    out->token_compares = (int64_t)st.token_compares;
+    unsigned long long probes = 0, compares = 0;
+    for (int i = 0; i < kCounterSlots; ++i) {
+        probes += st.slot[i].probes;
+        compares += st.slot[i].token_compares;
+    }
+    out->probes = (int64_t)probes;
+    out->token_compares = (int64_t)compares;
     out->cas_attempts = (int64_t)st.cas_attempts;
     out->cas_failures = (int64_t)st.cas_failures;
     return PTSTORE_OK;

@@ -19,11 +19,12 @@ constexpr uint64_t kM61 = (1ull << 61) - 1;
 constexpr uint64_t kEmptyKey = ~0ull;  // never a key: keys are < 2^61
 constexpr int kWave = 64;
 
-// One slot of the open-addressing block index.
+// One slot of the open-addressing block index. The parent id rides along
+// so that a probe learns a candidate's parent without another load.
 struct alignas(16) Slot {
-    uint64_t key;  // index key, kEmptyKey if free
-    int32_t id;    // block id
-    int32_t pad;
+    uint64_t key;    // index key, kEmptyKey if free
+    int32_t id;      // block id
+    int32_t parent;  // id of the block's parent, -1 for a child of the root
 };
 
 // Per-store constants of the key chain, in device memory.
@@ -37,16 +38,26 @@ struct HashTables {
     uint32_t pad;
 };
 
+// Event counters a lookup adds to are spread over this many slots, each on
+// its own 128-byte line, so that thousands of waves adding at once do not
+// serialise on one address; readers sum the slots.
+constexpr int kCounterSlots = 64;
+
+struct alignas(128) CounterSlot {
+    unsigned long long probes;
+    unsigned long long token_compares;
+    unsigned long long pad[14];
+};
+
 // Device-side counters and status of a store.
 struct DevState {
     unsigned long long count;         // blocks stored (= next id)
     unsigned long long full_events;
     unsigned long long bad_entries;
-    unsigned long long probes;
-    unsigned long long token_compares;
     unsigned long long cas_attempts;
     unsigned long long cas_failures;
     unsigned long long insert_old_count;  // scratch: count before the running insert
+    CounterSlot slot[kCounterSlots];
 };
 
 __host__ __device__ inline uint64_t mix64(uint64_t z) {
@@ -136,6 +147,12 @@ __device__ inline void wave_count(unsigned long long* ctr, unsigned long long v,
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) v += (unsigned long long)shfl_u64(v, lane ^ d);
     if (lane == 0 && v) atomicAdd(ctr, v);
+}
+
+// The counter slot a wave adds to.
+__device__ inline CounterSlot* counter_slot(DevState* st) {
+    const unsigned w = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    return &st->slot[w & (kCounterSlots - 1)];
 }
 
 }  // namespace ptsd

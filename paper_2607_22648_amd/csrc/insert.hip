@@ -224,6 +224,7 @@ __global__ __launch_bounds__(kThreads) void k_publish(InsertArgs a) {
                 ++cas;
                 if (prev == kEmptyKey) {
                     slots[pos].id = id;
+                    slots[pos].parent = parent;
                     break;
                 }
                 ++fails;

@@ -2,12 +2,13 @@
 // the longest prefix of a request that is stored, and the ids along it).
 //
 // One wavefront per request, lane j owns block w0+j of a 64-block window:
-//   1. each lane loads its block's tokens and hashes them;
+//   1. each lane reads its block's tokens and hashes them;
 //   2. a wave prefix scan chains the hashes into per-block prefix keys;
 //   3. each lane probes the open-addressing index for its key and accepts the
 //      first slot whose stored block has the same tokens;
 //   4. the candidate of lane j must have as parent the id accepted by lane
-//      j-1 (the root, -1, for block 0); a ballot finds the first lane that
+//      j-1 (the root, -1, for block 0; the slot carries the parent id, so this
+//      costs no extra load); a ballot finds the first lane that
 //      fails, which is the end of the match. If that lane did find a block
 //      with the right tokens but the wrong parent (two prefixes whose keys
 //      collide), it keeps probing for one with the right parent before the
@@ -21,30 +22,45 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWavesPerGroup = kThreads / kWave;
 
-// Tokens of one block held in registers (BT = 16) or read from memory (BT = 0).
+// A request's block of BT tokens (BT = 0: the block size is a run-time
+// value). Only a pointer is kept: the tokens are read for hashing and read
+// again, next to the stored row, when a candidate is compared, which keeps
+// the lookup's register count (and so its occupancy) down.
 template <int BT>
 struct BlockTokens {
-    int32_t t[BT];
-    __device__ inline void load(const int32_t* __restrict__ p) {
-        if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+    const int32_t* p;
+    __device__ inline void load(const int32_t* __restrict__ q) { p = q; }
+    __device__ inline bool aligned() const { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+    __device__ inline uint64_t hash(uint64_t seed, int) const {
+        if (aligned()) {
+            int32_t t[BT];
 #pragma unroll
             for (int i = 0; i < BT; i += 4) {
                 int4 v = *reinterpret_cast<const int4*>(p + i);
                 t[i] = v.x; t[i + 1] = v.y; t[i + 2] = v.z; t[i + 3] = v.w;
             }
-        } else {
-#pragma unroll
-            for (int i = 0; i < BT; ++i) t[i] = p[i];
+            return content_hash_regs<BT>(t, seed);
         }
+        return content_hash_mem(p, BT, seed);
     }
-    __device__ inline uint64_t hash(uint64_t seed, int) const { return content_hash_regs<BT>(t, seed); }
-    // stored rows are BT*4 = 64-byte aligned
+    // stored rows are BT*4 = 64-byte aligned; compared 32 bytes at a time
     __device__ inline bool equals(const int32_t* __restrict__ s, int) const {
         bool eq = true;
-#pragma unroll
-        for (int i = 0; i < BT; i += 4) {
-            int4 v = *reinterpret_cast<const int4*>(s + i);
-            eq &= (v.x == t[i]) & (v.y == t[i + 1]) & (v.z == t[i + 2]) & (v.w == t[i + 3]);
+        const bool al = aligned();
+#pragma unroll 1
+        for (int i = 0; i < BT; i += 8) {
+            const int4 v0 = *reinterpret_cast<const int4*>(s + i);
+            const int4 v1 = *reinterpret_cast<const int4*>(s + i + 4);
+            int4 w0, w1;
+            if (al) {
+                w0 = *reinterpret_cast<const int4*>(p + i);
+                w1 = *reinterpret_cast<const int4*>(p + i + 4);
+            } else {
+                w0 = make_int4(p[i], p[i + 1], p[i + 2], p[i + 3]);
+                w1 = make_int4(p[i + 4], p[i + 5], p[i + 6], p[i + 7]);
+            }
+            eq &= (v0.x == w0.x) & (v0.y == w0.y) & (v0.z == w0.z) & (v0.w == w0.w) &
+                  (v1.x == w1.x) & (v1.y == w1.y) & (v1.z == w1.z) & (v1.w == w1.w);
         }
         return eq;
     }
@@ -64,11 +80,12 @@ struct BlockTokens<0> {
 
 // Linear probing from `pos` for a slot holding `ikey` whose block has the
 // lane's tokens (and, if need_parent, parent id `want_parent`).
-// Returns the block id or -1 at the first empty slot; *pos_out is the slot.
+// Returns the block id or -1 at the first empty slot; *pos_out is the slot
+// and *parent_out the block's parent id.
 template <int BT>
 __device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos,
                                 const BlockTokens<BT>& bk, bool need_parent, int32_t want_parent,
-                                uint64_t* pos_out, unsigned long long* probes,
+                                uint64_t* pos_out, int32_t* parent_out, unsigned long long* probes,
                                 unsigned long long* cmps) {
     const int bt = BT ? BT : ix.block_tokens;
     while (true) {
@@ -78,11 +95,11 @@ __device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos
             *pos_out = pos;
             return -1;
         }
-        if (s.key == ikey) {
+        if (s.key == ikey && (!need_parent || s.parent == want_parent)) {
             ++*cmps;
-            if (bk.equals(ix.tokens + (int64_t)s.id * bt, bt) &&
-                (!need_parent || ix.parent[s.id] == want_parent)) {
+            if (bk.equals(ix.tokens + (int64_t)s.id * bt, bt)) {
                 *pos_out = pos;
+                *parent_out = s.parent;
                 return s.id;
             }
         }
@@ -134,16 +151,16 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
         }
         const uint64_t k = window_chain(c, carry_key, ht, lane);
         const uint64_t ik = index_key(k, *ht);
-        int32_t cand = -1;
+        int32_t cand = -1, cpar = -2;
         uint64_t pos = 0;
         if (active)
             cand = probe<BT>(ix, ik, slot_of(ik, ht->slot_seed, ix.slot_mask), bk, false, 0, &pos,
-                             &probes, &cmps);
+                             &cpar, &probes, &cmps);
         int first_bad = kWave;
         while (true) {
             int32_t prev = __shfl_up(cand, 1, kWave);
             if (lane == 0) prev = carry_id;
-            const int32_t par = cand >= 0 ? ix.parent[cand] : -2;
+            const int32_t par = cand >= 0 ? cpar : -2;
             const bool ok = active && cand >= 0 && par == prev;
             const unsigned long long bad = ballot64(!ok);
             if (bad == 0) break;
@@ -156,8 +173,8 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
             // keys of two different prefixes collided: lane f looks further
             // along its probe sequence for the block with the right parent
             if (lane == f)
-                cand = probe<BT>(ix, ik, (pos + 1) & ix.slot_mask, bk, true, prev, &pos, &probes,
-                                 &cmps);
+                cand = probe<BT>(ix, ik, (pos + 1) & ix.slot_mask, bk, true, prev, &pos, &cpar,
+                                 &probes, &cmps);
         }
         if (active) row[b] = lane < first_bad ? cand : -1;
         if (first_bad < kWave) {
@@ -173,8 +190,9 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
     for (int b = fill_from + lane; b < bat.max_blocks; b += kWave) row[b] = -1;
     if (lane == 0) m_out[r] = m;
     if (ix.counters) {
-        wave_count(&ix.state->probes, probes, lane);
-        wave_count(&ix.state->token_compares, cmps, lane);
+        CounterSlot* cs = counter_slot(ix.state);
+        wave_count(&cs->probes, probes, lane);
+        wave_count(&cs->token_compares, cmps, lane);
     }
 }
 
