@@ -216,6 +216,17 @@ int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64
 int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t threads,
                            int32_t grid);
 
+/*
+ * Streaming-bandwidth probe (not a store operation): enqueue on `stream` one
+ * kernel that, with the access pattern of the copy kernels (16-byte
+ * non-temporal vectors), reads `bytes` from `a` (kind 0), writes `bytes` to
+ * `b` (kind 1) or copies `bytes` from `a` to `b` (kind 2). Time it with
+ * events around the call to get the device's practical HBM ceiling.
+ * `a`, `b`: device buffers of at least `bytes`, 16-byte aligned; `bytes` a
+ * multiple of 16, at most 32 GiB. Errors: INVALID, HIP.
+ */
+int ptstore_bandwidth_probe(int32_t kind, const void *a, void *b, int64_t bytes, void *stream);
+
 /* Human-readable text for a return code. */
 const char *ptstore_strerror(int code);
 

@@ -1,0 +1,61 @@
+// Streaming-bandwidth probes: the practical HBM ceiling the copy kernels are
+// measured against, taken in the same process as the measurement itself.
+// Each probe moves 16-byte vectors with non-temporal loads / stores, the
+// access pattern of the gather and scatter copies:
+//   kind 0  read `bytes` from a (a read-only stream)
+//   kind 1  write `bytes` to b (a write-only stream)
+//   kind 2  copy `bytes` from a to b, one 32 KiB span per 1024-thread workgroup
+#include <hip/hip_runtime.h>
+
+#include "ptstore.h"
+
+namespace {
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void k_read(const v4u* __restrict__ src, long n16, v4u* sink) {
+    v4u acc = {0u, 0u, 0u, 0u};
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (long)gridDim.x * blockDim.x)
+        acc ^= __builtin_nontemporal_load(src + i);
+    // never true for real data; keeps the loads alive
+    if (acc.x == 0x9E3779B9u && acc.y == 0x7F4A7C15u && acc.z == 0xF39CC060u && acc.w == 0x5CEDC834u)
+        sink[0] = acc;
+}
+
+__global__ __launch_bounds__(256) void k_write(v4u* __restrict__ dst, long n16) {
+    const v4u v = {1u, 2u, 3u, 4u};
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (long)gridDim.x * blockDim.x)
+        __builtin_nontemporal_store(v, dst + i);
+}
+
+__global__ __launch_bounds__(1024) void k_copy(const v4u* __restrict__ src, v4u* __restrict__ dst, long n16) {
+    const long base = (long)blockIdx.x * 2048;  // 32 KiB per workgroup
+    for (int i = threadIdx.x; i < 2048; i += blockDim.x) {
+        const long j = base + i;
+        if (j < n16) __builtin_nontemporal_store(__builtin_nontemporal_load(src + j), dst + j);
+    }
+}
+
+}  // namespace
+
+extern "C" __attribute__((visibility("default"))) int ptstore_bandwidth_probe(
+    int32_t kind, const void* a, void* b, int64_t bytes, void* stream) {
+    if (kind < 0 || kind > 2 || bytes < 16 || bytes > (32ll << 30) || (bytes & 15) || !a || !b ||
+        (reinterpret_cast<uintptr_t>(a) & 15) || (reinterpret_cast<uintptr_t>(b) & 15))
+        return PTSTORE_ERR_INVALID;
+    hipStream_t s = (hipStream_t)stream;
+    const long n16 = (long)(bytes >> 4);
+    int cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return PTSTORE_ERR_HIP;
+    const unsigned stream_grid = (unsigned)(cus * 64);
+    if (kind == 0)
+        hipLaunchKernelGGL(k_read, dim3(stream_grid), dim3(256), 0, s, (const v4u*)a, n16, (v4u*)b);
+    else if (kind == 1)
+        hipLaunchKernelGGL(k_write, dim3(stream_grid), dim3(256), 0, s, (v4u*)b, n16);
+    else
+        hipLaunchKernelGGL(k_copy, dim3((unsigned)((n16 + 2047) / 2048)), dim3(1024), 0, s,
+                           (const v4u*)a, (v4u*)b, n16);
+    return hipGetLastError() == hipSuccess ? PTSTORE_OK : PTSTORE_ERR_HIP;
+}

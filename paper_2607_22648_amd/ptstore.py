@@ -49,7 +49,8 @@ class PTStoreError(RuntimeError):
 EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gather",
            "ptstore_lookup_gather", "ptstore_insert", "ptstore_scatter", "ptstore_stats",
            "ptstore_reset_counters", "ptstore_get_buffers", "ptstore_kernel_times",
-           "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error")
+           "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
+           "ptstore_bandwidth_probe")
 
 
 def _load() -> C.CDLL:
@@ -71,6 +72,7 @@ def _load() -> C.CDLL:
         "ptstore_get_buffers": [p, C.POINTER(ptstore_buffers_t)],
         "ptstore_kernel_times": [p, i32, C.POINTER(d), C.POINTER(i64)],
         "ptstore_set_copy_shape": [p, i32, i32, i32],
+        "ptstore_bandwidth_probe": [i32, p, p, i64, p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -202,6 +204,12 @@ def ptstore_kernel_times(h, kind: int) -> Tuple[float, int]:
 def ptstore_set_copy_shape(h, chunks_per_group: int = 0, threads: int = 0, grid: int = 0) -> None:
     _check("ptstore_set_copy_shape", _lib.ptstore_set_copy_shape(h, chunks_per_group, threads,
                                                                   grid))
+
+
+def ptstore_bandwidth_probe(kind: int, a: torch.Tensor, b: torch.Tensor, nbytes: int,
+                            stream=None) -> None:
+    _check("ptstore_bandwidth_probe", _lib.ptstore_bandwidth_probe(
+        kind, _dev(a, None, "a"), _dev(b, None, "b"), nbytes, _stream(stream)))
 
 
 def ptstore_strerror(code: int) -> str:
