@@ -99,6 +99,8 @@ typedef struct {
     int64_t token_compares; /* candidate blocks compared token by token */
     int64_t cas_attempts;   /* compare-and-swap attempts by inserts */
     int64_t cas_failures;
+    int64_t insert_fallbacks; /* inserts whose key collisions sent them to the exact
+                                 sequential claim (results are the same either way) */
 } ptstore_stats_t;
 
 /* Device buffers of a store, for inspection by tests (read-only use). */

@@ -443,15 +443,18 @@ int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     out->chunk_bytes = s->chunk_bytes;
     out->full_events = (int64_t)st.full_events;
     out->bad_entries = (int64_t)st.bad_entries;
-    unsigned long long probes = 0, compares = 0;
+    unsigned long long probes = 0, compares = 0, cas = 0, cas_fail = 0;
     for (int i = 0; i < kCounterSlots; ++i) {
         probes += st.slot[i].probes;
         compares += st.slot[i].token_compares;
+        cas += st.slot[i].cas_attempts;
+        cas_fail += st.slot[i].cas_failures;
     }
     out->probes = (int64_t)probes;
     out->token_compares = (int64_t)compares;
-    out->cas_attempts = (int64_t)st.cas_attempts;
-    out->cas_failures = (int64_t)st.cas_failures;
+    out->cas_attempts = (int64_t)cas;
+    out->cas_failures = (int64_t)cas_fail;
+    out->insert_fallbacks = (int64_t)st.insert_fallbacks;
     return PTSTORE_OK;
 }
 

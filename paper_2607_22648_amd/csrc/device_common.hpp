@@ -46,7 +46,9 @@ constexpr int kCounterSlots = 64;
 struct alignas(128) CounterSlot {
     unsigned long long probes;
     unsigned long long token_compares;
-    unsigned long long pad[14];
+    unsigned long long cas_attempts;
+    unsigned long long cas_failures;
+    unsigned long long pad[12];
 };
 
 // Device-side counters and status of a store.
@@ -54,9 +56,8 @@ struct DevState {
     unsigned long long count;         // blocks stored (= next id)
     unsigned long long full_events;
     unsigned long long bad_entries;
-    unsigned long long cas_attempts;
-    unsigned long long cas_failures;
     unsigned long long insert_old_count;  // scratch: count before the running insert
+    unsigned long long insert_fallbacks;  // inserts that took the exact sequential claim
     CounterSlot slot[kCounterSlots];
 };
 

@@ -6,23 +6,29 @@
 // The result equals inserting the requests one after another: a missing
 // block becomes a new node whose id is the next free one in (request, block)
 // order, and a block already created by an earlier request of the batch is
-// reused. The GPU gets there without serialising requests:
+// reused. The GPU gets there without serialising requests or blocks:
 //
 //   lookup     match every request against the store as it was (m0, ids)
-//   hash_all   chained keys of every block
-//   claim      one thread per request walks its missing blocks b >= m0.
-//              Each new block is named by (parent label, its tokens), where
-//              the parent label is the stored id of block m0-1 (or the root)
-//              for b = m0 and the batch-table slot of block b-1 otherwise.
-//              The walk claims or finds that name in a batch hash table by
-//              compare-and-swap, so every distinct new block gets exactly
-//              one slot, and records the smallest request that needs it.
+//   hash_all   chained keys of every block (the key of block b is a function
+//              of the whole prefix up to b)
+//   claim      wave per request, lane per missing block b >= m0: the block
+//              claims or joins the batch-table entry named by (key, depth)
+//              and records in it the smallest request that needs it
+//   verify     wave per request, lane per block: the entry's smallest request
+//              o must hold the same prefix. It does if block b's tokens are
+//              equal and either b is both requests' first missing block under
+//              the same stored parent, or both requests' blocks b-1 sit in
+//              the same entry (by induction, equal prefixes). Any failure --
+//              a key collision between different prefixes -- raises a flag.
+//   exact      only when the flag is up: the table is cleared and rebuilt one
+//              block after another per request, each block named exactly by
+//              (entry of its parent, its tokens); slower, same result
 //   count      per request, the blocks it is the first (smallest r) to need
 //   scan       exclusive scan of the counts -> rank base per request; the
 //              store count advances, clipped at capacity
-//   assign     new id = old count + base[r] + rank within r; ids at or
-//              beyond capacity are refused (children rank after parents, so
-//              what is refused is always a suffix of a path)
+//   assign     new id = old count + base[r] + rank within r (wave ballot);
+//              ids at or beyond capacity are refused (children rank after
+//              parents, so what is refused is always a suffix of a path)
 //   publish    ids / created / m_out, block metadata, index slots
 //
 // Ids come from a scan, never from an atomic counter, so they are
@@ -32,7 +38,7 @@
 namespace ptsd {
 
 struct alignas(16) BatchEntry {
-    unsigned long long word;  // (parent label << 32) | token position; kEmptyKey if free
+    unsigned long long word;  // claim: tag of (key, depth); exact: (parent label << 32) | token position
     int32_t owner;            // smallest request that needs this block
     int32_t node_id;          // id assigned, -1 if refused
 };
@@ -40,9 +46,19 @@ struct alignas(16) BatchEntry {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
 constexpr uint32_t kStoreLabel = 0x80000000u;  // parent label of a stored block: bit 31 | (id + 1)
 
-__global__ void k_table_clear(BatchEntry* __restrict__ t, uint64_t n) {
+__device__ inline unsigned long long lanes_below(int lane) {
+    return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+// Clears the batch table. The first clear of an insert (only_if_collision =
+// 0) also lowers the collision flag; the second runs only if it was raised.
+__global__ void k_table_clear(BatchEntry* __restrict__ t, uint64_t n, unsigned int* collision,
+                              int only_if_collision) {
+    if (only_if_collision && *collision == 0) return;
+    if (!only_if_collision && blockIdx.x == 0 && threadIdx.x == 0) *collision = 0;
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (uint64_t)gridDim.x * blockDim.x) {
         BatchEntry e;
@@ -71,6 +87,13 @@ __device__ inline int32_t n_blocks(const Batch& bat, int64_t r, int bt, int64_t*
     return (int32_t)(n < bat.max_blocks ? n : bat.max_blocks);
 }
 
+// Name of a new block in the batch table: its chained key and its depth.
+// The top bit is clear, so a tag never equals the empty marker.
+__device__ inline unsigned long long tag_of(uint64_t key, int32_t b, const HashTables& ht) {
+    return mix64(index_key(key, ht) ^ (0x9E3779B97F4A7C15ull * (uint64_t)(b + 1)) ^ ~ht.slot_seed) &
+           0x7FFFFFFFFFFFFFFFull;
+}
+
 struct InsertArgs {
     IndexView ix;
     InsertTarget tgt;
@@ -81,8 +104,79 @@ struct InsertArgs {
     uint8_t* created;
 };
 
+__device__ inline void count_cas(const InsertArgs& a, unsigned long long cas,
+                                 unsigned long long fails, int lane) {
+    if (!a.ix.counters) return;
+    CounterSlot* cs = counter_slot(a.ix.state);
+    wave_count(&cs->cas_attempts, cas, lane);
+    wave_count(&cs->cas_failures, fails, lane);
+}
+
 __global__ __launch_bounds__(kThreads) void k_claim(InsertArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
+    if (r >= a.bat.R) return;
+    const int64_t maxb = a.bat.max_blocks;
+    int64_t o0;
+    const int32_t n = n_blocks(a.bat, r, a.ix.block_tokens, &o0);
+    const int32_t m0 = a.sc.m0[r];
+    BatchEntry* __restrict__ tab = reinterpret_cast<BatchEntry*>(a.sc.table);
+    unsigned long long cas = 0, fails = 0;
+    for (int32_t w0 = m0; w0 < n; w0 += kWave) {
+        const int32_t b = w0 + lane;
+        if (b >= n) continue;
+        const unsigned long long tag = tag_of(a.sc.keys[r * maxb + b], b, *a.ix.ht);
+        uint64_t pos = tag & a.sc.table_mask;
+        while (true) {
+            const unsigned long long prev = atomicCAS(&tab[pos].word, kEmptyKey, tag);
+            ++cas;
+            if (prev == kEmptyKey || prev == tag) break;
+            ++fails;
+            pos = (pos + 1) & a.sc.table_mask;
+        }
+        atomicMin(&tab[pos].owner, (int32_t)r);
+        a.sc.label[r * maxb + b] = (int32_t)pos;
+    }
+    count_cas(a, cas, fails, lane);
+}
+
+__global__ __launch_bounds__(kThreads) void k_verify(InsertArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
+    if (r >= a.bat.R) return;
+    const int bt = a.ix.block_tokens;
+    const int64_t maxb = a.bat.max_blocks;
+    int64_t o0;
+    const int32_t n = n_blocks(a.bat, r, bt, &o0);
+    const int32_t m0 = a.sc.m0[r];
+    const BatchEntry* __restrict__ tab = reinterpret_cast<const BatchEntry*>(a.sc.table);
+    bool ok = true;
+    for (int32_t w0 = m0; w0 < n; w0 += kWave) {
+        const int32_t b = w0 + lane;
+        if (b >= n) continue;
+        const int64_t o = tab[a.sc.label[r * maxb + b]].owner;
+        if (o == r) continue;
+        int64_t oo0;
+        const int32_t on = n_blocks(a.bat, o, bt, &oo0);
+        const int32_t om0 = a.sc.m0[o];
+        bool good = b < on && b >= om0 &&
+                    same_tokens(a.bat.tokens + oo0 + (int64_t)b * bt, a.bat.tokens + o0 + (int64_t)b * bt, bt);
+        if (good) {
+            if (b == m0)
+                good = om0 == b && (b == 0 || a.ids[o * maxb + b - 1] == a.ids[r * maxb + b - 1]);
+            else
+                good = om0 <= b - 1 && a.sc.label[o * maxb + b - 1] == a.sc.label[r * maxb + b - 1];
+        }
+        ok &= good;
+    }
+    if (!ok) *a.sc.collision = 1;
+}
+
+// Exact claim, one block after another per request (runs only on a collision).
+__global__ __launch_bounds__(kThreads) void k_claim_exact(InsertArgs a) {
+    if (*a.sc.collision == 0) return;
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r == 0) atomicAdd(&a.ix.state->insert_fallbacks, 1ull);
     if (r >= a.bat.R) return;
     const int bt = a.ix.block_tokens;
     const int64_t maxb = a.bat.max_blocks;
@@ -92,7 +186,6 @@ __global__ __launch_bounds__(kThreads) void k_claim(InsertArgs a) {
     BatchEntry* __restrict__ tab = reinterpret_cast<BatchEntry*>(a.sc.table);
     const HashTables* __restrict__ ht = a.ix.ht;
     uint32_t plabel = m0 == 0 ? kStoreLabel : (kStoreLabel | (uint32_t)(a.ids[r * maxb + m0 - 1] + 1));
-    unsigned long long cas = 0, fails = 0;
     for (int32_t b = m0; b < n; ++b) {
         const uint64_t ik = index_key(a.sc.keys[r * maxb + b], *ht);
         const uint32_t tpos = (uint32_t)(o0 + (int64_t)b * bt);
@@ -100,34 +193,33 @@ __global__ __launch_bounds__(kThreads) void k_claim(InsertArgs a) {
         uint64_t pos = slot_of(ik, ~ht->slot_seed, a.sc.table_mask);
         while (true) {
             const unsigned long long prev = atomicCAS(&tab[pos].word, kEmptyKey, word);
-            ++cas;
             if (prev == kEmptyKey) break;
             if ((uint32_t)(prev >> 32) == plabel &&
                 same_tokens(a.bat.tokens + (uint32_t)prev, a.bat.tokens + tpos, bt))
                 break;
-            ++fails;
             pos = (pos + 1) & a.sc.table_mask;
         }
         atomicMin(&tab[pos].owner, (int32_t)r);
         a.sc.label[r * maxb + b] = (int32_t)pos;
         plabel = (uint32_t)pos;
     }
-    if (a.ix.counters) {
-        if (cas) atomicAdd(&a.ix.state->cas_attempts, cas);
-        if (fails) atomicAdd(&a.ix.state->cas_failures, fails);
-    }
 }
 
 __global__ __launch_bounds__(kThreads) void k_count(InsertArgs a) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
     if (r >= a.bat.R) return;
     const int64_t maxb = a.bat.max_blocks;
     int64_t o0;
     const int32_t n = n_blocks(a.bat, r, a.ix.block_tokens, &o0);
     const BatchEntry* __restrict__ tab = reinterpret_cast<const BatchEntry*>(a.sc.table);
     int32_t c = 0;
-    for (int32_t b = a.sc.m0[r]; b < n; ++b) c += tab[a.sc.label[r * maxb + b]].owner == (int32_t)r;
-    a.sc.cnt[r] = c;
+    for (int32_t w0 = a.sc.m0[r]; w0 < n; w0 += kWave) {
+        const int32_t b = w0 + lane;
+        const bool mine = b < n && tab[a.sc.label[r * maxb + b]].owner == (int32_t)r;
+        c += __popcll(ballot64(mine));
+    }
+    if (lane == 0) a.sc.cnt[r] = c;
 }
 
 // One workgroup: exclusive scan of cnt into base, then advance the count.
@@ -169,25 +261,30 @@ __global__ __launch_bounds__(1024) void k_scan(InsertArgs a) {
 }
 
 __global__ __launch_bounds__(kThreads) void k_assign(InsertArgs a) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
     if (r >= a.bat.R) return;
     const int64_t maxb = a.bat.max_blocks;
     int64_t o0;
     const int32_t n = n_blocks(a.bat, r, a.ix.block_tokens, &o0);
     BatchEntry* __restrict__ tab = reinterpret_cast<BatchEntry*>(a.sc.table);
-    const long long old = (long long)a.ix.state->insert_old_count;
-    long long id = old + a.sc.base[r];
-    for (int32_t b = a.sc.m0[r]; b < n; ++b) {
-        BatchEntry* e = &tab[a.sc.label[r * maxb + b]];
-        if (e->owner == (int32_t)r) {
+    long long run = (long long)a.ix.state->insert_old_count + a.sc.base[r];
+    for (int32_t w0 = a.sc.m0[r]; w0 < n; w0 += kWave) {
+        const int32_t b = w0 + lane;
+        BatchEntry* e = b < n ? &tab[a.sc.label[r * maxb + b]] : nullptr;
+        const bool mine = e && e->owner == (int32_t)r;
+        const unsigned long long mask = ballot64(mine);
+        if (mine) {
+            const long long id = run + __popcll(mask & lanes_below(lane));
             e->node_id = id < a.tgt.capacity ? (int32_t)id : -1;
-            ++id;
         }
+        run += __popcll(mask);
     }
 }
 
 __global__ __launch_bounds__(kThreads) void k_publish(InsertArgs a) {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
     if (r >= a.bat.R) return;
     const int bt = a.ix.block_tokens;
     const int64_t maxb = a.bat.max_blocks;
@@ -198,49 +295,59 @@ __global__ __launch_bounds__(kThreads) void k_publish(InsertArgs a) {
     const HashTables* __restrict__ ht = a.ix.ht;
     int32_t* __restrict__ row = a.ids + r * maxb;
     uint8_t* __restrict__ crow = a.created + r * maxb;
-    int32_t parent = m0 == 0 ? -1 : row[m0 - 1];
-    int32_t m = m0;
+    for (int32_t b = lane; b < maxb; b += kWave)
+        if (b < m0 || b >= n) crow[b] = 0;
+    int32_t carry = m0 == 0 ? -1 : row[m0 - 1];  // id of the block before the window
+    int32_t m = n;                               // resident blocks after the call
     unsigned long long cas = 0, fails = 0;
-    for (int32_t b = 0; b < m0; ++b) crow[b] = 0;
-    for (int32_t b = m0; b < n; ++b) {
-        const BatchEntry e = tab[a.sc.label[r * maxb + b]];
-        if (e.node_id < 0) break;
+    for (int32_t w0 = m0; w0 < n; w0 += kWave) {
+        const int32_t b = w0 + lane;
+        const bool valid = b < n;
+        BatchEntry e;
+        e.node_id = -1;
+        e.owner = -1;
+        if (valid) e = tab[a.sc.label[r * maxb + b]];
+        const unsigned long long refused = ballot64(valid && e.node_id < 0);
+        if (refused) {
+            const int32_t cut = w0 + __ffsll((long long)refused) - 1;
+            m = cut < m ? cut : m;
+        }
+        int32_t parent = __shfl_up(e.node_id, 1, kWave);
+        if (lane == 0) parent = carry;
+        carry = __shfl(e.node_id, kWave - 1, kWave);
+        if (!valid) continue;
+        if (b >= m) {
+            row[b] = -1;
+            crow[b] = 0;
+            continue;
+        }
         const int32_t id = e.node_id;
         row[b] = id;
         const bool mine = e.owner == (int32_t)r;
         crow[b] = mine ? 1 : 0;
-        if (mine) {
-            a.tgt.parent[id] = parent;
-            const int32_t* src = a.bat.tokens + o0 + (int64_t)b * bt;
-            int32_t* dst = a.tgt.tokens + (int64_t)id * bt;
-            for (int i = 0; i < bt; ++i) dst[i] = src[i];
-            const uint64_t ik = index_key(a.sc.keys[r * maxb + b], *ht);
-            uint64_t pos = slot_of(ik, ht->slot_seed, a.ix.slot_mask);
-            Slot* slots = a.tgt.slots;
-            while (true) {
-                const unsigned long long prev =
-                    atomicCAS(reinterpret_cast<unsigned long long*>(&slots[pos].key), kEmptyKey,
-                              (unsigned long long)ik);
-                ++cas;
-                if (prev == kEmptyKey) {
-                    slots[pos].id = id;
-                    slots[pos].parent = parent;
-                    break;
-                }
-                ++fails;
-                pos = (pos + 1) & a.ix.slot_mask;
+        if (!mine) continue;
+        a.tgt.parent[id] = parent;
+        const int32_t* src = a.bat.tokens + o0 + (int64_t)b * bt;
+        int32_t* dst = a.tgt.tokens + (int64_t)id * bt;
+        for (int i = 0; i < bt; ++i) dst[i] = src[i];
+        const uint64_t ik = index_key(a.sc.keys[r * maxb + b], *ht);
+        uint64_t pos = slot_of(ik, ht->slot_seed, a.ix.slot_mask);
+        Slot* slots = a.tgt.slots;
+        while (true) {
+            const unsigned long long prev = atomicCAS(
+                reinterpret_cast<unsigned long long*>(&slots[pos].key), kEmptyKey, (unsigned long long)ik);
+            ++cas;
+            if (prev == kEmptyKey) {
+                slots[pos].id = id;
+                slots[pos].parent = parent;
+                break;
             }
+            ++fails;
+            pos = (pos + 1) & a.ix.slot_mask;
         }
-        parent = id;
-        m = b + 1;
     }
-    for (int32_t b = m; b < maxb; ++b) crow[b] = 0;
-    for (int32_t b = m; b < n; ++b) row[b] = -1;
-    a.m_out[r] = m;
-    if (a.ix.counters) {
-        if (cas) atomicAdd(&a.ix.state->cas_attempts, cas);
-        if (fails) atomicAdd(&a.ix.state->cas_failures, fails);
-    }
+    if (lane == 0) a.m_out[r] = m;
+    count_cas(a, cas, fails, lane);
 }
 
 }  // namespace
@@ -251,7 +358,8 @@ size_t insert_scratch_bytes(int32_t R, int32_t max_blocks, uint64_t* table_entri
     while (t < 2 * rb) t <<= 1;
     *table_entries = t;
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return up(rb * 8) + up((size_t)R * 4) + up(rb * 4) + up((size_t)R * 4) * 2 + up(t * sizeof(BatchEntry));
+    return up(rb * 8) + up((size_t)R * 4) + up(rb * 4) + up((size_t)R * 4) * 2 +
+           up(t * sizeof(BatchEntry)) + 256;
 }
 
 void insert_scratch_carve(void* base, int32_t R, int32_t max_blocks, InsertScratch* out) {
@@ -272,6 +380,8 @@ void insert_scratch_carve(void* base, int32_t R, int32_t max_blocks, InsertScrat
     p += up((size_t)R * 4);
     out->table = p;
     out->table_mask = t - 1;
+    p += up(t * sizeof(BatchEntry));
+    out->collision = reinterpret_cast<unsigned int*>(p);
 }
 
 hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Batch& b,
@@ -281,21 +391,29 @@ hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Bat
     if ((e = launch_lookup(ix, b, sc.m0, ids, s)) != hipSuccess) return e;
     if ((e = launch_hash_all(ix, b, sc.keys, s)) != hipSuccess) return e;
     const uint64_t tn = sc.table_mask + 1;
-    const unsigned cgrid = (unsigned)((tn + kThreads - 1) / kThreads < 65536 ? (tn + kThreads - 1) / kThreads : 65536);
-    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s,
-                       reinterpret_cast<BatchEntry*>(sc.table), tn);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const uint64_t cg = (tn + kThreads - 1) / kThreads;
+    const unsigned cgrid = (unsigned)(cg < 65536 ? cg : 65536);
+    BatchEntry* table = reinterpret_cast<BatchEntry*>(sc.table);
     InsertArgs a{ix, tgt, b, sc, m_out, ids, created};
-    const unsigned grid = (unsigned)((b.R + kThreads - 1) / kThreads);
-    hipLaunchKernelGGL(k_claim, dim3(grid), dim3(kThreads), 0, s, a);
+    const unsigned wgrid = (unsigned)((b.R + kWaves - 1) / kWaves);      // wave per request
+    const unsigned tgrid = (unsigned)((b.R + kThreads - 1) / kThreads);  // thread per request
+    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_count, dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_claim, dim3(wgrid), dim3(kThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_verify, dim3(wgrid), dim3(kThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_claim_exact, dim3(tgrid), dim3(kThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_count, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_assign, dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_assign, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_publish, dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_publish, dim3(wgrid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -83,6 +83,7 @@ struct InsertScratch {
     int32_t* base;        // [R] exclusive scan of cnt
     void* table;          // batch table, table_mask + 1 entries of 16 bytes
     uint64_t table_mask;
+    unsigned int* collision;  // set when the fast claim must be redone exactly
 };
 size_t insert_scratch_bytes(int32_t R, int32_t max_blocks, uint64_t* table_entries);
 void insert_scratch_carve(void* base, int32_t R, int32_t max_blocks, InsertScratch* out);

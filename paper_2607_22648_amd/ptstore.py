@@ -32,7 +32,8 @@ class ptstore_config_t(C.Structure):
 class ptstore_stats_t(C.Structure):
     _fields_ = [(n, C.c_int64) for n in (
         "blocks_stored", "capacity", "index_slots", "block_bytes", "chunk_bytes", "full_events",
-        "bad_entries", "probes", "token_compares", "cas_attempts", "cas_failures")]
+        "bad_entries", "probes", "token_compares", "cas_attempts", "cas_failures",
+        "insert_fallbacks")]
 
 
 class ptstore_buffers_t(C.Structure):

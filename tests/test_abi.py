@@ -48,5 +48,5 @@ def test_config_struct_layout_matches_header():
     """ctypes mirrors of the C structs have the sizes the header implies."""
     from paper_2607_22648_amd import ptstore as P
     assert C.sizeof(P.ptstore_config_t) == 5 * 4 + 4 + 8 + 8 + 8 + 4 + 4  # incl. padding
-    assert C.sizeof(P.ptstore_stats_t) == 11 * 8
+    assert C.sizeof(P.ptstore_stats_t) == 12 * 8
     assert C.sizeof(P.ptstore_buffers_t) == 6 * 8

@@ -68,6 +68,7 @@ def test_random_tries(seed, bt):
         toks, offs = random_block_batch(rng, 48, atoms, 90)
         t.lookup(toks, offs, maxb)
     t.check_meta()
+    assert t.gpu.stats()["insert_fallbacks"] == 0  # 61-bit keys: the parallel claim held
     t.close()
 
 
@@ -83,6 +84,7 @@ def test_weak_hash_gives_same_results():
         t.lookup(toks, offs, 40)
     st = t.gpu.stats()
     assert st["token_compares"] > st["probes"] // 4  # collisions really happened
+    assert st["insert_fallbacks"] >= 1  # and the inserts took the exact path
     t.close()
 
 
