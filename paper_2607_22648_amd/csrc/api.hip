@@ -131,6 +131,10 @@ hipEvent_t take_event(ptstore_t* s) {
     return e;
 }
 
+// Most event pairs kept per kind between two ptstore_kernel_times() calls;
+// beyond that, launches are no longer recorded (the sum stays consistent).
+constexpr size_t kMaxTimed = 1 << 16;
+
 // Brackets the kernels enqueued during its lifetime with two events.
 struct Timed {
     ptstore_t* s;
@@ -138,7 +142,7 @@ struct Timed {
     hipStream_t st;
     hipEvent_t a = nullptr;
     Timed(ptstore_t* s_, int k, hipStream_t st_) : s(s_), kind(k), st(st_) {
-        if (s->cfg.flags & PTSTORE_FLAG_TIMING) {
+        if ((s->cfg.flags & PTSTORE_FLAG_TIMING) && s->ev[kind].size() < kMaxTimed) {
             a = take_event(s);
             if (a) (void)hipEventRecord(a, st);
         }
