@@ -56,7 +56,15 @@ def _load(path: str = _LIB):
     lib.orc_pool.restype = C.POINTER(C.c_uint8)
     lib.orc_pool.argtypes = [p]
     lib.orc_node.argtypes = [p, i64, C.POINTER(C.c_int32), p]
-    for f in (lib.orc_lookup, lib.orc_gather, lib.orc_insert, lib.orc_scatter, lib.orc_node):
+    lib.orc_set_evict.argtypes = [p, i32]
+    lib.orc_clock.restype = i64
+    lib.orc_clock.argtypes = [p]
+    lib.orc_evictions.restype = i64
+    lib.orc_evictions.argtypes = [p]
+    lib.orc_node_stats.argtypes = [p, i64, C.POINTER(C.c_int64), C.POINTER(C.c_int64),
+                                   C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
+    for f in (lib.orc_lookup, lib.orc_gather, lib.orc_insert, lib.orc_scatter, lib.orc_node,
+              lib.orc_node_stats):
         f.restype = C.c_int
     _lib_cache[path] = lib
     return lib
@@ -71,7 +79,7 @@ class OracleStore:
 
     def __init__(self, layers: int, kv_heads: int, head_dim: int, block_tokens: int = 16,
                  elem_bytes: int = 2, capacity: int = 1 << 16, with_payload: bool = True,
-                 lib_path: Optional[str] = None):
+                 lib_path: Optional[str] = None, evict: bool = False):
         self._lib = _load(lib_path or DEFAULT_LIB)
         self.layers, self.kv_heads, self.head_dim = layers, kv_heads, head_dim
         self.block_tokens, self.elem_bytes, self.capacity = block_tokens, elem_bytes, capacity
@@ -82,6 +90,8 @@ class OracleStore:
         if not self._h:
             raise MemoryError("oracle store allocation failed")
         self.with_payload = with_payload
+        self.evict = evict
+        self._lib.orc_set_evict(self._h, 1 if evict else 0)
 
     @classmethod
     def for_shape(cls, shape, capacity: int, with_payload: bool = True, **kw) -> "OracleStore":
@@ -161,6 +171,25 @@ class OracleStore:
     @property
     def bad_entries(self) -> int:
         return int(self._lib.orc_bad_entries(self._h))
+
+    @property
+    def clock(self) -> int:
+        """Eviction clock L (the largest priority evicted so far)."""
+        return int(self._lib.orc_clock(self._h))
+
+    @property
+    def evictions(self) -> int:
+        return int(self._lib.orc_evictions(self._h))
+
+    def node_stats(self, node_id: int) -> Tuple[int, int, int, int]:
+        """(frequency, priority, children holding an id, depth) of a node."""
+        f, p = C.c_int64(0), C.c_int64(0)
+        lc, d = C.c_int32(0), C.c_int32(0)
+        rc = self._lib.orc_node_stats(self._h, node_id, C.byref(f), C.byref(p), C.byref(lc),
+                                      C.byref(d))
+        if rc:
+            raise KeyError(node_id)
+        return int(f.value), int(p.value), int(lc.value), int(d.value)
 
     def node(self, node_id: int) -> Tuple[int, np.ndarray]:
         parent = C.c_int32(0)

@@ -17,13 +17,14 @@ import pytest
 
 import oracle.ref as ref
 from tests import test_oracle as pins
+from tests import test_oracle_eviction as evpins
 
 MUTANTS = {
     "match_first_token_only": ("if (memcmp(c->tokens, blk, nbytes) == 0)",
                                "if (memcmp(c->tokens, blk, sizeof(int32_t)) == 0)"),
     "lookup_m_off_by_one": ("        m[r] = b;\n        for (int32_t j = b; j < max_blocks; j++) row[j] = -1;\n    }\n    return ORC_OK;",
                             "        m[r] = b > 0 ? b - 1 : 0;\n        for (int32_t j = b; j < max_blocks; j++) row[j] = -1;\n    }\n    return ORC_OK;"),
-    "created_never_set": ("crow[b] = 1;", "crow[b] = 0;"),
+    "created_never_set": ("                crow[b] = 1;\n", "                crow[b] = 0;\n"),
     "capacity_off_by_one": ("if (s->count >= s->capacity) { full = 1; break; }",
                             "if (s->count + 1 >= s->capacity) { full = 1; break; }"),
     "cache_layout_transposed": ("return (((int64_t)l * 2 + kv) * cache_blocks + cb) * s->chunk_bytes;",
@@ -36,6 +37,16 @@ MUTANTS = {
     "scatter_every_occurrence": ("if (!created[k]) continue;", "if (ids[k] < 0) continue;"),
     "root_children_by_parent_ignored": ("        onode_t *node = &s->root;\n        int32_t b = 0;\n        for (; b < n; b++) {\n            const int32_t *blk",
                                         "        onode_t *node = &s->root;\n        int32_t b = 0;\n        for (; b < n; b++) {\n            node = &s->root;\n            const int32_t *blk"),
+    # eviction mode
+    "evict_ties_ignore_depth": ("    if (a->depth != b->depth) return a->depth > b->depth;\n", ""),
+    "evict_clock_never_raised": ("if (best->prio > s->clock) s->clock = best->prio;", ";"),
+    "evict_no_protection": ("c->protect = s->epoch;", "c->protect = 0;"),
+    "evict_ids_in_eviction_order": ("qsort(victims, (size_t)nv, sizeof(int32_t), cmp_i32);", ";"),
+    "evict_lookup_not_an_access": ("if (s->evict) touch(s, c);", ";"),
+    "evict_plain_lfu": ("n->prio = s->clock + n->freq;", "n->prio = n->freq;"),
+    "evict_no_cascade": ("if (best->parent != &s->root) best->parent->live_children--;", ";"),
+    "evict_created_for_every_user": ("if (c->born == s->epoch && c->creator == r) crow[b] = 1;",
+                                     "if (c->born == s->epoch) crow[b] = 1;"),
 }
 
 # pins that need no mutable global state; each gets a fresh store
@@ -49,6 +60,9 @@ PIN_CALLS = [
     pins.test_ground_truth_tiny,
     pins.test_full_match_and_max_blocks_truncation,
     pins.test_capacity_zero,
+    lambda: [evpins.test_golden_eviction_oracle(c) for c in pins.load_golden("eviction.json")["cases"]],
+    lambda: [evpins.test_evict_random_vs_brute(k) for k in range(4)],
+    lambda: [evpins.test_evict_invariants(k) for k in range(2)],
 ]
 
 
