@@ -69,7 +69,21 @@ enum {
     PTSTORE_FLAG_COUNTERS = 2u,
     /* Record HIP events around every gather / scatter / lookup kernel so
      * that ptstore_kernel_times() can report their durations. */
-    PTSTORE_FLAG_TIMING = 4u
+    PTSTORE_FLAG_TIMING = 4u,
+    /* Evict instead of refusing once the store is full (Section 4.1,
+     * "Access pattern-aware eviction policy": frequency-based, GDSF adapted
+     * to shared prefixes). Every lookup and insert counts accesses: an
+     * access adds 1 to a block's frequency F and sets its priority
+     * H = L + F, L being the store's clock. An insert that needs more new
+     * blocks than the never-used ids left frees the difference first: it
+     * evicts, one at a time, a block with no resident child that no request
+     * of the batch matched, the one with the lowest H, then the deepest,
+     * then the smallest id, and raises L to that block's H. What stays
+     * resident is therefore always a set of whole prefixes. New blocks take
+     * never-used ids first, then the freed ids from the smallest up; blocks
+     * still without an id are refused as without this flag. Costs 44 bytes
+     * of device memory per pool block. */
+    PTSTORE_FLAG_EVICT = 8u
 };
 
 typedef struct {
@@ -101,6 +115,9 @@ typedef struct {
     int64_t cas_failures;
     int64_t insert_fallbacks; /* inserts whose key collisions sent them to the exact
                                  sequential claim (results are the same either way) */
+    int64_t evictions;      /* blocks evicted so far (PTSTORE_FLAG_EVICT) */
+    int64_t clock;          /* eviction clock L: the largest priority evicted so far */
+    int64_t index_rebuilds; /* times the index was rebuilt to clear deleted slots */
 } ptstore_stats_t;
 
 /* Device buffers of a store, for inspection by tests (read-only use). */
@@ -111,6 +128,8 @@ typedef struct {
     const void *slots;      /* [index_slots] of {uint64 key, int32 id, int32 parent} */
     int64_t capacity;
     int64_t index_slots;
+    const uint64_t *freq;   /* [capacity] access counts F (NULL without PTSTORE_FLAG_EVICT) */
+    const uint64_t *prio;   /* [capacity] priorities H (NULL without PTSTORE_FLAG_EVICT) */
 } ptstore_buffers_t;
 
 /*
@@ -128,7 +147,8 @@ int ptstore_destroy(ptstore_t *store);
  * LCP query (Section 4.1): for each request r, m[r] = the largest k such that
  * its blocks 0..k-1 are a stored prefix (blocks beyond max_blocks ignored),
  * and ids[r][b] = the id of the stored block at depth b for b < m[r], -1
- * beyond. Outputs: m [R] int32, ids [R][max_blocks] int32.
+ * beyond. Outputs: m [R] int32, ids [R][max_blocks] int32. With
+ * PTSTORE_FLAG_EVICT every matched block of every request counts one access.
  * Errors: INVALID (store NULL, R < 0, max_blocks < 1, n_tokens < 0 or
  * >= 2^32, a NULL pointer with R > 0).
  */
@@ -168,9 +188,11 @@ int ptstore_lookup_gather(ptstore_t *store, const int32_t *tokens, const int64_t
  * common prefix (including blocks created by earlier requests of this
  * batch) and creates one new block per missing block, ids handed out
  * densely in (request, block) order. Once the store holds `capacity`
- * blocks nothing more is created; a request then keeps only the blocks it
+ * blocks nothing more is created (with PTSTORE_FLAG_EVICT: once no block can
+ * be evicted, see there); a request then keeps only the blocks it
  * could reuse or create (the cut is always a prefix) and full_events is
- * incremented. Outputs: m_out [R] = blocks of r resident after the call;
+ * incremented. With PTSTORE_FLAG_EVICT, after the evictions every block on
+ * each request's resident path counts one access. Outputs: m_out [R] = blocks of r resident after the call;
  * ids [R][max_blocks] their ids (-1 beyond m_out); created [R][max_blocks]
  * = 1 exactly where request r created the block (a block shared by several
  * requests of the batch is created by the first of them).
@@ -194,7 +216,9 @@ int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created
 /* Wait for the device and read the store's counters into *stats. */
 int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);
 
-/* Zero the event counters (probes, compares, CAS, full_events, bad_entries). */
+/* Zero the event counters (probes, compares, CAS, full_events, bad_entries,
+ * insert_fallbacks, index_rebuilds); blocks_stored, evictions and the clock
+ * are state and stay. */
 int ptstore_reset_counters(ptstore_t *store);
 
 /* Device buffers of the store (see ptstore_buffers_t). */

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libptstore.so")
-SOURCES = ["api.hip", "lookup.hip", "copy.hip", "insert.hip", "probe.hip"]
+SOURCES = ["api.hip", "lookup.hip", "copy.hip", "insert.hip", "evict.hip", "probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

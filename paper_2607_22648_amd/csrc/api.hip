@@ -5,6 +5,9 @@
 //   parent  [capacity] int32, tokens [capacity][block_tokens] int32   block metadata
 //   slots   [index_slots] {key, id}                  open-addressing block index
 //   ht      key-chain constants, state: counters and the block count
+//   evs     with eviction on: per-block access counts, priorities, child
+//           counts, depths, index keys and slots, and the victim-selection
+//           scratch (all sized by the capacity, allocated here once)
 //   scratch insert work space; copy_scratch gather/scatter descriptor lists
 //           (both grown on demand, so the hot path allocates only when a
 //           batch is larger than every earlier one)
@@ -40,6 +43,8 @@ struct ptstore {
     size_t copy_scratch_bytes;
     int32_t chunks_per_group, threads, grid;
     int32_t cus;  // compute units of the device
+    EvictView evs;  // evs.on = 0 without PTSTORE_FLAG_EVICT
+    void* ev_mem;  // one allocation holding every ev array
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[5];
     std::vector<hipEvent_t> free_ev;
@@ -100,6 +105,8 @@ IndexView index_view(ptstore_t* s) {
     ix.tokens = s->tokens;
     ix.ht = s->ht;
     ix.state = s->state;
+    ix.freq = s->evs.on ? s->evs.freq : nullptr;
+    ix.prio = s->evs.on ? s->evs.prio : nullptr;
     ix.block_tokens = s->cfg.block_tokens;
     ix.counters = (s->cfg.flags & PTSTORE_FLAG_COUNTERS) ? 1 : 0;
     return ix;
@@ -187,6 +194,35 @@ int ensure_scratch(void** buf, size_t* have, size_t need, hipStream_t st, const 
     }
     *have = grow;
     return PTSTORE_OK;
+}
+
+// Carves the eviction arrays out of one block of device memory; returns the
+// bytes needed (base may be null to only size them).
+size_t carve_evict(void* base, int64_t capacity, EvictView* ev) {
+    const int64_t cap = capacity > 0 ? capacity : 1;
+    const int64_t words = (cap + kWave - 1) / kWave;
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    uint8_t* p = static_cast<uint8_t*>(base);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        void* q = p ? p + off : nullptr;
+        off += up(bytes);
+        return q;
+    };
+    ev->freq = static_cast<uint64_t*>(take(cap * 8));
+    ev->prio = static_cast<uint64_t*>(take(cap * 8));
+    ev->live = static_cast<int32_t*>(take(cap * 4));
+    ev->prot = static_cast<int32_t*>(take(cap * 4));
+    ev->depth = static_cast<int32_t*>(take(cap * 4));
+    ev->nkey = static_cast<uint64_t*>(take(cap * 8));
+    ev->spos = static_cast<uint32_t*>(take(cap * 4));
+    ev->victims = static_cast<int32_t*>(take(cap * 4));
+    ev->wmask = static_cast<uint64_t*>(take(words * 8));
+    ev->wcnt = static_cast<uint32_t*>(take(words * 4));
+    ev->wbase = static_cast<uint32_t*>(take(words * 4));
+    ev->hist = static_cast<uint32_t*>(take(kSelPasses * 256 * 4));
+    ev->words = words;
+    return off;
 }
 
 }  // namespace
@@ -281,6 +317,18 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         (void)hipGetLastError();
         return fail(PTSTORE_ERR_NOMEM, "ptstore_create: hipMalloc", e);
     }
+    if (c.flags & PTSTORE_FLAG_EVICT) {
+        const size_t evb = carve_evict(nullptr, s->capacity, &s->evs);
+        if ((e = hipMalloc(&s->ev_mem, evb)) != hipSuccess ||
+            (e = hipMemset(s->ev_mem, 0, evb)) != hipSuccess) {
+            ptstore_destroy(s);
+            (void)hipGetLastError();
+            return fail(PTSTORE_ERR_NOMEM, "ptstore_create: eviction arrays", e);
+        }
+        carve_evict(s->ev_mem, s->capacity, &s->evs);
+        s->evs.on = 1;
+        s->evs.epoch = 0;
+    }
     HashTables h;
     make_hash_tables(c.hash_seed, (c.flags & PTSTORE_FLAG_WEAK_HASH) != 0, &h);
     DevState st;
@@ -314,6 +362,7 @@ int ptstore_destroy(ptstore_t* s) {
     (void)hipFree(s->state);
     (void)hipFree(s->scratch);
     (void)hipFree(s->copy_scratch);
+    (void)hipFree(s->ev_mem);
     delete s;
     return PTSTORE_OK;
 }
@@ -395,9 +444,13 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     insert_scratch_carve(s->scratch, R, max_blocks, &sc);
     InsertTarget tgt{s->slots, s->parent, s->tokens, s->capacity};
     Batch b{tokens, offsets, n_tokens, R, max_blocks};
+    if (s->evs.on) {
+        // protection marks are compared with the epoch; 0 marks nothing
+        if (++s->evs.epoch == 0x7FFFFFFF) s->evs.epoch = 1;
+    }
     {
         Timed t(s, 3, st);
-        e = launch_insert(index_view(s), tgt, b, sc, m_out, ids, created, st);
+        e = launch_insert(index_view(s), tgt, s->evs, b, sc, m_out, ids, created, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_insert: launch", e);
 }
@@ -459,6 +512,9 @@ int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     out->cas_attempts = (int64_t)cas;
     out->cas_failures = (int64_t)cas_fail;
     out->insert_fallbacks = (int64_t)st.insert_fallbacks;
+    out->evictions = (int64_t)st.evictions;
+    out->clock = (int64_t)st.clock;
+    out->index_rebuilds = (int64_t)st.rebuilds;
     return PTSTORE_OK;
 }
 
@@ -470,10 +526,13 @@ int ptstore_reset_counters(ptstore_t* s) {
     hipError_t e = hipDeviceSynchronize();
     if (e == hipSuccess) e = hipMemcpy(&st, s->state, sizeof st, hipMemcpyDeviceToHost);
     if (e == hipSuccess) {
-        const unsigned long long count = st.count;
-        memset(&st, 0, sizeof st);
-        st.count = count;
-        e = hipMemcpy(s->state, &st, sizeof st, hipMemcpyHostToDevice);
+        DevState keep;
+        memset(&keep, 0, sizeof keep);
+        keep.count = st.count;
+        keep.clock = st.clock;
+        keep.evictions = st.evictions;
+        keep.tombstones = st.tombstones;
+        e = hipMemcpy(s->state, &keep, sizeof keep, hipMemcpyHostToDevice);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_reset_counters", e);
 }
@@ -486,6 +545,8 @@ int ptstore_get_buffers(ptstore_t* s, ptstore_buffers_t* out) {
     out->slots = s->slots;
     out->capacity = s->capacity;
     out->index_slots = (int64_t)s->slots_n;
+    out->freq = s->evs.on ? s->evs.freq : nullptr;
+    out->prio = s->evs.on ? s->evs.prio : nullptr;
     return PTSTORE_OK;
 }
 

@@ -17,6 +17,7 @@ namespace ptsd {
 
 constexpr uint64_t kM61 = (1ull << 61) - 1;
 constexpr uint64_t kEmptyKey = ~0ull;  // never a key: keys are < 2^61
+constexpr uint64_t kTombKey = ~1ull;   // slot of an evicted block: probing goes on past it
 constexpr int kWave = 64;
 
 // One slot of the open-addressing block index. The parent id rides along
@@ -51,6 +52,9 @@ struct alignas(128) CounterSlot {
     unsigned long long pad[12];
 };
 
+// Digit passes of the eviction threshold search: 8 bits of a 128-bit key each.
+constexpr int kSelPasses = 16;
+
 // Device-side counters and status of a store.
 struct DevState {
     unsigned long long count;         // blocks stored (= next id)
@@ -58,6 +62,20 @@ struct DevState {
     unsigned long long bad_entries;
     unsigned long long insert_old_count;  // scratch: count before the running insert
     unsigned long long insert_fallbacks;  // inserts that took the exact sequential claim
+    // eviction (state)
+    unsigned long long clock;         // L: largest priority evicted so far
+    unsigned long long evictions;
+    unsigned long long tombstones;    // upper bound on deleted index slots
+    unsigned long long rebuilds;
+    // eviction (scratch of the running insert)
+    unsigned long long ev_new;        // distinct new blocks the batch needs
+    unsigned long long ev_want;       // blocks to evict
+    unsigned long long ev_all;        // 1: every candidate goes (no more than ev_want)
+    unsigned long long ev_nv;         // blocks evicted
+    unsigned long long ev_rebuild;    // 1: rebuild the index in this insert
+    unsigned long long sel_hi, sel_lo;  // threshold key found so far
+    unsigned long long sel_need;        // rank of the threshold among what matches it
+    unsigned int sel_done[kSelPasses];  // workgroups finished per pass
     CounterSlot slot[kCounterSlots];
 };
 
@@ -148,6 +166,13 @@ __device__ inline void wave_count(unsigned long long* ctr, unsigned long long v,
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) v += (unsigned long long)shfl_u64(v, lane ^ d);
     if (lane == 0 && v) atomicAdd(ctr, v);
+}
+
+// Sum of a per-lane count over the wave, taken once from a device counter.
+__device__ inline void wave_sub(unsigned long long* ctr, unsigned long long v, int lane) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v += (unsigned long long)shfl_u64(v, lane ^ d);
+    if (lane == 0 && v) atomicSub(ctr, v);
 }
 
 // The counter slot a wave adds to.

@@ -33,6 +33,12 @@
 //
 // Ids come from a scan, never from an atomic counter, so they are
 // deterministic and equal the sequential ones.
+//
+// With eviction on, count also marks the blocks the batch matched
+// (protected), scan computes how many blocks must be evicted, evict.hip
+// frees them between scan and assign, assign hands out never-used ids and
+// then the freed ones, publish may take a deleted index slot, and the
+// resident paths are accessed last.
 #include "kernels.hpp"
 
 namespace ptsd {
@@ -97,6 +103,7 @@ __device__ inline unsigned long long tag_of(uint64_t key, int32_t b, const HashT
 struct InsertArgs {
     IndexView ix;
     InsertTarget tgt;
+    EvictView ev;
     Batch bat;
     InsertScratch sc;
     int32_t* m_out;
@@ -213,6 +220,8 @@ __global__ __launch_bounds__(kThreads) void k_count(InsertArgs a) {
     int64_t o0;
     const int32_t n = n_blocks(a.bat, r, a.ix.block_tokens, &o0);
     const BatchEntry* __restrict__ tab = reinterpret_cast<const BatchEntry*>(a.sc.table);
+    if (a.ev.on)  // the blocks this request matched cannot be evicted by this insert
+        for (int32_t b = lane; b < a.sc.m0[r]; b += kWave) a.ev.prot[a.ids[r * maxb + b]] = a.ev.epoch;
     int32_t c = 0;
     for (int32_t w0 = a.sc.m0[r]; w0 < n; w0 += kWave) {
         const int32_t b = w0 + lane;
@@ -245,17 +254,31 @@ __global__ __launch_bounds__(1024) void k_scan(InsertArgs a) {
         a.sc.base[i] = (int32_t)run;
         run += a.sc.cnt[i];
     }
+    DevState* st = a.ix.state;
+    if (a.ev.on) {  // fresh selection state for evict.hip
+        for (int i = t; i < kSelPasses * 256; i += nt) a.ev.hist[i] = 0;
+        if (t < kSelPasses) st->sel_done[t] = 0;
+    }
     if (t == nt - 1) {
         const long long total = part[nt - 1];
-        DevState* st = a.ix.state;
         const long long old = (long long)st->count;
         const long long cap = a.tgt.capacity;
         st->insert_old_count = (unsigned long long)old;
         if (old + total > cap) {
-            st->full_events += 1;
+            if (!a.ev.on) st->full_events += 1;  // with eviction: decided once victims are known
             st->count = (unsigned long long)cap;
         } else {
             st->count = (unsigned long long)(old + total);
+        }
+        if (a.ev.on) {
+            const long long want = total - (cap - old);
+            st->ev_new = (unsigned long long)total;
+            st->ev_want = want > 0 ? (unsigned long long)want : 0ull;
+            st->ev_all = 0;
+            st->ev_nv = 0;
+            st->sel_hi = 0;
+            st->sel_lo = 0;
+            st->sel_need = st->ev_want;
         }
     }
 }
@@ -268,15 +291,30 @@ __global__ __launch_bounds__(kThreads) void k_assign(InsertArgs a) {
     int64_t o0;
     const int32_t n = n_blocks(a.bat, r, a.ix.block_tokens, &o0);
     BatchEntry* __restrict__ tab = reinterpret_cast<BatchEntry*>(a.sc.table);
-    long long run = (long long)a.ix.state->insert_old_count + a.sc.base[r];
+    const long long old = (long long)a.ix.state->insert_old_count;
+    const long long fresh = a.tgt.capacity - old;                        // never-used ids
+    const long long nv = a.ev.on ? (long long)a.ix.state->ev_nv : 0;    // freed ids
+    long long run = a.sc.base[r];  // rank among the batch's new blocks
     for (int32_t w0 = a.sc.m0[r]; w0 < n; w0 += kWave) {
         const int32_t b = w0 + lane;
         BatchEntry* e = b < n ? &tab[a.sc.label[r * maxb + b]] : nullptr;
         const bool mine = e && e->owner == (int32_t)r;
         const unsigned long long mask = ballot64(mine);
         if (mine) {
-            const long long id = run + __popcll(mask & lanes_below(lane));
-            e->node_id = id < a.tgt.capacity ? (int32_t)id : -1;
+            const long long k = run + __popcll(mask & lanes_below(lane));
+            int32_t id = -1;
+            if (k < fresh)
+                id = (int32_t)(old + k);
+            else if (k - fresh < nv)
+                id = a.ev.victims[k - fresh];
+            e->node_id = id;
+            if (a.ev.on && id >= 0) {  // a new block starts unaccessed, with no resident child
+                a.ev.freq[id] = 0;
+                a.ev.prio[id] = 0;
+                a.ev.live[id] = 0;
+                a.ev.prot[id] = 0;
+                a.ev.depth[id] = b;
+            }
         }
         run += __popcll(mask);
     }
@@ -299,7 +337,7 @@ __global__ __launch_bounds__(kThreads) void k_publish(InsertArgs a) {
         if (b < m0 || b >= n) crow[b] = 0;
     int32_t carry = m0 == 0 ? -1 : row[m0 - 1];  // id of the block before the window
     int32_t m = n;                               // resident blocks after the call
-    unsigned long long cas = 0, fails = 0;
+    unsigned long long cas = 0, fails = 0, tombs_taken = 0;
     for (int32_t w0 = m0; w0 < n; w0 += kWave) {
         const int32_t b = w0 + lane;
         const bool valid = b < n;
@@ -333,11 +371,20 @@ __global__ __launch_bounds__(kThreads) void k_publish(InsertArgs a) {
         const uint64_t ik = index_key(a.sc.keys[r * maxb + b], *ht);
         uint64_t pos = slot_of(ik, ht->slot_seed, a.ix.slot_mask);
         Slot* slots = a.tgt.slots;
-        while (true) {
-            const unsigned long long prev = atomicCAS(
-                reinterpret_cast<unsigned long long*>(&slots[pos].key), kEmptyKey, (unsigned long long)ik);
+        // at most half the slots hold blocks and at most a quarter are
+        // deleted, so a free slot is always found
+        for (uint64_t step = 0; step <= a.ix.slot_mask; ++step) {
+            unsigned long long* kp = reinterpret_cast<unsigned long long*>(&slots[pos].key);
+            unsigned long long prev = atomicCAS(kp, kEmptyKey, (unsigned long long)ik);
             ++cas;
-            if (prev == kEmptyKey) {
+            bool got = prev == kEmptyKey;
+            if (!got && a.ev.on && prev == kTombKey) {
+                prev = atomicCAS(kp, kTombKey, (unsigned long long)ik);
+                ++cas;
+                got = prev == kTombKey;
+                tombs_taken += got ? 1 : 0;
+            }
+            if (got) {
                 slots[pos].id = id;
                 slots[pos].parent = parent;
                 break;
@@ -345,9 +392,15 @@ __global__ __launch_bounds__(kThreads) void k_publish(InsertArgs a) {
             ++fails;
             pos = (pos + 1) & a.ix.slot_mask;
         }
+        if (a.ev.on) {  // (the rest was reset by assign, before any child counts itself here)
+            a.ev.nkey[id] = ik;
+            a.ev.spos[id] = (uint32_t)pos;
+            if (parent >= 0) atomicAdd(&a.ev.live[parent], 1);
+        }
     }
     if (lane == 0) a.m_out[r] = m;
     count_cas(a, cas, fails, lane);
+    if (a.ev.on) wave_sub(&a.ix.state->tombstones, tombs_taken, lane);
 }
 
 }  // namespace
@@ -384,17 +437,20 @@ void insert_scratch_carve(void* base, int32_t R, int32_t max_blocks, InsertScrat
     out->collision = reinterpret_cast<unsigned int*>(p);
 }
 
-hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Batch& b,
-                         const InsertScratch& sc, int32_t* m_out, int32_t* ids, uint8_t* created,
-                         hipStream_t s) {
+hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                         const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+                         uint8_t* created, hipStream_t s) {
     hipError_t e;
-    if ((e = launch_lookup(ix, b, sc.m0, ids, s)) != hipSuccess) return e;
+    IndexView quiet = ix;  // the insert's own match is not an access
+    quiet.freq = nullptr;
+    quiet.prio = nullptr;
+    if ((e = launch_lookup(quiet, b, sc.m0, ids, s)) != hipSuccess) return e;
     if ((e = launch_hash_all(ix, b, sc.keys, s)) != hipSuccess) return e;
     const uint64_t tn = sc.table_mask + 1;
     const uint64_t cg = (tn + kThreads - 1) / kThreads;
     const unsigned cgrid = (unsigned)(cg < 65536 ? cg : 65536);
     BatchEntry* table = reinterpret_cast<BatchEntry*>(sc.table);
-    InsertArgs a{ix, tgt, b, sc, m_out, ids, created};
+    InsertArgs a{quiet, tgt, ev, b, sc, m_out, ids, created};
     const unsigned wgrid = (unsigned)((b.R + kWaves - 1) / kWaves);      // wave per request
     const unsigned tgrid = (unsigned)((b.R + kThreads - 1) / kThreads);  // thread per request
     hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 0);
@@ -411,10 +467,13 @@ hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Bat
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev.on && (e = launch_evict(quiet, tgt, ev, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_assign, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_publish, dim3(wgrid), dim3(kThreads), 0, s, a);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev.on) return launch_touch_paths(quiet, ev, m_out, ids, b.R, b.max_blocks, s);
+    return hipSuccess;
 }
 
 }  // namespace ptsd

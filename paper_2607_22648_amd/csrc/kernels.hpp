@@ -8,7 +8,8 @@
 
 namespace ptsd {
 
-// Read-only view of the store used by the lookup kernels.
+// View of the store used by the lookup kernels (read-only but for the
+// access counts).
 struct IndexView {
     const Slot* slots;
     uint64_t slot_mask;
@@ -16,8 +17,30 @@ struct IndexView {
     const int32_t* tokens;   // [capacity][block_tokens]
     const HashTables* ht;
     DevState* state;
+    uint64_t* freq;          // [capacity] access counts, or null: no accounting
+    uint64_t* prio;          // [capacity] priorities H = L + F
     int32_t block_tokens;
     int32_t counters;        // 1: count probes and comparisons
+};
+
+// Per-block eviction state and the scratch of the victim selection
+// (allocated with the store when eviction is on).
+struct EvictView {
+    uint64_t* freq;     // [capacity] F
+    uint64_t* prio;     // [capacity] H
+    int32_t* live;      // [capacity] children that hold an id
+    int32_t* prot;      // [capacity] last insert epoch whose batch matched the block
+    int32_t* depth;     // [capacity] 0 for a child of the root
+    uint64_t* nkey;     // [capacity] index key, to rebuild the index
+    uint32_t* spos;     // [capacity] index slot, to delete the entry
+    uint64_t* wmask;    // [words] victims of the running insert, one bit per id
+    uint32_t* wcnt;     // [words] victims per word
+    uint32_t* wbase;    // [words] exclusive scan of wcnt
+    int32_t* victims;   // [capacity] freed ids, ascending
+    uint32_t* hist;     // [kSelPasses][256] digit histograms
+    int64_t words;      // ceil(capacity / 64)
+    int32_t epoch;      // of the running insert, >= 1
+    int32_t on;         // 0: eviction disabled, nothing here is touched
 };
 
 struct Batch {
@@ -94,9 +117,17 @@ struct InsertTarget {
     int32_t* tokens;
     int64_t capacity;
 };
-hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Batch& b,
-                         const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                         const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
                          uint8_t* created, hipStream_t s);
+
+// evict.hip: victim selection and index maintenance of an insert (between
+// its id scan and its assignment), and the accesses of its resident paths
+// (after its publish).
+hipError_t launch_evict(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                        hipStream_t s);
+hipError_t launch_touch_paths(const IndexView& ix, const EvictView& ev, const int32_t* m,
+                              const int32_t* ids, int32_t R, int32_t max_blocks, hipStream_t s);
 
 // api.hip helpers
 hipError_t launch_fill_slots(Slot* slots, int64_t n, hipStream_t s);

@@ -14,6 +14,9 @@
 //      collide), it keeps probing for one with the right parent before the
 //      window is decided, so the answer never depends on the hash.
 // Windows are walked in order and the walk stops at the first miss.
+// With eviction on, every matched block counts one access: its frequency F
+// grows by one and its priority becomes max(H, L + F), which is L + F for
+// the final F whatever order the atomics land in.
 #include "kernels.hpp"
 
 namespace ptsd {
@@ -121,7 +124,9 @@ __device__ inline int32_t request_blocks(const Batch& b, int64_t r, int bt, int 
     return (int32_t)(n < b.max_blocks ? n : b.max_blocks);
 }
 
-template <int BT>
+// TOUCH: count accesses (eviction on); a variant of its own so that the
+// plain lookup keeps its register count.
+template <int BT, bool TOUCH>
 __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, int32_t* __restrict__ m_out,
                                                      int32_t* __restrict__ ids_out) {
     const int lane = threadIdx.x & (kWave - 1);
@@ -134,6 +139,7 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
     const int32_t* __restrict__ seq = bat.tokens + o0;
     int32_t* __restrict__ row = ids_out + r * bat.max_blocks;
 
+    const uint64_t clock = TOUCH ? ix.state->clock : 0;
     uint64_t carry_key = ht->root_key;
     int32_t carry_id = -1;  // the root
     int32_t m = 0;
@@ -177,6 +183,10 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
                                  &probes, &cmps);
         }
         if (active) row[b] = lane < first_bad ? cand : -1;
+        if (TOUCH && active && lane < first_bad) {
+            const uint64_t f = atomicAdd((unsigned long long*)&ix.freq[cand], 1ull) + 1ull;
+            atomicMax((unsigned long long*)&ix.prio[cand], (unsigned long long)(clock + f));
+        }
         if (first_bad < kWave) {
             m = w0 + first_bad;
             done = true;
@@ -234,10 +244,18 @@ __global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, 
 
 hipError_t launch_lookup(const IndexView& ix, const Batch& b, int32_t* m, int32_t* ids, hipStream_t s) {
     const unsigned grid = (unsigned)((b.R + kWavesPerGroup - 1) / kWavesPerGroup);
-    if (ix.block_tokens == 16)
-        hipLaunchKernelGGL(k_lookup<16>, dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
-    else
-        hipLaunchKernelGGL(k_lookup<0>, dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+    const bool touch = ix.freq != nullptr;
+    if (ix.block_tokens == 16) {
+        if (touch)
+            hipLaunchKernelGGL((k_lookup<16, true>), dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+        else
+            hipLaunchKernelGGL((k_lookup<16, false>), dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+    } else {
+        if (touch)
+            hipLaunchKernelGGL((k_lookup<0, true>), dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+        else
+            hipLaunchKernelGGL((k_lookup<0, false>), dim3(grid), dim3(kThreads), 0, s, ix, b, m, ids);
+    }
     return hipGetLastError();
 }
 

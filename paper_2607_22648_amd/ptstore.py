@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libptstore.so")
 
 PTSTORE_OK, PTSTORE_ERR_INVALID, PTSTORE_ERR_FULL, PTSTORE_ERR_HIP, PTSTORE_ERR_NOMEM = 0, 1, 2, 3, 4
 PTSTORE_FLAG_WEAK_HASH, PTSTORE_FLAG_COUNTERS, PTSTORE_FLAG_TIMING = 1, 2, 4
+PTSTORE_FLAG_EVICT = 8
 KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT, KIND_SELECT = 0, 1, 2, 3, 4
 
 
@@ -33,12 +34,13 @@ class ptstore_stats_t(C.Structure):
     _fields_ = [(n, C.c_int64) for n in (
         "blocks_stored", "capacity", "index_slots", "block_bytes", "chunk_bytes", "full_events",
         "bad_entries", "probes", "token_compares", "cas_attempts", "cas_failures",
-        "insert_fallbacks")]
+        "insert_fallbacks", "evictions", "clock", "index_rebuilds")]
 
 
 class ptstore_buffers_t(C.Structure):
     _fields_ = [("pool", C.c_void_p), ("parent", C.c_void_p), ("tokens", C.c_void_p),
-                ("slots", C.c_void_p), ("capacity", C.c_int64), ("index_slots", C.c_int64)]
+                ("slots", C.c_void_p), ("capacity", C.c_int64), ("index_slots", C.c_int64),
+                ("freq", C.c_void_p), ("prio", C.c_void_p)]
 
 
 class PTStoreError(RuntimeError):
@@ -327,6 +329,15 @@ class PrefixStore:
         tok = _wrap_device(b.tokens, b.capacity * self.shape.block_tokens, torch.int32)
         return par, tok.view(b.capacity, self.shape.block_tokens)
 
+    def evict_tensors(self) -> Tuple[torch.Tensor, torch.Tensor]:
+        """(access counts F, priorities H), each [capacity] int64, device, no copy
+        (the values are unsigned 64-bit; they stay far below 2^63)."""
+        b = self.buffers()
+        if not b.freq:
+            raise ValueError("store created without PTSTORE_FLAG_EVICT")
+        return (_wrap_device(b.freq, b.capacity, torch.int64),
+                _wrap_device(b.prio, b.capacity, torch.int64))
+
 
 class _CudaArray:
     def __init__(self, ptr: int, n: int, typestr: str):
@@ -335,5 +346,5 @@ class _CudaArray:
 
 
 def _wrap_device(ptr: int, n: int, dtype) -> torch.Tensor:
-    typestr = {torch.uint8: "|u1", torch.int32: "<i4"}[dtype]
+    typestr = {torch.uint8: "|u1", torch.int32: "<i4", torch.int64: "<i8"}[dtype]
     return torch.as_tensor(_CudaArray(ptr, n, typestr), device="cuda")

@@ -4,6 +4,7 @@ from __future__ import annotations
 import ctypes as C
 import os
 import re
+import subprocess
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "ptstore.h")
@@ -44,9 +45,27 @@ def test_strerror_without_gpu():
     assert lib.ptstore_strerror(1) == b"invalid argument"
 
 
-def test_config_struct_layout_matches_header():
-    """ctypes mirrors of the C structs have the sizes the header implies."""
+def _c_layout(tmp_path, struct, fields):
+    """sizeof and offsetof of `fields` in `struct`, as gcc lays out the header."""
+    lines = [f'printf("%zu\\n", sizeof({struct}));']
+    lines += [f'printf("%zu\\n", offsetof({struct}, {f}));' for f in fields]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stddef.h>\n#include <stdio.h>\n#include \"ptstore.h\"\n"
+                   "int main(void) {\n" + "\n".join(lines) + "\nreturn 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), "-o", str(exe), str(src)],
+                   check=True)
+    out = [int(x) for x in subprocess.run([str(exe)], check=True, capture_output=True,
+                                          text=True).stdout.split()]
+    return out[0], out[1:]
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """The ctypes mirrors have the size and field offsets gcc gives the C structs."""
     from paper_2607_22648_amd import ptstore as P
-    assert C.sizeof(P.ptstore_config_t) == 5 * 4 + 4 + 8 + 8 + 8 + 4 + 4  # incl. padding
-    assert C.sizeof(P.ptstore_stats_t) == 12 * 8
-    assert C.sizeof(P.ptstore_buffers_t) == 6 * 8
+    for cls, name in ((P.ptstore_config_t, "ptstore_config_t"), (P.ptstore_stats_t, "ptstore_stats_t"),
+                      (P.ptstore_buffers_t, "ptstore_buffers_t")):
+        fields = [f for f, _ in cls._fields_]
+        size, offs = _c_layout(tmp_path, name, fields)
+        assert C.sizeof(cls) == size, name
+        assert [getattr(cls, f).offset for f in fields] == offs, name

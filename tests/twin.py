@@ -13,7 +13,7 @@ import numpy as np
 import torch
 
 from oracle import OracleStore, ORC_ERR_FULL
-from paper_2607_22648_amd.ptstore import PrefixStore, StoreShape
+from paper_2607_22648_amd.ptstore import PrefixStore, StoreShape, PTSTORE_FLAG_EVICT
 
 DEV = torch.device("cuda:0")
 
@@ -39,7 +39,9 @@ class Twin:
         self.gpu = PrefixStore(self.shape, capacity, index_slots=index_slots, hash_seed=hash_seed,
                                flags=flags)
         cap = self.gpu.stats()["capacity"]
-        self.ref = OracleStore(layers, kv_heads, head_dim, block_tokens, elem_bytes, cap, payload)
+        self.evict = bool(flags & PTSTORE_FLAG_EVICT)
+        self.ref = OracleStore(layers, kv_heads, head_dim, block_tokens, elem_bytes, cap, payload,
+                               evict=self.evict)
         self.capacity = cap
         self.payload = payload
 
@@ -54,6 +56,7 @@ class Twin:
 
     # ---- operations -------------------------------------------------------
     def insert(self, tokens: np.ndarray, offsets: np.ndarray, max_blocks: int, check=True):
+        full0 = self.gpu.stats()["full_events"] if check else 0
         m, ids, created = self.gpu.insert(to_dev(tokens), to_dev(offsets), max_blocks)
         rc, rm, rids, rcr = self.ref.insert(tokens, offsets, max_blocks)
         if check:
@@ -63,8 +66,8 @@ class Twin:
             np.testing.assert_array_equal(host(created), rcr, err_msg="insert created")
             st = self.gpu.stats()
             assert st["blocks_stored"] == self.ref.count
-            if rc == ORC_ERR_FULL:
-                assert st["full_events"] > 0
+            # a full event exactly when the oracle refused a block
+            assert st["full_events"] - full0 == (1 if rc == ORC_ERR_FULL else 0)
         return (m, ids, created), (rc, rm, rids, rcr)
 
     def lookup(self, tokens, offsets, max_blocks, check=True):
@@ -122,3 +125,16 @@ class Twin:
             p, t = self.ref.node(i)
             assert par[i] == p, f"parent of {i}"
             np.testing.assert_array_equal(tok[i], t, err_msg=f"tokens of {i}")
+
+    def check_evict(self):
+        """Access counts, priorities, clock and eviction count equal the oracle's."""
+        torch.cuda.synchronize()
+        n = self.ref.count
+        f, h = self.gpu.evict_tensors()
+        f, h = host(f[:n]), host(h[:n])
+        exp = np.array([self.ref.node_stats(i)[:2] for i in range(n)], dtype=np.int64).reshape(n, 2)
+        np.testing.assert_array_equal(f, exp[:, 0], err_msg="access counts")
+        np.testing.assert_array_equal(h, exp[:, 1], err_msg="priorities")
+        st = self.gpu.stats()
+        assert st["clock"] == self.ref.clock, (st["clock"], self.ref.clock)
+        assert st["evictions"] == self.ref.evictions, (st["evictions"], self.ref.evictions)

@@ -285,7 +285,9 @@ class StreamWorkload:
     fresh tokens to the request length, else passage + fresh question.
     Inserts: a stored sequence (Zipf by passage, then uniform among the
     sequences grown from it) cut at a uniform block depth d >= 1, extended
-    with 1 or 2 fresh blocks; with probability 1/4 an exact repeat of an
+    with ``fresh_blocks`` = (lo, hi) fresh blocks, uniform in lo..hi (1 or 2
+    by default; 32, a 512-token question, in the reading where every insert
+    stores a whole question); with probability 1/4 an exact repeat of an
     earlier insert.
     """
 
@@ -297,7 +299,8 @@ class StreamWorkload:
 
 def make_stream_workload(base: PassageWorkload, n_rounds: int = 100, per_round: int = 128,
                          pool_blocks: int = 76293, seed: int = 4321,
-                         repeat_p: float = 0.25, history_p: float = 0.5) -> StreamWorkload:
+                         repeat_p: float = 0.25, history_p: float = 0.5,
+                         fresh_blocks: Tuple[int, int] = (1, 2)) -> StreamWorkload:
     rng = np.random.default_rng(seed)
     bt = base.shape.block_tokens
     req_len = int(np.diff(base.offsets).max())
@@ -330,7 +333,7 @@ def make_stream_workload(base: PassageWorkload, n_rounds: int = 100, per_round: 
             src = cands[int(rng.integers(len(cands)))]
             nb = len(src) // bt
             d = int(rng.integers(1, nb + 1))
-            k = int(rng.integers(1, 3))
+            k = int(rng.integers(fresh_blocks[0], fresh_blocks[1] + 1))
             s = np.concatenate([src[: d * bt], _fresh(rng, k * bt)])
             branches.setdefault(p, []).append(s)
             history.append(s)
@@ -396,6 +399,10 @@ CONFIGS = {
     # 160 GB (76,293 blocks of 2 MiB).
     "stream": dict(kind="stream", base="llama8b", n_rounds=100, per_round=128,
                    pool_blocks=76293),
+    # the same with every insert storing a 512-token question (32 fresh
+    # blocks): the pool fills within a few rounds and the store must evict.
+    "stream_evict": dict(kind="stream", base="llama8b", n_rounds=100, per_round=128,
+                         pool_blocks=76293, fresh_blocks=(32, 32)),
 }
 
 
