@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama8b",
-                    choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream"])
+                    choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream", "stream_evict"])
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="requests the CPU oracle is timed on (0: skip; -1: the whole batch, "
                          "8 requests for the 70B-shaped shard)")
@@ -215,6 +215,9 @@ WORKLOAD_TEXT = {
             "blocks, 1 x 8 x 128 fp16 KV",
     "stream": "llama8b-shaped store, rounds of 128 lookups+gathers and 128 dedup inserts + "
               "scatter, 160 GB pool",
+    "stream_evict": "llama8b-shaped store, rounds of 128 lookups+gathers and 128 dedup inserts "
+                    "of 512-token questions + scatter, 160 GB pool with frequency-based leaf "
+                    "eviction",
 }
 
 
@@ -420,11 +423,13 @@ def run_trie(args, torch, P, synth, dev):
 
 
 def run_stream(args, torch, P, synth, dev):
-    sw = synth.build("stream", seed=args.seed)
+    sw = synth.build(args.config, seed=args.seed)
     base = sw.base
     sh = base.shape
     shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
-    store = P.PrefixStore(shape, sw.pool_blocks, flags=P.PTSTORE_FLAG_TIMING)
+    evict = args.config == "stream_evict"
+    flags = P.PTSTORE_FLAG_TIMING | (P.PTSTORE_FLAG_EVICT if evict else 0)
+    store = P.PrefixStore(shape, sw.pool_blocks, flags=flags)
     pre = prefill(store, base, dev, torch, batch_passages=32)
     maxb = base.max_blocks
     per = len(sw.rounds[0].lookup_offsets) - 1
@@ -451,7 +456,7 @@ def run_stream(args, torch, P, synth, dev):
     for i in range(args.warmup):
         one_round(i, False)
     torch.cuda.synchronize()
-    for k in (P.KIND_GATHER, P.KIND_LOOKUP, P.KIND_INSERT, P.KIND_SCATTER):
+    for k in (P.KIND_GATHER, P.KIND_LOOKUP, P.KIND_INSERT, P.KIND_SCATTER, P.KIND_EVICT):
         store.kernel_times(k)
     blocks0 = store.stats()["blocks_stored"]
     keep = []
@@ -463,8 +468,9 @@ def run_stream(args, torch, P, synth, dev):
     elapsed = time.perf_counter() - t0
     matched = int(sum(int(a.item()) for a, _ in keep))
     created = int(sum(int(b.item()) for _, b in keep))
-    t = {k: store.kernel_times(v) for k, v in (("gather", P.KIND_GATHER), ("lookup", P.KIND_LOOKUP),
-                                               ("insert", P.KIND_INSERT), ("scatter", P.KIND_SCATTER))}
+    kinds = [("gather", P.KIND_GATHER), ("lookup", P.KIND_LOOKUP), ("insert", P.KIND_INSERT),
+             ("scatter", P.KIND_SCATTER)] + ([("evict (part of insert)", P.KIND_EVICT)] if evict else [])
+    t = {k: store.kernel_times(v) for k, v in kinds}
     st = store.stats()
     store.close()
     del cache
@@ -472,7 +478,7 @@ def run_stream(args, torch, P, synth, dev):
     g_ms, g_n = t["gather"]
     ms_round = elapsed * 1e3 / n_timed
     out = base_line(args, per * n_timed / elapsed, "requests/s", ms_round, {
-        "workload": WORKLOAD_TEXT["stream"], "lookups_per_round": per, "inserts_per_round": per,
+        "workload": WORKLOAD_TEXT[args.config], "lookups_per_round": per, "inserts_per_round": per,
         "timed_rounds": n_timed, "pool_blocks": sw.pool_blocks, "block_bytes": sh.block_bytes})
     out["steps"] = n_timed
     out.update({
@@ -480,7 +486,9 @@ def run_stream(args, torch, P, synth, dev):
         "matched_blocks": matched, "created_blocks": created,
         "blocks_stored": {"before": blocks0, "after": st["blocks_stored"]},
         "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
-                             g_ms / max(g_n, 1), g_n, recorded_traffic("stream")),
+                             g_ms / max(g_n, 1), g_n, recorded_traffic(args.config)),
+        "evictions": st["evictions"], "index_rebuilds": st["index_rebuilds"],
+        "full_events": st["full_events"],
         "kernel_ms_per_round": {k: round(v[0] / n_timed, 4) for k, v in t.items()},
         "scatter_GBps": round(created * 2 * sh.block_bytes / (t["scatter"][0] * 1e6), 1)
         if t["scatter"][0] else None,
@@ -504,7 +512,7 @@ def main():
     torch.cuda.set_device(dev)
     if args.config == "trie":
         out = run_trie(args, torch, P, synth, dev)
-    elif args.config == "stream":
+    elif args.config in ("stream", "stream_evict"):
         out = run_stream(args, torch, P, synth, dev)
     else:
         out = run_passage(args, torch, P, synth, dev)

@@ -229,7 +229,8 @@ int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
  * durations (ms) and launch counts of the kernels recorded since the last
  * call, for kind 0 = gather copy kernel, 1 = lookup, 2 = scatter copy
  * kernel, 3 = insert (all its kernels), 4 = descriptor-list build of gather
- * and scatter. Resets the records of that kind. At most 65,536 launches
+ * and scatter, 5 = the eviction part of an insert (PTSTORE_FLAG_EVICT;
+ * included in kind 3). Resets the records of that kind. At most 65,536 launches
  * per kind are recorded between two calls.
  */
 int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64_t *launches);

@@ -46,7 +46,7 @@ struct ptstore {
     EvictView evs;  // evs.on = 0 without PTSTORE_FLAG_EVICT
     void* ev_mem;  // one allocation holding every ev array
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[5];
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[6];
     std::vector<hipEvent_t> free_ev;
 };
 
@@ -220,7 +220,8 @@ size_t carve_evict(void* base, int64_t capacity, EvictView* ev) {
     ev->wmask = static_cast<uint64_t*>(take(words * 8));
     ev->wcnt = static_cast<uint32_t*>(take(words * 4));
     ev->wbase = static_cast<uint32_t*>(take(words * 4));
-    ev->hist = static_cast<uint32_t*>(take(kSelPasses * 256 * 4));
+    ev->hist = static_cast<uint32_t*>(take((size_t)kSelPasses * kSelBins * 4));
+    ev->part = static_cast<uint64_t*>(take((size_t)kSelGroups * 8 * 8));
     ev->words = words;
     return off;
 }
@@ -450,7 +451,13 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     }
     {
         Timed t(s, 3, st);
-        e = launch_insert(index_view(s), tgt, s->evs, b, sc, m_out, ids, created, st);
+        const IndexView ix = index_view(s);
+        e = launch_insert_match(ix, tgt, s->evs, b, sc, m_out, ids, created, st);
+        if (e == hipSuccess && s->evs.on) {
+            Timed te(s, 5, st);
+            e = launch_evict(ix, tgt, s->evs, st);
+        }
+        if (e == hipSuccess) e = launch_insert_commit(ix, tgt, s->evs, b, sc, m_out, ids, created, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_insert: launch", e);
 }
@@ -551,7 +558,7 @@ int ptstore_get_buffers(ptstore_t* s, ptstore_buffers_t* out) {
 }
 
 int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* launches) {
-    if (!s || kind < 0 || kind > 4 || !total_ms || !launches)
+    if (!s || kind < 0 || kind > 5 || !total_ms || !launches)
         return fail(PTSTORE_ERR_INVALID, "ptstore_kernel_times: bad argument");
     int rc = set_device(s);
     if (rc) return rc;

@@ -52,8 +52,11 @@ struct alignas(128) CounterSlot {
     unsigned long long pad[12];
 };
 
-// Digit passes of the eviction threshold search: 8 bits of a 128-bit key each.
-constexpr int kSelPasses = 16;
+// Eviction threshold search: at most this many digit passes of kSelBits bits
+// each over a key of at most 128 bits.
+constexpr int kSelBits = 11;
+constexpr int kSelBins = 1 << kSelBits;
+constexpr int kSelPasses = (128 + kSelBits - 1) / kSelBits;
 
 // Device-side counters and status of a store.
 struct DevState {
@@ -73,9 +76,14 @@ struct DevState {
     unsigned long long ev_all;        // 1: every candidate goes (no more than ev_want)
     unsigned long long ev_nv;         // blocks evicted
     unsigned long long ev_rebuild;    // 1: rebuild the index in this insert
-    unsigned long long sel_hi, sel_lo;  // threshold key found so far
+    // key layout: only the bits in which candidates differ are kept
+    unsigned long long sel_pmin, sel_dmax, sel_imin;  // smallest H, largest depth, smallest id
+    unsigned int sel_wd, sel_wi;        // bit widths of the depth and id fields
+    unsigned int sel_w, sel_npass;      // key width, digit passes it needs
+    unsigned long long sel_hi, sel_lo;  // threshold key found so far (left-aligned)
     unsigned long long sel_need;        // rank of the threshold among what matches it
-    unsigned int sel_done[kSelPasses];  // workgroups finished per pass
+    unsigned int sel_range_done;        // workgroups finished the range pass
+    unsigned int sel_done[kSelPasses];  // workgroups finished per digit pass
     CounterSlot slot[kCounterSlots];
 };
 

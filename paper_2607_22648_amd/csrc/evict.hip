@@ -17,9 +17,13 @@
 //   the one-at-a-time walk takes exactly the first `want` of them in that
 //   order.
 //
-// So the victims are the `want` smallest 128-bit keys (H, 2^31-1-depth, id)
-// among the unmatched blocks, found by a radix select: 16 passes, each a
-// 256-bin histogram of the next 8-bit digit among the keys that agree with
+// So the victims are the `want` smallest keys (H, depth descending, id)
+// among the unmatched blocks, found by a radix select. A range pass first
+// takes the minimum and maximum of each field over the candidates; the key
+// then keeps only the bits in which candidates can differ,
+//   (H - Hmin) | (depth_max - depth) | (id - id_min),
+// left-aligned in 128 bits (typically some 40 bits wide). Each digit pass
+// is a 2048-bin histogram of the next 11 bits among the keys that agree with
 // the threshold found so far; the last workgroup of a pass to finish picks
 // the digit. Then the victims are marked in a bit mask, their index slots
 // become tombstones, their parents lose a child, L takes their largest H,
@@ -33,76 +37,168 @@ namespace {
 
 constexpr int kThreads = 256;
 
-__device__ inline void evict_key(const EvictView& ev, int64_t id, uint64_t* hi, uint64_t* lo) {
-    *hi = ev.prio[id];
-    *lo = ((uint64_t)(uint32_t)(0x7FFFFFFF - ev.depth[id]) << 32) | (uint32_t)id;
+typedef unsigned __int128 u128;
+
+__device__ inline unsigned bit_width(uint64_t x) { return x ? 64u - (unsigned)__clzll((long long)x) : 0u; }
+
+// The candidate's compressed key, left-aligned in 128 bits (state written by
+// the range pass).
+__device__ inline u128 sel_key(const EvictView& ev, const DevState* st, int64_t id) {
+    const u128 p = (u128)(ev.prio[id] - st->sel_pmin);
+    const u128 d = (u128)(st->sel_dmax - (uint64_t)ev.depth[id]);
+    const u128 i = (u128)((uint64_t)id - st->sel_imin);
+    const unsigned wd = st->sel_wd, wi = st->sel_wi, w = st->sel_w;
+    const u128 c = (p << (wd + wi)) | (d << wi) | i;
+    return w == 0 ? (u128)0 : c << (128u - w);
 }
 
 __device__ inline unsigned long long lanes_below(int lane) {
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// One digit pass of the threshold search.
-__global__ __launch_bounds__(kThreads) void k_sel_pass(EvictView ev, DevState* st, int pass) {
-    if (st->ev_want == 0 || st->ev_all) return;  // uniform over the grid
-    __shared__ unsigned int h[256];
-    __shared__ int last;
-    const int t = threadIdx.x;
-    h[t] = 0;
-    __syncthreads();
+template <typename T, typename Op>
+__device__ inline T wave_reduce(T v, Op op, int lane) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v = op(v, (T)shfl_u64((uint64_t)v, lane ^ d));
+    return v;
+}
+
+// Ranges of H, depth and id over the candidates, their number, and from them
+// the key layout. Also clears the digit histograms. Each workgroup writes its
+// own partial (no shared-address atomics); the last one to finish combines
+// them.
+__global__ __launch_bounds__(kThreads) void k_sel_range(EvictView ev, DevState* st) {
+    if (st->ev_want == 0) return;  // uniform over the grid
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < (int64_t)kSelPasses * kSelBins;
+         i += (int64_t)gridDim.x * kThreads)
+        ev.hist[i] = 0;
     const int64_t old = (int64_t)st->insert_old_count;
-    const uint64_t phi = st->sel_hi, plo = st->sel_lo;
-    // bits above the digit must equal the threshold's
-    const int word = pass < 8 ? 0 : 1;
-    const int sh = 56 - 8 * (pass & 7);
-    const uint64_t above = (pass & 7) == 0 ? 0ull : (~0ull << (sh + 8));
-    for (int64_t id = (int64_t)blockIdx.x * kThreads + t; id < old; id += (int64_t)gridDim.x * kThreads) {
+    // [0] min H, [1] -max H, [2] min depth, [3] -max depth, [4] min id, [5] -max id: all minima
+    uint64_t v[6] = {~0ull, ~0ull, ~0ull, ~0ull, ~0ull, ~0ull};
+    uint64_t n = 0;
+    for (int64_t id = (int64_t)blockIdx.x * kThreads + threadIdx.x; id < old;
+         id += (int64_t)gridDim.x * kThreads) {
         if (ev.prot[id] == ev.epoch) continue;
-        uint64_t hi, lo;
-        evict_key(ev, id, &hi, &lo);
-        bool match;
-        unsigned digit;
-        if (word == 0) {
-            match = (hi & above) == (phi & above);
-            digit = (unsigned)(hi >> sh) & 255u;
-        } else {
-            match = hi == phi && (lo & above) == (plo & above);
-            digit = (unsigned)(lo >> sh) & 255u;
-        }
-        if (match) atomicAdd(&h[digit], 1u);
+        const uint64_t x[6] = {ev.prio[id], ~ev.prio[id], (uint64_t)ev.depth[id], ~(uint64_t)ev.depth[id],
+                               (uint64_t)id, ~(uint64_t)id};
+#pragma unroll
+        for (int k = 0; k < 6; ++k) v[k] = x[k] < v[k] ? x[k] : v[k];
+        ++n;
+    }
+    auto mn = [](uint64_t a, uint64_t b) { return a < b ? a : b; };
+    auto sum = [](uint64_t a, uint64_t b) { return a + b; };
+    __shared__ uint64_t red[kThreads / kWave][8];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) v[k] = wave_reduce(v[k], mn, lane);
+    n = wave_reduce(n, sum, lane);
+    if (lane == 0) {
+        for (int k = 0; k < 6; ++k) red[wv][k] = v[k];
+        red[wv][6] = n;
     }
     __syncthreads();
-    uint32_t* gh = ev.hist + pass * 256;
-    if (h[t]) atomicAdd(&gh[t], h[t]);
+    if (threadIdx.x < 7) {
+        const int k = threadIdx.x;
+        uint64_t a = red[0][k];
+        for (int w = 1; w < kThreads / kWave; ++w) a = k < 6 ? mn(a, red[w][k]) : a + red[w][k];
+        ev.part[(int64_t)blockIdx.x * 8 + k] = a;
+    }
+    __shared__ int last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) last = atomicAdd(&st->sel_range_done, 1u) == gridDim.x - 1;
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    // last workgroup: combine the partials (one wave per field)
+    __shared__ uint64_t tot[8];
+    for (int k = wv; k < 7; k += kThreads / kWave) {
+        uint64_t a = k < 6 ? ~0ull : 0ull;
+        for (int64_t g = lane; g < gridDim.x; g += kWave) {
+            const uint64_t x = __hip_atomic_load(&ev.part[g * 8 + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            a = k < 6 ? mn(a, x) : a + x;
+        }
+        a = k < 6 ? wave_reduce(a, mn, lane) : wave_reduce(a, sum, lane);
+        if (lane == 0) tot[k] = a;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    if (tot[6] <= st->ev_want) {  // every candidate goes
+        st->ev_all = 1;
+        return;
+    }
+    const uint64_t pmin = tot[0], pmax = ~tot[1], dmin = tot[2], dmax = ~tot[3], imin = tot[4],
+                   imax = ~tot[5];
+    const unsigned wp = bit_width(pmax - pmin), wd = bit_width(dmax - dmin), wi = bit_width(imax - imin);
+    st->sel_pmin = pmin;
+    st->sel_dmax = dmax;
+    st->sel_imin = imin;
+    st->sel_wd = wd;
+    st->sel_wi = wi;
+    st->sel_w = wp + wd + wi;  // <= 64 + 31 + 31
+    st->sel_npass = (wp + wd + wi + kSelBits - 1) / kSelBits;
+}
+
+// One digit pass of the threshold search.
+__global__ __launch_bounds__(kThreads) void k_sel_pass(EvictView ev, DevState* st, int pass) {
+    if (st->ev_want == 0 || st->ev_all || (unsigned)pass >= st->sel_npass) return;  // uniform
+    __shared__ unsigned int h[kSelBins];
+    __shared__ unsigned int part[kThreads];
+    __shared__ int last;
+    const int t = threadIdx.x;
+    for (int b = t; b < kSelBins; b += kThreads) h[b] = 0;
+    __syncthreads();
+    const int64_t old = (int64_t)st->insert_old_count;
+    const u128 thr = ((u128)st->sel_hi << 64) | (u128)st->sel_lo;
+    const int hi_bit = 128 - kSelBits * pass;          // digit = key bits [lo_bit, hi_bit)
+    const int lo_bit = hi_bit - kSelBits > 0 ? hi_bit - kSelBits : 0;
+    const unsigned dmask = (1u << (hi_bit - lo_bit)) - 1u;
+    for (int64_t id = (int64_t)blockIdx.x * kThreads + t; id < old; id += (int64_t)gridDim.x * kThreads) {
+        if (ev.prot[id] == ev.epoch) continue;
+        const u128 k = sel_key(ev, st, id);
+        if (pass > 0 && (k >> hi_bit) != (thr >> hi_bit)) continue;
+        atomicAdd(&h[(unsigned)(k >> lo_bit) & dmask], 1u);
+    }
+    __syncthreads();
+    uint32_t* gh = ev.hist + pass * kSelBins;
+    for (int b = t; b < kSelBins; b += kThreads)
+        if (h[b]) atomicAdd(&gh[b], h[b]);
     __threadfence();
     __syncthreads();
     if (t == 0) last = atomicAdd(&st->sel_done[pass], 1u) == gridDim.x - 1;
     __syncthreads();
     if (!last) return;
     __threadfence();
-    h[t] = __hip_atomic_load(&gh[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // last workgroup: the digit whose bin holds the need-th smallest key
+    constexpr int kPer = kSelBins / kThreads;
+    unsigned own = 0;
+    for (int j = 0; j < kPer; ++j) {
+        h[t * kPer + j] = __hip_atomic_load(&gh[t * kPer + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        own += h[t * kPer + j];
+    }
+    part[t] = own;
     __syncthreads();
-    if (t != 0) return;
-    const uint64_t want = st->ev_want;
-    if (pass == 0) {
-        uint64_t total = 0;
-        for (int d = 0; d < 256; ++d) total += h[d];
-        if (total <= want) {  // every candidate goes
-            st->ev_all = 1;
-            return;
+    for (int d = 1; d < kThreads; d <<= 1) {  // inclusive scan of the per-thread sums
+        const unsigned v = t >= d ? part[t - d] : 0u;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    const uint64_t need = st->sel_need;
+    const uint64_t before = part[t] - own;
+    if (before < need && need <= part[t]) {  // exactly one thread
+        uint64_t cum = before;
+        int j = 0;
+        for (; j < kPer - 1; ++j) {
+            if (cum + h[t * kPer + j] >= need) break;
+            cum += h[t * kPer + j];
         }
+        const unsigned digit = (unsigned)(t * kPer + j);
+        const u128 nt = thr | ((u128)digit << lo_bit);
+        st->sel_need = need - cum;
+        st->sel_hi = (uint64_t)(nt >> 64);
+        st->sel_lo = (uint64_t)nt;
     }
-    uint64_t need = st->sel_need, cum = 0;
-    int d = 0;
-    for (; d < 255; ++d) {
-        if (cum + h[d] >= need) break;
-        cum += h[d];
-    }
-    st->sel_need = need - cum;
-    if (word == 0)
-        st->sel_hi = phi | ((uint64_t)d << sh);
-    else
-        st->sel_lo = plo | ((uint64_t)d << sh);
 }
 
 // Marks the victims (one bit per id), deletes their index entries, takes a
@@ -112,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void k_ev_mark(EvictView ev, DevState* st
     if (st->ev_want == 0) return;
     const int lane = threadIdx.x & (kWave - 1);
     const bool all = st->ev_all != 0;
-    const uint64_t thi = st->sel_hi, tlo = st->sel_lo;
+    const u128 thr = ((u128)st->sel_hi << 64) | (u128)st->sel_lo;
     const int64_t old = (int64_t)st->insert_old_count;
     const int64_t span = ev.words * kWave;
     uint64_t maxp = 0;
@@ -120,11 +216,10 @@ __global__ __launch_bounds__(kThreads) void k_ev_mark(EvictView ev, DevState* st
         const int64_t id = base + threadIdx.x;
         bool sel = false;
         if (id < old && ev.prot[id] != ev.epoch) {
-            uint64_t hi, lo;
-            evict_key(ev, id, &hi, &lo);
-            sel = all || hi < thi || (hi == thi && lo <= tlo);
+            sel = all || sel_key(ev, st, id) <= thr;
             if (sel) {
-                maxp = hi > maxp ? hi : maxp;
+                const uint64_t hp = ev.prio[id];
+                maxp = hp > maxp ? hp : maxp;
                 slots[ev.spos[id]].key = kTombKey;
                 const int32_t p = parent[id];
                 if (p >= 0) atomicSub(&ev.live[p], 1);
@@ -270,7 +365,10 @@ unsigned grid_for(int64_t n, int64_t cap_groups) {
 hipError_t launch_evict(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
                         hipStream_t s) {
     hipError_t e;
-    const unsigned g = grid_for(tgt.capacity, 2048);
+    // about four candidates per thread: few workgroups add to the same bins
+    const unsigned g = grid_for((tgt.capacity + 3) / 4, kSelGroups);
+    hipLaunchKernelGGL(k_sel_range, dim3(g), dim3(kThreads), 0, s, ev, ix.state);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     for (int p = 0; p < kSelPasses; ++p) {
         hipLaunchKernelGGL(k_sel_pass, dim3(g), dim3(kThreads), 0, s, ev, ix.state, p);
         if ((e = hipGetLastError()) != hipSuccess) return e;

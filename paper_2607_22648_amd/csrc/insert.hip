@@ -255,10 +255,7 @@ __global__ __launch_bounds__(1024) void k_scan(InsertArgs a) {
         run += a.sc.cnt[i];
     }
     DevState* st = a.ix.state;
-    if (a.ev.on) {  // fresh selection state for evict.hip
-        for (int i = t; i < kSelPasses * 256; i += nt) a.ev.hist[i] = 0;
-        if (t < kSelPasses) st->sel_done[t] = 0;
-    }
+    if (a.ev.on && t < kSelPasses) st->sel_done[t] = 0;  // fresh selection state for evict.hip
     if (t == nt - 1) {
         const long long total = part[nt - 1];
         const long long old = (long long)st->count;
@@ -276,6 +273,8 @@ __global__ __launch_bounds__(1024) void k_scan(InsertArgs a) {
             st->ev_want = want > 0 ? (unsigned long long)want : 0ull;
             st->ev_all = 0;
             st->ev_nv = 0;
+            st->sel_range_done = 0;
+            st->sel_npass = 0;
             st->sel_hi = 0;
             st->sel_lo = 0;
             st->sel_need = st->ev_want;
@@ -437,9 +436,9 @@ void insert_scratch_carve(void* base, int32_t R, int32_t max_blocks, InsertScrat
     out->collision = reinterpret_cast<unsigned int*>(p);
 }
 
-hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
-                         const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
-                         uint8_t* created, hipStream_t s) {
+hipError_t launch_insert_match(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                               const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+                               uint8_t* created, hipStream_t s) {
     hipError_t e;
     IndexView quiet = ix;  // the insert's own match is not an access
     quiet.freq = nullptr;
@@ -466,8 +465,18 @@ hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const Evi
     hipLaunchKernelGGL(k_count, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (ev.on && (e = launch_evict(quiet, tgt, ev, s)) != hipSuccess) return e;
+    return hipGetLastError();
+}
+
+hipError_t launch_insert_commit(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                                const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+                                uint8_t* created, hipStream_t s) {
+    hipError_t e;
+    IndexView quiet = ix;
+    quiet.freq = nullptr;
+    quiet.prio = nullptr;
+    InsertArgs a{quiet, tgt, ev, b, sc, m_out, ids, created};
+    const unsigned wgrid = (unsigned)((b.R + kWaves - 1) / kWaves);
     hipLaunchKernelGGL(k_assign, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_publish, dim3(wgrid), dim3(kThreads), 0, s, a);

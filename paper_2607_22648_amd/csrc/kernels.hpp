@@ -23,6 +23,9 @@ struct IndexView {
     int32_t counters;        // 1: count probes and comparisons
 };
 
+// Most workgroups of a selection pass.
+constexpr int kSelGroups = 256;
+
 // Per-block eviction state and the scratch of the victim selection
 // (allocated with the store when eviction is on).
 struct EvictView {
@@ -37,7 +40,8 @@ struct EvictView {
     uint32_t* wcnt;     // [words] victims per word
     uint32_t* wbase;    // [words] exclusive scan of wcnt
     int32_t* victims;   // [capacity] freed ids, ascending
-    uint32_t* hist;     // [kSelPasses][256] digit histograms
+    uint32_t* hist;     // [kSelPasses][kSelBins] digit histograms
+    uint64_t* part;     // [kSelGroups][8] per-workgroup partials of the range pass
     int64_t words;      // ceil(capacity / 64)
     int32_t epoch;      // of the running insert, >= 1
     int32_t on;         // 0: eviction disabled, nothing here is touched
@@ -117,13 +121,18 @@ struct InsertTarget {
     int32_t* tokens;
     int64_t capacity;
 };
-hipError_t launch_insert(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
-                         const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
-                         uint8_t* created, hipStream_t s);
+// An insert is enqueued in three parts: match (lookup .. id scan), then,
+// with eviction on, launch_evict, then commit (assign, publish, accesses).
+hipError_t launch_insert_match(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                               const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+                               uint8_t* created, hipStream_t s);
+hipError_t launch_insert_commit(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
+                                const Batch& b, const InsertScratch& sc, int32_t* m_out, int32_t* ids,
+                                uint8_t* created, hipStream_t s);
 
 // evict.hip: victim selection and index maintenance of an insert (between
-// its id scan and its assignment), and the accesses of its resident paths
-// (after its publish).
+// its match and its commit), and the accesses of its resident paths (at the
+// end of its commit).
 hipError_t launch_evict(const IndexView& ix, const InsertTarget& tgt, const EvictView& ev,
                         hipStream_t s);
 hipError_t launch_touch_paths(const IndexView& ix, const EvictView& ev, const int32_t* m,

@@ -130,10 +130,20 @@ def lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec=None):
     return m_h, seen
 
 
-def _passage_store(w, capacity, batch, rec):
+def check_access_counts(store, ref):
+    """Access counts and priorities of every block equal the oracle's."""
+    torch.cuda.synchronize()
+    n = ref.count
+    f, h = store.evict_tensors()
+    exp = np.array([ref.node_stats(i)[:2] for i in range(n)], dtype=np.int64).reshape(n, 2)
+    np.testing.assert_array_equal(host(f[:n]), exp[:, 0])
+    np.testing.assert_array_equal(host(h[:n]), exp[:, 1])
+
+
+def _passage_store(w, capacity, batch, rec, evict=False):
     kv = w.shape
-    store = P.PrefixStore(_shape(kv), capacity)
-    ref = OracleStore.for_shape(kv, capacity, with_payload=False)
+    store = P.PrefixStore(_shape(kv), capacity, flags=P.PTSTORE_FLAG_EVICT if evict else 0)
+    ref = OracleStore.for_shape(kv, capacity, with_payload=False, evict=evict)
     st, so = w.store_batch()
     Rs = len(so) - 1
     for lo in range(0, Rs, batch):
@@ -207,12 +217,17 @@ def test_trie_full():
     _free(store, ref)
 
 
-def test_stream_full():
-    sw = synth.build("stream")
+@pytest.mark.parametrize("name,rounds", [("stream", None), ("stream_evict", 14)])
+def test_stream_full(name, rounds):
+    """100 rounds of the stream on the 160 GB pool; with eviction, 14 rounds (the
+    pool fills in the sixth; the oracle's one-leaf-at-a-time eviction is slow)."""
+    over = {} if rounds is None else {"n_rounds": rounds}
+    sw = synth.build(name, **over)
+    evict = name == "stream_evict"
     base = sw.base
     kv = base.shape
     rec = Recorder(kv, 64, 4)
-    store, ref = _passage_store(base, sw.pool_blocks, 32, rec)
+    store, ref = _passage_store(base, sw.pool_blocks, 32, rec, evict=evict)
     maxb = base.max_blocks
     per = len(sw.rounds[0].lookup_offsets) - 1
     cache = torch.empty(kv.layers * 2 * per * maxb * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
@@ -243,9 +258,16 @@ def test_stream_full():
             sel_ids = to_dev(ids_h[cr_h != 0].astype(np.int64))
             sel_bt = to_dev(bt_h[cr_h != 0].astype(np.int64))
             assert torch.equal(cv[:, :, sel_bt], pv[sel_ids].permute(1, 2, 0, 3))
+            for reused in ids_h[cr_h != 0].tolist():  # an evicted id now holds another block
+                rec.bytes.pop(int(reused), None)
             rec.take(cache, nb_cache, ids_h, cr_h, bt_h, 1)
+        if evict and (i % 4 == 3 or i == len(sw.rounds) - 1):
+            check_access_counts(store, ref)
     assert store.stats()["blocks_stored"] == ref.count
     assert ref.count > len(base.stored) * base.passage_blocks
     assert seen > 0
+    if evict:
+        st = store.stats()
+        assert st["evictions"] == ref.evictions > 0 and st["clock"] == ref.clock
     del cache
     _free(store, ref)
