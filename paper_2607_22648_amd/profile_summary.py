@@ -1,7 +1,9 @@
 """Summarise rocprofv3 output of bench.py into short text notes under profiles/.
 
 Inputs (directories written by rocprofv3 ``--output-format csv``):
-  --trace DIR   a ``--kernel-trace --stats`` run (uses *_kernel_stats.csv)
+  --trace DIR   a ``--kernel-trace --stats`` run (uses *_kernel_stats.csv);
+                alone (with --trace-bench), only the per-kernel table of the
+                store's own kernels is written
   --fetch DIR   a ``--pmc FETCH_SIZE`` run (uses *_counter_collection.csv)
   --write DIR   a ``--pmc WRITE_SIZE`` run
   --bench FILE  the JSON line bench.py printed in the counter runs
@@ -70,14 +72,16 @@ def plain_copy_value(vals):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
-    ap.add_argument("--bench", required=True, help="bench.py JSON line of a counter run")
+    ap.add_argument("--fetch", default=None)
+    ap.add_argument("--write", default=None)
+    ap.add_argument("--bench", default=None, help="bench.py JSON line of a counter run")
     ap.add_argument("--trace-bench", default=None, help="bench.py JSON line of the trace run")
     ap.add_argument("--out", default=os.path.join(os.path.dirname(HERE), "profiles"))
     ap.add_argument("--name", default="gather_llama8b")
     ap.add_argument("--cmd", required=True, help="the command that produced the inputs")
     a = ap.parse_args()
+    if not (a.fetch and a.write and a.bench):
+        return store_kernels_only(a)
 
     bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
     algo = bench["roofline"]["bytes_per_launch"]
@@ -142,6 +146,33 @@ def main():
     with open(os.path.join(a.out, f"{a.name}_hbm_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(rec))
+
+
+def store_kernels_only(a):
+    """Per-kernel table of every store kernel in a trace run, plus the
+    per-round kernel times bench.py measured with HIP events in that run."""
+    stats = kernel_stats(a.trace)
+    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the GPU box):", "",
+             "```", a.cmd.strip(), "```", "",
+             "| kernel | calls | avg us | % of GPU time |", "|---|---|---|---|"]
+    for name, calls, avg, pct in stats:
+        if "ptsd::" not in name:
+            continue
+        short = name.replace("ptsd::(anonymous namespace)::", "").replace("void ", "")
+        short = short.replace("(anonymous namespace)::", "").split("(")[0]
+        lines.append(f"| `{short}` | {calls} | {avg * 1e3:.2f} | {pct:.2f} |")
+    if a.trace_bench:
+        tb = json.loads(open(a.trace_bench).read().strip().splitlines()[-1])
+        lines += ["", f"bench.py in the same run: {tb['value']} {tb['unit']}, "
+                  f"{tb['ms_per_step']} ms per step; kernel time per step (HIP events, ms):", ""]
+        for k, v in tb.get("kernel_ms_per_round", {}).items():
+            lines.append(f"- {k}: {v}")
+        if "evictions" in tb:
+            lines.append(f"- evictions in the timed steps and warm-up: {tb['evictions']}, "
+                         f"index rebuilds: {tb['index_rebuilds']}")
+    os.makedirs(a.out, exist_ok=True)
+    with open(os.path.join(a.out, f"{a.name}_kernel_trace.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 if __name__ == "__main__":
