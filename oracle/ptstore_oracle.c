@@ -31,6 +31,10 @@
  *     policy"): when an insert needs more ids than remain, leaf nodes are
  *     evicted by frequency with a GDSF-style priority, so that the trie stays
  *     prefix-closed. The exact rules are spelt out at insert_evict() below.
+ *   - hot set (Section 4.1, "Replication of popular prefixes"): the nodes of
+ *     an id range with the highest priorities, those a faster tier keeps
+ *     copies of. Where a block's bytes live never changes any result, so
+ *     the oracle keeps one flat pool whatever the tiers.
  *
  * Trie representation: each node keeps a pointer to its parent, its first
  * child and its next sibling; a child is found by comparing the block's
@@ -477,6 +481,35 @@ int64_t orc_count(const ostore_t *s) { return s->count; }
 void orc_set_evict(ostore_t *s, int32_t on) { s->evict = on ? 1 : 0; }
 int64_t orc_clock(const ostore_t *s) { return s->clock; }
 int64_t orc_evictions(const ostore_t *s) { return s->evictions; }
+
+/*
+ * Hot set (Section 4.1, replication of popular prefixes): of the nodes with
+ * ids in [lo, hi), the `k` with the highest priority H, ties going to the
+ * smaller id; written to out[] in ascending id order. Returns how many were
+ * written (fewer than k if the range holds fewer nodes).
+ */
+int64_t orc_hot_set(const ostore_t *s, int64_t lo, int64_t hi, int64_t k, int32_t *out)
+{
+    if (lo < 0) lo = 0;
+    if (hi > s->count) hi = s->count;
+    int64_t n = 0;
+    for (int64_t round = 0; round < k; round++) {
+        /* the best node not taken yet: highest H, then smallest id */
+        const onode_t *best = NULL;
+        for (int64_t i = lo; i < hi; i++) {
+            const onode_t *c = s->by_id[i];
+            if (!c) continue;
+            int taken = 0;
+            for (int64_t j = 0; j < n && !taken; j++) taken = out[j] == c->id;
+            if (taken) continue;
+            if (!best || c->prio > best->prio) best = c;
+        }
+        if (!best) break;
+        out[n++] = best->id;
+    }
+    qsort(out, (size_t)n, sizeof(int32_t), cmp_i32);
+    return n;
+}
 
 /* Eviction bookkeeping of node `id`; ORC_ERR_INVALID if it holds no node. */
 int orc_node_stats(const ostore_t *s, int64_t id, int64_t *freq, int64_t *prio,

@@ -22,10 +22,15 @@ ORC_OK, ORC_ERR_INVALID, ORC_ERR_FULL, ORC_ERR_NOMEM = 0, 1, 2, 3
 
 
 def build_oracle(out: str = _LIB, extra_flags=(), src: str = _SRC) -> str:
-    """Compile the oracle with gcc into a shared library; returns its path."""
+    """Compile the oracle with gcc into a shared library; returns its path.
+
+    The library is written under a temporary name and renamed into place, so
+    that a process loading it meanwhile never sees a partial file."""
+    tmp = f"{out}.{os.getpid()}.tmp"
     cmd = ["gcc", "-O2", "-g", "-std=c99", "-Wall", "-Wextra", "-shared", "-fPIC",
-           *extra_flags, "-o", out, src]
+           *extra_flags, "-o", tmp, src]
     subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
     return out
 
 
@@ -57,6 +62,8 @@ def _load(path: str = _LIB):
     lib.orc_pool.argtypes = [p]
     lib.orc_node.argtypes = [p, i64, C.POINTER(C.c_int32), p]
     lib.orc_set_evict.argtypes = [p, i32]
+    lib.orc_hot_set.restype = i64
+    lib.orc_hot_set.argtypes = [p, i64, i64, i64, p]
     lib.orc_clock.restype = i64
     lib.orc_clock.argtypes = [p]
     lib.orc_evictions.restype = i64
@@ -180,6 +187,13 @@ class OracleStore:
     @property
     def evictions(self) -> int:
         return int(self._lib.orc_evictions(self._h))
+
+    def hot_set(self, lo: int, hi: int, k: int) -> np.ndarray:
+        """Ids in [lo, hi) of the k nodes with the highest priority (ties: smaller
+        id), ascending."""
+        out = np.zeros(max(k, 1), dtype=np.int32)
+        n = int(self._lib.orc_hot_set(self._h, lo, hi, k, _ptr(out)))
+        return out[:n].copy()
 
     def node_stats(self, node_id: int) -> Tuple[int, int, int, int]:
         """(frequency, priority, children holding an id, depth) of a node."""

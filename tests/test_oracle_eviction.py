@@ -281,3 +281,30 @@ def test_evict_gather_returns_the_prefix_payload(seed):
                 p = _payload_of(seq[:(j + 1) * bt], L * 2 * chunk).reshape(L, 2, chunk)
                 assert (ov[:, :, bt_tab[r, j]] == p).all()
     assert o.evictions > 0
+
+
+# --------------------------------------------------------------------------
+# hot set (replication of popular prefixes)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(6))
+def test_hot_set_is_top_priorities(seed):
+    """The oracle's hot set of an id range = the k nodes of the brute force with
+    the highest H, ties to the smaller id (a plain sort of the definition)."""
+    rng = np.random.default_rng(4000 + seed)
+    bt, cap, maxb = 2, 12, 6
+    atoms = _atoms(rng, 4, bt, 50)
+    o = evict_store(bt, cap)
+    b = brute.BruteEvictStore(bt, cap)
+    for step in range(25):
+        toks, offs = random_block_batch(rng, int(rng.integers(1, 7)), atoms, 6)
+        if rng.random() < 0.5:
+            o.lookup(toks, offs, maxb)
+            b.lookup(toks, offs, maxb)
+        else:
+            o.insert(toks, offs, maxb)
+            b.insert(toks, offs, maxb)
+        stats = b.by_id()
+        for lo, hi, k in ((0, cap, 3), (4, cap, 2), (2, 9, 5), (0, cap, cap + 3), (5, 6, 1)):
+            pool = sorted((i for i in stats if lo <= i < hi), key=lambda i: (-stats[i][1], i))
+            assert o.hot_set(lo, hi, k).tolist() == sorted(pool[:k]), (step, lo, hi, k)

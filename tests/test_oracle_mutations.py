@@ -45,6 +45,8 @@ MUTANTS = {
     "evict_lookup_not_an_access": ("if (s->evict) touch(s, c);", ";"),
     "evict_plain_lfu": ("n->prio = s->clock + n->freq;", "n->prio = n->freq;"),
     "evict_no_cascade": ("if (best->parent != &s->root) best->parent->live_children--;", ";"),
+    "hot_set_ties_to_larger_id": ("if (!best || c->prio > best->prio) best = c;",
+                                  "if (!best || c->prio >= best->prio) best = c;"),
     "evict_created_for_every_user": ("if (c->born == s->epoch && c->creator == r) crow[b] = 1;",
                                      "if (c->born == s->epoch) crow[b] = 1;"),
 }
@@ -63,6 +65,7 @@ PIN_CALLS = [
     lambda: [evpins.test_golden_eviction_oracle(c) for c in pins.load_golden("eviction.json")["cases"]],
     lambda: [evpins.test_evict_random_vs_brute(k) for k in range(4)],
     lambda: [evpins.test_evict_invariants(k) for k in range(2)],
+    lambda: [evpins.test_hot_set_is_top_priorities(k) for k in range(3)],
 ]
 
 
