@@ -99,6 +99,16 @@ typedef struct {
                               index_slots/2) blocks. */
     uint64_t hash_seed;    /* results never depend on it */
     uint32_t flags;        /* PTSTORE_FLAG_* */
+    /* Tiers (Section 4.1, "Fine-grain multi-level caching" and "Replication
+     * of popular prefixes"). Block ids 0 .. pool_blocks-replica_blocks-1
+     * live in device memory; the next host_blocks ids live in pinned host
+     * memory that the same copy kernels read and write over the host link.
+     * replica_blocks of the pool_blocks device slots hold copies of hot
+     * host-tier blocks (see ptstore_replicate); at most pool_blocks/2, and
+     * only with PTSTORE_FLAG_EVICT (the hot set is ranked by its access
+     * counts). Where a block's bytes are read from never changes a result. */
+    int64_t host_blocks;     /* 0: no host tier */
+    int64_t replica_blocks;  /* 0: no replicas */
 } ptstore_config_t;
 
 typedef struct {
@@ -118,6 +128,9 @@ typedef struct {
     int64_t evictions;      /* blocks evicted so far (PTSTORE_FLAG_EVICT) */
     int64_t clock;          /* eviction clock L: the largest priority evicted so far */
     int64_t index_rebuilds; /* times the index was rebuilt to clear deleted slots */
+    int64_t device_blocks;  /* ids below this live in device memory */
+    int64_t replicas;       /* host-tier blocks with a device copy now */
+    int64_t replica_copies; /* blocks copied into replica slots so far */
 } ptstore_stats_t;
 
 /* Device buffers of a store, for inspection by tests (read-only use). */
@@ -130,6 +143,12 @@ typedef struct {
     int64_t index_slots;
     const uint64_t *freq;   /* [capacity] access counts F (NULL without PTSTORE_FLAG_EVICT) */
     const uint64_t *prio;   /* [capacity] priorities H (NULL without PTSTORE_FLAG_EVICT) */
+    void *host_pool;        /* [host_blocks][block_bytes] pinned host tier, or NULL; block
+                               id device_blocks + j is row j. Device-accessible. */
+    int64_t host_blocks;
+    int64_t device_blocks;  /* ids below this are rows of `pool` */
+    const int32_t *replica_of; /* [host_blocks] device replica slot of host-tier block j
+                                  (its bytes are pool row device_blocks + slot), or -1 */
 } ptstore_buffers_t;
 
 /*
@@ -213,6 +232,18 @@ int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created
                     const int32_t *block_table, int32_t R, int32_t max_blocks,
                     const void *cache, int64_t cache_blocks, void *stream);
 
+/*
+ * Replication of popular prefixes (Section 4.1): make the device replica
+ * slots hold exactly the hot set of the host tier -- the replica_blocks
+ * host-tier blocks with the highest priority H, ties going to the smaller
+ * id. Replicas that left the hot set free their slots; blocks that entered
+ * it are copied from host memory into free slots (lowest slot to lowest id).
+ * Gathers then read those blocks from device memory. A scatter into a block
+ * drops its replica; an eviction too. Enqueued on `stream`; errors: INVALID
+ * (no replica tier), HIP.
+ */
+int ptstore_replicate(ptstore_t *store, void *stream);
+
 /* Wait for the device and read the store's counters into *stats. */
 int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);
 
@@ -230,7 +261,8 @@ int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
  * call, for kind 0 = gather copy kernel, 1 = lookup, 2 = scatter copy
  * kernel, 3 = insert (all its kernels), 4 = descriptor-list build of gather
  * and scatter, 5 = the eviction part of an insert (PTSTORE_FLAG_EVICT;
- * included in kind 3). Resets the records of that kind. At most 65,536 launches
+ * included in kind 3), 6 = ptstore_replicate. Resets the records of that
+ * kind. At most 65,536 launches
  * per kind are recorded between two calls.
  */
 int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64_t *launches);

@@ -1,7 +1,9 @@
 // Host runtime of the prefix store: the C ABI declared in include/ptstore.h.
 //
 // The store owns, on one device:
-//   pool    [capacity][layer][K|V][head][slot][dim]  KV payload, per-block contiguous
+//   pool    [dev rows][layer][K|V][head][slot][dim]  KV payload, per-block contiguous:
+//           the home of ids below `owned`, then the replica slots
+//   host    [host rows][...] pinned host tier, the home of ids owned..
 //   parent  [capacity] int32, tokens [capacity][block_tokens] int32   block metadata
 //   slots   [index_slots] {key, id}                  open-addressing block index
 //   ht      key-chain constants, state: counters and the block count
@@ -45,8 +47,11 @@ struct ptstore {
     int32_t cus;  // compute units of the device
     EvictView evs;  // evs.on = 0 without PTSTORE_FLAG_EVICT
     void* ev_mem;  // one allocation holding every ev array
+    TierView tier;  // owned = capacity and no host rows for a device-only store
+    void* tier_mem; // replica map and replicate scratch
+    void* host_mem; // the host tier as allocated (tier.host is its device address)
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[6];
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[7];
     std::vector<hipEvent_t> free_ev;
 };
 
@@ -124,6 +129,7 @@ CopyPlan copy_plan(ptstore_t* s) {
     // a looping copy: every compute unit holds its full share, four times over
     p.loop_grid = s->cus * (2048 / s->threads) * 4;
     p.state = s->state;
+    p.tier = s->tier;
     return p;
 }
 
@@ -272,14 +278,20 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     if (c.num_layers < 1 || c.num_kv_heads < 1 || c.head_dim < 1 || c.block_tokens < 1 ||
         c.block_tokens > 64 || c.elem_bytes < 1)
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: bad shape");
-    if (c.pool_blocks < 0 || c.pool_blocks > (int64_t)0x7FFFFFFC)
-        return fail(PTSTORE_ERR_INVALID, "ptstore_create: pool_blocks out of range");
+    if (c.pool_blocks < 0 || c.host_blocks < 0 || c.pool_blocks + c.host_blocks > (int64_t)0x7FFFFFFC)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_create: pool_blocks / host_blocks out of range");
+    if (c.replica_blocks < 0 || c.replica_blocks > c.pool_blocks / 2 ||
+        (c.replica_blocks > 0 && (c.host_blocks == 0 || !(c.flags & PTSTORE_FLAG_EVICT))))
+        return fail(PTSTORE_ERR_INVALID,
+                    "ptstore_create: replica_blocks must be <= pool_blocks/2 and needs host_blocks "
+                    "and PTSTORE_FLAG_EVICT");
+    const int64_t want_ids = c.pool_blocks - c.replica_blocks + c.host_blocks;
     const int64_t chunk = (int64_t)c.num_kv_heads * c.block_tokens * c.head_dim * c.elem_bytes;
     if (chunk % 16 != 0 || chunk > (1ll << 30))
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: chunk bytes must be a multiple of 16");
     uint64_t slots_n;
     if (c.index_slots == 0) {
-        slots_n = next_pow2((uint64_t)(2 * (c.pool_blocks > 1 ? c.pool_blocks : 1)));
+        slots_n = next_pow2((uint64_t)(2 * (want_ids > 1 ? want_ids : 1)));
         if (slots_n < 64) slots_n = 64;
     } else {
         if (c.index_slots < 2 || (c.index_slots & (c.index_slots - 1)) != 0 ||
@@ -293,7 +305,14 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     s->chunk_bytes = chunk;
     s->block_bytes = chunk * 2 * c.num_layers;
     s->slots_n = slots_n;
-    s->capacity = c.pool_blocks < (int64_t)(slots_n / 2) ? c.pool_blocks : (int64_t)(slots_n / 2);
+    s->capacity = want_ids < (int64_t)(slots_n / 2) ? want_ids : (int64_t)(slots_n / 2);
+    {
+        const int64_t owned = c.pool_blocks - c.replica_blocks;
+        s->tier.owned = owned < s->capacity ? owned : s->capacity;
+        s->tier.replicas = c.replica_blocks;
+        s->tier.dev_rows = s->tier.owned + c.replica_blocks;
+        s->tier.host_blocks = s->capacity - s->tier.owned;
+    }
     // one 32 KiB-class chunk per 1024-thread workgroup: the shape whose
     // bandwidth held up best whatever the physical placement of pool and cache
     s->chunks_per_group = 1;
@@ -306,7 +325,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         delete s;
         return fail(PTSTORE_ERR_HIP, "ptstore_create: device query", e);
     }
-    const size_t pool_bytes = (size_t)(s->capacity > 0 ? s->capacity : 1) * (size_t)s->block_bytes;
+    const size_t pool_bytes = (size_t)(s->tier.dev_rows > 0 ? s->tier.dev_rows : 1) * (size_t)s->block_bytes;
     const size_t cap1 = (size_t)(s->capacity > 0 ? s->capacity : 1);
     if ((e = hipMalloc(&s->pool, pool_bytes)) != hipSuccess ||
         (e = hipMalloc(&s->parent, cap1 * 4)) != hipSuccess ||
@@ -317,6 +336,43 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         ptstore_destroy(s);
         (void)hipGetLastError();
         return fail(PTSTORE_ERR_NOMEM, "ptstore_create: hipMalloc", e);
+    }
+    if (s->tier.host_blocks > 0) {
+        void* h = nullptr;
+        if ((e = hipHostMalloc(&h, (size_t)s->tier.host_blocks * (size_t)s->block_bytes,
+                               hipHostMallocDefault)) != hipSuccess ||
+            (e = hipHostGetDevicePointer((void**)&s->tier.host, h, 0)) != hipSuccess) {
+            if (h) (void)hipHostFree(h);
+            s->tier.host = nullptr;
+            ptstore_destroy(s);
+            (void)hipGetLastError();
+            return fail(PTSTORE_ERR_NOMEM, "ptstore_create: host tier", e);
+        }
+        s->host_mem = h;
+    }
+    if (s->tier.replicas > 0) {
+        const int64_t R = s->tier.replicas, H = s->tier.host_blocks;
+        const int64_t words = (H + kWave - 1) / kWave;
+        auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+        const size_t bytes = up(H * 4) + up(R * 4) * 3 + up(words * 8) + up(R * sizeof(Pair));
+        if ((e = hipMalloc(&s->tier_mem, bytes)) != hipSuccess ||
+            (e = hipMemset(s->tier_mem, 0xFF, bytes)) != hipSuccess) {  // every map entry -1
+            ptstore_destroy(s);
+            (void)hipGetLastError();
+            return fail(PTSTORE_ERR_NOMEM, "ptstore_create: replica map", e);
+        }
+        uint8_t* q = static_cast<uint8_t*>(s->tier_mem);
+        s->tier.rep_of = reinterpret_cast<int32_t*>(q);
+        q += up(H * 4);
+        s->tier.rep_id = reinterpret_cast<int32_t*>(q);
+        q += up(R * 4);
+        s->tier.free_list = reinterpret_cast<int32_t*>(q);
+        q += up(R * 4);
+        s->tier.enter_list = reinterpret_cast<int32_t*>(q);
+        q += up(R * 4);
+        s->tier.enter_mask = reinterpret_cast<uint64_t*>(q);
+        q += up(words * 8);
+        s->tier.copies = reinterpret_cast<Pair*>(q);
     }
     if (c.flags & PTSTORE_FLAG_EVICT) {
         const size_t evb = carve_evict(nullptr, s->capacity, &s->evs);
@@ -330,6 +386,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         s->evs.on = 1;
         s->evs.epoch = 0;
     }
+    s->evs.tier = s->tier;
     HashTables h;
     make_hash_tables(c.hash_seed, (c.flags & PTSTORE_FLAG_WEAK_HASH) != 0, &h);
     DevState st;
@@ -364,6 +421,8 @@ int ptstore_destroy(ptstore_t* s) {
     (void)hipFree(s->scratch);
     (void)hipFree(s->copy_scratch);
     (void)hipFree(s->ev_mem);
+    (void)hipFree(s->tier_mem);
+    if (s->host_mem) (void)hipHostFree(s->host_mem);
     delete s;
     return PTSTORE_OK;
 }
@@ -492,6 +551,21 @@ int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_scatter: launch", e);
 }
 
+int ptstore_replicate(ptstore_t* s, void* stream) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_replicate: null store");
+    if (s->tier.replicas == 0)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_replicate: store has no replica slots");
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    {
+        Timed t(s, 6, st);
+        e = launch_replicate(index_view(s), s->evs, copy_plan(s), st);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_replicate: launch", e);
+}
+
 int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     if (!s || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_stats: null argument");
     int rc = set_device(s);
@@ -522,6 +596,9 @@ int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     out->evictions = (int64_t)st.evictions;
     out->clock = (int64_t)st.clock;
     out->index_rebuilds = (int64_t)st.rebuilds;
+    out->device_blocks = s->tier.owned;
+    out->replicas = (int64_t)st.rep_count;
+    out->replica_copies = (int64_t)st.rep_copies;
     return PTSTORE_OK;
 }
 
@@ -539,6 +616,8 @@ int ptstore_reset_counters(ptstore_t* s) {
         keep.clock = st.clock;
         keep.evictions = st.evictions;
         keep.tombstones = st.tombstones;
+        keep.rep_count = st.rep_count;
+        keep.rep_copies = st.rep_copies;
         e = hipMemcpy(s->state, &keep, sizeof keep, hipMemcpyHostToDevice);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_reset_counters", e);
@@ -554,11 +633,15 @@ int ptstore_get_buffers(ptstore_t* s, ptstore_buffers_t* out) {
     out->index_slots = (int64_t)s->slots_n;
     out->freq = s->evs.on ? s->evs.freq : nullptr;
     out->prio = s->evs.on ? s->evs.prio : nullptr;
+    out->host_pool = s->host_mem;
+    out->host_blocks = s->tier.host_blocks;
+    out->device_blocks = s->tier.owned;
+    out->replica_of = s->tier.rep_of;
     return PTSTORE_OK;
 }
 
 int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* launches) {
-    if (!s || kind < 0 || kind > 5 || !total_ms || !launches)
+    if (!s || kind < 0 || kind > 6 || !total_ms || !launches)
         return fail(PTSTORE_ERR_INVALID, "ptstore_kernel_times: bad argument");
     int rc = set_device(s);
     if (rc) return rc;

@@ -4,8 +4,12 @@
 // their tensors into application-supplied GPU memory); scatter stores the
 // tensors of blocks an insert created. Both move whole (layer, K|V) chunks
 // of heads x slots x dim elements, which are contiguous on both sides:
-//   pool  [id][layer][K|V][head][slot][dim]        chunk c at id*block + c*chunk
+//   pool  [row][layer][K|V][head][slot][dim]       chunk c at row*block + c*chunk
 //   cache [layer][K|V][cache block][head][slot][dim] chunk c at (c*NB + cb)*chunk
+// A block's row is where its bytes are read from: its home in device memory,
+// a device replica of a host-tier block, or its home in the pinned host tier
+// (rows past the device pool), which the same kernel reads over the host
+// link.
 //
 // A call runs in two parts, like the paper's bulk transfer of a list of
 // (offset, size) segments in one request (Section 4.1, RDMA-aware
@@ -61,7 +65,25 @@ struct SelectArgs {
     int64_t cache_blocks;
     DevState* state;
     CopyScratch sc;
+    TierView tier;
 };
+
+// The row a gather reads block `id` from: its device home, its replica, or
+// its host-tier home.
+__device__ inline int32_t gather_row(const TierView& t, int32_t id) {
+    if (id < t.owned) return id;
+    const int64_t h = id - t.owned;
+    if (t.rep_of) {
+        const int32_t slot = t.rep_of[h];
+        if (slot >= 0) return (int32_t)(t.owned + slot);
+    }
+    return (int32_t)(t.dev_rows + h);
+}
+
+// The row a scatter writes block `id` to: always its home.
+__device__ inline int32_t home_row(const TierView& t, int32_t id) {
+    return id < t.owned ? id : (int32_t)(t.dev_rows + (id - t.owned));
+}
 
 // Should (r, b) be moved? Sets *bad for an entry out of range.
 template <bool GATHER>
@@ -76,7 +98,7 @@ __device__ inline bool selected(const SelectArgs& a, int64_t rb, unsigned long l
         *bad = true;
         return false;
     }
-    out->id = id;
+    out->row = GATHER ? gather_row(a.tier, id) : home_row(a.tier, id);
     out->cb = cb;
     return true;
 }
@@ -155,11 +177,22 @@ __global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
         const unsigned long long mask = ballot64(sel);
         if (sel) a.sc.pairs[pos + __popcll(mask & lanes_below(lane))] = p;
         pos += __popcll(mask);
+        // new bytes for a host-tier block: its device replica is stale, drop it
+        if (!GATHER && sel && a.tier.rep_of && p.row >= a.tier.dev_rows) {
+            const int64_t h = p.row - a.tier.dev_rows;
+            const int32_t slot = atomicExch(&a.tier.rep_of[h], -1);
+            if (slot >= 0) {
+                a.tier.rep_id[slot] = -1;
+                atomicSub(&a.state->rep_count, 1ull);
+            }
+        }
     }
 }
 
 struct CopyArgs {
     uint8_t* pool;
+    uint8_t* host;      // host tier: rows dev_rows.. of the pool's row space
+    int64_t dev_rows;
     uint8_t* cache;
     const Pair* pairs;
     const unsigned long long* total;
@@ -187,8 +220,10 @@ __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
         const Pair p = a.pairs[d];
         const int c0 = g * a.chunks_per_group;
         const int c1 = min(c0 + a.chunks_per_group, a.chunks_per_block);
+        uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
+                                          : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
         for (int c = c0; c < c1; ++c) {
-            uint8_t* src = a.pool + (int64_t)p.id * a.block_bytes + (int64_t)c * a.chunk_bytes;
+            uint8_t* src = blk + (int64_t)c * a.chunk_bytes;
             uint8_t* dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
             if (GATHER)
                 copy_span(reinterpret_cast<const v4u*>(src), reinterpret_cast<v4u*>(dst), n16);
@@ -198,11 +233,30 @@ __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
     }
 }
 
+// Whole blocks from one row to another (replication): pairs[k].row is the
+// source row, pairs[k].cb the destination row; *total pairs.
+__global__ __launch_bounds__(1024) void k_copy_rows(CopyArgs a) {
+    const unsigned long long units = *a.total * (unsigned long long)a.chunks_per_block;
+    const int n16 = (int)(a.chunk_bytes >> 4);
+    for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
+        const unsigned long long d = unit / (unsigned)a.chunks_per_block;
+        const int c = (int)(unit - d * (unsigned)a.chunks_per_block);
+        const Pair p = a.pairs[d];
+        const int64_t rows[2] = {p.row, p.cb};
+        uint8_t* blk[2];
+        for (int k = 0; k < 2; ++k)
+            blk[k] = rows[k] < a.dev_rows ? a.pool + rows[k] * a.block_bytes
+                                          : a.host + (rows[k] - a.dev_rows) * a.block_bytes;
+        copy_span(reinterpret_cast<const v4u*>(blk[0] + (int64_t)c * a.chunk_bytes),
+                  reinterpret_cast<v4u*>(blk[1] + (int64_t)c * a.chunk_bytes), n16);
+    }
+}
+
 template <bool GATHER>
 hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, const int32_t* m,
                   const uint8_t* created, const int32_t* bt, int32_t R, int32_t max_blocks,
                   int64_t cache_blocks, hipStream_t s) {
-    SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc};
+    SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc, p.tier};
     const unsigned grid = (unsigned)((R + kSelWaves - 1) / kSelWaves);
     hipLaunchKernelGGL(k_select_count<GATHER>, dim3(grid), dim3(kSelThreads), 0, s, a);
     hipError_t e = hipGetLastError();
@@ -218,6 +272,8 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
                 int32_t R, int32_t max_blocks, hipStream_t s) {
     CopyArgs a{};
     a.pool = p.pool;
+    a.host = p.tier.host;
+    a.dev_rows = p.tier.dev_rows;
     a.cache = cache;
     a.pairs = sc.pairs;
     a.total = sc.total;
@@ -238,6 +294,25 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
 }
 
 }  // namespace
+
+hipError_t launch_copy_rows(const CopyPlan& p, const Pair* pairs, const unsigned long long* total,
+                            int64_t max_pairs, hipStream_t s) {
+    CopyArgs a{};
+    a.pool = p.pool;
+    a.host = p.tier.host;
+    a.dev_rows = p.tier.dev_rows;
+    a.pairs = pairs;
+    a.total = total;
+    a.block_bytes = p.block_bytes;
+    a.chunk_bytes = p.chunk_bytes;
+    a.chunks_per_block = p.chunks_per_block;
+    int64_t grid = (int64_t)p.loop_grid;
+    const int64_t bound = max_pairs * p.chunks_per_block;
+    if (grid > bound) grid = bound;
+    if (grid < 1) return hipSuccess;
+    hipLaunchKernelGGL(k_copy_rows, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+    return hipGetLastError();
+}
 
 size_t copy_scratch_bytes(int32_t R, int32_t max_blocks) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };

@@ -77,13 +77,22 @@ struct DevState {
     unsigned long long ev_nv;         // blocks evicted
     unsigned long long ev_rebuild;    // 1: rebuild the index in this insert
     // key layout: only the bits in which candidates differ are kept
-    unsigned long long sel_pmin, sel_dmax, sel_imin;  // smallest H, largest depth, smallest id
+    unsigned long long sel_pbase, sel_dmax, sel_imin;  // H base, largest depth, smallest id
     unsigned int sel_wd, sel_wi;        // bit widths of the depth and id fields
     unsigned int sel_w, sel_npass;      // key width, digit passes it needs
     unsigned long long sel_hi, sel_lo;  // threshold key found so far (left-aligned)
     unsigned long long sel_need;        // rank of the threshold among what matches it
     unsigned int sel_range_done;        // workgroups finished the range pass
     unsigned int sel_done[kSelPasses];  // workgroups finished per digit pass
+    // what the search ranks: 0 = eviction candidates (ids below sel_hi_id
+    // that the batch did not match, key (H, deeper, id)); 1 = the host tier,
+    // ids sel_lo_id .. sel_hi_id-1, key (H descending, id)
+    unsigned int sel_hot, sel_pad;
+    unsigned long long sel_lo_id, sel_hi_id;
+    // replication
+    unsigned long long rep_count;       // host-tier blocks with a device replica
+    unsigned long long rep_copies;      // blocks copied into replica slots so far
+    unsigned long long rep_new;         // blocks the running replicate copies
     CounterSlot slot[kCounterSlots];
 };
 

@@ -41,11 +41,18 @@ typedef unsigned __int128 u128;
 
 __device__ inline unsigned bit_width(uint64_t x) { return x ? 64u - (unsigned)__clzll((long long)x) : 0u; }
 
+// Is `id` ranked by the running search? (sel_lo_id <= id < sel_hi_id holds.)
+__device__ inline bool sel_candidate(const EvictView& ev, const DevState* st, int64_t id) {
+    return st->sel_hot || ev.prot[id] != ev.epoch;
+}
+
 // The candidate's compressed key, left-aligned in 128 bits (state written by
-// the range pass).
+// the range pass). Eviction: (H - Hmin, depth_max - depth, id - id_min), the
+// smallest go. Hot set: (Hmax - H, id - id_min), the smallest stay.
 __device__ inline u128 sel_key(const EvictView& ev, const DevState* st, int64_t id) {
-    const u128 p = (u128)(ev.prio[id] - st->sel_pmin);
-    const u128 d = (u128)(st->sel_dmax - (uint64_t)ev.depth[id]);
+    const bool hot = st->sel_hot != 0;
+    const u128 p = (u128)(hot ? st->sel_pbase - ev.prio[id] : ev.prio[id] - st->sel_pbase);
+    const u128 d = hot ? (u128)0 : (u128)(st->sel_dmax - (uint64_t)ev.depth[id]);
     const u128 i = (u128)((uint64_t)id - st->sel_imin);
     const unsigned wd = st->sel_wd, wi = st->sel_wi, w = st->sel_w;
     const u128 c = (p << (wd + wi)) | (d << wi) | i;
@@ -66,20 +73,20 @@ __device__ inline T wave_reduce(T v, Op op, int lane) {
 // Ranges of H, depth and id over the candidates, their number, and from them
 // the key layout. Also clears the digit histograms. Each workgroup writes its
 // own partial (no shared-address atomics); the last one to finish combines
-// them.
+// them. Serves both searches (eviction and hot set, see sel_key).
 __global__ __launch_bounds__(kThreads) void k_sel_range(EvictView ev, DevState* st) {
     if (st->ev_want == 0) return;  // uniform over the grid
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < (int64_t)kSelPasses * kSelBins;
          i += (int64_t)gridDim.x * kThreads)
         ev.hist[i] = 0;
-    const int64_t old = (int64_t)st->insert_old_count;
+    const int64_t lo_id = (int64_t)st->sel_lo_id, hi_id = (int64_t)st->sel_hi_id;
     // [0] min H, [1] -max H, [2] min depth, [3] -max depth, [4] min id, [5] -max id: all minima
     uint64_t v[6] = {~0ull, ~0ull, ~0ull, ~0ull, ~0ull, ~0ull};
     uint64_t n = 0;
-    for (int64_t id = (int64_t)blockIdx.x * kThreads + threadIdx.x; id < old;
+    for (int64_t id = lo_id + (int64_t)blockIdx.x * kThreads + threadIdx.x; id < hi_id;
          id += (int64_t)gridDim.x * kThreads) {
-        if (ev.prot[id] == ev.epoch) continue;
+        if (!sel_candidate(ev, st, id)) continue;
         const uint64_t x[6] = {ev.prio[id], ~ev.prio[id], (uint64_t)ev.depth[id], ~(uint64_t)ev.depth[id],
                                (uint64_t)id, ~(uint64_t)id};
 #pragma unroll
@@ -129,8 +136,10 @@ __global__ __launch_bounds__(kThreads) void k_sel_range(EvictView ev, DevState* 
     }
     const uint64_t pmin = tot[0], pmax = ~tot[1], dmin = tot[2], dmax = ~tot[3], imin = tot[4],
                    imax = ~tot[5];
-    const unsigned wp = bit_width(pmax - pmin), wd = bit_width(dmax - dmin), wi = bit_width(imax - imin);
-    st->sel_pmin = pmin;
+    const bool hot = st->sel_hot != 0;
+    const unsigned wp = bit_width(pmax - pmin), wd = hot ? 0u : bit_width(dmax - dmin),
+                   wi = bit_width(imax - imin);
+    st->sel_pbase = hot ? pmax : pmin;
     st->sel_dmax = dmax;
     st->sel_imin = imin;
     st->sel_wd = wd;
@@ -148,13 +157,14 @@ __global__ __launch_bounds__(kThreads) void k_sel_pass(EvictView ev, DevState* s
     const int t = threadIdx.x;
     for (int b = t; b < kSelBins; b += kThreads) h[b] = 0;
     __syncthreads();
-    const int64_t old = (int64_t)st->insert_old_count;
+    const int64_t lo_id = (int64_t)st->sel_lo_id, hi_id = (int64_t)st->sel_hi_id;
     const u128 thr = ((u128)st->sel_hi << 64) | (u128)st->sel_lo;
     const int hi_bit = 128 - kSelBits * pass;          // digit = key bits [lo_bit, hi_bit)
     const int lo_bit = hi_bit - kSelBits > 0 ? hi_bit - kSelBits : 0;
     const unsigned dmask = (1u << (hi_bit - lo_bit)) - 1u;
-    for (int64_t id = (int64_t)blockIdx.x * kThreads + t; id < old; id += (int64_t)gridDim.x * kThreads) {
-        if (ev.prot[id] == ev.epoch) continue;
+    for (int64_t id = lo_id + (int64_t)blockIdx.x * kThreads + t; id < hi_id;
+         id += (int64_t)gridDim.x * kThreads) {
+        if (!sel_candidate(ev, st, id)) continue;
         const u128 k = sel_key(ev, st, id);
         if (pass > 0 && (k >> hi_bit) != (thr >> hi_bit)) continue;
         atomicAdd(&h[(unsigned)(k >> lo_bit) & dmask], 1u);
@@ -223,6 +233,15 @@ __global__ __launch_bounds__(kThreads) void k_ev_mark(EvictView ev, DevState* st
                 slots[ev.spos[id]].key = kTombKey;
                 const int32_t p = parent[id];
                 if (p >= 0) atomicSub(&ev.live[p], 1);
+                if (ev.tier.rep_of && id >= ev.tier.owned) {  // its replica goes too
+                    const int64_t h = id - ev.tier.owned;
+                    const int32_t slot = ev.tier.rep_of[h];
+                    if (slot >= 0) {
+                        ev.tier.rep_of[h] = -1;
+                        ev.tier.rep_id[slot] = -1;
+                        atomicSub(&st->rep_count, 1ull);
+                    }
+                }
             }
         }
         const unsigned long long mask = ballot64(sel);
@@ -353,6 +372,129 @@ __global__ __launch_bounds__(kThreads) void k_touch(EvictView ev, DevState* st, 
     }
 }
 
+// ---------------------------------------------------------------------------
+// Replication of the hot set (Section 4.1, "Replication of popular
+// prefixes"): the replica slots hold the `replicas` host-tier blocks with the
+// highest H. The same threshold search ranks the host tier by (H descending,
+// id); blocks that left the set free their slots, blocks that entered it are
+// paired, in ascending id order, with the free slots in ascending order and
+// copied in.
+// ---------------------------------------------------------------------------
+
+__global__ void k_rep_setup(DevState* st, TierView tier) {
+    const int t = threadIdx.x;
+    if (t < kSelPasses) st->sel_done[t] = 0;
+    if (t != 0) return;
+    const uint64_t count = st->count;
+    st->sel_hot = 1;
+    st->sel_lo_id = (uint64_t)tier.owned;
+    st->sel_hi_id = count > (uint64_t)tier.owned ? count : (uint64_t)tier.owned;
+    st->ev_want = (uint64_t)tier.replicas;
+    st->ev_all = 0;
+    st->sel_range_done = 0;
+    st->sel_npass = 0;
+    st->sel_hi = 0;
+    st->sel_lo = 0;
+    st->sel_need = (uint64_t)tier.replicas;
+    st->rep_new = 0;
+}
+
+// Host-tier blocks that left the hot set give up their slot; those that
+// entered it get a bit in enter_mask.
+__global__ __launch_bounds__(kThreads) void k_rep_diff(EvictView ev, DevState* st) {
+    const TierView& t = ev.tier;
+    const int lane = threadIdx.x & (kWave - 1);
+    const bool all = st->ev_all != 0;
+    const u128 thr = ((u128)st->sel_hi << 64) | (u128)st->sel_lo;
+    const int64_t hi_id = (int64_t)st->sel_hi_id;
+    const int64_t span = ((t.host_blocks + kWave - 1) / kWave) * kWave;
+    unsigned long long dropped = 0;
+    for (int64_t h = (int64_t)blockIdx.x * kThreads + threadIdx.x; h - threadIdx.x < span;
+         h += (int64_t)gridDim.x * kThreads) {
+        const int64_t id = t.owned + h;
+        bool hot = false, have = false;
+        if (h < t.host_blocks) {
+            hot = id < hi_id && (all || sel_key(ev, st, id) <= thr);
+            const int32_t slot = t.rep_of[h];
+            have = slot >= 0;
+            if (have && !hot) {
+                t.rep_of[h] = -1;
+                t.rep_id[slot] = -1;
+                ++dropped;
+            }
+        }
+        const unsigned long long mask = ballot64(hot && !have);
+        if (lane == 0 && h / kWave < span / kWave) t.enter_mask[h / kWave] = mask;
+    }
+    dropped = wave_reduce(dropped, [](uint64_t a, uint64_t b) { return a + b; }, lane);
+    if (lane == 0 && dropped) atomicSub(&st->rep_count, dropped);
+}
+
+// Exclusive scan over the block (blockDim.x = 1024) of one value per thread;
+// returns this thread's offset, *total the sum.
+__device__ inline uint32_t block_scan(uint32_t v, uint32_t* part, uint32_t* total) {
+    const int t = threadIdx.x, nt = blockDim.x;
+    part[t] = v;
+    __syncthreads();
+    for (int d = 1; d < nt; d <<= 1) {
+        const uint32_t x = t >= d ? part[t - d] : 0u;
+        __syncthreads();
+        part[t] += x;
+        __syncthreads();
+    }
+    const uint32_t incl = part[t];
+    *total = part[nt - 1];
+    __syncthreads();
+    return incl - v;
+}
+
+// One workgroup: lists the free slots and the entering blocks in ascending
+// order, pairs them and writes the copies to make.
+__global__ __launch_bounds__(1024) void k_rep_assign(EvictView ev, DevState* st) {
+    const TierView& t = ev.tier;
+    __shared__ uint32_t part[1024];
+    const int tid = threadIdx.x, nt = blockDim.x;
+    uint32_t nfree = 0;
+    for (int64_t base = 0; base < t.replicas; base += nt) {
+        const int64_t slot = base + tid;
+        const uint32_t f = slot < t.replicas && t.rep_id[slot] < 0 ? 1u : 0u;
+        uint32_t tot;
+        const uint32_t off = block_scan(f, part, &tot);
+        if (f) t.free_list[nfree + off] = (int32_t)slot;
+        nfree += tot;
+    }
+    const int64_t words = (t.host_blocks + kWave - 1) / kWave;
+    uint32_t nenter = 0;
+    for (int64_t base = 0; base < words; base += nt) {
+        const int64_t w = base + tid;
+        const uint64_t mask = w < words ? t.enter_mask[w] : 0ull;
+        uint32_t tot;
+        uint32_t off = block_scan((uint32_t)__popcll(mask), part, &tot);
+        for (uint64_t m = mask; m; m &= m - 1) {  // the hot set never exceeds the slots
+            const int b = __ffsll((long long)m) - 1;
+            const uint32_t k = nenter + off++;
+            if (k < nfree) t.enter_list[k] = (int32_t)(w * kWave + b);
+        }
+        nenter += tot;
+    }
+    if (nenter > nfree) nenter = nfree;
+    __syncthreads();
+    for (uint32_t k = tid; k < nenter; k += nt) {
+        const int32_t h = t.enter_list[k], slot = t.free_list[k];
+        t.rep_of[h] = slot;
+        t.rep_id[slot] = h;
+        Pair p;
+        p.row = (int32_t)(t.dev_rows + h);   // host-tier home
+        p.cb = (int32_t)(t.owned + slot);    // device replica row
+        t.copies[k] = p;
+    }
+    if (tid == 0) {
+        st->rep_new = nenter;
+        st->rep_count += nenter;
+        st->rep_copies += nenter;
+    }
+}
+
 unsigned grid_for(int64_t n, int64_t cap_groups) {
     int64_t g = (n + kThreads - 1) / kThreads;
     if (g > cap_groups) g = cap_groups;
@@ -388,6 +530,27 @@ hipError_t launch_evict(const IndexView& ix, const InsertTarget& tgt, const Evic
     hipLaunchKernelGGL(k_rebuild_insert, dim3(g), dim3(kThreads), 0, s, ev, ix.state, tgt.slots,
                        ix.slot_mask, (const int32_t*)tgt.parent, ix.ht);
     return hipGetLastError();
+}
+
+hipError_t launch_replicate(const IndexView& ix, const EvictView& ev, const CopyPlan& p,
+                            hipStream_t s) {
+    hipError_t e;
+    const TierView& t = ev.tier;
+    hipLaunchKernelGGL(k_rep_setup, dim3(1), dim3(64), 0, s, ix.state, t);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const unsigned g = grid_for((t.host_blocks + 3) / 4, kSelGroups);
+    hipLaunchKernelGGL(k_sel_range, dim3(g), dim3(kThreads), 0, s, ev, ix.state);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    for (int k = 0; k < kSelPasses; ++k) {
+        hipLaunchKernelGGL(k_sel_pass, dim3(g), dim3(kThreads), 0, s, ev, ix.state, k);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const unsigned gw = grid_for(((t.host_blocks + kWave - 1) / kWave) * kWave, 2048);
+    hipLaunchKernelGGL(k_rep_diff, dim3(gw), dim3(kThreads), 0, s, ev, ix.state);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_rep_assign, dim3(1), dim3(1024), 0, s, ev, ix.state);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_copy_rows(p, t.copies, &ix.state->rep_new, t.replicas, s);
 }
 
 hipError_t launch_touch_paths(const IndexView& ix, const EvictView& ev, const int32_t* m,

@@ -275,6 +275,9 @@ __global__ __launch_bounds__(1024) void k_scan(InsertArgs a) {
             st->ev_nv = 0;
             st->sel_range_done = 0;
             st->sel_npass = 0;
+            st->sel_hot = 0;
+            st->sel_lo_id = 0;
+            st->sel_hi_id = (unsigned long long)old;
             st->sel_hi = 0;
             st->sel_lo = 0;
             st->sel_need = st->ev_want;

@@ -23,6 +23,30 @@ struct IndexView {
     int32_t counters;        // 1: count probes and comparisons
 };
 
+// One block to move: physical row (see TierView) <-> cache block cb.
+struct Pair {
+    int32_t row;
+    int32_t cb;
+};
+
+// Where block bytes live. Physical rows 0 .. dev_rows-1 are rows of the
+// device pool (rows below `owned` are the home of ids below `owned`, the
+// rest are replica slots); rows dev_rows + j are rows of the pinned host
+// tier, the home of id owned + j.
+struct TierView {
+    uint8_t* host;        // host tier base (device-accessible), null if none
+    int64_t owned;        // ids below live in device memory
+    int64_t dev_rows;     // device pool rows: owned + replica slots
+    int64_t host_blocks;
+    int32_t* rep_of;      // [host_blocks] replica slot or -1; null without replicas
+    int32_t* rep_id;      // [replicas] host-tier index (id - owned) held, or -1
+    int64_t replicas;
+    uint64_t* enter_mask; // [ceil(host_blocks / 64)] blocks entering the hot set
+    int32_t* free_list;   // [replicas] free slots, ascending (replicate scratch)
+    int32_t* enter_list;  // [replicas] entering host-tier indices, ascending
+    Pair* copies;         // [replicas] {host row, replica row} to copy
+};
+
 // Most workgroups of a selection pass.
 constexpr int kSelGroups = 256;
 
@@ -45,6 +69,7 @@ struct EvictView {
     int64_t words;      // ceil(capacity / 64)
     int32_t epoch;      // of the running insert, >= 1
     int32_t on;         // 0: eviction disabled, nothing here is touched
+    TierView tier;      // an evicted host-tier block loses its replica
 };
 
 struct Batch {
@@ -71,13 +96,9 @@ struct CopyPlan {
     int32_t grid;              // workgroups of the copy kernel, 0 = chosen per call
     int32_t loop_grid;         // workgroups of a looping (sparse) copy
     DevState* state;
+    TierView tier;
 };
 
-// One block to move: pool block id <-> cache block cb.
-struct Pair {
-    int32_t id;
-    int32_t cb;
-};
 
 // Descriptor list of one gather / scatter call.
 struct CopyScratch {
@@ -99,6 +120,9 @@ hipError_t launch_gather_copy(const CopyPlan& p, const CopyScratch& sc, uint8_t*
                               int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s);
 hipError_t launch_scatter_copy(const CopyPlan& p, const CopyScratch& sc, const uint8_t* cache,
                                int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s);
+// Whole-block copies between rows: pairs[k] = {source row, destination row}.
+hipError_t launch_copy_rows(const CopyPlan& p, const Pair* pairs, const unsigned long long* total,
+                            int64_t max_pairs, hipStream_t s);
 
 // insert.hip
 struct BatchEntry;  // defined in insert.hip
@@ -137,6 +161,10 @@ hipError_t launch_evict(const IndexView& ix, const InsertTarget& tgt, const Evic
                         hipStream_t s);
 hipError_t launch_touch_paths(const IndexView& ix, const EvictView& ev, const int32_t* m,
                               const int32_t* ids, int32_t R, int32_t max_blocks, hipStream_t s);
+
+// evict.hip: make the replica slots hold the hot set of the host tier.
+hipError_t launch_replicate(const IndexView& ix, const EvictView& ev, const CopyPlan& p,
+                            hipStream_t s);
 
 // api.hip helpers
 hipError_t launch_fill_slots(Slot* slots, int64_t n, hipStream_t s);

@@ -21,26 +21,30 @@ PTSTORE_OK, PTSTORE_ERR_INVALID, PTSTORE_ERR_FULL, PTSTORE_ERR_HIP, PTSTORE_ERR_
 PTSTORE_FLAG_WEAK_HASH, PTSTORE_FLAG_COUNTERS, PTSTORE_FLAG_TIMING = 1, 2, 4
 PTSTORE_FLAG_EVICT = 8
 KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT, KIND_SELECT, KIND_EVICT = 0, 1, 2, 3, 4, 5
+KIND_REPLICATE = 6
 
 
 class ptstore_config_t(C.Structure):
     _fields_ = [("num_layers", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("block_tokens", C.c_int32), ("elem_bytes", C.c_int32),
                 ("pool_blocks", C.c_int64), ("index_slots", C.c_int64),
-                ("hash_seed", C.c_uint64), ("flags", C.c_uint32)]
+                ("hash_seed", C.c_uint64), ("flags", C.c_uint32),
+                ("host_blocks", C.c_int64), ("replica_blocks", C.c_int64)]
 
 
 class ptstore_stats_t(C.Structure):
     _fields_ = [(n, C.c_int64) for n in (
         "blocks_stored", "capacity", "index_slots", "block_bytes", "chunk_bytes", "full_events",
         "bad_entries", "probes", "token_compares", "cas_attempts", "cas_failures",
-        "insert_fallbacks", "evictions", "clock", "index_rebuilds")]
+        "insert_fallbacks", "evictions", "clock", "index_rebuilds", "device_blocks", "replicas",
+        "replica_copies")]
 
 
 class ptstore_buffers_t(C.Structure):
     _fields_ = [("pool", C.c_void_p), ("parent", C.c_void_p), ("tokens", C.c_void_p),
                 ("slots", C.c_void_p), ("capacity", C.c_int64), ("index_slots", C.c_int64),
-                ("freq", C.c_void_p), ("prio", C.c_void_p)]
+                ("freq", C.c_void_p), ("prio", C.c_void_p), ("host_pool", C.c_void_p),
+                ("host_blocks", C.c_int64), ("device_blocks", C.c_int64), ("replica_of", C.c_void_p)]
 
 
 class PTStoreError(RuntimeError):
@@ -53,7 +57,7 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_lookup_gather", "ptstore_insert", "ptstore_scatter", "ptstore_stats",
            "ptstore_reset_counters", "ptstore_get_buffers", "ptstore_kernel_times",
            "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
-           "ptstore_bandwidth_probe")
+           "ptstore_bandwidth_probe", "ptstore_replicate")
 
 
 def _load() -> C.CDLL:
@@ -76,6 +80,7 @@ def _load() -> C.CDLL:
         "ptstore_kernel_times": [p, i32, C.POINTER(d), C.POINTER(i64)],
         "ptstore_set_copy_shape": [p, i32, i32, i32],
         "ptstore_bandwidth_probe": [i32, p, p, i64, p],
+        "ptstore_replicate": [p, p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -188,6 +193,10 @@ def ptstore_stats(h) -> dict:
     return {n: getattr(s, n) for n, _ in s._fields_}
 
 
+def ptstore_replicate(h, stream=None) -> None:
+    _check("ptstore_replicate", _lib.ptstore_replicate(h, _stream(stream)))
+
+
 def ptstore_reset_counters(h) -> None:
     _check("ptstore_reset_counters", _lib.ptstore_reset_counters(h))
 
@@ -248,11 +257,14 @@ class PrefixStore:
     """A store on the current device; methods take device tensors."""
 
     def __init__(self, shape: StoreShape, pool_blocks: int, index_slots: int = 0,
-                 hash_seed: int = 0x5EED, flags: int = 0):
+                 hash_seed: int = 0x5EED, flags: int = 0, host_blocks: int = 0,
+                 replica_blocks: int = 0):
         self.shape = shape
         cfg = ptstore_config_t(shape.layers, shape.kv_heads, shape.head_dim, shape.block_tokens,
-                               shape.elem_bytes, pool_blocks, index_slots, hash_seed, flags)
+                               shape.elem_bytes, pool_blocks, index_slots, hash_seed, flags,
+                               host_blocks, replica_blocks)
         self.h = ptstore_create(cfg)
+        self._replicas = replica_blocks
 
     def close(self):
         if getattr(self, "h", None):
@@ -301,6 +313,9 @@ class PrefixStore:
     def scatter(self, ids, created, block_table, cache, stream=None):
         ptstore_scatter(self.h, ids, created, block_table, cache, self.cache_blocks(cache), stream)
 
+    def replicate(self, stream=None):
+        ptstore_replicate(self.h, stream)
+
     def stats(self) -> dict:
         return ptstore_stats(self.h)
 
@@ -317,10 +332,44 @@ class PrefixStore:
         return ptstore_get_buffers(self.h)
 
     def pool_tensor(self) -> torch.Tensor:
-        """The pool as a uint8 [capacity, block_bytes] device tensor (no copy)."""
+        """The device pool as a uint8 [rows, block_bytes] device tensor (no copy): the
+        home of ids below device_blocks, then the replica slots."""
         b = self.buffers()
-        n = b.capacity * self.shape.block_bytes
-        return _wrap_device(b.pool, n, torch.uint8).view(b.capacity, self.shape.block_bytes)
+        rows = b.device_blocks + self._replicas
+        n = rows * self.shape.block_bytes
+        return _wrap_device(b.pool, n, torch.uint8).view(rows, self.shape.block_bytes)
+
+    def host_tensor(self) -> torch.Tensor:
+        """The pinned host tier as a uint8 [host_blocks, block_bytes] CPU tensor (no
+        copy); row j holds block id device_blocks + j."""
+        b = self.buffers()
+        if not b.host_pool:
+            raise ValueError("store has no host tier")
+        n = b.host_blocks * self.shape.block_bytes
+        arr = (C.c_uint8 * n).from_address(b.host_pool)
+        return torch.frombuffer(arr, dtype=torch.uint8).view(b.host_blocks, self.shape.block_bytes)
+
+    def block_bytes_of(self, ids) -> torch.Tensor:
+        """Home bytes of the given block ids, [len(ids), block_bytes] on the device
+        (device tier rows and host tier rows alike; a test helper)."""
+        b = self.buffers()
+        ids = torch.as_tensor(ids, dtype=torch.int64)
+        dev = self.pool_tensor()
+        out = torch.empty((ids.numel(), self.shape.block_bytes), dtype=torch.uint8, device=dev.device)
+        on_dev = ids < b.device_blocks
+        if bool(on_dev.any()):
+            out[on_dev.to(dev.device)] = dev[ids[on_dev].to(dev.device)]
+        if bool((~on_dev).any()):
+            host = self.host_tensor()
+            out[(~on_dev).to(dev.device)] = host[ids[~on_dev] - b.device_blocks].to(dev.device)
+        return out
+
+    def replica_map(self) -> torch.Tensor:
+        """[host_blocks] int32 device tensor: replica slot of each host-tier block, or -1."""
+        b = self.buffers()
+        if not b.replica_of:
+            raise ValueError("store has no replica slots")
+        return _wrap_device(b.replica_of, b.host_blocks, torch.int32)
 
     def meta_tensors(self) -> Tuple[torch.Tensor, torch.Tensor]:
         """(parent [capacity] int32, tokens [capacity, block_tokens] int32), device, no copy."""

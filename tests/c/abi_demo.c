@@ -35,7 +35,9 @@ static int to_dev(void **d, const void *h, size_t n) {
 }
 
 int main(void) {
-    ptstore_config_t cfg = {L, H, D, BT, E, 16, 0, 12345u, 0u};
+    ptstore_config_t cfg = {.num_layers = L, .num_kv_heads = H, .head_dim = D, .block_tokens = BT,
+                            .elem_bytes = E, .pool_blocks = 16, .index_slots = 0,
+                            .hash_seed = 12345u, .flags = 0u, .host_blocks = 0, .replica_blocks = 0};
     ptstore_t *s = NULL;
     CHECK(ptstore_create(&cfg, &s) == PTSTORE_OK, "create");
 

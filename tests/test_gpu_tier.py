@@ -1,0 +1,122 @@
+"""Host-DRAM tier and device replicas of hot host-tier blocks, against the oracle.
+
+Section 4.1 ("Fine-grain multi-level caching", "Replication of popular
+prefixes"): block ids past the device-owned range live in pinned host memory,
+read and written by the same copy kernels; replica slots in device memory
+hold the hot set of the host tier. No result may depend on where bytes live,
+so every output is compared with the oracle's single flat pool, bit for bit;
+the replica set is compared with the oracle's hot set.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from tests.helpers import random_block_batch, block_table_identity, spell_batch
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2607_22648_amd import ptstore as P
+    from tests.twin import Twin, host, to_dev, random_bytes
+
+    EVICT = P.PTSTORE_FLAG_EVICT
+
+
+def _atoms(rng, n, bt, vocab):
+    while True:
+        a = rng.integers(0, vocab, size=(n, bt), dtype=np.int32)
+        if len({r.tobytes() for r in a}) == n:
+            return a
+
+
+def _run(seed, *, pool, host_blocks, replicas=0, flags=0, bt=4, n_atoms=5, max_len=8, maxb=8,
+         rounds=30, p_lookup=0.4, p_replicate=0.3):
+    rng = np.random.default_rng(seed)
+    atoms = _atoms(rng, n_atoms, bt, 1000)
+    t = Twin(2, 1, 8, bt, pool, flags=flags, host_blocks=host_blocks, replica_blocks=replicas)
+    st = t.gpu.stats()
+    assert st["device_blocks"] == pool - replicas
+    assert st["capacity"] == pool - replicas + host_blocks
+    for i in range(rounds):
+        toks, offs = random_block_batch(rng, int(rng.integers(1, 9)), atoms, max_len)
+        R = len(offs) - 1
+        u = rng.random()
+        if replicas and u < p_replicate:
+            t.gpu.replicate()  # not an access: the oracle has nothing to do
+            t.check_replicas(hot_set=True)
+        elif u < p_replicate + p_lookup:
+            t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
+        else:
+            (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, maxb)
+            t.scatter_random(ids, cr, rids, rcr, block_table_identity(R, maxb), seed=seed * 100 + i)
+            if replicas:
+                t.check_replicas(hot_set=False)
+        if flags & EVICT:
+            t.check_evict()
+    t.check_pool()
+    t.check_meta()
+    out = t.gpu.stats()
+    t.close()
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_host_tier_parity(seed):
+    """Ids past the device range live in host memory; everything matches the oracle."""
+    st = _run(seed, pool=6, host_blocks=40)
+    assert st["blocks_stored"] > 6  # the host tier is in use
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_host_tier_full_and_evicting(seed):
+    st = _run(seed, pool=5, host_blocks=9, flags=EVICT, rounds=40)
+    assert st["evictions"] > 0
+
+
+@pytest.mark.parametrize("seed", [5, 6, 7, 8])
+def test_replicas_follow_the_hot_set(seed):
+    st = _run(seed, pool=10, host_blocks=20, replicas=4, flags=EVICT, rounds=50)
+    assert st["replica_copies"] > 0 and st["evictions"] > 0
+
+
+def test_replicas_weak_hash():
+    st = _run(9, pool=8, host_blocks=30, replicas=4, flags=EVICT | P.PTSTORE_FLAG_WEAK_HASH,
+              rounds=40)
+    assert st["replica_copies"] > 0
+
+
+def test_scatter_drops_a_stale_replica():
+    """A replica made before a block's bytes are scattered is dropped by the
+    scatter, and gathers then read the new bytes from the block's home."""
+    blocks = {"A": [1, 2], "B": [3, 4], "C": [5, 6]}
+    t = Twin(1, 1, 8, 2, 4, flags=EVICT, host_blocks=8, replica_blocks=2)
+    toks, offs = spell_batch(["A", "AB", "ABC"], blocks)  # A=0, AB=1 on device; ABC=2 on the host
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, 3)
+    assert t.gpu.stats()["device_blocks"] == 2 and rids[2].tolist() == [0, 1, 2]
+    t.gpu.replicate()
+    t.check_replicas()
+    assert t.gpu.stats()["replicas"] == 1  # block 2, the only host-tier block
+    t.scatter_random(ids, cr, rids, rcr, block_table_identity(3, 3), seed=5)
+    assert t.gpu.stats()["replicas"] == 0
+    t.lookup_gather(toks, offs, 3, block_table_identity(3, 3), 9)
+    t.gpu.replicate()
+    t.check_replicas()
+    t.lookup_gather(toks, offs, 3, block_table_identity(3, 3), 9)  # now from the replica
+    t.check_pool()
+    t.close()
+
+
+def test_tier_config_is_checked():
+    sh = P.StoreShape(1, 1, 8, 2, 2)
+    for kw in (dict(replica_blocks=3, host_blocks=8, flags=EVICT),   # more than half of 4
+               dict(replica_blocks=1, host_blocks=0, flags=EVICT),   # no host tier
+               dict(replica_blocks=1, host_blocks=8, flags=0),       # no access counts
+               dict(host_blocks=-1)):
+        with pytest.raises(P.PTStoreError):
+            P.PrefixStore(sh, 4, **kw)
+    s = P.PrefixStore(sh, 4, host_blocks=8)
+    with pytest.raises(P.PTStoreError):
+        s.replicate()  # no replica slots
+    s.close()

@@ -34,10 +34,11 @@ def random_bytes(n: int, seed: int) -> torch.Tensor:
 
 class Twin:
     def __init__(self, layers, kv_heads, head_dim, block_tokens, capacity, *, elem_bytes=2,
-                 index_slots=0, hash_seed=0x5EED, flags=0, payload=True):
+                 index_slots=0, hash_seed=0x5EED, flags=0, payload=True, host_blocks=0,
+                 replica_blocks=0):
         self.shape = StoreShape(layers, kv_heads, head_dim, block_tokens, elem_bytes)
         self.gpu = PrefixStore(self.shape, capacity, index_slots=index_slots, hash_seed=hash_seed,
-                               flags=flags)
+                               flags=flags, host_blocks=host_blocks, replica_blocks=replica_blocks)
         cap = self.gpu.stats()["capacity"]
         self.evict = bool(flags & PTSTORE_FLAG_EVICT)
         self.ref = OracleStore(layers, kv_heads, head_dim, block_tokens, elem_bytes, cap, payload,
@@ -108,9 +109,10 @@ class Twin:
         return (m, ids, dst), (rm, rids, rdst)
 
     def check_pool(self):
+        """Every block's home bytes (device or host tier) equal the oracle's pool."""
         torch.cuda.synchronize()
         n = self.ref.count
-        got = host(self.gpu.pool_tensor()[:n])
+        got = host(self.gpu.block_bytes_of(np.arange(n)))
         exp = self.ref.pool()[:n]
         if not np.array_equal(got, exp):
             bad = np.flatnonzero((got != exp).any(axis=1))
@@ -138,3 +140,22 @@ class Twin:
         st = self.gpu.stats()
         assert st["clock"] == self.ref.clock, (st["clock"], self.ref.clock)
         assert st["evictions"] == self.ref.evictions, (st["evictions"], self.ref.evictions)
+
+    def check_replicas(self, hot_set=True):
+        """Replica bytes equal their blocks' home bytes; right after a replicate,
+        the replicated blocks are the oracle's hot set of the host tier."""
+        torch.cuda.synchronize()
+        st = self.gpu.stats()
+        owned, R = st["device_blocks"], self.gpu._replicas
+        rep = host(self.gpu.replica_map())
+        have = np.flatnonzero(rep >= 0)
+        assert len(have) == st["replicas"] <= R
+        assert len(set(rep[have].tolist())) == len(have), "two blocks share a replica slot"
+        if len(have):
+            dev = self.gpu.pool_tensor()
+            got = host(dev[torch.from_numpy(owned + rep[have].astype(np.int64)).to(DEV)])
+            exp = host(self.gpu.block_bytes_of(owned + have))
+            np.testing.assert_array_equal(got, exp, err_msg="replica bytes")
+        if hot_set:
+            want = self.ref.hot_set(owned, self.ref.count, R)
+            np.testing.assert_array_equal(owned + have, want, err_msg="replica set")
