@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama8b",
-                    choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream", "stream_evict"])
+                    choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream", "stream_evict",
+                             "llama70b_full"])
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="requests the CPU oracle is timed on (0: skip; -1: the whole batch, "
                          "8 requests for the 70B-shaped shard)")
@@ -211,6 +212,9 @@ WORKLOAD_TEXT = {
     "llama70b_shard": "llama70b-shaped KV (80 x 8 x 128 bf16), 64 req x 32768 tok (30720-tok "
                       "Zipf-1.2 passage of 64 + 2048 fresh), one GPU's shard = odd ranks 1..31 "
                       "(16 passages)",
+    "llama70b_full": "llama70b-shaped KV, all 32 stored passages (322 GB) on one GPU: 48,640 "
+                     "blocks in HBM + 1,920 HBM replica slots + 12,800 blocks in pinned host "
+                     "memory (stored in a seeded random order); 64 req x 32768 tok, 1 per call",
     "trie": "divergent trie, 8192 walks of a 64-level tree (4 children at p=0.1), 1M stored "
             "blocks, 1 x 8 x 128 fp16 KV",
     "stream": "llama8b-shaped store, rounds of 128 lookups+gathers and 128 dedup inserts + "
@@ -309,6 +313,139 @@ def run_passage(args, torch, P, synth, dev):
         "hbm_ceiling": ceiling,
         "prefill": pre,
         "cpu_baseline": cpu,
+    })
+    return out
+
+
+def host_link_ceiling(torch, P, host_ptr: int, sink: torch.Tensor, nbytes: int) -> dict:
+    """Read-only stream over the host tier with the copy kernels' access
+    pattern: the practical host-link rate the tier's gathers can reach."""
+    st = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = 0.0
+    for _ in range(3):
+        a.record(st)
+        P.ptstore_bandwidth_probe(0, host_ptr, sink, nbytes, st)
+        b.record(st)
+        b.synchronize()
+        best = max(best, nbytes / (a.elapsed_time(b) * 1e6))
+    return {"read_GBps": round(best, 1), "bytes": nbytes}
+
+
+def run_tiered(args, torch, P, synth, dev):
+    """All of a too-large store on one GPU: device tier, replica slots, host tier.
+    Steps are timed before and after one ptstore_replicate."""
+    w = synth.build(args.config, seed=args.seed)
+    sh = w.shape
+    tiers = w.tiers
+    owned, R_rep, H_blocks = tiers["device_blocks"], tiers["replica_blocks"], tiers["host_blocks"]
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    t0 = time.time()
+    log(f"allocating {(owned + R_rep) * sh.block_bytes / 2**30:.0f} GiB device + "
+        f"{H_blocks * sh.block_bytes / 2**30:.0f} GiB pinned host ...")
+    store = P.PrefixStore(shape, owned + R_rep, host_blocks=H_blocks, replica_blocks=R_rep,
+                          flags=P.PTSTORE_FLAG_TIMING | P.PTSTORE_FLAG_EVICT)
+    log(f"store: {owned} device + {R_rep} replica rows, {H_blocks} host blocks "
+        f"({time.time() - t0:.1f}s to allocate)")
+    t0 = time.time()
+    pre = prefill(store, w, dev, torch, batch_passages=1)
+    log(f"prefill: {pre} ({time.time() - t0:.1f}s)")
+    subs = w.sub_batches()
+    maxb = w.max_blocks
+    sub_inputs = []
+    for lo, hi in subs:
+        toks, offs = w.request_slice(lo, hi)
+        R = hi - lo
+        sub_inputs.append(dict(
+            R=R, toks=torch.from_numpy(toks).to(dev), offs=torch.from_numpy(offs).to(dev),
+            bt=torch.arange(R * maxb, dtype=torch.int32, device=dev).view(R, maxb),
+            m=torch.empty(R, dtype=torch.int32, device=dev),
+            ids=torch.empty((R, maxb), dtype=torch.int32, device=dev)))
+    max_R = max(s["R"] for s in sub_inputs)
+    cache = torch.full((sh.layers * 2 * max_R * maxb * sh.chunk_bytes,), 0xA5, dtype=torch.uint8,
+                       device=dev)
+    host_ptr = store.buffers().host_pool
+    link = host_link_ceiling(torch, P, host_ptr, cache, min(16 << 30, H_blocks * sh.block_bytes))
+    log(f"host link: {link}")
+
+    def step():
+        for s in sub_inputs:
+            store.lookup_gather(s["toks"], s["offs"], maxb, s["bt"], cache, m=s["m"], ids=s["ids"])
+
+    def where_blocks():
+        """(device-resident, host-resident) gathered blocks per step."""
+        rep = store.replica_map().cpu().numpy()
+        dev_n = host_n = 0
+        for s in sub_inputs:
+            m = s["m"].cpu().numpy()
+            ids = s["ids"].cpu().numpy()
+            for r in range(len(m)):
+                row = ids[r, :m[r]]
+                hr = row[row >= owned] - owned
+                on_host = int((rep[hr] < 0).sum())
+                host_n += on_host
+                dev_n += len(row) - on_host
+        return dev_n, host_n
+
+    def phase(n_steps, n_warm):
+        for _ in range(n_warm):
+            step()
+        torch.cuda.synchronize()
+        store.kernel_times(P.KIND_GATHER)
+        store.kernel_times(P.KIND_LOOKUP)
+        t = time.perf_counter()
+        for _ in range(n_steps):
+            step()
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t
+        g_ms, g_n = store.kernel_times(P.KIND_GATHER)
+        d_n, h_n = where_blocks()
+        host_bytes = h_n * sh.block_bytes  # read over the host link per step
+        return {"requests_per_s": round(w.n_requests * n_steps / el, 2),
+                "ms_per_step": round(el * 1e3 / n_steps, 2),
+                "gather_ms_per_step": round(g_ms / n_steps, 2),
+                "blocks_from_device": d_n, "blocks_from_host": h_n,
+                "host_GB_per_step": round(host_bytes / 1e9, 2),
+                "host_link_GBps": round(host_bytes / (g_ms / n_steps * 1e6), 1) if g_ms else None,
+                "gather_launches": g_n, "_elapsed": el, "_g_ms": g_ms, "_matched": d_n + h_n}
+
+    steps = max(1, min(args.steps, 4))
+    a = phase(steps, args.warmup)
+    log(f"without replicas: {a}")
+    store.kernel_times(P.KIND_REPLICATE)
+    store.replicate()
+    torch.cuda.synchronize()
+    r_ms, _ = store.kernel_times(P.KIND_REPLICATE)
+    st = store.stats()
+    rep = {"replicate_ms": round(r_ms, 2), "blocks_copied": st["replica_copies"],
+           "GBps": round(st["replica_copies"] * sh.block_bytes / (r_ms * 1e6), 1) if r_ms else None}
+    log(f"replicate: {rep}")
+    b = phase(steps, 0)
+    log(f"with replicas: {b}")
+    del cache
+    store.close()
+    torch.cuda.empty_cache()
+    gather_bytes_step = b["_matched"] * 2 * sh.block_bytes
+    out = base_line(args, w.n_requests * steps / b["_elapsed"], "requests/s",
+                    b["_elapsed"] * 1e3 / steps, {
+        "workload": WORKLOAD_TEXT[args.config],
+        "layers": sh.layers, "kv_heads": sh.kv_heads, "head_dim": sh.head_dim,
+        "block_tokens": sh.block_tokens, "kv_dtype": sh.dtype, "requests": w.n_requests,
+        "sub_batch": w.sub_batch, "device_blocks": owned, "replica_blocks": R_rep,
+        "host_blocks": H_blocks, "block_bytes": sh.block_bytes})
+    out["steps"] = steps
+    clean = lambda d: {k: v for k, v in d.items() if not k.startswith("_")}
+    out.update({
+        "roofline": roofline("k_copy_pairs<true> (gather)", gather_bytes_step / len(subs),
+                             b["_g_ms"] / max(b["gather_launches"], 1), b["gather_launches"], None),
+        # the path is bound by the host link: host-tier bytes per step over the
+        # gather time, against the read stream measured on the tier itself
+        "host_link": {"achieved": b["host_link_GBps"], "ceiling": link["read_GBps"],
+                      "frac_of_ceiling": round(b["host_link_GBps"] / link["read_GBps"], 4)
+                      if b["host_link_GBps"] else None, "unit": "GB/s",
+                      "spec": "PCIe 5.0 x16, 64 GB/s per direction"},
+        "with_replicas": clean(b), "without_replicas": clean(a), "replicate": rep,
+        "host_link_ceiling": link, "prefill": pre, "cpu_baseline": None,
     })
     return out
 
@@ -514,6 +651,8 @@ def main():
         out = run_trie(args, torch, P, synth, dev)
     elif args.config in ("stream", "stream_evict"):
         out = run_stream(args, torch, P, synth, dev)
+    elif args.config == "llama70b_full":
+        out = run_tiered(args, torch, P, synth, dev)
     else:
         out = run_passage(args, torch, P, synth, dev)
     print(json.dumps(out), flush=True)

@@ -218,10 +218,13 @@ def ptstore_set_copy_shape(h, chunks_per_group: int = 0, threads: int = 0, grid:
                                                                   grid))
 
 
-def ptstore_bandwidth_probe(kind: int, a: torch.Tensor, b: torch.Tensor, nbytes: int,
-                            stream=None) -> None:
-    _check("ptstore_bandwidth_probe", _lib.ptstore_bandwidth_probe(
-        kind, _dev(a, None, "a"), _dev(b, None, "b"), nbytes, _stream(stream)))
+def ptstore_bandwidth_probe(kind: int, a, b, nbytes: int, stream=None) -> None:
+    """a, b: device tensors, or integer addresses the device can access (such as
+    the pinned host tier)."""
+    pa = a if isinstance(a, int) else _dev(a, None, "a")
+    pb = b if isinstance(b, int) else _dev(b, None, "b")
+    _check("ptstore_bandwidth_probe", _lib.ptstore_bandwidth_probe(kind, pa, pb, nbytes,
+                                                                   _stream(stream)))
 
 
 def ptstore_strerror(code: int) -> str:

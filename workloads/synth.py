@@ -137,6 +137,8 @@ def make_passage_workload(
     stored_ranks: Sequence[int],
     sub_batch: int,
     seed: int = 1234,
+    store_order_seed: Optional[int] = None,
+    tiers: Optional[dict] = None,
 ) -> PassageWorkload:
     rng = np.random.default_rng(seed)
     P = _draw_passages(rng, n_passages, passage_tokens, shape.block_tokens)
@@ -145,7 +147,11 @@ def make_passage_workload(
     seqs = [np.concatenate([P[p], _fresh(rng, suffix_tokens)]) for p in req_passage]
     tokens, offsets = concat_requests(seqs)
     stored = np.asarray([r - 1 for r in stored_ranks], dtype=np.int64)
-    return PassageWorkload(name, shape, P, stored, req_passage, tokens, offsets, sub_batch, seed)
+    if store_order_seed is not None:  # a store filled over time is not sorted by popularity
+        stored = np.random.default_rng(store_order_seed).permutation(stored)
+    w = PassageWorkload(name, shape, P, stored, req_passage, tokens, offsets, sub_batch, seed)
+    w.tiers = tiers
+    return w
 
 
 # ---------------------------------------------------------------------------
@@ -392,6 +398,16 @@ CONFIGS = {
     "llama70b_shard": dict(kind="passage", shape=SHAPE_70B, n_passages=64, passage_tokens=30720,
                            suffix_tokens=2048, n_requests=64, zipf_s=1.2,
                            stored_ranks=list(range(1, 33, 2)), sub_batch=4),
+    # All 32 passages of the 70B-shaped configuration (322 GB) on one GPU:
+    # 48,640 blocks (237.5 GiB) in device memory, one passage's worth of device
+    # replica slots, the remaining 12,800 blocks (62.5 GiB) in pinned host
+    # memory. Passages are inserted in a seeded random order, so hot ones can
+    # land on the host tier; one request per call keeps the paged cache at
+    # 10 GiB.
+    "llama70b_full": dict(kind="passage", shape=SHAPE_70B, n_passages=64, passage_tokens=30720,
+                          suffix_tokens=2048, n_requests=64, zipf_s=1.2,
+                          stored_ranks=list(range(1, 33)), sub_batch=1, store_order_seed=7,
+                          tiers=dict(device_blocks=48640, replica_blocks=1920, host_blocks=12800)),
     # 8192 walks of a 64-level tree (fanout 4 with p=0.1), store = 1M blocks.
     "trie": dict(kind="trie", shape=SHAPE_TRIE, n_requests=8192, depth=64, branch_p=0.1,
                  fanout=4, capacity=1_000_000),
