@@ -488,25 +488,34 @@ int64_t orc_evictions(const ostore_t *s) { return s->evictions; }
  * smaller id; written to out[] in ascending id order. Returns how many were
  * written (fewer than k if the range holds fewer nodes).
  */
+typedef struct { int64_t prio; int32_t id; } hot_key_t;
+
+/* Highest priority first, then the smaller id. */
+static int cmp_hot(const void *a, const void *b)
+{
+    const hot_key_t *x = (const hot_key_t *)a, *y = (const hot_key_t *)b;
+    if (x->prio != y->prio) return x->prio > y->prio ? -1 : 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
 int64_t orc_hot_set(const ostore_t *s, int64_t lo, int64_t hi, int64_t k, int32_t *out)
 {
     if (lo < 0) lo = 0;
     if (hi > s->count) hi = s->count;
+    if (hi <= lo || k <= 0) return 0;
+    hot_key_t *all = (hot_key_t *)malloc((size_t)(hi - lo) * sizeof(hot_key_t));
+    if (!all) abort();  /* test infrastructure: no recovery */
     int64_t n = 0;
-    for (int64_t round = 0; round < k; round++) {
-        /* the best node not taken yet: highest H, then smallest id */
-        const onode_t *best = NULL;
-        for (int64_t i = lo; i < hi; i++) {
-            const onode_t *c = s->by_id[i];
-            if (!c) continue;
-            int taken = 0;
-            for (int64_t j = 0; j < n && !taken; j++) taken = out[j] == c->id;
-            if (taken) continue;
-            if (!best || c->prio > best->prio) best = c;
-        }
-        if (!best) break;
-        out[n++] = best->id;
+    for (int64_t i = lo; i < hi; i++) {
+        if (!s->by_id[i]) continue;
+        all[n].prio = s->by_id[i]->prio;
+        all[n].id = (int32_t)i;
+        n++;
     }
+    qsort(all, (size_t)n, sizeof(hot_key_t), cmp_hot);
+    if (n > k) n = k;
+    for (int64_t j = 0; j < n; j++) out[j] = all[j].id;
+    free(all);
     qsort(out, (size_t)n, sizeof(int32_t), cmp_i32);
     return n;
 }

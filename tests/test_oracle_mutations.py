@@ -45,8 +45,8 @@ MUTANTS = {
     "evict_lookup_not_an_access": ("if (s->evict) touch(s, c);", ";"),
     "evict_plain_lfu": ("n->prio = s->clock + n->freq;", "n->prio = n->freq;"),
     "evict_no_cascade": ("if (best->parent != &s->root) best->parent->live_children--;", ";"),
-    "hot_set_ties_to_larger_id": ("if (!best || c->prio > best->prio) best = c;",
-                                  "if (!best || c->prio >= best->prio) best = c;"),
+    "hot_set_ties_to_larger_id": ("return (x->id > y->id) - (x->id < y->id);",
+                                  "return (x->id < y->id) - (x->id > y->id);"),
     "evict_created_for_every_user": ("if (c->born == s->epoch && c->creator == r) crow[b] = 1;",
                                      "if (c->born == s->epoch) crow[b] = 1;"),
 }
