@@ -271,3 +271,83 @@ def test_stream_full(name, rounds):
         assert st["evictions"] == ref.evictions > 0 and st["clock"] == ref.clock
     del cache
     _free(store, ref)
+
+
+def _check_gather_tiered(store, kv, cache, m_h, ids_h, bt_h, rng, rec=None, per_row=8):
+    """Sampled gathered blocks equal their home bytes (device or host tier);
+    sampled unmatched blocks keep the sentinel; recorded bytes where seen."""
+    nb_cache = cache.numel() // (kv.layers * 2 * kv.chunk_bytes)
+    cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
+    seen = 0
+    for r in range(len(m_h)):
+        if m_h[r]:
+            bs = rng.choice(m_h[r], size=min(per_row, m_h[r]), replace=False)
+            got = cv[:, :, torch.from_numpy(bt_h[r, bs].astype(np.int64)).to(DEV)].permute(2, 0, 1, 3)
+            exp = store.block_bytes_of(ids_h[r, bs]).view(len(bs), kv.layers, 2, kv.chunk_bytes)
+            assert torch.equal(got, exp), f"request {r}: gathered blocks differ from their home"
+        rest = np.arange(m_h[r], ids_h.shape[1])
+        if len(rest):
+            bs = rng.choice(rest, size=min(per_row, len(rest)), replace=False)
+            sel = torch.from_numpy(bt_h[r, bs].astype(np.int64)).to(DEV)
+            assert bool((cv[:, :, sel] == SENTINEL).all()), "gather wrote outside its blocks"
+        if rec is not None:
+            for b in range(m_h[r]):
+                i = int(ids_h[r, b])
+                if i in rec.bytes:
+                    np.testing.assert_array_equal(host(cv[:, :, int(bt_h[r, b])]), rec.bytes[i])
+                    seen += 1
+    return seen
+
+
+def test_llama70b_full_tiered():
+    """All 32 passages (322 GB) on one GPU: HBM, HBM replicas and the pinned
+    host tier. Metadata against the oracle everywhere; payload by sampled
+    home-byte checks and recorded scatter bytes; replicas against the
+    oracle's hot set."""
+    w = synth.build("llama70b_full")
+    kv, tiers = w.shape, w.tiers
+    store = P.PrefixStore(_shape(kv), tiers["device_blocks"] + tiers["replica_blocks"],
+                          flags=P.PTSTORE_FLAG_EVICT, host_blocks=tiers["host_blocks"],
+                          replica_blocks=tiers["replica_blocks"])
+    cap = store.stats()["capacity"]
+    assert cap == len(w.stored) * w.passage_blocks
+    ref = OracleStore.for_shape(kv, cap, with_payload=False, evict=True)
+    rec = Recorder(kv, 96, 9)
+    st_, so = w.store_batch()
+    for k in range(len(so) - 1):
+        insert_scatter(store, ref, kv, st_[so[k]:so[k + 1]], (so[k:k + 2] - so[k]).astype(np.int64),
+                       w.passage_blocks, seed=k, rec=rec, k=3)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    assert store.stats()["blocks_stored"] == ref.count == cap
+    owned = store.stats()["device_blocks"]
+    maxb = w.max_blocks
+    cache = torch.empty(kv.layers * 2 * maxb * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
+    rng = np.random.default_rng(3)
+    seen = 0
+    host_hits = 0
+    for rnd in range(2):
+        for lo, hi in w.sub_batches():
+            toks, offs = w.request_slice(lo, hi)
+            bt_h = np.arange((hi - lo) * maxb, dtype=np.int32).reshape(hi - lo, maxb)
+            cache.fill_(SENTINEL)
+            m, ids = store.lookup_gather(to_dev(toks), to_dev(offs), maxb, to_dev(bt_h), cache)
+            rm, rids = ref.lookup(toks, offs, maxb)
+            m_h, ids_h = host(m), host(ids)
+            np.testing.assert_array_equal(m_h, rm)
+            np.testing.assert_array_equal(ids_h, rids)
+            host_hits += int((ids_h[0, :m_h[0]] >= owned).sum())
+            seen += _check_gather_tiered(store, kv, cache, m_h, ids_h, bt_h, rng, rec)
+        check_access_counts(store, ref)
+        if rnd == 0:  # replicate the host tier's hot set, then read through it
+            store.replicate()
+            torch.cuda.synchronize()
+            rep = host(store.replica_map())
+            have = np.flatnonzero(rep >= 0)
+            np.testing.assert_array_equal(owned + have, ref.hot_set(owned, ref.count, tiers["replica_blocks"]))
+            sample = rng.choice(have, size=min(64, len(have)), replace=False)
+            dev_rows = store.pool_tensor()[torch.from_numpy(owned + rep[sample].astype(np.int64)).to(DEV)]
+            assert torch.equal(dev_rows, store.block_bytes_of(owned + sample))
+    assert host_hits > 0 and seen > 0
+    del cache
+    _free(store, ref)
