@@ -21,7 +21,10 @@
  *     everything stored (Section 4.1, the LCP query), plus the ids along it.
  *   - gather: a load iterates over those ids and copies their tensors into
  *     application-supplied memory (Section 4.1), here a paged cache laid out
- *     [layer][K|V][cache block][head][slot][dim].
+ *     [layer][K|V][cache block][head][slot][dim]. A load may ask for a range
+ *     of layers only (Section 5: clients read and write subsets of tensors),
+ *     and layers may differ in size (Section 5: prefixes are combinations
+ *     of tensors of variable sizes).
  *   - insert: a store saves only the increment beyond the LCP (Section 4),
  *     processing the batch one request after another; new nodes get the next
  *     free id. No node is created beyond the capacity.
@@ -67,9 +70,10 @@ typedef struct onode {
 } onode_t;
 
 typedef struct {
-    int32_t layers, kv_heads, head_dim, block_tokens, elem_bytes;
-    int64_t chunk_bytes;        /* kv_heads * block_tokens * head_dim * elem_bytes */
-    int64_t block_bytes;        /* layers * 2 * chunk_bytes */
+    int32_t layers, block_tokens;
+    int64_t *chunk;             /* [layers] bytes of one (layer, K|V) slab of a block */
+    int64_t *lbase;             /* [layers + 1] 2 * sum of chunk[0..l-1] */
+    int64_t block_bytes;        /* lbase[layers] */
     int64_t capacity;           /* maximum number of nodes */
     int64_t count;              /* nodes created so far (= next id) */
     int64_t bad_entries;        /* skipped out-of-range ids / cache blocks */
@@ -82,31 +86,54 @@ typedef struct {
     uint8_t *pool;              /* capacity * block_bytes, or NULL */
 } ostore_t;
 
-ostore_t *orc_create(int32_t layers, int32_t kv_heads, int32_t head_dim,
-                     int32_t block_tokens, int32_t elem_bytes,
-                     int64_t capacity, int32_t with_payload)
+/*
+ * A store whose layer l keeps slabs of chunk_bytes[l] bytes per block, for
+ * K and for V. Layers of one model may differ (Section 5: tensors of
+ * variable size).
+ */
+ostore_t *orc_create_layers(int32_t layers, int32_t block_tokens, const int64_t *chunk_bytes,
+                            int64_t capacity, int32_t with_payload)
 {
-    if (layers < 1 || kv_heads < 1 || head_dim < 1 || block_tokens < 1 ||
-        elem_bytes < 1 || capacity < 0)
-        return NULL;
+    if (layers < 1 || block_tokens < 1 || capacity < 0 || !chunk_bytes) return NULL;
+    for (int32_t l = 0; l < layers; l++)
+        if (chunk_bytes[l] < 1) return NULL;
     ostore_t *s = (ostore_t *)calloc(1, sizeof(ostore_t));
     if (!s) return NULL;
     s->layers = layers;
-    s->kv_heads = kv_heads;
-    s->head_dim = head_dim;
     s->block_tokens = block_tokens;
-    s->elem_bytes = elem_bytes;
-    s->chunk_bytes = (int64_t)kv_heads * block_tokens * head_dim * elem_bytes;
-    s->block_bytes = (int64_t)layers * 2 * s->chunk_bytes;
+    s->chunk = (int64_t *)malloc((size_t)layers * sizeof(int64_t));
+    s->lbase = (int64_t *)malloc((size_t)(layers + 1) * sizeof(int64_t));
+    if (!s->chunk || !s->lbase) abort();  /* test infrastructure: no recovery */
+    s->lbase[0] = 0;
+    for (int32_t l = 0; l < layers; l++) {
+        s->chunk[l] = chunk_bytes[l];
+        s->lbase[l + 1] = s->lbase[l] + 2 * chunk_bytes[l];
+    }
+    s->block_bytes = s->lbase[layers];
     s->capacity = capacity;
     s->root.id = -1;
     s->root.depth = -1;
     s->by_id = (onode_t **)calloc(capacity > 0 ? (size_t)capacity : 1, sizeof(onode_t *));
-    if (!s->by_id) { free(s); return NULL; }
+    if (!s->by_id) abort();
     if (with_payload && capacity > 0) {
         s->pool = (uint8_t *)calloc((size_t)capacity, (size_t)s->block_bytes);
-        if (!s->pool) { free(s->by_id); free(s); return NULL; }
+        if (!s->pool) { free(s->by_id); free(s->chunk); free(s->lbase); free(s); return NULL; }
     }
+    return s;
+}
+
+/* Every layer the same: slabs of kv_heads * block_tokens * head_dim elements. */
+ostore_t *orc_create(int32_t layers, int32_t kv_heads, int32_t head_dim,
+                     int32_t block_tokens, int32_t elem_bytes,
+                     int64_t capacity, int32_t with_payload)
+{
+    if (layers < 1 || kv_heads < 1 || head_dim < 1 || block_tokens < 1 || elem_bytes < 1)
+        return NULL;
+    int64_t *c = (int64_t *)malloc((size_t)layers * sizeof(int64_t));
+    if (!c) return NULL;
+    for (int32_t l = 0; l < layers; l++) c[l] = (int64_t)kv_heads * block_tokens * head_dim * elem_bytes;
+    ostore_t *s = orc_create_layers(layers, block_tokens, c, capacity, with_payload);
+    free(c);
     return s;
 }
 
@@ -120,6 +147,8 @@ void orc_destroy(ostore_t *s)
     }
     free(s->by_id);
     free(s->pool);
+    free(s->chunk);
+    free(s->lbase);
     free(s);
 }
 
@@ -205,29 +234,34 @@ int orc_lookup(ostore_t *s, const int32_t *tokens, const int64_t *offsets,
     return ORC_OK;
 }
 
-/* Byte offset of (layer l, K|V kv, cache block cb) in the paged cache. */
+/* Byte offset of (layer l, K|V kv, cache block cb) in the paged cache: layer
+ * l occupies 2 * cache_blocks slabs of chunk[l] bytes, after all earlier
+ * layers. */
 static int64_t cache_off(const ostore_t *s, int64_t cache_blocks, int32_t l, int32_t kv,
                          int64_t cb)
 {
-    return (((int64_t)l * 2 + kv) * cache_blocks + cb) * s->chunk_bytes;
+    return cache_blocks * s->lbase[l] + ((int64_t)kv * cache_blocks + cb) * s->chunk[l];
 }
 
 /* Byte offset of (node id, layer l, K|V kv) in the pool. */
 static int64_t pool_off(const ostore_t *s, int64_t id, int32_t l, int32_t kv)
 {
-    return id * s->block_bytes + ((int64_t)l * 2 + kv) * s->chunk_bytes;
+    return id * s->block_bytes + s->lbase[l] + (int64_t)kv * s->chunk[l];
 }
 
 /*
  * Load (Section 4.1): for every matched block b < m[r] whose block-table
- * entry is >= 0, copy each (layer, K|V) slab of pool[ids[r][b]] into
- * cache[layer][K|V][block_table[r][b]]. Out-of-range ids or cache blocks
- * are skipped and counted in bad_entries.
+ * entry is >= 0, copy the (layer, K|V) slabs of layers l0 .. l1-1 of
+ * pool[ids[r][b]] into cache[layer][K|V][block_table[r][b]]. Out-of-range
+ * ids or cache blocks are skipped and counted in bad_entries.
  */
-int orc_gather(ostore_t *s, const int32_t *ids, const int32_t *m, const int32_t *block_table,
-               int32_t R, int32_t max_blocks, uint8_t *cache, int64_t cache_blocks)
+int orc_gather_layers(ostore_t *s, const int32_t *ids, const int32_t *m, const int32_t *block_table,
+                      int32_t R, int32_t max_blocks, int32_t l0, int32_t l1, uint8_t *cache,
+                      int64_t cache_blocks)
 {
-    if (!s->pool || R < 0 || max_blocks < 1 || cache_blocks < 0) return ORC_ERR_INVALID;
+    if (!s->pool || R < 0 || max_blocks < 1 || cache_blocks < 0 || l0 < 0 || l1 > s->layers ||
+        l0 >= l1)
+        return ORC_ERR_INVALID;
     for (int32_t r = 0; r < R; r++) {
         int32_t mr = m[r] < max_blocks ? m[r] : max_blocks;
         for (int32_t b = 0; b < mr; b++) {
@@ -238,13 +272,19 @@ int orc_gather(ostore_t *s, const int32_t *ids, const int32_t *m, const int32_t 
                 s->bad_entries++;
                 continue;
             }
-            for (int32_t l = 0; l < s->layers; l++)
+            for (int32_t l = l0; l < l1; l++)
                 for (int32_t kv = 0; kv < 2; kv++)
                     memcpy(cache + cache_off(s, cache_blocks, l, kv, cb),
-                           s->pool + pool_off(s, id, l, kv), (size_t)s->chunk_bytes);
+                           s->pool + pool_off(s, id, l, kv), (size_t)s->chunk[l]);
         }
     }
     return ORC_OK;
+}
+
+int orc_gather(ostore_t *s, const int32_t *ids, const int32_t *m, const int32_t *block_table,
+               int32_t R, int32_t max_blocks, uint8_t *cache, int64_t cache_blocks)
+{
+    return orc_gather_layers(s, ids, m, block_table, R, max_blocks, 0, s->layers, cache, cache_blocks);
 }
 
 /*
@@ -447,14 +487,16 @@ static int insert_evict(ostore_t *s, const int32_t *tokens, const int64_t *offse
 
 /*
  * Store data: for every (r, b) with created[r][b] = 1 and a block-table
- * entry >= 0, copy each (layer, K|V) slab of cache[..][block_table[r][b]]
- * into pool[ids[r][b]].
+ * entry >= 0, copy the (layer, K|V) slabs of layers l0 .. l1-1 of
+ * cache[..][block_table[r][b]] into pool[ids[r][b]].
  */
-int orc_scatter(ostore_t *s, const int32_t *ids, const uint8_t *created,
-                const int32_t *block_table, int32_t R, int32_t max_blocks,
-                const uint8_t *cache, int64_t cache_blocks)
+int orc_scatter_layers(ostore_t *s, const int32_t *ids, const uint8_t *created,
+                       const int32_t *block_table, int32_t R, int32_t max_blocks, int32_t l0,
+                       int32_t l1, const uint8_t *cache, int64_t cache_blocks)
 {
-    if (!s->pool || R < 0 || max_blocks < 1 || cache_blocks < 0) return ORC_ERR_INVALID;
+    if (!s->pool || R < 0 || max_blocks < 1 || cache_blocks < 0 || l0 < 0 || l1 > s->layers ||
+        l0 >= l1)
+        return ORC_ERR_INVALID;
     for (int32_t r = 0; r < R; r++) {
         for (int32_t b = 0; b < max_blocks; b++) {
             int64_t k = (int64_t)r * max_blocks + b;
@@ -466,13 +508,21 @@ int orc_scatter(ostore_t *s, const int32_t *ids, const uint8_t *created,
                 s->bad_entries++;
                 continue;
             }
-            for (int32_t l = 0; l < s->layers; l++)
+            for (int32_t l = l0; l < l1; l++)
                 for (int32_t kv = 0; kv < 2; kv++)
                     memcpy(s->pool + pool_off(s, id, l, kv),
-                           cache + cache_off(s, cache_blocks, l, kv, cb), (size_t)s->chunk_bytes);
+                           cache + cache_off(s, cache_blocks, l, kv, cb), (size_t)s->chunk[l]);
         }
     }
     return ORC_OK;
+}
+
+int orc_scatter(ostore_t *s, const int32_t *ids, const uint8_t *created,
+                const int32_t *block_table, int32_t R, int32_t max_blocks,
+                const uint8_t *cache, int64_t cache_blocks)
+{
+    return orc_scatter_layers(s, ids, created, block_table, R, max_blocks, 0, s->layers, cache,
+                              cache_blocks);
 }
 
 /* ---- inspection helpers for the tests ---- */

@@ -47,6 +47,12 @@ def _load(path: str = _LIB):
     p, i32, i64, u8p = C.c_void_p, C.c_int32, C.c_int64, C.c_void_p
     lib.orc_create.restype = p
     lib.orc_create.argtypes = [i32, i32, i32, i32, i32, i64, i32]
+    lib.orc_create_layers.restype = p
+    lib.orc_create_layers.argtypes = [i32, i32, p, i64, i32]
+    lib.orc_gather_layers.argtypes = [p, p, p, p, i32, i32, i32, i32, u8p, i64]
+    lib.orc_scatter_layers.argtypes = [p, p, p, p, i32, i32, i32, i32, u8p, i64]
+    lib.orc_gather_layers.restype = C.c_int
+    lib.orc_scatter_layers.restype = C.c_int
     lib.orc_destroy.argtypes = [p]
     lib.orc_lookup.argtypes = [p, p, p, i32, i32, p, p]
     lib.orc_gather.argtypes = [p, p, p, p, i32, i32, u8p, i64]
@@ -82,18 +88,26 @@ def _ptr(a: Optional[np.ndarray]):
 
 
 class OracleStore:
-    """A store of ``capacity`` blocks of ``layers x 2 x heads x block_tokens x head_dim`` elements."""
+    """A store of ``capacity`` blocks of ``layers x 2 x heads x block_tokens x head_dim`` elements,
+    or, with ``layer_chunk_bytes``, of ``layers x 2`` slabs whose size depends on the layer."""
 
     def __init__(self, layers: int, kv_heads: int, head_dim: int, block_tokens: int = 16,
                  elem_bytes: int = 2, capacity: int = 1 << 16, with_payload: bool = True,
-                 lib_path: Optional[str] = None, evict: bool = False):
+                 lib_path: Optional[str] = None, evict: bool = False, layer_chunk_bytes=None):
         self._lib = _load(lib_path or DEFAULT_LIB)
         self.layers, self.kv_heads, self.head_dim = layers, kv_heads, head_dim
         self.block_tokens, self.elem_bytes, self.capacity = block_tokens, elem_bytes, capacity
-        self.chunk_bytes = kv_heads * block_tokens * head_dim * elem_bytes
-        self.block_bytes = layers * 2 * self.chunk_bytes
-        self._h = self._lib.orc_create(layers, kv_heads, head_dim, block_tokens, elem_bytes,
-                                       capacity, 1 if with_payload else 0)
+        if layer_chunk_bytes is None:
+            self.layer_chunk_bytes = [kv_heads * block_tokens * head_dim * elem_bytes] * layers
+            self._h = self._lib.orc_create(layers, kv_heads, head_dim, block_tokens, elem_bytes,
+                                           capacity, 1 if with_payload else 0)
+        else:
+            self.layer_chunk_bytes = [int(c) for c in layer_chunk_bytes]
+            arr = np.asarray(self.layer_chunk_bytes, dtype=np.int64)
+            self._h = self._lib.orc_create_layers(layers, block_tokens, _ptr(arr), capacity,
+                                                  1 if with_payload else 0)
+        self.chunk_bytes = self.layer_chunk_bytes[0]
+        self.block_bytes = 2 * sum(self.layer_chunk_bytes)
         if not self._h:
             raise MemoryError("oracle store allocation failed")
         self.with_payload = with_payload
@@ -145,28 +159,30 @@ class OracleStore:
         return rc, m, ids, created
 
     def gather(self, ids: np.ndarray, m: np.ndarray, block_table: np.ndarray,
-               cache: np.ndarray, cache_blocks: int) -> None:
+               cache: np.ndarray, cache_blocks: int, layers: Optional[Tuple[int, int]] = None) -> None:
         ids = np.ascontiguousarray(ids, dtype=np.int32)
         m = np.ascontiguousarray(m, dtype=np.int32)
         bt = np.ascontiguousarray(block_table, dtype=np.int32)
         assert cache.dtype == np.uint8 and cache.flags.c_contiguous
-        assert cache.size == self.layers * 2 * cache_blocks * self.chunk_bytes
+        assert cache.size == cache_blocks * self.block_bytes
         R, maxb = ids.shape
-        rc = self._lib.orc_gather(self._h, _ptr(ids), _ptr(m), _ptr(bt), R, maxb,
-                                  _ptr(cache), cache_blocks)
+        l0, l1 = layers if layers is not None else (0, self.layers)
+        rc = self._lib.orc_gather_layers(self._h, _ptr(ids), _ptr(m), _ptr(bt), R, maxb, l0, l1,
+                                         _ptr(cache), cache_blocks)
         if rc:
             raise ValueError(f"orc_gather failed: {rc}")
 
     def scatter(self, ids: np.ndarray, created: np.ndarray, block_table: np.ndarray,
-                cache: np.ndarray, cache_blocks: int) -> None:
+                cache: np.ndarray, cache_blocks: int, layers: Optional[Tuple[int, int]] = None) -> None:
         ids = np.ascontiguousarray(ids, dtype=np.int32)
         created = np.ascontiguousarray(created, dtype=np.uint8)
         bt = np.ascontiguousarray(block_table, dtype=np.int32)
         assert cache.dtype == np.uint8 and cache.flags.c_contiguous
-        assert cache.size == self.layers * 2 * cache_blocks * self.chunk_bytes
+        assert cache.size == cache_blocks * self.block_bytes
         R, maxb = ids.shape
-        rc = self._lib.orc_scatter(self._h, _ptr(ids), _ptr(created), _ptr(bt), R, maxb,
-                                   _ptr(cache), cache_blocks)
+        l0, l1 = layers if layers is not None else (0, self.layers)
+        rc = self._lib.orc_scatter_layers(self._h, _ptr(ids), _ptr(created), _ptr(bt), R, maxb,
+                                          l0, l1, _ptr(cache), cache_blocks)
         if rc:
             raise ValueError(f"orc_scatter failed: {rc}")
 

@@ -18,6 +18,7 @@ import pytest
 import oracle.ref as ref
 from tests import test_oracle as pins
 from tests import test_oracle_eviction as evpins
+from tests import test_oracle_layers as lpins
 
 MUTANTS = {
     "match_first_token_only": ("if (memcmp(c->tokens, blk, nbytes) == 0)",
@@ -27,10 +28,14 @@ MUTANTS = {
     "created_never_set": ("                crow[b] = 1;\n", "                crow[b] = 0;\n"),
     "capacity_off_by_one": ("if (s->count >= s->capacity) { full = 1; break; }",
                             "if (s->count + 1 >= s->capacity) { full = 1; break; }"),
-    "cache_layout_transposed": ("return (((int64_t)l * 2 + kv) * cache_blocks + cb) * s->chunk_bytes;",
-                                "return (((int64_t)cb * s->layers + l) * 2 + kv) * s->chunk_bytes;"),
-    "pool_kv_layer_swapped": ("return id * s->block_bytes + ((int64_t)l * 2 + kv) * s->chunk_bytes;",
-                              "return id * s->block_bytes + ((int64_t)kv * s->layers + l) * s->chunk_bytes;"),
+    "cache_layout_transposed": ("return cache_blocks * s->lbase[l] + ((int64_t)kv * cache_blocks + cb) * s->chunk[l];",
+                                "return cb * s->block_bytes + s->lbase[l] + (int64_t)kv * s->chunk[l];"),
+    "pool_kv_layer_swapped": ("return id * s->block_bytes + s->lbase[l] + (int64_t)kv * s->chunk[l];",
+                              "return id * s->block_bytes + (int64_t)kv * (s->block_bytes / 2) + s->lbase[l] / 2;"),
+    "layer_base_off_by_one": ("s->lbase[l + 1] = s->lbase[l] + 2 * chunk_bytes[l];",
+                              "s->lbase[l + 1] = s->lbase[l] + 2 * chunk_bytes[l > 0 ? l - 1 : 0];"),
+    "layer_range_end_inclusive": ("            for (int32_t l = l0; l < l1; l++)\n                for (int32_t kv = 0; kv < 2; kv++)\n                    memcpy(cache",
+                                  "            for (int32_t l = l0; l <= l1 && l < s->layers; l++)\n                for (int32_t kv = 0; kv < 2; kv++)\n                    memcpy(cache"),
     "partial_block_counted": ("int64_t n = len / s->block_tokens;",
                               "int64_t n = (len + s->block_tokens - 1) / s->block_tokens;"),
     "ids_start_at_one": ("c->id = (int32_t)s->count;", "c->id = (int32_t)s->count + 1;"),
@@ -66,6 +71,8 @@ PIN_CALLS = [
     lambda: [evpins.test_evict_random_vs_brute(k) for k in range(4)],
     lambda: [evpins.test_evict_invariants(k) for k in range(2)],
     lambda: [evpins.test_hot_set_is_top_priorities(k) for k in range(3)],
+    lambda: lpins.test_variable_slabs_scatter_then_gather(lpins.CHUNKS),
+    lambda: [lpins.test_layer_range_gather_writes_only_its_layers(a, b) for a, b in ((1, 3), (4, 5))],
 ]
 
 
