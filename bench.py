@@ -307,7 +307,7 @@ def run_passage(args, torch, P, synth, dev):
         "hbm_GBps": round(step_GBps, 1),
         "hbm_frac": round(step_GBps / HBM_PEAK_GBPS, 4),
         "matched_blocks_per_step": matched,
-        "roofline": roofline("k_copy_pairs<true> (gather)", gather_bytes_step / len(subs),
+        "roofline": roofline("k_copy_pairs<true, false> (gather)", gather_bytes_step / len(subs),
                              g_ms / max(g_n, 1), g_n, recorded_traffic(args.config), ceiling),
         "lookup_kernel_avg_ms": round(l_ms / max(l_n, 1), 4),
         "hbm_ceiling": ceiling,
@@ -436,7 +436,7 @@ def run_tiered(args, torch, P, synth, dev):
     out["steps"] = steps
     clean = lambda d: {k: v for k, v in d.items() if not k.startswith("_")}
     out.update({
-        "roofline": roofline("k_copy_pairs<true> (gather)", gather_bytes_step / len(subs),
+        "roofline": roofline("k_copy_pairs<true, false> (gather)", gather_bytes_step / len(subs),
                              b["_g_ms"] / max(b["gather_launches"], 1), b["gather_launches"], None),
         # the path is bound by the host link: host-tier bytes per step over the
         # gather time, against the read stream measured on the tier itself
@@ -550,7 +550,7 @@ def run_trie(args, torch, P, synth, dev):
                         "algorithmic_GBps": round(R * w.depth * LOOKUP_BYTES_PER_BLOCK
                                                   / (lk_avg * 1e6), 1)},
         "matched_blocks": matched,
-        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
+        "roofline": roofline("k_copy_pairs<true, false> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
                              g_n, recorded_traffic("trie")),
         "prefill": {"insert_ms": round(ins_ms, 3), "insert_calls": ins_n,
                     "scatter_ms": round(sc_ms, 3), "blocks": created_total},
@@ -622,7 +622,7 @@ def run_stream(args, torch, P, synth, dev):
         "inserts_per_s": round(per * n_timed / elapsed, 2),
         "matched_blocks": matched, "created_blocks": created,
         "blocks_stored": {"before": blocks0, "after": st["blocks_stored"]},
-        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
+        "roofline": roofline("k_copy_pairs<true, false> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
                              g_ms / max(g_n, 1), g_n, recorded_traffic(args.config)),
         "evictions": st["evictions"], "index_rebuilds": st["index_rebuilds"],
         "full_events": st["full_events"],

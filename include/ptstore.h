@@ -109,14 +109,24 @@ typedef struct {
      * counts). Where a block's bytes are read from never changes a result. */
     int64_t host_blocks;     /* 0: no host tier */
     int64_t replica_blocks;  /* 0: no replicas */
+    /* Per-layer slab sizes (Section 5: prefixes are combinations of tensors
+     * of variable sizes): NULL, or num_layers byte counts, each a positive
+     * multiple of 16, read at create time. Layer l's K and V slabs of a block
+     * are then layer_chunk_bytes[l] bytes each (num_kv_heads, head_dim and
+     * elem_bytes are ignored); a pool block is layer after layer, and layer l
+     * of the paged cache takes 2 * cache_blocks * layer_chunk_bytes[l] bytes
+     * after all earlier layers, as [K|V][cache block][slab]. */
+    const int64_t *layer_chunk_bytes;
 } ptstore_config_t;
 
 typedef struct {
     int64_t blocks_stored;  /* blocks (trie nodes) held, = next id */
     int64_t capacity;       /* maximum blocks_stored */
     int64_t index_slots;
-    int64_t block_bytes;    /* L * 2 * H * block_tokens * D * elem_bytes */
-    int64_t chunk_bytes;    /* H * block_tokens * D * elem_bytes */
+    int64_t block_bytes;    /* L * 2 * H * block_tokens * D * elem_bytes (2 * sum of the
+                               per-layer slab sizes when those are given) */
+    int64_t chunk_bytes;    /* H * block_tokens * D * elem_bytes (layer 0's slab size
+                               when per-layer sizes are given) */
     int64_t full_events;    /* inserts that refused blocks for lack of room */
     int64_t bad_entries;    /* skipped malformed requests, ids or cache blocks */
     int64_t probes;         /* index slots read (PTSTORE_FLAG_COUNTERS) */
@@ -202,6 +212,19 @@ int ptstore_lookup_gather(ptstore_t *store, const int32_t *tokens, const int64_t
                           void *cache, int64_t cache_blocks, void *stream);
 
 /*
+ * Load of a range of layers (Section 4.1: transfers overlap computation;
+ * Section 5: clients read subsets of tensors): as ptstore_gather, but only
+ * the K and V slabs of layers layer_begin .. layer_end-1 are copied; the
+ * cache's other layers are not touched. A caller can so bring in layer l+1
+ * while it computes on layer l. Errors as ptstore_gather, plus INVALID
+ * unless 0 <= layer_begin < layer_end <= num_layers.
+ */
+int ptstore_gather_layers(ptstore_t *store, const int32_t *ids, const int32_t *m,
+                          const int32_t *block_table, int32_t R, int32_t max_blocks,
+                          int32_t layer_begin, int32_t layer_end, void *cache,
+                          int64_t cache_blocks, void *stream);
+
+/*
  * Store (Sections 1 and 4): with the same result as taking the requests one
  * after another, each request reuses the stored blocks of its longest
  * common prefix (including blocks created by earlier requests of this
@@ -243,6 +266,18 @@ int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created
  * (no replica tier), HIP.
  */
 int ptstore_replicate(ptstore_t *store, void *stream);
+
+/*
+ * Store the tensors of a range of layers of new blocks (a prefill can hand
+ * each layer's KV to the store as soon as it is computed): as
+ * ptstore_scatter, but only layers layer_begin .. layer_end-1. Errors as
+ * ptstore_scatter, plus INVALID for a bad range. A block's replica, if any,
+ * is dropped as by ptstore_scatter.
+ */
+int ptstore_scatter_layers(ptstore_t *store, const int32_t *ids, const uint8_t *created,
+                           const int32_t *block_table, int32_t R, int32_t max_blocks,
+                           int32_t layer_begin, int32_t layer_end, const void *cache,
+                           int64_t cache_blocks, void *stream);
 
 /* Wait for the device and read the store's counters into *stats. */
 int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);

@@ -50,6 +50,7 @@ struct ptstore {
     TierView tier;  // owned = capacity and no host rows for a device-only store
     void* tier_mem; // replica map and replicate scratch
     void* host_mem; // the host tier as allocated (tier.host is its device address)
+    void* layer_tab; // per-layer slab sizes then bases, int64 [2][L]; null if uniform
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[7];
     std::vector<hipEvent_t> free_ev;
@@ -130,6 +131,8 @@ CopyPlan copy_plan(ptstore_t* s) {
     p.loop_grid = s->cus * (2048 / s->threads) * 4;
     p.state = s->state;
     p.tier = s->tier;
+    p.lchunk = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) : nullptr;
+    p.lbase = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) + s->cfg.num_layers : nullptr;
     return p;
 }
 
@@ -286,9 +289,24 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
                     "ptstore_create: replica_blocks must be <= pool_blocks/2 and needs host_blocks "
                     "and PTSTORE_FLAG_EVICT");
     const int64_t want_ids = c.pool_blocks - c.replica_blocks + c.host_blocks;
-    const int64_t chunk = (int64_t)c.num_kv_heads * c.block_tokens * c.head_dim * c.elem_bytes;
-    if (chunk % 16 != 0 || chunk > (1ll << 30))
+    int64_t chunk = (int64_t)c.num_kv_heads * c.block_tokens * c.head_dim * c.elem_bytes;
+    int64_t block = chunk * 2 * c.num_layers;
+    std::vector<int64_t> lchunk, lbase;
+    if (c.layer_chunk_bytes) {  // per-layer slab sizes
+        lchunk.assign(c.layer_chunk_bytes, c.layer_chunk_bytes + c.num_layers);
+        lbase.resize(c.num_layers);
+        block = 0;
+        for (int l = 0; l < c.num_layers; ++l) {
+            if (lchunk[l] < 16 || lchunk[l] % 16 != 0 || lchunk[l] > (1ll << 30))
+                return fail(PTSTORE_ERR_INVALID,
+                            "ptstore_create: layer_chunk_bytes must be positive multiples of 16");
+            lbase[l] = block;
+            block += 2 * lchunk[l];
+        }
+        chunk = lchunk[0];
+    } else if (chunk % 16 != 0 || chunk > (1ll << 30)) {
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: chunk bytes must be a multiple of 16");
+    }
     uint64_t slots_n;
     if (c.index_slots == 0) {
         slots_n = next_pow2((uint64_t)(2 * (want_ids > 1 ? want_ids : 1)));
@@ -303,7 +321,8 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     if (!s) return fail(PTSTORE_ERR_NOMEM, "ptstore_create: host allocation");
     s->cfg = c;
     s->chunk_bytes = chunk;
-    s->block_bytes = chunk * 2 * c.num_layers;
+    s->block_bytes = block;
+    s->cfg.layer_chunk_bytes = nullptr;  // the caller's array is not kept
     s->slots_n = slots_n;
     s->capacity = want_ids < (int64_t)(slots_n / 2) ? want_ids : (int64_t)(slots_n / 2);
     {
@@ -336,6 +355,17 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         ptstore_destroy(s);
         (void)hipGetLastError();
         return fail(PTSTORE_ERR_NOMEM, "ptstore_create: hipMalloc", e);
+    }
+    if (!lchunk.empty()) {
+        const size_t n = (size_t)c.num_layers * sizeof(int64_t);
+        if ((e = hipMalloc(&s->layer_tab, 2 * n)) != hipSuccess ||
+            (e = hipMemcpy(s->layer_tab, lchunk.data(), n, hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(static_cast<int64_t*>(s->layer_tab) + c.num_layers, lbase.data(), n,
+                           hipMemcpyHostToDevice)) != hipSuccess) {
+            ptstore_destroy(s);
+            (void)hipGetLastError();
+            return fail(PTSTORE_ERR_NOMEM, "ptstore_create: layer tables", e);
+        }
     }
     if (s->tier.host_blocks > 0) {
         void* h = nullptr;
@@ -422,6 +452,7 @@ int ptstore_destroy(ptstore_t* s) {
     (void)hipFree(s->copy_scratch);
     (void)hipFree(s->ev_mem);
     (void)hipFree(s->tier_mem);
+    (void)hipFree(s->layer_tab);
     if (s->host_mem) (void)hipHostFree(s->host_mem);
     delete s;
     return PTSTORE_OK;
@@ -444,11 +475,14 @@ int ptstore_lookup(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_lookup: launch", e);
 }
 
-int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int32_t* block_table,
-                   int32_t R, int32_t max_blocks, void* cache, int64_t cache_blocks, void* stream) {
+int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
+                          const int32_t* block_table, int32_t R, int32_t max_blocks,
+                          int32_t layer_begin, int32_t layer_end, void* cache, int64_t cache_blocks,
+                          void* stream) {
     if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
         (R > 0 && (!ids || !m || !block_table || !cache)) ||
-        (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        (reinterpret_cast<uintptr_t>(cache) & 15) != 0 || layer_begin < 0 ||
+        layer_end > s->cfg.num_layers || layer_begin >= layer_end)
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather: bad argument");
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
@@ -468,9 +502,16 @@ int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int
     if (e == hipSuccess) {
         Timed t(s, 0, st);
         e = launch_gather_copy(plan, sc, static_cast<uint8_t*>(cache), cache_blocks, R, max_blocks,
-                               st);
+                               layer_begin, layer_end, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_gather: launch", e);
+}
+
+int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int32_t* block_table,
+                   int32_t R, int32_t max_blocks, void* cache, int64_t cache_blocks, void* stream) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_gather: bad argument");
+    return ptstore_gather_layers(s, ids, m, block_table, R, max_blocks, 0, s->cfg.num_layers, cache,
+                                 cache_blocks, stream);
 }
 
 int ptstore_lookup_gather(ptstore_t* s, const int32_t* tokens, const int64_t* offsets,
@@ -521,12 +562,14 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_insert: launch", e);
 }
 
-int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
-                    const int32_t* block_table, int32_t R, int32_t max_blocks, const void* cache,
-                    int64_t cache_blocks, void* stream) {
+int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* created,
+                           const int32_t* block_table, int32_t R, int32_t max_blocks,
+                           int32_t layer_begin, int32_t layer_end, const void* cache,
+                           int64_t cache_blocks, void* stream) {
     if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
         (R > 0 && (!ids || !created || !block_table || !cache)) ||
-        (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        (reinterpret_cast<uintptr_t>(cache) & 15) != 0 || layer_begin < 0 ||
+        layer_end > s->cfg.num_layers || layer_begin >= layer_end)
         return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: bad argument");
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
@@ -546,9 +589,17 @@ int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
     if (e == hipSuccess) {
         Timed t(s, 2, st);
         e = launch_scatter_copy(plan, sc, static_cast<const uint8_t*>(cache), cache_blocks, R,
-                                max_blocks, st);
+                                max_blocks, layer_begin, layer_end, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_scatter: launch", e);
+}
+
+int ptstore_scatter(ptstore_t* s, const int32_t* ids, const uint8_t* created,
+                    const int32_t* block_table, int32_t R, int32_t max_blocks, const void* cache,
+                    int64_t cache_blocks, void* stream) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: bad argument");
+    return ptstore_scatter_layers(s, ids, created, block_table, R, max_blocks, 0, s->cfg.num_layers,
+                                  cache, cache_blocks, stream);
 }
 
 int ptstore_replicate(ptstore_t* s, void* stream) {

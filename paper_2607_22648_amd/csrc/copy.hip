@@ -6,6 +6,10 @@
 // of heads x slots x dim elements, which are contiguous on both sides:
 //   pool  [row][layer][K|V][head][slot][dim]       chunk c at row*block + c*chunk
 //   cache [layer][K|V][cache block][head][slot][dim] chunk c at (c*NB + cb)*chunk
+// (chunk c = layer c/2, K or V by c%2). With per-layer slab sizes, layer l's
+// slabs are lchunk[l] bytes: at row*block + lbase[l] + kv*lchunk[l] in the
+// pool, at NB*lbase[l] + (kv*NB + cb)*lchunk[l] in the cache. A call may
+// move a range of layers only.
 // A block's row is where its bytes are read from: its home in device memory,
 // a device replica of a host-tier block, or its home in the pinned host tier
 // (rows past the device pool), which the same kernel reads over the host
@@ -201,7 +205,10 @@ struct CopyArgs {
     int64_t cache_blocks;
     int32_t chunks_per_block;
     int32_t chunks_per_group;
-    int32_t groups;            // ceil(chunks_per_block / chunks_per_group)
+    int32_t groups;            // ceil((c_hi - c_lo) / chunks_per_group)
+    int32_t c_lo, c_hi;        // chunks moved: 2*l0 .. 2*l1-1
+    const int64_t* lchunk;     // per-layer slab sizes (VAR only)
+    const int64_t* lbase;
 };
 
 // The (descriptor, chunk group) units are visited grid-stride. The host
@@ -210,21 +217,33 @@ struct CopyArgs {
 // workgroups copy neighbouring chunks, the few workgroups past the end exit
 // at once); a scatter, whose created blocks are sparse, launches a few
 // workgroups per compute unit that loop.
-template <bool GATHER>
+// VAR: per-layer slab sizes, read from the layer tables.
+template <bool GATHER, bool VAR>
 __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
     const unsigned long long units = *a.total * (unsigned long long)a.groups;
-    const int n16 = (int)(a.chunk_bytes >> 4);
     for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const unsigned long long d = unit / (unsigned)a.groups;
         const int g = (int)(unit - d * (unsigned)a.groups);
         const Pair p = a.pairs[d];
-        const int c0 = g * a.chunks_per_group;
-        const int c1 = min(c0 + a.chunks_per_group, a.chunks_per_block);
+        const int c0 = a.c_lo + g * a.chunks_per_group;
+        const int c1 = min(c0 + a.chunks_per_group, a.c_hi);
         uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
                                           : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
         for (int c = c0; c < c1; ++c) {
-            uint8_t* src = blk + (int64_t)c * a.chunk_bytes;
-            uint8_t* dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
+            uint8_t* src;
+            uint8_t* dst;
+            int n16;
+            if (VAR) {
+                const int l = c >> 1, kv = c & 1;
+                const int64_t ch = a.lchunk[l], lb = a.lbase[l];
+                src = blk + lb + kv * ch;
+                dst = a.cache + a.cache_blocks * lb + ((int64_t)kv * a.cache_blocks + p.cb) * ch;
+                n16 = (int)(ch >> 4);
+            } else {
+                src = blk + (int64_t)c * a.chunk_bytes;
+                dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
+                n16 = (int)(a.chunk_bytes >> 4);
+            }
             if (GATHER)
                 copy_span(reinterpret_cast<const v4u*>(src), reinterpret_cast<v4u*>(dst), n16);
             else
@@ -234,21 +253,24 @@ __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
 }
 
 // Whole blocks from one row to another (replication): pairs[k].row is the
-// source row, pairs[k].cb the destination row; *total pairs.
+// source row, pairs[k].cb the destination row; *total pairs. A block is
+// moved in pieces of kRowPiece bytes whatever its layers.
+constexpr int64_t kRowPiece = 32 << 10;
+
 __global__ __launch_bounds__(1024) void k_copy_rows(CopyArgs a) {
-    const unsigned long long units = *a.total * (unsigned long long)a.chunks_per_block;
-    const int n16 = (int)(a.chunk_bytes >> 4);
+    const int64_t pieces = (a.block_bytes + kRowPiece - 1) / kRowPiece;
+    const unsigned long long units = *a.total * (unsigned long long)pieces;
     for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
-        const unsigned long long d = unit / (unsigned)a.chunks_per_block;
-        const int c = (int)(unit - d * (unsigned)a.chunks_per_block);
+        const unsigned long long d = unit / (unsigned long long)pieces;
+        const int64_t off = (int64_t)(unit - d * (unsigned long long)pieces) * kRowPiece;
+        const int n16 = (int)(min(kRowPiece, a.block_bytes - off) >> 4);
         const Pair p = a.pairs[d];
         const int64_t rows[2] = {p.row, p.cb};
         uint8_t* blk[2];
         for (int k = 0; k < 2; ++k)
             blk[k] = rows[k] < a.dev_rows ? a.pool + rows[k] * a.block_bytes
                                           : a.host + (rows[k] - a.dev_rows) * a.block_bytes;
-        copy_span(reinterpret_cast<const v4u*>(blk[0] + (int64_t)c * a.chunk_bytes),
-                  reinterpret_cast<v4u*>(blk[1] + (int64_t)c * a.chunk_bytes), n16);
+        copy_span(reinterpret_cast<const v4u*>(blk[0] + off), reinterpret_cast<v4u*>(blk[1] + off), n16);
     }
 }
 
@@ -269,7 +291,7 @@ hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, 
 
 template <bool GATHER>
 hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_t cache_blocks,
-                int32_t R, int32_t max_blocks, hipStream_t s) {
+                int32_t R, int32_t max_blocks, int32_t l0, int32_t l1, hipStream_t s) {
     CopyArgs a{};
     a.pool = p.pool;
     a.host = p.tier.host;
@@ -282,14 +304,21 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     a.cache_blocks = cache_blocks;
     a.chunks_per_block = p.chunks_per_block;
     a.chunks_per_group = p.chunks_per_group;
-    a.groups = (p.chunks_per_block + p.chunks_per_group - 1) / p.chunks_per_group;
+    a.c_lo = 2 * l0;
+    a.c_hi = 2 * l1;
+    a.lchunk = p.lchunk;
+    a.lbase = p.lbase;
+    a.groups = (a.c_hi - a.c_lo + p.chunks_per_group - 1) / p.chunks_per_group;
     const int64_t bound = (int64_t)R * max_blocks * a.groups;  // units if every entry moves
     const int64_t cap = (1ll << 31) / p.threads;                 // launch limit on work-items
     int64_t grid = p.grid ? p.grid : (GATHER ? bound : (int64_t)p.loop_grid);
     if (grid > bound) grid = bound;
     if (grid > cap) grid = cap;
     if (grid < 1) return hipSuccess;
-    hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+    if (p.lchunk)
+        hipLaunchKernelGGL((k_copy_pairs<GATHER, true>), dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_copy_pairs<GATHER, false>), dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     return hipGetLastError();
 }
 
@@ -307,7 +336,7 @@ hipError_t launch_copy_rows(const CopyPlan& p, const Pair* pairs, const unsigned
     a.chunk_bytes = p.chunk_bytes;
     a.chunks_per_block = p.chunks_per_block;
     int64_t grid = (int64_t)p.loop_grid;
-    const int64_t bound = max_pairs * p.chunks_per_block;
+    const int64_t bound = max_pairs * ((p.block_bytes + kRowPiece - 1) / kRowPiece);
     if (grid > bound) grid = bound;
     if (grid < 1) return hipSuccess;
     hipLaunchKernelGGL(k_copy_rows, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
@@ -344,13 +373,15 @@ hipError_t launch_scatter_select(const CopyPlan& p, const CopyScratch& sc, const
 }
 
 hipError_t launch_gather_copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache,
-                              int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s) {
-    return copy<true>(p, sc, cache, cache_blocks, R, max_blocks, s);
+                              int64_t cache_blocks, int32_t R, int32_t max_blocks, int32_t l0,
+                              int32_t l1, hipStream_t s) {
+    return copy<true>(p, sc, cache, cache_blocks, R, max_blocks, l0, l1, s);
 }
 
 hipError_t launch_scatter_copy(const CopyPlan& p, const CopyScratch& sc, const uint8_t* cache,
-                               int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s) {
-    return copy<false>(p, sc, const_cast<uint8_t*>(cache), cache_blocks, R, max_blocks, s);
+                               int64_t cache_blocks, int32_t R, int32_t max_blocks, int32_t l0,
+                               int32_t l1, hipStream_t s) {
+    return copy<false>(p, sc, const_cast<uint8_t*>(cache), cache_blocks, R, max_blocks, l0, l1, s);
 }
 
 }  // namespace ptsd

@@ -97,6 +97,10 @@ struct CopyPlan {
     int32_t loop_grid;         // workgroups of a looping (sparse) copy
     DevState* state;
     TierView tier;
+    // per-layer slab sizes (null when every layer has chunk_bytes): device
+    // tables lchunk[l] and lbase[l] = 2 * sum of lchunk[0..l-1]
+    const int64_t* lchunk;
+    const int64_t* lbase;
 };
 
 
@@ -116,10 +120,13 @@ hipError_t launch_gather_select(const CopyPlan& p, const CopyScratch& sc, const 
 hipError_t launch_scatter_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,
                                  const uint8_t* created, const int32_t* block_table, int32_t R,
                                  int32_t max_blocks, int64_t cache_blocks, hipStream_t s);
+// Copies of layers l0 .. l1-1 of the listed blocks.
 hipError_t launch_gather_copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache,
-                              int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s);
+                              int64_t cache_blocks, int32_t R, int32_t max_blocks, int32_t l0,
+                              int32_t l1, hipStream_t s);
 hipError_t launch_scatter_copy(const CopyPlan& p, const CopyScratch& sc, const uint8_t* cache,
-                               int64_t cache_blocks, int32_t R, int32_t max_blocks, hipStream_t s);
+                               int64_t cache_blocks, int32_t R, int32_t max_blocks, int32_t l0,
+                               int32_t l1, hipStream_t s);
 // Whole-block copies between rows: pairs[k] = {source row, destination row}.
 hipError_t launch_copy_rows(const CopyPlan& p, const Pair* pairs, const unsigned long long* total,
                             int64_t max_pairs, hipStream_t s);

@@ -29,7 +29,8 @@ class ptstore_config_t(C.Structure):
                 ("block_tokens", C.c_int32), ("elem_bytes", C.c_int32),
                 ("pool_blocks", C.c_int64), ("index_slots", C.c_int64),
                 ("hash_seed", C.c_uint64), ("flags", C.c_uint32),
-                ("host_blocks", C.c_int64), ("replica_blocks", C.c_int64)]
+                ("host_blocks", C.c_int64), ("replica_blocks", C.c_int64),
+                ("layer_chunk_bytes", C.c_void_p)]
 
 
 class ptstore_stats_t(C.Structure):
@@ -57,7 +58,8 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_lookup_gather", "ptstore_insert", "ptstore_scatter", "ptstore_stats",
            "ptstore_reset_counters", "ptstore_get_buffers", "ptstore_kernel_times",
            "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
-           "ptstore_bandwidth_probe", "ptstore_replicate")
+           "ptstore_bandwidth_probe", "ptstore_replicate", "ptstore_gather_layers",
+           "ptstore_scatter_layers")
 
 
 def _load() -> C.CDLL:
@@ -81,6 +83,8 @@ def _load() -> C.CDLL:
         "ptstore_set_copy_shape": [p, i32, i32, i32],
         "ptstore_bandwidth_probe": [i32, p, p, i64, p],
         "ptstore_replicate": [p, p],
+        "ptstore_gather_layers": [p, p, p, p, i32, i32, i32, i32, p, i64, p],
+        "ptstore_scatter_layers": [p, p, p, p, i32, i32, i32, i32, p, i64, p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -145,9 +149,10 @@ def ptstore_lookup(h, tokens, offsets, max_blocks, m, ids, stream=None) -> None:
         _stream(stream)))
 
 
-def _cache_blocks(cache: torch.Tensor, chunk_bytes: int, layers: int) -> int:
+def _cache_blocks(cache: torch.Tensor, block_bytes: int) -> int:
+    """Cache blocks a flat paged cache holds (every layer's slabs of one block)."""
     nbytes = cache.numel() * cache.element_size()
-    per = chunk_bytes * 2 * layers
+    per = block_bytes
     if nbytes % per:
         raise ValueError("cache size is not a whole number of blocks")
     return nbytes // per
@@ -159,6 +164,24 @@ def ptstore_gather(h, ids, m, block_table, cache, cache_blocks, stream=None) -> 
         h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, _dev(cache, None, "cache"),
         cache_blocks, _stream(stream)))
+
+
+def ptstore_gather_layers(h, ids, m, block_table, layer_begin, layer_end, cache, cache_blocks,
+                          stream=None) -> None:
+    R, maxb = ids.shape
+    _check("ptstore_gather_layers", _lib.ptstore_gather_layers(
+        h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
+        _dev(block_table, torch.int32, "block_table"), R, maxb, layer_begin, layer_end,
+        _dev(cache, None, "cache"), cache_blocks, _stream(stream)))
+
+
+def ptstore_scatter_layers(h, ids, created, block_table, layer_begin, layer_end, cache,
+                           cache_blocks, stream=None) -> None:
+    R, maxb = ids.shape
+    _check("ptstore_scatter_layers", _lib.ptstore_scatter_layers(
+        h, _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"),
+        _dev(block_table, torch.int32, "block_table"), R, maxb, layer_begin, layer_end,
+        _dev(cache, None, "cache"), cache_blocks, _stream(stream)))
 
 
 def ptstore_lookup_gather(h, tokens, offsets, max_blocks, m, ids, block_table, cache, cache_blocks,
@@ -246,13 +269,19 @@ class StoreShape:
     head_dim: int
     block_tokens: int = 16
     elem_bytes: int = 2
+    layer_chunk_bytes: Optional[Tuple[int, ...]] = None  # per-layer slab sizes, or uniform
 
     @property
     def chunk_bytes(self) -> int:
+        """Slab bytes of layer 0 (of every layer when they are uniform)."""
+        if self.layer_chunk_bytes:
+            return int(self.layer_chunk_bytes[0])
         return self.kv_heads * self.block_tokens * self.head_dim * self.elem_bytes
 
     @property
     def block_bytes(self) -> int:
+        if self.layer_chunk_bytes:
+            return 2 * int(sum(self.layer_chunk_bytes))
         return self.layers * 2 * self.chunk_bytes
 
 
@@ -263,10 +292,14 @@ class PrefixStore:
                  hash_seed: int = 0x5EED, flags: int = 0, host_blocks: int = 0,
                  replica_blocks: int = 0):
         self.shape = shape
+        lcb = None
+        if shape.layer_chunk_bytes:
+            lcb = (C.c_int64 * shape.layers)(*[int(x) for x in shape.layer_chunk_bytes])
         cfg = ptstore_config_t(shape.layers, shape.kv_heads, shape.head_dim, shape.block_tokens,
                                shape.elem_bytes, pool_blocks, index_slots, hash_seed, flags,
-                               host_blocks, replica_blocks)
-        self.h = ptstore_create(cfg)
+                               host_blocks, replica_blocks,
+                               C.cast(lcb, C.c_void_p) if lcb is not None else None)
+        self.h = ptstore_create(cfg)  # the slab-size array is read here and not kept
         self._replicas = replica_blocks
 
     def close(self):
@@ -281,7 +314,7 @@ class PrefixStore:
             pass
 
     def cache_blocks(self, cache: torch.Tensor) -> int:
-        return _cache_blocks(cache, self.shape.chunk_bytes, self.shape.layers)
+        return _cache_blocks(cache, self.shape.block_bytes)
 
     def lookup(self, tokens, offsets, max_blocks, m=None, ids=None, stream=None):
         R = offsets.numel() - 1
@@ -291,8 +324,13 @@ class PrefixStore:
         ptstore_lookup(self.h, tokens, offsets, max_blocks, m, ids, stream)
         return m, ids
 
-    def gather(self, ids, m, block_table, cache, stream=None):
-        ptstore_gather(self.h, ids, m, block_table, cache, self.cache_blocks(cache), stream)
+    def gather(self, ids, m, block_table, cache, stream=None, layers=None):
+        """layers = (begin, end): only those layers' slabs (None: all)."""
+        if layers is None:
+            ptstore_gather(self.h, ids, m, block_table, cache, self.cache_blocks(cache), stream)
+        else:
+            ptstore_gather_layers(self.h, ids, m, block_table, layers[0], layers[1], cache,
+                                  self.cache_blocks(cache), stream)
 
     def lookup_gather(self, tokens, offsets, max_blocks, block_table, cache, m=None, ids=None,
                       stream=None):
@@ -313,8 +351,14 @@ class PrefixStore:
         ptstore_insert(self.h, tokens, offsets, max_blocks, m, ids, created, stream)
         return m, ids, created
 
-    def scatter(self, ids, created, block_table, cache, stream=None):
-        ptstore_scatter(self.h, ids, created, block_table, cache, self.cache_blocks(cache), stream)
+    def scatter(self, ids, created, block_table, cache, stream=None, layers=None):
+        """layers = (begin, end): only those layers' slabs (None: all)."""
+        if layers is None:
+            ptstore_scatter(self.h, ids, created, block_table, cache, self.cache_blocks(cache),
+                            stream)
+        else:
+            ptstore_scatter_layers(self.h, ids, created, block_table, layers[0], layers[1], cache,
+                                   self.cache_blocks(cache), stream)
 
     def replicate(self, stream=None):
         ptstore_replicate(self.h, stream)

@@ -35,14 +35,15 @@ def random_bytes(n: int, seed: int) -> torch.Tensor:
 class Twin:
     def __init__(self, layers, kv_heads, head_dim, block_tokens, capacity, *, elem_bytes=2,
                  index_slots=0, hash_seed=0x5EED, flags=0, payload=True, host_blocks=0,
-                 replica_blocks=0):
-        self.shape = StoreShape(layers, kv_heads, head_dim, block_tokens, elem_bytes)
+                 replica_blocks=0, layer_chunk_bytes=None):
+        lcb = tuple(layer_chunk_bytes) if layer_chunk_bytes else None
+        self.shape = StoreShape(layers, kv_heads, head_dim, block_tokens, elem_bytes, lcb)
         self.gpu = PrefixStore(self.shape, capacity, index_slots=index_slots, hash_seed=hash_seed,
                                flags=flags, host_blocks=host_blocks, replica_blocks=replica_blocks)
         cap = self.gpu.stats()["capacity"]
         self.evict = bool(flags & PTSTORE_FLAG_EVICT)
         self.ref = OracleStore(layers, kv_heads, head_dim, block_tokens, elem_bytes, cap, payload,
-                               evict=self.evict)
+                               evict=self.evict, layer_chunk_bytes=lcb)
         self.capacity = cap
         self.payload = payload
 
@@ -81,17 +82,18 @@ class Twin:
         return (m, ids), (rm, rids)
 
     def scatter_random(self, ids_dev, created_dev, rids, rcreated, block_table: np.ndarray,
-                       seed: int, cache_blocks: Optional[int] = None):
-        """Fill a cache with seeded random bytes and scatter the created blocks."""
+                       seed: int, cache_blocks: Optional[int] = None, layers=None):
+        """Fill a cache with seeded random bytes and scatter the created blocks
+        (only layers[0] .. layers[1]-1 if given)."""
         nb = int(block_table.max()) + 1 if block_table.size else 1
         nb = max(nb, cache_blocks or 0)
-        cache = random_bytes(self.shape.layers * 2 * nb * self.shape.chunk_bytes, seed)
-        self.gpu.scatter(ids_dev, created_dev, to_dev(block_table), cache)
-        self.ref.scatter(rids, rcreated, block_table, host(cache), nb)
+        cache = random_bytes(nb * self.shape.block_bytes, seed)
+        self.gpu.scatter(ids_dev, created_dev, to_dev(block_table), cache, layers=layers)
+        self.ref.scatter(rids, rcreated, block_table, host(cache), nb, layers=layers)
 
     def lookup_gather(self, tokens, offsets, max_blocks, block_table: np.ndarray, cache_blocks: int,
                       sentinel=0xA5, check=True):
-        n = self.shape.layers * 2 * cache_blocks * self.shape.chunk_bytes
+        n = cache_blocks * self.shape.block_bytes
         dst = torch.full((n,), sentinel, dtype=torch.uint8, device=DEV)
         m, ids = self.gpu.lookup_gather(to_dev(tokens), to_dev(offsets), max_blocks,
                                         to_dev(block_table), dst)
@@ -107,6 +109,24 @@ class Twin:
                 bad = np.flatnonzero(got != rdst)
                 raise AssertionError(f"gathered bytes differ at {bad.size} positions, first {bad[:8]}")
         return (m, ids, dst), (rm, rids, rdst)
+
+    def gather_layers(self, m_dev, ids_dev, rm, rids, block_table: np.ndarray, cache_blocks: int,
+                      layers, dst: Optional[torch.Tensor] = None, rdst: Optional[np.ndarray] = None,
+                      sentinel=0xA5):
+        """Gather layers[0] .. layers[1]-1 of already-looked-up blocks on both sides
+        into caches (new sentinel-filled ones unless given) and compare all bytes."""
+        n = cache_blocks * self.shape.block_bytes
+        if dst is None:
+            dst = torch.full((n,), sentinel, dtype=torch.uint8, device=DEV)
+            rdst = np.full(n, sentinel, dtype=np.uint8)
+        self.gpu.gather(ids_dev, m_dev, to_dev(block_table), dst, layers=layers)
+        self.ref.gather(rids, rm, block_table, rdst, cache_blocks, layers=layers)
+        torch.cuda.synchronize()
+        got = host(dst)
+        if not np.array_equal(got, rdst):
+            bad = np.flatnonzero(got != rdst)
+            raise AssertionError(f"layers {layers}: bytes differ at {bad.size} positions, first {bad[:8]}")
+        return dst, rdst
 
     def check_pool(self):
         """Every block's home bytes (device or host tier) equal the oracle's pool."""
