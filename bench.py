@@ -48,13 +48,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama8b",
                     choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream", "stream_evict",
-                             "llama70b_full"])
+                             "llama70b_full", "hybrid8b"])
     ap.add_argument("--cpu-sample", type=int, default=-1,
                     help="requests the CPU oracle is timed on (0: skip; -1: the whole batch, "
                          "8 requests for the 70B-shaped shard)")
     ap.add_argument("--copy-shape", default="",
                     help="chunks_per_group,threads[,grid] of the copy kernels")
     ap.add_argument("--seed", type=int, default=1234)
+    ap.add_argument("--per-layer", action="store_true",
+                    help="passage configs: gather one layer per call (a pipelined load)")
     return ap.parse_args()
 
 
@@ -93,7 +95,7 @@ def prefill(store, w, dev, torch, batch_passages: int):
         R = hi - lo
         toks = torch.from_numpy(st_toks[st_offs[lo]:st_offs[hi]]).to(dev)
         offs = torch.from_numpy((st_offs[lo:hi + 1] - st_offs[lo]).astype(np.int64)).to(dev)
-        n_cache = sh.layers * 2 * R * nb * sh.chunk_bytes
+        n_cache = R * nb * sh.block_bytes
         if cache is None or cache.numel() != n_cache:
             cache = torch.empty(n_cache, dtype=torch.uint8, device=dev)
         g.manual_seed(1000 + lo)
@@ -131,7 +133,7 @@ def cpu_baseline(w, sample: int):
     subs = [(lo, min(hi, sample)) for lo, hi in w.sub_batches() if lo < sample]
     max_R = max(hi - lo for lo, hi in subs)
     cache_blocks = max_R * maxb
-    cache = np.empty(sh.layers * 2 * cache_blocks * sh.chunk_bytes, dtype=np.uint8)
+    cache = np.empty(cache_blocks * sh.block_bytes, dtype=np.uint8)
     cache[:] = 0xA5
     moved = 0
     dt = 0.0
@@ -215,6 +217,9 @@ WORKLOAD_TEXT = {
     "llama70b_full": "llama70b-shaped KV, all 32 stored passages (322 GB) on one GPU: 48,640 "
                      "blocks in HBM + 1,920 HBM replica slots + 12,800 blocks in pinned host "
                      "memory (stored in a seeded random order); 64 req x 32768 tok, 1 per call",
+    "hybrid8b": "hybrid 32-layer KV (layers alternate 8 and 2 KV heads of 128, bf16: 32 KiB and "
+                "8 KiB slabs, 1.25 MiB blocks), 256 req x 4096 tok (3584-tok Zipf-1.1 passage of "
+                "512 + 512 fresh), store = top-256 passages",
     "trie": "divergent trie, 8192 walks of a 64-level tree (4 children at p=0.1), 1M stored "
             "blocks, 1 x 8 x 128 fp16 KV",
     "stream": "llama8b-shaped store, rounds of 128 lookups+gathers and 128 dedup inserts + "
@@ -230,7 +235,8 @@ def run_passage(args, torch, P, synth, dev):
     log(f"workload {args.config}: {w.n_requests} requests, max_blocks {w.max_blocks}, "
         f"{len(w.stored)} stored passages")
     sh = w.shape
-    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes,
+                         sh.layer_chunk_bytes)
     pool_blocks = len(w.stored) * w.passage_blocks
     store = P.PrefixStore(shape, pool_blocks, flags=P.PTSTORE_FLAG_TIMING)
     if args.copy_shape:
@@ -255,13 +261,18 @@ def run_passage(args, torch, P, synth, dev):
             m=torch.empty(R, dtype=torch.int32, device=dev),
             ids=torch.empty((R, maxb), dtype=torch.int32, device=dev)))
     max_R = max(s["R"] for s in sub_inputs)
-    cache = torch.full((sh.layers * 2 * max_R * maxb * sh.chunk_bytes,), 0xA5, dtype=torch.uint8,
-                       device=dev)
+    cache = torch.full((max_R * maxb * sh.block_bytes,), 0xA5, dtype=torch.uint8, device=dev)
     log(f"cache {cache.numel() / 1e9:.1f} GB, {len(subs)} sub-batches")
 
     def step():
         for s in sub_inputs:
-            store.lookup_gather(s["toks"], s["offs"], maxb, s["bt"], cache, m=s["m"], ids=s["ids"])
+            if args.per_layer:  # a pipelined load: one gather per layer
+                store.lookup(s["toks"], s["offs"], maxb, m=s["m"], ids=s["ids"])
+                for l in range(sh.layers):
+                    store.gather(s["ids"], s["m"], s["bt"], cache, layers=(l, l + 1))
+            else:
+                store.lookup_gather(s["toks"], s["offs"], maxb, s["bt"], cache, m=s["m"],
+                                    ids=s["ids"])
 
     for _ in range(args.warmup):
         step()
@@ -302,13 +313,17 @@ def run_passage(args, torch, P, synth, dev):
         "layers": sh.layers, "kv_heads": sh.kv_heads, "head_dim": sh.head_dim,
         "block_tokens": sh.block_tokens, "kv_dtype": sh.dtype,
         "requests": w.n_requests, "sub_batches": len(subs), "sub_batch": w.sub_batch,
-        "stored_blocks": st["blocks_stored"], "block_bytes": sh.block_bytes})
+        "stored_blocks": st["blocks_stored"], "block_bytes": sh.block_bytes,
+        "gather_calls": "one per layer" if args.per_layer else "one per sub-batch"})
     out.update({
         "hbm_GBps": round(step_GBps, 1),
         "hbm_frac": round(step_GBps / HBM_PEAK_GBPS, 4),
         "matched_blocks_per_step": matched,
-        "roofline": roofline("k_copy_pairs<true, false> (gather)", gather_bytes_step / len(subs),
-                             g_ms / max(g_n, 1), g_n, recorded_traffic(args.config), ceiling),
+        "roofline": roofline("k_copy_pairs<true> (gather)" if not sh.layer_chunk_bytes
+                             else "k_copy_spans<true> (gather)",
+                             gather_bytes_step * args.steps / max(g_n, 1),
+                             g_ms / max(g_n, 1), g_n,
+                             None if args.per_layer else recorded_traffic(args.config), ceiling),
         "lookup_kernel_avg_ms": round(l_ms / max(l_n, 1), 4),
         "hbm_ceiling": ceiling,
         "prefill": pre,
@@ -339,7 +354,8 @@ def run_tiered(args, torch, P, synth, dev):
     sh = w.shape
     tiers = w.tiers
     owned, R_rep, H_blocks = tiers["device_blocks"], tiers["replica_blocks"], tiers["host_blocks"]
-    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes,
+                         sh.layer_chunk_bytes)
     t0 = time.time()
     log(f"allocating {(owned + R_rep) * sh.block_bytes / 2**30:.0f} GiB device + "
         f"{H_blocks * sh.block_bytes / 2**30:.0f} GiB pinned host ...")
@@ -436,7 +452,7 @@ def run_tiered(args, torch, P, synth, dev):
     out["steps"] = steps
     clean = lambda d: {k: v for k, v in d.items() if not k.startswith("_")}
     out.update({
-        "roofline": roofline("k_copy_pairs<true, false> (gather)", gather_bytes_step / len(subs),
+        "roofline": roofline("k_copy_pairs<true> (gather)", gather_bytes_step / len(subs),
                              b["_g_ms"] / max(b["gather_launches"], 1), b["gather_launches"], None),
         # the path is bound by the host link: host-tier bytes per step over the
         # gather time, against the read stream measured on the tier itself
@@ -456,7 +472,8 @@ def run_trie(args, torch, P, synth, dev):
     log(f"trie workload: {len(w.store_offsets) - 1} store walks, {w.n_requests} requests "
         f"({time.time() - t0:.1f}s)")
     sh = w.shape
-    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes,
+                         sh.layer_chunk_bytes)
     store = P.PrefixStore(shape, w.capacity, flags=P.PTSTORE_FLAG_TIMING | P.PTSTORE_FLAG_COUNTERS)
     W = len(w.store_offsets) - 1
     g = torch.Generator(device=dev)
@@ -550,7 +567,7 @@ def run_trie(args, torch, P, synth, dev):
                         "algorithmic_GBps": round(R * w.depth * LOOKUP_BYTES_PER_BLOCK
                                                   / (lk_avg * 1e6), 1)},
         "matched_blocks": matched,
-        "roofline": roofline("k_copy_pairs<true, false> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
+        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
                              g_n, recorded_traffic("trie")),
         "prefill": {"insert_ms": round(ins_ms, 3), "insert_calls": ins_n,
                     "scatter_ms": round(sc_ms, 3), "blocks": created_total},
@@ -563,7 +580,8 @@ def run_stream(args, torch, P, synth, dev):
     sw = synth.build(args.config, seed=args.seed)
     base = sw.base
     sh = base.shape
-    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes)
+    shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes,
+                         sh.layer_chunk_bytes)
     evict = args.config == "stream_evict"
     flags = P.PTSTORE_FLAG_TIMING | (P.PTSTORE_FLAG_EVICT if evict else 0)
     store = P.PrefixStore(shape, sw.pool_blocks, flags=flags)
@@ -622,7 +640,7 @@ def run_stream(args, torch, P, synth, dev):
         "inserts_per_s": round(per * n_timed / elapsed, 2),
         "matched_blocks": matched, "created_blocks": created,
         "blocks_stored": {"before": blocks0, "after": st["blocks_stored"]},
-        "roofline": roofline("k_copy_pairs<true, false> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
+        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
                              g_ms / max(g_n, 1), g_n, recorded_traffic(args.config)),
         "evictions": st["evictions"], "index_rebuilds": st["index_rebuilds"],
         "full_events": st["full_events"],

@@ -110,8 +110,8 @@ typedef struct {
     int64_t host_blocks;     /* 0: no host tier */
     int64_t replica_blocks;  /* 0: no replicas */
     /* Per-layer slab sizes (Section 5: prefixes are combinations of tensors
-     * of variable sizes): NULL, or num_layers byte counts, each a positive
-     * multiple of 16, read at create time. Layer l's K and V slabs of a block
+     * of variable sizes): NULL, or num_layers (at most 1024) byte counts, each
+     * a positive multiple of 16, read at create time. Layer l's K and V slabs of a block
      * are then layer_chunk_bytes[l] bytes each (num_kv_heads, head_dim and
      * elem_bytes are ignored); a pool block is layer after layer, and layer l
      * of the paged cache takes 2 * cache_blocks * layer_chunk_bytes[l] bytes

@@ -116,6 +116,7 @@ class OracleStore:
 
     @classmethod
     def for_shape(cls, shape, capacity: int, with_payload: bool = True, **kw) -> "OracleStore":
+        kw.setdefault("layer_chunk_bytes", getattr(shape, "layer_chunk_bytes", None))
         return cls(shape.layers, shape.kv_heads, shape.head_dim, shape.block_tokens,
                    shape.elem_bytes, capacity, with_payload, **kw)
 

@@ -50,7 +50,8 @@ struct ptstore {
     TierView tier;  // owned = capacity and no host rows for a device-only store
     void* tier_mem; // replica map and replicate scratch
     void* host_mem; // the host tier as allocated (tier.host is its device address)
-    void* layer_tab; // per-layer slab sizes then bases, int64 [2][L]; null if uniform
+    void* layer_tab; // per-layer slab sizes [L] then bases [L + 1], int64; null if uniform
+    std::vector<int64_t> lbase_host;  // the bases, for launch shapes
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[7];
     std::vector<hipEvent_t> free_ev;
@@ -133,6 +134,7 @@ CopyPlan copy_plan(ptstore_t* s) {
     p.tier = s->tier;
     p.lchunk = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) : nullptr;
     p.lbase = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) + s->cfg.num_layers : nullptr;
+    p.lbase_host = s->layer_tab ? s->lbase_host.data() : nullptr;
     return p;
 }
 
@@ -293,8 +295,10 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     int64_t block = chunk * 2 * c.num_layers;
     std::vector<int64_t> lchunk, lbase;
     if (c.layer_chunk_bytes) {  // per-layer slab sizes
+        if (c.num_layers > kMaxVarLayers)
+            return fail(PTSTORE_ERR_INVALID, "ptstore_create: too many layers for per-layer sizes");
         lchunk.assign(c.layer_chunk_bytes, c.layer_chunk_bytes + c.num_layers);
-        lbase.resize(c.num_layers);
+        lbase.resize(c.num_layers + 1);
         block = 0;
         for (int l = 0; l < c.num_layers; ++l) {
             if (lchunk[l] < 16 || lchunk[l] % 16 != 0 || lchunk[l] > (1ll << 30))
@@ -303,6 +307,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
             lbase[l] = block;
             block += 2 * lchunk[l];
         }
+        lbase[c.num_layers] = block;
         chunk = lchunk[0];
     } else if (chunk % 16 != 0 || chunk > (1ll << 30)) {
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: chunk bytes must be a multiple of 16");
@@ -358,10 +363,11 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     }
     if (!lchunk.empty()) {
         const size_t n = (size_t)c.num_layers * sizeof(int64_t);
-        if ((e = hipMalloc(&s->layer_tab, 2 * n)) != hipSuccess ||
+        s->lbase_host = lbase;
+        if ((e = hipMalloc(&s->layer_tab, 2 * n + sizeof(int64_t))) != hipSuccess ||
             (e = hipMemcpy(s->layer_tab, lchunk.data(), n, hipMemcpyHostToDevice)) != hipSuccess ||
-            (e = hipMemcpy(static_cast<int64_t*>(s->layer_tab) + c.num_layers, lbase.data(), n,
-                           hipMemcpyHostToDevice)) != hipSuccess) {
+            (e = hipMemcpy(static_cast<int64_t*>(s->layer_tab) + c.num_layers, lbase.data(),
+                           n + sizeof(int64_t), hipMemcpyHostToDevice)) != hipSuccess) {
             ptstore_destroy(s);
             (void)hipGetLastError();
             return fail(PTSTORE_ERR_NOMEM, "ptstore_create: layer tables", e);

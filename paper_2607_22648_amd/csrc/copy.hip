@@ -217,10 +217,11 @@ struct CopyArgs {
 // workgroups copy neighbouring chunks, the few workgroups past the end exit
 // at once); a scatter, whose created blocks are sparse, launches a few
 // workgroups per compute unit that loop.
-// VAR: per-layer slab sizes, read from the layer tables.
-template <bool GATHER, bool VAR>
+// Uniform slabs: a unit is (descriptor, group of chunks_per_group slabs).
+template <bool GATHER>
 __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
     const unsigned long long units = *a.total * (unsigned long long)a.groups;
+    const int n16 = (int)(a.chunk_bytes >> 4);
     for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const unsigned long long d = unit / (unsigned)a.groups;
         const int g = (int)(unit - d * (unsigned)a.groups);
@@ -230,24 +231,62 @@ __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
         uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
                                           : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
         for (int c = c0; c < c1; ++c) {
-            uint8_t* src;
-            uint8_t* dst;
-            int n16;
-            if (VAR) {
-                const int l = c >> 1, kv = c & 1;
-                const int64_t ch = a.lchunk[l], lb = a.lbase[l];
-                src = blk + lb + kv * ch;
-                dst = a.cache + a.cache_blocks * lb + ((int64_t)kv * a.cache_blocks + p.cb) * ch;
-                n16 = (int)(ch >> 4);
-            } else {
-                src = blk + (int64_t)c * a.chunk_bytes;
-                dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
-                n16 = (int)(a.chunk_bytes >> 4);
-            }
+            uint8_t* src = blk + (int64_t)c * a.chunk_bytes;
+            uint8_t* dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
             if (GATHER)
                 copy_span(reinterpret_cast<const v4u*>(src), reinterpret_cast<v4u*>(dst), n16);
             else
                 copy_span(reinterpret_cast<const v4u*>(dst), reinterpret_cast<v4u*>(src), n16);
+        }
+    }
+}
+
+// Per-layer slab sizes. Layers l0 .. l1-1 of a pool row are one contiguous
+// byte range [lbase[l0], lbase[l1]); a unit is (descriptor, kSpanBytes of
+// that range), so every workgroup moves the same amount however small the
+// slabs. Each 16-byte vector finds its slab (layer, K|V) by a binary search
+// over the layer bases, kept in LDS.
+constexpr int kSpanBytes = 32 << 10;
+
+__device__ inline void slab_of(const int64_t* lb, int l0, int l1, int64_t o, int* l_out) {
+    int lo = l0, hi = l1 - 1;  // largest l with lb[l] <= o
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (lb[mid] <= o) lo = mid; else hi = mid - 1;
+    }
+    *l_out = lo;
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(1024) void k_copy_spans(CopyArgs a) {
+    __shared__ int64_t lb[kMaxVarLayers + 1];
+    const int l0 = a.c_lo >> 1, l1 = a.c_hi >> 1;
+    for (int l = l0 + (int)threadIdx.x; l <= l1; l += blockDim.x) lb[l - l0] = a.lbase[l];
+    __syncthreads();
+    const int64_t b0 = lb[0], b1 = lb[l1 - l0];
+    const unsigned long long spans = (unsigned long long)((b1 - b0 + kSpanBytes - 1) / kSpanBytes);
+    const unsigned long long units = *a.total * spans;
+    for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
+        const unsigned long long d = unit / spans;
+        const int64_t s0 = b0 + (int64_t)(unit - d * spans) * kSpanBytes;
+        const int64_t s1 = min(s0 + (int64_t)kSpanBytes, b1);
+        const Pair p = a.pairs[d];
+        uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
+                                          : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
+        for (int64_t o = s0 + 16 * (int64_t)threadIdx.x; o < s1; o += 16 * (int64_t)blockDim.x) {
+            int li;
+            slab_of(lb, 0, l1 - l0, o, &li);
+            const int64_t ch = a.lchunk[l0 + li];
+            const int64_t in = o - lb[li];
+            const int kv = in >= ch ? 1 : 0;
+            uint8_t* c = a.cache + a.cache_blocks * lb[li] + ((int64_t)kv * a.cache_blocks + p.cb) * ch +
+                         (in - kv * ch);
+            v4u* pv = reinterpret_cast<v4u*>(blk + o);
+            v4u* cv = reinterpret_cast<v4u*>(c);
+            if (GATHER)
+                st_nt(cv, ld_nt(pv));
+            else
+                st_nt(pv, ld_nt(cv));
         }
     }
 }
@@ -308,7 +347,12 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     a.c_hi = 2 * l1;
     a.lchunk = p.lchunk;
     a.lbase = p.lbase;
-    a.groups = (a.c_hi - a.c_lo + p.chunks_per_group - 1) / p.chunks_per_group;
+    if (p.lchunk) {  // units are kSpanBytes spans of the layer range
+        const int64_t lo = p.lbase_host[l0], hi = p.lbase_host[l1];
+        a.groups = (int32_t)((hi - lo + kSpanBytes - 1) / kSpanBytes);
+    } else {
+        a.groups = (a.c_hi - a.c_lo + p.chunks_per_group - 1) / p.chunks_per_group;
+    }
     const int64_t bound = (int64_t)R * max_blocks * a.groups;  // units if every entry moves
     const int64_t cap = (1ll << 31) / p.threads;                 // launch limit on work-items
     int64_t grid = p.grid ? p.grid : (GATHER ? bound : (int64_t)p.loop_grid);
@@ -316,9 +360,9 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     if (grid > cap) grid = cap;
     if (grid < 1) return hipSuccess;
     if (p.lchunk)
-        hipLaunchKernelGGL((k_copy_pairs<GATHER, true>), dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+        hipLaunchKernelGGL(k_copy_spans<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     else
-        hipLaunchKernelGGL((k_copy_pairs<GATHER, false>), dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+        hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     return hipGetLastError();
 }
 

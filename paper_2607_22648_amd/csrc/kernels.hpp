@@ -98,10 +98,15 @@ struct CopyPlan {
     DevState* state;
     TierView tier;
     // per-layer slab sizes (null when every layer has chunk_bytes): device
-    // tables lchunk[l] and lbase[l] = 2 * sum of lchunk[0..l-1]
+    // tables lchunk[l] (L entries) and lbase[l] = 2 * sum of lchunk[0..l-1]
+    // (L + 1 entries), and the host's copy of lbase
     const int64_t* lchunk;
     const int64_t* lbase;
+    const int64_t* lbase_host;
 };
+
+// Most layers a store with per-layer slab sizes may have.
+constexpr int kMaxVarLayers = 1024;
 
 
 // Descriptor list of one gather / scatter call.

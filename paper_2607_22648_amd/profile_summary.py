@@ -27,8 +27,8 @@ from collections import defaultdict
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 COPY_SRC = os.path.join(HERE, "csrc", "copy.hip")
-GATHER = "k_copy_pairs<true, false>"   # uniform-layer gather
-SCATTER = "k_copy_pairs<false, false>"
+GATHER = "k_copy_pairs<true>"
+SCATTER = "k_copy_pairs<false>"
 PLAIN_COPY = "__amd_rocclr_copyBuffer"
 PLAIN_COPY_BYTES = 8 << 30  # bench.py's copy-ceiling tensor
 

@@ -351,3 +351,91 @@ def test_llama70b_full_tiered():
     assert host_hits > 0 and seen > 0
     del cache
     _free(store, ref)
+
+
+def _block_of(cache: torch.Tensor, nb: int, chunks, cb: int) -> torch.Tensor:
+    """Bytes of cache block cb in pool-block order (layer after layer, K then V):
+    layer l of the cache takes the next 2 * nb * chunks[l] bytes."""
+    out, off = [], 0
+    for ch in chunks:
+        v = cache[off:off + 2 * nb * ch].view(2, nb, ch)
+        out.append(v[:, cb].reshape(-1))
+        off += 2 * nb * ch
+    return torch.cat(out)
+
+
+def test_hybrid8b_full():
+    """Per-layer slab sizes (32 KiB / 8 KiB alternating) at the 8B-shaped
+    workload's full size: metadata against the oracle, sampled blocks against
+    the pool and the bytes recorded at scatter, and a layer-range gather."""
+    w = synth.build("hybrid8b")
+    kv = w.shape
+    chunks = kv.layer_chunk_bytes
+    cap = len(w.stored) * w.passage_blocks
+    shape = P.StoreShape(kv.layers, kv.kv_heads, kv.head_dim, kv.block_tokens, kv.elem_bytes, chunks)
+    store = P.PrefixStore(shape, cap)
+    ref = OracleStore.for_shape(kv, cap, with_payload=False)
+    rng = np.random.default_rng(8)
+    recorded = {}
+    st_, so = w.store_batch()
+    g = torch.Generator(device=DEV)
+    for lo in range(0, len(so) - 1, 16):
+        hi = min(len(so) - 1, lo + 16)
+        toks, offs = st_[so[lo]:so[hi]], (so[lo:hi + 1] - so[lo]).astype(np.int64)
+        m, ids, cr = store.insert(to_dev(toks), to_dev(offs), w.passage_blocks)
+        rc, rm, rids, rcr = ref.insert(toks, offs, w.passage_blocks)
+        ids_h, cr_h = host(ids), host(cr)
+        np.testing.assert_array_equal(ids_h, rids)
+        np.testing.assert_array_equal(cr_h, rcr)
+        nb = (hi - lo) * w.passage_blocks
+        cache = torch.empty(nb * kv.block_bytes, dtype=torch.uint8, device=DEV)
+        g.manual_seed(lo)
+        cache.random_(0, 256, generator=g)
+        bt_h = np.arange(nb, dtype=np.int32).reshape(hi - lo, w.passage_blocks)
+        store.scatter(ids, cr, to_dev(bt_h), cache)
+        for r, b in np.argwhere(cr_h != 0)[rng.choice(int((cr_h != 0).sum()), 4, replace=False)]:
+            recorded[int(ids_h[r, b])] = host(_block_of(cache, nb, chunks, int(bt_h[r, b])))
+        del cache
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    assert store.stats()["block_bytes"] == kv.block_bytes == 2 * sum(chunks)
+    pool = store.pool_tensor()
+    maxb = w.max_blocks
+    nbc = w.sub_batch * maxb
+    cache = torch.empty(nbc * kv.block_bytes, dtype=torch.uint8, device=DEV)
+    seen = 0
+    for k, (lo, hi) in enumerate(w.sub_batches()):
+        toks, offs = w.request_slice(lo, hi)
+        R = hi - lo
+        bt_h = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
+        cache.fill_(SENTINEL)
+        layers = None if k == 0 else (3, 7)
+        m, ids = store.lookup(to_dev(toks), to_dev(offs), maxb)
+        store.gather(ids, m, to_dev(bt_h), cache, layers=layers)
+        rm, rids = ref.lookup(toks, offs, maxb)
+        m_h, ids_h = host(m), host(ids)
+        np.testing.assert_array_equal(m_h, rm)
+        np.testing.assert_array_equal(ids_h, rids)
+        lb = np.concatenate([[0], np.cumsum([2 * c for c in chunks])])
+        for r in rng.choice(R, 12, replace=False):
+            for b in rng.choice(maxb, 6, replace=False):
+                got = _block_of(cache, nbc, chunks, int(bt_h[r, b]))
+                if b >= m_h[r]:
+                    assert bool((got == SENTINEL).all())
+                    continue
+                row = pool[int(ids_h[r, b])]
+                if layers is None:
+                    assert torch.equal(got, row)
+                    if int(ids_h[r, b]) in recorded:
+                        np.testing.assert_array_equal(host(got), recorded[int(ids_h[r, b])])
+                        seen += 1
+                else:
+                    a, e = int(lb[layers[0]]), int(lb[layers[1]])
+                    assert torch.equal(got[a:e], row[a:e])
+                    assert bool((got[:a] == SENTINEL).all()) and bool((got[e:] == SENTINEL).all())
+        for i, want in recorded.items():  # the pool keeps what was scattered
+            np.testing.assert_array_equal(host(pool[i]), want)
+            seen += 1
+    assert seen > 0
+    del cache
+    _free(store, ref)

@@ -29,18 +29,31 @@ class KVShape:
     head_dim: int
     block_tokens: int = 16
     dtype: str = "bf16"
+    layer_kv_heads: Optional[Tuple[int, ...]] = None  # per-layer KV heads (hybrid models)
 
     @property
     def elem_bytes(self) -> int:
         return 2
 
     @property
+    def layer_chunk_bytes(self) -> Optional[Tuple[int, ...]]:
+        """Per-layer slab bytes when layers differ, else None."""
+        if self.layer_kv_heads is None:
+            return None
+        return tuple(h * self.block_tokens * self.head_dim * self.elem_bytes
+                     for h in self.layer_kv_heads)
+
+    @property
     def chunk_bytes(self) -> int:
-        """Bytes of one (layer, K|V) slab of a block: heads x slots x dim."""
+        """Bytes of one (layer, K|V) slab of a block: heads x slots x dim (layer 0's)."""
+        if self.layer_kv_heads is not None:
+            return self.layer_chunk_bytes[0]
         return self.kv_heads * self.block_tokens * self.head_dim * self.elem_bytes
 
     @property
     def block_bytes(self) -> int:
+        if self.layer_kv_heads is not None:
+            return 2 * sum(self.layer_chunk_bytes)
         return self.layers * 2 * self.chunk_bytes
 
 
@@ -379,6 +392,9 @@ SHAPE_TINY = KVShape(2, 8, 128, 16, "fp16")
 SHAPE_8B = KVShape(32, 8, 128, 16, "bf16")
 SHAPE_70B = KVShape(80, 8, 128, 16, "bf16")
 SHAPE_TRIE = KVShape(1, 8, 128, 16, "fp16")
+# a hybrid 32-layer model: full-attention layers (8 KV heads) alternate with
+# layers of 2 KV heads, so slabs alternate 32 KiB and 8 KiB (1.25 MiB blocks)
+SHAPE_HYBRID = KVShape(32, 8, 128, 16, "bf16", layer_kv_heads=tuple([8, 2] * 16))
 
 CONFIGS = {
     # 64 requests x 1024 tokens: one of 32 passages of 768 tokens (Zipf 1.0)
@@ -398,6 +414,10 @@ CONFIGS = {
     "llama70b_shard": dict(kind="passage", shape=SHAPE_70B, n_passages=64, passage_tokens=30720,
                            suffix_tokens=2048, n_requests=64, zipf_s=1.2,
                            stored_ranks=list(range(1, 33, 2)), sub_batch=4),
+    # The 8B-shaped workload on the hybrid shape (per-layer slab sizes).
+    "hybrid8b": dict(kind="passage", shape=SHAPE_HYBRID, n_passages=512, passage_tokens=3584,
+                     suffix_tokens=512, n_requests=256, zipf_s=1.1,
+                     stored_ranks=list(range(1, 257)), sub_batch=128),
     # All 32 passages of the 70B-shaped configuration (322 GB) on one GPU:
     # 48,640 blocks (237.5 GiB) in device memory, one passage's worth of device
     # replica slots, the remaining 12,800 blocks (62.5 GiB) in pinned host
