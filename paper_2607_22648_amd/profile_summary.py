@@ -10,8 +10,9 @@ Inputs (directories written by rocprofv3 ``--output-format csv``):
 
 HBM traffic of a kernel = FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
 scaled by the factor that maps the same counter onto the known byte count of
-a plain device-to-device copy in the same run (the 8 GiB copy bench.py does
-for its copy ceiling, a ``__amd_rocclr_copyBuffer`` dispatch). The record
+a plain device-to-device copy in the same run (the copy bench.py times for
+its ceiling, a ``__amd_rocclr_copyBuffer`` dispatch of ``hbm_ceiling.bytes``
+bytes as that run's JSON line states). The record
 carries the SHA-256 of the copy kernel's source; bench.py reports the traffic
 only while that source is unchanged.
 """
@@ -30,7 +31,6 @@ COPY_SRC = os.path.join(HERE, "csrc", "copy.hip")
 GATHER = "k_copy_pairs<true>"
 SCATTER = "k_copy_pairs<false>"
 PLAIN_COPY = "__amd_rocclr_copyBuffer"
-PLAIN_COPY_BYTES = 8 << 30  # bench.py's copy-ceiling tensor
 
 
 def copy_source_sha() -> str:
@@ -89,7 +89,7 @@ def main():
     write = counter_per_dispatch(a.write, "WRITE_SIZE")
     pf = plain_copy_value(fetch[PLAIN_COPY])
     pw = plain_copy_value(write[PLAIN_COPY])
-    known_kib = PLAIN_COPY_BYTES / 1024
+    known_kib = bench["hbm_ceiling"]["bytes"] / 1024  # the plain copy's size in that run
     f_factor = known_kib / (sum(pf) / len(pf))
     w_factor = known_kib / (sum(pw) / len(pw))
     g_fetch = sum(fetch[GATHER]) / len(fetch[GATHER])
@@ -137,8 +137,8 @@ def main():
              "| quantity | value |", "|---|---|",
              f"| gather FETCH_SIZE per dispatch | {g_fetch:,.0f} KiB ({len(fetch[GATHER])} dispatches) |",
              f"| gather WRITE_SIZE per dispatch | {g_write:,.0f} KiB |",
-             f"| plain 8 GiB copy FETCH_SIZE | {sum(pf) / len(pf):,.0f} KiB -> factor {f_factor:.4f} |",
-             f"| plain 8 GiB copy WRITE_SIZE | {sum(pw) / len(pw):,.0f} KiB -> factor {w_factor:.4f} |",
+             f"| plain {known_kib / 2**20:.0f} GiB copy FETCH_SIZE | {sum(pf) / len(pf):,.0f} KiB -> factor {f_factor:.4f} |",
+             f"| plain {known_kib / 2**20:.0f} GiB copy WRITE_SIZE | {sum(pw) / len(pw):,.0f} KiB -> factor {w_factor:.4f} |",
              f"| traffic per gather launch (scaled) | {traffic / 1e9:.3f} GB |",
              f"| algorithmic bytes per launch | {algo / 1e9:.3f} GB |",
              f"| traffic / algorithmic | {traffic / algo:.4f} |",
