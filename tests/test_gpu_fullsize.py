@@ -19,6 +19,19 @@ from workloads import synth
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
+
+@pytest.fixture(autouse=True)
+def _device_memory_released(request):
+    """Each test starts from a released device: these tests use up to 260 GiB."""
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    free, total = torch.cuda.mem_get_info()
+    print(f"[{request.node.name}] device memory free {free / 2**30:.1f} of {total / 2**30:.1f} GiB "
+          f"(torch reserved {torch.cuda.memory_reserved() / 2**30:.1f} GiB)", flush=True)
+    yield
+
 if torch.cuda.is_available():
     from paper_2607_22648_amd import ptstore as P
     from tests.twin import to_dev, host, DEV
