@@ -153,7 +153,17 @@ def cpu_baseline(w, sample: int):
                       f"({moved / 1e9:.1f} GB moved); the oracle store holds the {len(need)} "
                       f"stored passages they reference",
             "seconds": round(dt, 3), "GBps": round(moved / dt / 1e9, 2),
-            "host_cpus": os.cpu_count()}
+            "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def hbm_ceiling(torch, P, src, dst, nbytes: int) -> dict:
@@ -284,11 +294,18 @@ def run_passage(args, torch, P, synth, dev):
                                          maxb).sum()) for lo, hi in subs)
 
     torch.cuda.synchronize()
+    # per-step HIP events on the stream the store's kernels run on (torch's
+    # current stream), for the median; the K steps are timed as a whole too
+    cur = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    evs[0].record(cur)
+    for k in range(args.steps):
         step()
+        evs[k + 1].record(cur)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
     g_ms, g_n = store.kernel_times(P.KIND_GATHER)
     l_ms, l_n = store.kernel_times(P.KIND_LOOKUP)
 
@@ -316,6 +333,8 @@ def run_passage(args, torch, P, synth, dev):
         "stored_blocks": st["blocks_stored"], "block_bytes": sh.block_bytes,
         "gather_calls": "one per layer" if args.per_layer else "one per sub-batch"})
     out.update({
+        "ms_per_step_median": round(per_step[len(per_step) // 2], 3),
+        "ms_per_step_min_max": [round(per_step[0], 3), round(per_step[-1], 3)],
         "hbm_GBps": round(step_GBps, 1),
         "hbm_frac": round(step_GBps / HBM_PEAK_GBPS, 4),
         "matched_blocks_per_step": matched,
