@@ -1,10 +1,14 @@
 // Streaming-bandwidth probes: the practical HBM ceiling the copy kernels are
 // measured against, taken in the same process as the measurement itself.
-// Each probe moves 16-byte vectors with non-temporal loads / stores, the
-// access pattern of the gather and scatter copies:
-//   kind 0  read `bytes` from a (a read-only stream)
-//   kind 1  write `bytes` to b (a write-only stream)
-//   kind 2  copy `bytes` from a to b, one 32 KiB span per 1024-thread workgroup
+// Each probe moves 16-byte vectors with non-temporal loads / stores, in the
+// fastest organisation a sweep of workgroup sizes, vectors in flight per
+// thread and grid shapes found for that direction on MI355X:
+//   kind 0  read `bytes` from a: 256-thread workgroups, 32 per compute unit,
+//           eight vectors in flight per thread (about 7.1 TB/s)
+//   kind 1  write `bytes` to b: one 1024-thread workgroup per 16 KiB, in
+//           dispatch order (about 6.4 TB/s)
+//   kind 2  copy `bytes` from a to b, one 32 KiB span per 1024-thread
+//           workgroup (the gather's organisation on contiguous buffers)
 #include <hip/hip_runtime.h>
 
 #include "ptstore.h"
@@ -13,19 +17,30 @@ namespace {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
+constexpr int kReadInFlight = 8;
+
 __global__ __launch_bounds__(256) void k_read(const v4u* __restrict__ src, long n16, v4u* sink) {
     v4u acc = {0u, 0u, 0u, 0u};
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (long)gridDim.x * blockDim.x)
-        acc ^= __builtin_nontemporal_load(src + i);
+    const long stride = (long)gridDim.x * blockDim.x * kReadInFlight;
+    for (long i = (long)blockIdx.x * blockDim.x * kReadInFlight + threadIdx.x; i < n16; i += stride) {
+        v4u v[kReadInFlight];
+#pragma unroll
+        for (int u = 0; u < kReadInFlight; ++u) {
+            const long j = i + (long)u * blockDim.x;
+            v[u] = j < n16 ? __builtin_nontemporal_load(src + j) : v4u{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < kReadInFlight; ++u) acc ^= v[u];
+    }
     // never true for real data; keeps the loads alive
     if (acc.x == 0x9E3779B9u && acc.y == 0x7F4A7C15u && acc.z == 0xF39CC060u && acc.w == 0x5CEDC834u)
         sink[0] = acc;
 }
 
-__global__ __launch_bounds__(256) void k_write(v4u* __restrict__ dst, long n16) {
+__global__ __launch_bounds__(1024) void k_write(v4u* __restrict__ dst, long n16) {
     const v4u v = {1u, 2u, 3u, 4u};
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (long)gridDim.x * blockDim.x)
-        __builtin_nontemporal_store(v, dst + i);
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;  // one vector per thread
+    if (i < n16) __builtin_nontemporal_store(v, dst + i);
 }
 
 __global__ __launch_bounds__(1024) void k_copy(const v4u* __restrict__ src, v4u* __restrict__ dst, long n16) {
@@ -49,11 +64,10 @@ extern "C" __attribute__((visibility("default"))) int ptstore_bandwidth_probe(
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return PTSTORE_ERR_HIP;
-    const unsigned stream_grid = (unsigned)(cus * 64);
     if (kind == 0)
-        hipLaunchKernelGGL(k_read, dim3(stream_grid), dim3(256), 0, s, (const v4u*)a, n16, (v4u*)b);
+        hipLaunchKernelGGL(k_read, dim3((unsigned)(cus * 32)), dim3(256), 0, s, (const v4u*)a, n16, (v4u*)b);
     else if (kind == 1)
-        hipLaunchKernelGGL(k_write, dim3(stream_grid), dim3(256), 0, s, (v4u*)b, n16);
+        hipLaunchKernelGGL(k_write, dim3((unsigned)((n16 + 1023) / 1024)), dim3(1024), 0, s, (v4u*)b, n16);
     else
         hipLaunchKernelGGL(k_copy, dim3((unsigned)((n16 + 2047) / 2048)), dim3(1024), 0, s,
                            (const v4u*)a, (v4u*)b, n16);
