@@ -225,6 +225,24 @@ int ptstore_gather_layers(ptstore_t *store, const int32_t *ids, const int32_t *m
                           int64_t cache_blocks, void *stream);
 
 /*
+ * A load in layer steps without rebuilding its block list each step.
+ * ptstore_gather_prepare lists, once, the blocks a gather of (ids, m,
+ * block_table) moves (bad entries are counted here); each
+ * ptstore_gather_prepared then copies layers layer_begin .. layer_end-1 of
+ * those blocks into `cache`, exactly as ptstore_gather_layers with the
+ * prepare's arguments would. The list lives in store-owned scratch; any
+ * other call on the store except lookups (gather, gather_layers,
+ * lookup_gather, scatter, scatter_layers, insert, replicate) discards it.
+ * ptstore_gather_prepared returns INVALID when there is no list, or when
+ * cache_blocks differs from the prepare's.
+ */
+int ptstore_gather_prepare(ptstore_t *store, const int32_t *ids, const int32_t *m,
+                           const int32_t *block_table, int32_t R, int32_t max_blocks,
+                           int64_t cache_blocks, void *stream);
+int ptstore_gather_prepared(ptstore_t *store, int32_t layer_begin, int32_t layer_end, void *cache,
+                            int64_t cache_blocks, void *stream);
+
+/*
  * Store (Sections 1 and 4): with the same result as taking the requests one
  * after another, each request reuses the stored blocks of its longest
  * common prefix (including blocks created by earlier requests of this

@@ -52,6 +52,10 @@ struct ptstore {
     void* host_mem; // the host tier as allocated (tier.host is its device address)
     void* layer_tab; // per-layer slab sizes [L] then bases [L + 1], int64; null if uniform
     std::vector<int64_t> lbase_host;  // the bases, for launch shapes
+    // the block list of ptstore_gather_prepare, while it is valid
+    bool prep_valid;
+    int32_t prep_R, prep_max_blocks;
+    int64_t prep_cache_blocks;
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[7];
     std::vector<hipEvent_t> free_ev;
@@ -490,6 +494,7 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0 || layer_begin < 0 ||
         layer_end > s->cfg.num_layers || layer_begin >= layer_end)
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather: bad argument");
+    s->prep_valid = false;
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
     if (rc) return rc;
@@ -511,6 +516,58 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
                                layer_begin, layer_end, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_gather: launch", e);
+}
+
+int ptstore_gather_prepare(ptstore_t* s, const int32_t* ids, const int32_t* m,
+                           const int32_t* block_table, int32_t R, int32_t max_blocks,
+                           int64_t cache_blocks, void* stream) {
+    if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
+        (R > 0 && (!ids || !m || !block_table)))
+        return fail(PTSTORE_ERR_INVALID, "ptstore_gather_prepare: bad argument");
+    s->prep_valid = false;
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    if (R > 0) {
+        rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes,
+                            copy_scratch_bytes(R, max_blocks), st, "ptstore_gather_prepare: scratch");
+        if (rc) return rc;
+        CopyScratch sc;
+        copy_scratch_carve(s->copy_scratch, R, max_blocks, &sc);
+        hipError_t e;
+        {
+            Timed t(s, 4, st);
+            e = launch_gather_select(copy_plan(s), sc, ids, m, block_table, R, max_blocks,
+                                     cache_blocks, st);
+        }
+        if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, "ptstore_gather_prepare: launch", e);
+    }
+    s->prep_valid = true;
+    s->prep_R = R;
+    s->prep_max_blocks = max_blocks;
+    s->prep_cache_blocks = cache_blocks;
+    return PTSTORE_OK;
+}
+
+int ptstore_gather_prepared(ptstore_t* s, int32_t layer_begin, int32_t layer_end, void* cache,
+                            int64_t cache_blocks, void* stream) {
+    if (!s || !s->prep_valid || cache_blocks != s->prep_cache_blocks || layer_begin < 0 ||
+        layer_end > s->cfg.num_layers || layer_begin >= layer_end ||
+        (s->prep_R > 0 && !cache) || (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_gather_prepared: no prepared list or bad argument");
+    if (s->prep_R == 0) return PTSTORE_OK;
+    int rc = set_device(s);
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    CopyScratch sc;
+    copy_scratch_carve(s->copy_scratch, s->prep_R, s->prep_max_blocks, &sc);
+    hipError_t e;
+    {
+        Timed t(s, 0, st);
+        e = launch_gather_copy(copy_plan(s), sc, static_cast<uint8_t*>(cache), cache_blocks, s->prep_R,
+                               s->prep_max_blocks, layer_begin, layer_end, st);
+    }
+    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_gather_prepared: launch", e);
 }
 
 int ptstore_gather(ptstore_t* s, const int32_t* ids, const int32_t* m, const int32_t* block_table,
@@ -538,6 +595,7 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     if (!s || !check_batch(s, tokens, offsets, n_tokens, R, max_blocks) ||
         (R > 0 && (!m_out || !ids || !created)))
         return fail(PTSTORE_ERR_INVALID, "ptstore_insert: bad argument");
+    s->prep_valid = false;
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
     if (rc) return rc;
@@ -577,6 +635,7 @@ int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* crea
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0 || layer_begin < 0 ||
         layer_end > s->cfg.num_layers || layer_begin >= layer_end)
         return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: bad argument");
+    s->prep_valid = false;
     if (R == 0) return PTSTORE_OK;
     int rc = set_device(s);
     if (rc) return rc;
@@ -612,6 +671,7 @@ int ptstore_replicate(ptstore_t* s, void* stream) {
     if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_replicate: null store");
     if (s->tier.replicas == 0)
         return fail(PTSTORE_ERR_INVALID, "ptstore_replicate: store has no replica slots");
+    s->prep_valid = false;
     int rc = set_device(s);
     if (rc) return rc;
     hipStream_t st = (hipStream_t)stream;

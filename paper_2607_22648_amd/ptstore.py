@@ -59,7 +59,7 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_reset_counters", "ptstore_get_buffers", "ptstore_kernel_times",
            "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
            "ptstore_bandwidth_probe", "ptstore_replicate", "ptstore_gather_layers",
-           "ptstore_scatter_layers")
+           "ptstore_scatter_layers", "ptstore_gather_prepare", "ptstore_gather_prepared")
 
 
 def _load() -> C.CDLL:
@@ -85,6 +85,8 @@ def _load() -> C.CDLL:
         "ptstore_replicate": [p, p],
         "ptstore_gather_layers": [p, p, p, p, i32, i32, i32, i32, p, i64, p],
         "ptstore_scatter_layers": [p, p, p, p, i32, i32, i32, i32, p, i64, p],
+        "ptstore_gather_prepare": [p, p, p, p, i32, i32, i64, p],
+        "ptstore_gather_prepared": [p, i32, i32, p, i64, p],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -173,6 +175,18 @@ def ptstore_gather_layers(h, ids, m, block_table, layer_begin, layer_end, cache,
         h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, layer_begin, layer_end,
         _dev(cache, None, "cache"), cache_blocks, _stream(stream)))
+
+
+def ptstore_gather_prepare(h, ids, m, block_table, cache_blocks, stream=None) -> None:
+    R, maxb = ids.shape
+    _check("ptstore_gather_prepare", _lib.ptstore_gather_prepare(
+        h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
+        _dev(block_table, torch.int32, "block_table"), R, maxb, cache_blocks, _stream(stream)))
+
+
+def ptstore_gather_prepared(h, layer_begin, layer_end, cache, cache_blocks, stream=None) -> None:
+    _check("ptstore_gather_prepared", _lib.ptstore_gather_prepared(
+        h, layer_begin, layer_end, _dev(cache, None, "cache"), cache_blocks, _stream(stream)))
 
 
 def ptstore_scatter_layers(h, ids, created, block_table, layer_begin, layer_end, cache,
@@ -350,6 +364,14 @@ class PrefixStore:
         created = torch.empty((R, max_blocks), dtype=torch.uint8, device=dev)
         ptstore_insert(self.h, tokens, offsets, max_blocks, m, ids, created, stream)
         return m, ids, created
+
+    def gather_prepare(self, ids, m, block_table, cache, stream=None):
+        """List once the blocks a gather of (ids, m, block_table) into `cache` moves."""
+        ptstore_gather_prepare(self.h, ids, m, block_table, self.cache_blocks(cache), stream)
+
+    def gather_prepared(self, cache, layers, stream=None):
+        """Copy layers[0] .. layers[1]-1 of the prepared blocks into `cache`."""
+        ptstore_gather_prepared(self.h, layers[0], layers[1], cache, self.cache_blocks(cache), stream)
 
     def scatter(self, ids, created, block_table, cache, stream=None, layers=None):
         """layers = (begin, end): only those layers' slabs (None: all)."""

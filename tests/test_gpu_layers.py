@@ -157,3 +157,38 @@ def test_bad_layer_ranges_and_sizes_are_rejected():
     for bad in ([32, 8], [32, 0], [32, -16]):
         with pytest.raises(P.PTStoreError):
             P.PrefixStore(P.StoreShape(2, 1, 1, 2, 1, tuple(bad)), 8)
+
+
+@pytest.mark.parametrize("chunks", [CHUNKS, None])
+def test_prepared_per_layer_gather(chunks):
+    """The block list built once, then one copy per layer: the same bytes as
+    layer-range gathers; any other call discards the list."""
+    rng = np.random.default_rng(7)
+    t = _twin(chunks)
+    atoms = _fill(t, rng)
+    toks, offs = random_block_batch(rng, 12, atoms, 6, tail_p=0.3)
+    R = len(offs) - 1
+    (m, ids), (rm, rids) = t.lookup(toks, offs, 6)
+    bt = block_table_identity(R, 6)
+    n = R * 6 * t.shape.block_bytes
+    dst = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")
+    t.gpu.gather_prepare(ids, m, to_dev(bt), dst)
+    for l in range(t.shape.layers):
+        t.gpu.gather_prepared(dst, (l, l + 1))
+    rdst = np.full(n, 0xA5, dtype=np.uint8)
+    t.ref.gather(rids, rm, bt, rdst, R * 6)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(dst), rdst)
+    # still valid for another range, then discarded by a gather
+    t.gpu.gather_prepared(dst, (0, t.shape.layers))
+    t.gpu.gather(ids, m, to_dev(bt), dst)
+    with pytest.raises(P.PTStoreError):
+        t.gpu.gather_prepared(dst, (0, 1))
+    # discarded by an insert; a cache of another size is refused
+    t.gpu.gather_prepare(ids, m, to_dev(bt), dst)
+    with pytest.raises(P.PTStoreError):
+        t.gpu.gather_prepared(dst[: n - t.shape.block_bytes], (0, 1))
+    t.insert(toks, offs, 6)
+    with pytest.raises(P.PTStoreError):
+        t.gpu.gather_prepared(dst, (0, 1))
+    t.close()
