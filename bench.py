@@ -636,11 +636,13 @@ def run_stream(args, torch, P, synth, dev):
     evict = args.config == "stream_evict"
     flags = P.PTSTORE_FLAG_TIMING | (P.PTSTORE_FLAG_EVICT if evict else 0)
     store = make_store(P, shape, sw.pool_blocks, flags=flags)
-    pre = prefill(store, base, dev, torch, batch_passages=32)
     maxb = base.max_blocks
     per = len(sw.rounds[0].lookup_offsets) - 1
+    # the paged cache before the prefill's temporary caches: allocated after
+    # them (right after their free) its gathers ran 3.7 % slower
     cache = torch.full((sh.layers * 2 * per * maxb * sh.chunk_bytes,), 0xA5, dtype=torch.uint8,
                        device=dev)
+    pre = prefill(store, base, dev, torch, batch_passages=32)
     bt = torch.arange(per * maxb, dtype=torch.int32, device=dev).view(per, maxb)
     m = torch.empty(per, dtype=torch.int32, device=dev)
     ids = torch.empty((per, maxb), dtype=torch.int32, device=dev)
