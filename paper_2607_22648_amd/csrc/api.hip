@@ -172,7 +172,10 @@ struct Timed {
     ~Timed() {
         if (!a) return;
         hipEvent_t b = take_event(s);
-        if (!b) return;
+        if (!b) {  // not recorded after all: the first event goes back to the pool
+            s->free_ev.push_back(a);
+            return;
+        }
         (void)hipEventRecord(b, st);
         s->ev[kind].push_back({a, b});
     }
@@ -188,10 +191,24 @@ bool check_batch(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, in
     return true;
 }
 
-int set_device(ptstore_t* s) {
-    hipError_t e = hipSetDevice(s->device);
-    return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "hipSetDevice", e);
-}
+// Makes the store's device current for the rest of a call and gives the
+// caller's current device back when the call returns.
+struct DeviceScope {
+    int prev = -1;
+    int rc = PTSTORE_OK;
+    explicit DeviceScope(ptstore_t* s) {
+        hipError_t e = hipGetDevice(&prev);
+        if (e == hipSuccess && prev != s->device) e = hipSetDevice(s->device);
+        if (e != hipSuccess) {
+            prev = -1;
+            rc = fail(PTSTORE_ERR_HIP, "hipSetDevice", e);
+        }
+    }
+    ~DeviceScope() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
 
 // Make *buf hold at least `need` bytes. Growing waits for `st` first, since
 // work already enqueued on it may still read the old buffer.
@@ -444,7 +461,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
 
 int ptstore_destroy(ptstore_t* s) {
     if (!s) return PTSTORE_OK;
-    (void)hipSetDevice(s->device);
+    DeviceScope dev(s);
     (void)hipDeviceSynchronize();
     for (auto& v : s->ev)
         for (auto& p : v) {
@@ -473,8 +490,8 @@ int ptstore_lookup(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     if (!s || !check_batch(s, tokens, offsets, n_tokens, R, max_blocks) || (R > 0 && (!m || !ids)))
         return fail(PTSTORE_ERR_INVALID, "ptstore_lookup: bad argument");
     if (R == 0) return PTSTORE_OK;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     hipStream_t st = (hipStream_t)stream;
     Batch b{tokens, offsets, n_tokens, R, max_blocks};
     hipError_t e;
@@ -496,8 +513,9 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather: bad argument");
     s->prep_valid = false;
     if (R == 0) return PTSTORE_OK;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
+    int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
     rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes, copy_scratch_bytes(R, max_blocks),
                         st, "ptstore_gather: scratch");
@@ -525,8 +543,9 @@ int ptstore_gather_prepare(ptstore_t* s, const int32_t* ids, const int32_t* m,
         (R > 0 && (!ids || !m || !block_table)))
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather_prepare: bad argument");
     s->prep_valid = false;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
+    int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
     if (R > 0) {
         rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes,
@@ -556,8 +575,8 @@ int ptstore_gather_prepared(ptstore_t* s, int32_t layer_begin, int32_t layer_end
         (s->prep_R > 0 && !cache) || (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather_prepared: no prepared list or bad argument");
     if (s->prep_R == 0) return PTSTORE_OK;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     hipStream_t st = (hipStream_t)stream;
     CopyScratch sc;
     copy_scratch_carve(s->copy_scratch, s->prep_R, s->prep_max_blocks, &sc);
@@ -597,8 +616,8 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
         return fail(PTSTORE_ERR_INVALID, "ptstore_insert: bad argument");
     s->prep_valid = false;
     if (R == 0) return PTSTORE_OK;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     hipStream_t st = (hipStream_t)stream;
     uint64_t tn;
     const size_t need = insert_scratch_bytes(R, max_blocks, &tn);
@@ -637,8 +656,9 @@ int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* crea
         return fail(PTSTORE_ERR_INVALID, "ptstore_scatter: bad argument");
     s->prep_valid = false;
     if (R == 0) return PTSTORE_OK;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
+    int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
     rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes, copy_scratch_bytes(R, max_blocks),
                         st, "ptstore_scatter: scratch");
@@ -672,8 +692,8 @@ int ptstore_replicate(ptstore_t* s, void* stream) {
     if (s->tier.replicas == 0)
         return fail(PTSTORE_ERR_INVALID, "ptstore_replicate: store has no replica slots");
     s->prep_valid = false;
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
     {
@@ -685,8 +705,8 @@ int ptstore_replicate(ptstore_t* s, void* stream) {
 
 int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     if (!s || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_stats: null argument");
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     DevState st;
     hipError_t e = hipDeviceSynchronize();
     if (e == hipSuccess) e = hipMemcpy(&st, s->state, sizeof st, hipMemcpyDeviceToHost);
@@ -721,8 +741,8 @@ int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
 
 int ptstore_reset_counters(ptstore_t* s) {
     if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_reset_counters: null store");
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     DevState st;
     hipError_t e = hipDeviceSynchronize();
     if (e == hipSuccess) e = hipMemcpy(&st, s->state, sizeof st, hipMemcpyDeviceToHost);
@@ -760,8 +780,8 @@ int ptstore_get_buffers(ptstore_t* s, ptstore_buffers_t* out) {
 int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* launches) {
     if (!s || kind < 0 || kind > 6 || !total_ms || !launches)
         return fail(PTSTORE_ERR_INVALID, "ptstore_kernel_times: bad argument");
-    int rc = set_device(s);
-    if (rc) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
     double sum = 0;
     int64_t n = 0;
     for (auto& p : s->ev[kind]) {
