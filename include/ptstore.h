@@ -321,8 +321,10 @@ int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
 int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64_t *launches);
 
 /* Launch shape of the copy kernels (gather and scatter); 0 keeps a field's
- * current value. chunks_per_group: (layer, K|V) chunks one unit moves;
- * threads: workgroup size, 64..1024, a multiple of 64; grid: workgroups of
+ * current value. chunks_per_group: (layer, K|V) chunks one unit moves (by
+ * default the smallest divisor of 2 * num_layers that leaves at most 64
+ * units per block); threads: workgroup size, 64..1024, a multiple of 64
+ * (default 1024); grid: workgroups of
  * the copy kernels (by default a gather launches one per possible unit and
  * a scatter four times what every compute unit holds). For tuning sweeps;
  * results never depend on it. */
