@@ -634,7 +634,7 @@ def run_stream(args, torch, P, synth, dev):
     shape = P.StoreShape(sh.layers, sh.kv_heads, sh.head_dim, sh.block_tokens, sh.elem_bytes,
                          sh.layer_chunk_bytes)
     evict = args.config == "stream_evict"
-    flags = P.PTSTORE_FLAG_TIMING | (P.PTSTORE_FLAG_EVICT if evict else 0)
+    flags = P.PTSTORE_FLAG_TIMING | P.PTSTORE_FLAG_COUNTERS | (P.PTSTORE_FLAG_EVICT if evict else 0)
     store = make_store(P, shape, sw.pool_blocks, flags=flags)
     maxb = base.max_blocks
     per = len(sw.rounds[0].lookup_offsets) - 1
@@ -667,6 +667,8 @@ def run_stream(args, torch, P, synth, dev):
     for k in (P.KIND_GATHER, P.KIND_LOOKUP, P.KIND_INSERT, P.KIND_SCATTER, P.KIND_EVICT):
         store.kernel_times(k)
     blocks0 = store.stats()["blocks_stored"]
+    evictions0 = store.stats()["evictions"]
+    store.reset_counters()
     keep = []
     t0 = time.perf_counter()
     for i in range(args.warmup, args.warmup + n_timed):
@@ -697,6 +699,14 @@ def run_stream(args, torch, P, synth, dev):
                              g_ms / max(g_n, 1), g_n, recorded_traffic(args.config)),
         "evictions": st["evictions"], "index_rebuilds": st["index_rebuilds"],
         "full_events": st["full_events"],
+        "library_counters": {
+            "timed_rounds": n_timed,
+            "evictions_per_round": round((st["evictions"] - evictions0) / n_timed, 1),
+            "index_rebuilds": st["index_rebuilds"],
+            "probes_per_round": round(st["probes"] / n_timed, 1),
+            "token_compares_per_round": round(st["token_compares"] / n_timed, 1),
+            "cas_attempts_per_round": round(st["cas_attempts"] / n_timed, 1),
+            "cas_failures_per_round": round(st["cas_failures"] / n_timed, 1)},
         "kernel_ms_per_round": {k: round(v[0] / n_timed, 4) for k, v in t.items()},
         "scatter_GBps": round(created * 2 * sh.block_bytes / (t["scatter"][0] * 1e6), 1)
         if t["scatter"][0] else None,

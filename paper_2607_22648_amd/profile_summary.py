@@ -7,6 +7,10 @@ Inputs (directories written by rocprofv3 ``--output-format csv``):
   --fetch DIR   a ``--pmc FETCH_SIZE`` run (uses *_counter_collection.csv)
   --write DIR   a ``--pmc WRITE_SIZE`` run
   --bench FILE  the JSON line bench.py printed in the counter runs
+  --pmc DIR     (repeatable, instead of --fetch/--write) any ``--pmc`` runs:
+                the average per dispatch of every counter collected, for
+                every store kernel, plus the L2 hit rate where TCC_HIT and
+                TCC_MISS were both collected
 
 HBM traffic of a kernel = FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
 scaled by the factor that maps the same counter onto the known byte count of
@@ -79,7 +83,10 @@ def main():
     ap.add_argument("--out", default=os.path.join(os.path.dirname(HERE), "profiles"))
     ap.add_argument("--name", default="gather_llama8b")
     ap.add_argument("--cmd", required=True, help="the command that produced the inputs")
+    ap.add_argument("--pmc", action="append", default=[], help="a --pmc run directory")
     a = ap.parse_args()
+    if a.pmc:
+        return store_counters(a)
     if not (a.fetch and a.write and a.bench):
         return store_kernels_only(a)
 
@@ -148,6 +155,54 @@ def main():
     print(json.dumps(rec))
 
 
+def short_name(name: str) -> str:
+    short = name.replace("ptsd::(anonymous namespace)::", "").replace("void ", "")
+    return short.replace("(anonymous namespace)::", "").split("(")[0]
+
+
+def store_counters(a):
+    """Per-kernel averages of the counters of one or more --pmc runs."""
+    vals = defaultdict(lambda: defaultdict(list))  # kernel -> counter -> values
+    order = []
+    for d in a.pmc:
+        for r in csv.DictReader(open(_one(os.path.join(d, "*counter_collection.csv")))):
+            if "ptsd::" not in r["Kernel_Name"]:
+                continue
+            c = r["Counter_Name"]
+            if c not in order:
+                order.append(c)
+            vals[short_name(r["Kernel_Name"])][c].append(float(r["Counter_Value"]))
+    hit = "TCC_HIT_sum" in order and "TCC_MISS_sum" in order
+    head = ["kernel", "dispatches"] + [f"{c} / dispatch" for c in order] + (["L2 hit rate"] if hit else [])
+    lines = [f"# Counters: {a.name}", "", "Commands (run from the repository root on the GPU box):",
+             "", "```", a.cmd.strip(), "```", "",
+             "Averages per dispatch over every dispatch of the runs (FETCH_SIZE in KiB, "
+             "unscaled).", "",
+             "| " + " | ".join(head) + " |", "|" + "---|" * len(head)]
+    rows = sorted(vals.items(), key=lambda kv: -sum(kv[1].get("FETCH_SIZE", [0])))
+    for k, cs in rows:
+        n = max(len(v) for v in cs.values())
+        cells = [f"`{k}`", str(n)]
+        for c in order:
+            v = cs.get(c)
+            cells.append(f"{sum(v) / len(v):,.1f}" if v else "")
+        if hit:
+            h, m = sum(cs.get("TCC_HIT_sum", [0])), sum(cs.get("TCC_MISS_sum", [0]))
+            cells.append(f"{h / (h + m):.3f}" if h + m else "")
+        lines.append("| " + " | ".join(cells) + " |")
+    if a.bench:
+        tb = json.loads(open(a.bench).read().strip().splitlines()[-1])
+        extra = {k: tb[k] for k in ("lookup_only", "library_counters") if k in tb}
+        if extra:
+            lines += ["", "bench.py in the first counter run (its own library counters; its "
+                      "timings are not the kernels' own, since counter collection serialises "
+                      "and lengthens every dispatch):", "", "```",
+                      json.dumps(extra, indent=1), "```"]
+    os.makedirs(a.out, exist_ok=True)
+    with open(os.path.join(a.out, f"{a.name}_counters.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def store_kernels_only(a):
     """Per-kernel table of every store kernel in a trace run, plus the
     per-round kernel times bench.py measured with HIP events in that run."""
@@ -158,8 +213,7 @@ def store_kernels_only(a):
     for name, calls, avg, pct in stats:
         if "ptsd::" not in name:
             continue
-        short = name.replace("ptsd::(anonymous namespace)::", "").replace("void ", "")
-        short = short.replace("(anonymous namespace)::", "").split("(")[0]
+        short = short_name(name)
         lines.append(f"| `{short}` | {calls} | {avg * 1e3:.2f} | {pct:.2f} |")
     if a.trace_bench:
         tb = json.loads(open(a.trace_bench).read().strip().splitlines()[-1])
@@ -168,8 +222,8 @@ def store_kernels_only(a):
         for k, v in tb.get("kernel_ms_per_round", {}).items():
             lines.append(f"- {k}: {v}")
         if "evictions" in tb:
-            lines.append(f"- evictions in the timed steps and warm-up: {tb['evictions']}, "
-                         f"index rebuilds: {tb['index_rebuilds']}")
+            lines.append(f"- evictions in the warm-up and timed steps: {tb['evictions']}; "
+                         f"index rebuilds in the timed steps: {tb['index_rebuilds']}")
     os.makedirs(a.out, exist_ok=True)
     with open(os.path.join(a.out, f"{a.name}_kernel_trace.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
