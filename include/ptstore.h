@@ -87,7 +87,7 @@ enum {
 };
 
 typedef struct {
-    int32_t num_layers;    /* L >= 1 */
+    int32_t num_layers;    /* L, 1 .. 2^20 */
     int32_t num_kv_heads;  /* H >= 1 */
     int32_t head_dim;      /* D >= 1 */
     int32_t block_tokens;  /* tokens per block, 1..64 */
@@ -165,7 +165,9 @@ typedef struct {
  * Create a store on the current HIP device: allocates the pool, the block
  * metadata and the hash index, and waits until they are initialised.
  * On success *out owns them until ptstore_destroy(). Errors: INVALID (bad
- * shape, chunk bytes not a multiple of 16, sizes out of range), NOMEM, HIP.
+ * shape, a (layer, K|V) slab not a multiple of 16 bytes or over 1 GiB, the
+ * device pool or the host tier over 2^56 bytes, other sizes out of range;
+ * returned before any HIP call), NOMEM, HIP.
  */
 int ptstore_create(const ptstore_config_t *cfg, ptstore_t **out);
 

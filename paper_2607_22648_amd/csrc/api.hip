@@ -75,6 +75,11 @@ int fail(int code, const char* what, hipError_t e = hipSuccess) {
     return code;
 }
 
+// Shape limits that keep every size and offset well inside 64 bits.
+constexpr int32_t kMaxLayers = 1 << 20;
+constexpr uint64_t kMaxChunkBytes = 1ull << 30;
+constexpr uint64_t kMaxTierBytes = 1ull << 56;
+
 uint64_t next_pow2(uint64_t x) {
     uint64_t p = 1;
     while (p < x) p <<= 1;
@@ -301,8 +306,8 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     if (!cfg || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_create: null argument");
     *out = nullptr;
     const ptstore_config_t c = *cfg;
-    if (c.num_layers < 1 || c.num_kv_heads < 1 || c.head_dim < 1 || c.block_tokens < 1 ||
-        c.block_tokens > 64 || c.elem_bytes < 1)
+    if (c.num_layers < 1 || c.num_layers > kMaxLayers || c.num_kv_heads < 1 || c.head_dim < 1 ||
+        c.block_tokens < 1 || c.block_tokens > 64 || c.elem_bytes < 1)
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: bad shape");
     if (c.pool_blocks < 0 || c.host_blocks < 0 || c.pool_blocks + c.host_blocks > (int64_t)0x7FFFFFFC)
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: pool_blocks / host_blocks out of range");
@@ -312,7 +317,12 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
                     "ptstore_create: replica_blocks must be <= pool_blocks/2 and needs host_blocks "
                     "and PTSTORE_FLAG_EVICT");
     const int64_t want_ids = c.pool_blocks - c.replica_blocks + c.host_blocks;
-    int64_t chunk = (int64_t)c.num_kv_heads * c.block_tokens * c.head_dim * c.elem_bytes;
+    // the slab size in 128 bits: four int32 factors can overflow 64
+    const unsigned __int128 chunk_wide = (unsigned __int128)c.num_kv_heads * (uint32_t)c.block_tokens *
+                                         (uint32_t)c.head_dim * (uint32_t)c.elem_bytes;
+    if (!c.layer_chunk_bytes && chunk_wide > kMaxChunkBytes)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_create: a (layer, K|V) slab exceeds 1 GiB");
+    int64_t chunk = (int64_t)chunk_wide;
     int64_t block = chunk * 2 * c.num_layers;
     std::vector<int64_t> lchunk, lbase;
     if (c.layer_chunk_bytes) {  // per-layer slab sizes
@@ -322,7 +332,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         lbase.resize(c.num_layers + 1);
         block = 0;
         for (int l = 0; l < c.num_layers; ++l) {
-            if (lchunk[l] < 16 || lchunk[l] % 16 != 0 || lchunk[l] > (1ll << 30))
+            if (lchunk[l] < 16 || lchunk[l] % 16 != 0 || lchunk[l] > (int64_t)kMaxChunkBytes)
                 return fail(PTSTORE_ERR_INVALID,
                             "ptstore_create: layer_chunk_bytes must be positive multiples of 16");
             lbase[l] = block;
@@ -330,7 +340,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         }
         lbase[c.num_layers] = block;
         chunk = lchunk[0];
-    } else if (chunk % 16 != 0 || chunk > (1ll << 30)) {
+    } else if (chunk % 16 != 0) {
         return fail(PTSTORE_ERR_INVALID, "ptstore_create: chunk bytes must be a multiple of 16");
     }
     uint64_t slots_n;
@@ -357,6 +367,13 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         s->tier.replicas = c.replica_blocks;
         s->tier.dev_rows = s->tier.owned + c.replica_blocks;
         s->tier.host_blocks = s->capacity - s->tier.owned;
+    }
+    // rows < 2^31 and block bytes <= 2^51: the byte sizes are formed in 128
+    // bits, and one beyond any memory is refused here, not left to wrap
+    if ((unsigned __int128)s->tier.dev_rows * (uint64_t)block > kMaxTierBytes ||
+        (unsigned __int128)s->tier.host_blocks * (uint64_t)block > kMaxTierBytes) {
+        delete s;
+        return fail(PTSTORE_ERR_INVALID, "ptstore_create: pool larger than 2^56 bytes");
     }
     // 1024-thread workgroups, each moving the smallest whole number of
     // 32 KiB-class chunks that leaves at most 64 units per block: one chunk up
@@ -794,17 +811,21 @@ int ptstore_kernel_times(ptstore_t* s, int32_t kind, double* total_ms, int64_t* 
     if (dev.rc) return dev.rc;
     double sum = 0;
     int64_t n = 0;
-    for (auto& p : s->ev[kind]) {
+    auto& v = s->ev[kind];
+    for (auto& p : v) {
         hipError_t e = hipEventSynchronize(p.second);
         float ms = 0;
         if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.first, p.second);
-        if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, "ptstore_kernel_times", e);
+        if (e != hipSuccess) {  // the pairs read so far are back in the pool: not kept twice
+            v.erase(v.begin(), v.begin() + n);
+            return fail(PTSTORE_ERR_HIP, "ptstore_kernel_times", e);
+        }
         sum += ms;
         ++n;
         s->free_ev.push_back(p.first);
         s->free_ev.push_back(p.second);
     }
-    s->ev[kind].clear();
+    v.clear();
     *total_ms = sum;
     *launches = n;
     return PTSTORE_OK;

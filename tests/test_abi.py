@@ -69,3 +69,44 @@ def test_struct_layouts_match_header(tmp_path):
         size, offs = _c_layout(tmp_path, name, fields)
         assert C.sizeof(cls) == size, name
         assert [getattr(cls, f).offset for f in fields] == offs, name
+
+
+
+def test_create_refuses_bad_shapes_without_gpu():
+    """Shape checks run on the host before any HIP call: slab sizes whose
+    product overflows 64 bits, slabs over 1 GiB, pools beyond 2^56 bytes."""
+    from paper_2607_22648_amd import ptstore as P
+    lib = C.CDLL(LIB)
+    lib.ptstore_last_error.restype = C.c_char_p
+
+    def create(**kw):
+        base = dict(num_layers=2, num_kv_heads=8, head_dim=128, block_tokens=16, elem_bytes=2,
+                    pool_blocks=16, index_slots=0, hash_seed=1, flags=0, host_blocks=0,
+                    replica_blocks=0, layer_chunk_bytes=None)
+        base.update(kw)
+        cfg = P.ptstore_config_t(**base)
+        h = C.c_void_p()
+        rc = lib.ptstore_create(C.byref(cfg), C.byref(h))
+        return rc, h.value, lib.ptstore_last_error().decode()
+
+    refused = [
+        dict(num_layers=0), dict(num_layers=(1 << 20) + 1), dict(block_tokens=65),
+        dict(elem_bytes=0), dict(pool_blocks=-1), dict(pool_blocks=1 << 31),
+        # 2^16 * 64 * 2^21 * 2^21 = 2^64: zero in 64-bit arithmetic
+        dict(num_kv_heads=1 << 16, block_tokens=64, head_dim=1 << 21, elem_bytes=1 << 21),
+        # a 2 GiB slab
+        dict(num_kv_heads=64, block_tokens=64, head_dim=1 << 16, elem_bytes=8),
+        # 1 GiB slabs x 2^20 layers x 2^20 blocks = 2^71 bytes of pool
+        dict(num_layers=1 << 20, num_kv_heads=1 << 14, block_tokens=16, head_dim=1 << 10,
+             elem_bytes=4, pool_blocks=1 << 20),
+        # the same blocks in a host tier
+        dict(num_layers=1 << 20, num_kv_heads=1 << 14, block_tokens=16, head_dim=1 << 10,
+             elem_bytes=4, pool_blocks=0, host_blocks=1 << 20),
+        dict(replica_blocks=1),  # replicas need a host tier and eviction
+        dict(index_slots=3),
+        dict(num_kv_heads=1, block_tokens=8, head_dim=1, elem_bytes=1),  # 8-byte slab
+    ]
+    for kw in refused:
+        rc, h, msg = create(**kw)
+        assert rc == P.PTSTORE_ERR_INVALID and h is None, (kw, rc, msg)
+        assert msg.startswith("ptstore_create"), (kw, msg)
