@@ -121,6 +121,29 @@ def _dev(t: Optional[torch.Tensor], dtype, name: str) -> int:
     return t.data_ptr()
 
 
+def _need(t: Optional[torch.Tensor], n: int, name: str) -> None:
+    """The device arrays a call reads or writes are sized by R and max_blocks;
+    the library cannot see an allocation's size, so it is checked here."""
+    if t is None:
+        if n:
+            raise ValueError(f"{name} is required")
+        return
+    if t.numel() < n:
+        raise ValueError(f"{name} holds {t.numel()} elements, the call needs {n}")
+
+
+def _rows(ids: torch.Tensor, name: str = "ids") -> Tuple[int, int]:
+    if ids.dim() != 2:
+        raise ValueError(f"{name} must be [R, max_blocks], got shape {tuple(ids.shape)}")
+    return int(ids.shape[0]), int(ids.shape[1])
+
+
+def _requests(offsets: torch.Tensor) -> int:
+    if offsets.dim() != 1 or offsets.numel() < 1:
+        raise ValueError("offsets must be a 1-D tensor of R + 1 entries")
+    return offsets.numel() - 1
+
+
 def _stream(stream) -> int:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -144,7 +167,9 @@ def ptstore_destroy(h) -> None:
 
 
 def ptstore_lookup(h, tokens, offsets, max_blocks, m, ids, stream=None) -> None:
-    R = offsets.numel() - 1
+    R = _requests(offsets)
+    _need(m, R, "m")
+    _need(ids, R * max_blocks, "ids")
     _check("ptstore_lookup", _lib.ptstore_lookup(
         h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
         tokens.numel(), R, max_blocks, _dev(m, torch.int32, "m"), _dev(ids, torch.int32, "ids"),
@@ -161,7 +186,9 @@ def _cache_blocks(cache: torch.Tensor, block_bytes: int) -> int:
 
 
 def ptstore_gather(h, ids, m, block_table, cache, cache_blocks, stream=None) -> None:
-    R, maxb = ids.shape
+    R, maxb = _rows(ids)
+    _need(m, R, "m")
+    _need(block_table, R * maxb, "block_table")
     _check("ptstore_gather", _lib.ptstore_gather(
         h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, _dev(cache, None, "cache"),
@@ -170,7 +197,9 @@ def ptstore_gather(h, ids, m, block_table, cache, cache_blocks, stream=None) -> 
 
 def ptstore_gather_layers(h, ids, m, block_table, layer_begin, layer_end, cache, cache_blocks,
                           stream=None) -> None:
-    R, maxb = ids.shape
+    R, maxb = _rows(ids)
+    _need(m, R, "m")
+    _need(block_table, R * maxb, "block_table")
     _check("ptstore_gather_layers", _lib.ptstore_gather_layers(
         h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, layer_begin, layer_end,
@@ -178,7 +207,9 @@ def ptstore_gather_layers(h, ids, m, block_table, layer_begin, layer_end, cache,
 
 
 def ptstore_gather_prepare(h, ids, m, block_table, cache_blocks, stream=None) -> None:
-    R, maxb = ids.shape
+    R, maxb = _rows(ids)
+    _need(m, R, "m")
+    _need(block_table, R * maxb, "block_table")
     _check("ptstore_gather_prepare", _lib.ptstore_gather_prepare(
         h, _dev(ids, torch.int32, "ids"), _dev(m, torch.int32, "m"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, cache_blocks, _stream(stream)))
@@ -191,7 +222,9 @@ def ptstore_gather_prepared(h, layer_begin, layer_end, cache, cache_blocks, stre
 
 def ptstore_scatter_layers(h, ids, created, block_table, layer_begin, layer_end, cache,
                            cache_blocks, stream=None) -> None:
-    R, maxb = ids.shape
+    R, maxb = _rows(ids)
+    _need(created, R * maxb, "created")
+    _need(block_table, R * maxb, "block_table")
     _check("ptstore_scatter_layers", _lib.ptstore_scatter_layers(
         h, _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, layer_begin, layer_end,
@@ -200,7 +233,10 @@ def ptstore_scatter_layers(h, ids, created, block_table, layer_begin, layer_end,
 
 def ptstore_lookup_gather(h, tokens, offsets, max_blocks, m, ids, block_table, cache, cache_blocks,
                           stream=None) -> None:
-    R = offsets.numel() - 1
+    R = _requests(offsets)
+    _need(m, R, "m")
+    _need(ids, R * max_blocks, "ids")
+    _need(block_table, R * max_blocks, "block_table")
     _check("ptstore_lookup_gather", _lib.ptstore_lookup_gather(
         h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
         tokens.numel(), R, max_blocks, _dev(m, torch.int32, "m"), _dev(ids, torch.int32, "ids"),
@@ -209,7 +245,10 @@ def ptstore_lookup_gather(h, tokens, offsets, max_blocks, m, ids, block_table, c
 
 
 def ptstore_insert(h, tokens, offsets, max_blocks, m_out, ids, created, stream=None) -> None:
-    R = offsets.numel() - 1
+    R = _requests(offsets)
+    _need(m_out, R, "m_out")
+    _need(ids, R * max_blocks, "ids")
+    _need(created, R * max_blocks, "created")
     _check("ptstore_insert", _lib.ptstore_insert(
         h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
         tokens.numel(), R, max_blocks, _dev(m_out, torch.int32, "m_out"),
@@ -217,7 +256,9 @@ def ptstore_insert(h, tokens, offsets, max_blocks, m_out, ids, created, stream=N
 
 
 def ptstore_scatter(h, ids, created, block_table, cache, cache_blocks, stream=None) -> None:
-    R, maxb = ids.shape
+    R, maxb = _rows(ids)
+    _need(created, R * maxb, "created")
+    _need(block_table, R * maxb, "block_table")
     _check("ptstore_scatter", _lib.ptstore_scatter(
         h, _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"),
         _dev(block_table, torch.int32, "block_table"), R, maxb, _dev(cache, None, "cache"),

@@ -110,3 +110,31 @@ def test_create_refuses_bad_shapes_without_gpu():
         rc, h, msg = create(**kw)
         assert rc == P.PTSTORE_ERR_INVALID and h is None, (kw, rc, msg)
         assert msg.startswith("ptstore_create"), (kw, msg)
+
+
+def test_binding_checks_array_sizes_without_gpu():
+    """The binding refuses arrays smaller than R and max_blocks require before
+    anything reaches the library (which cannot see allocation sizes)."""
+    import pytest
+    import torch
+    from paper_2607_22648_amd import ptstore as P
+    offs = torch.tensor([0, 32, 64], dtype=torch.int64)
+    toks = torch.zeros(64, dtype=torch.int32)
+    m = torch.zeros(2, dtype=torch.int32)
+    ids = torch.zeros((2, 4), dtype=torch.int32)
+    with pytest.raises(ValueError, match="ids holds 7"):
+        P.ptstore_lookup(None, toks, offs, 4, m, ids.view(-1)[:7])
+    with pytest.raises(ValueError, match="m holds 1"):
+        P.ptstore_lookup(None, toks, offs, 4, m[:1], ids)
+    with pytest.raises(ValueError, match="block_table holds 4"):
+        P.ptstore_gather(None, ids, m, ids[:1], None, 0)
+    with pytest.raises(ValueError, match="created holds 6"):
+        P.ptstore_scatter(None, ids, torch.zeros(6, dtype=torch.uint8), ids, None, 0)
+    with pytest.raises(ValueError, match=r"must be \[R, max_blocks\]"):
+        P.ptstore_gather(None, ids.view(-1), m, ids, None, 0)
+    with pytest.raises(ValueError, match="created holds 4"):
+        P.ptstore_insert(None, toks, offs, 4, m, ids, torch.zeros(4, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="block_table holds 2"):
+        P.ptstore_lookup_gather(None, toks, offs, 4, m, ids, ids.view(-1)[:2], None, 0)
+    with pytest.raises(ValueError, match="offsets"):
+        P.ptstore_lookup(None, toks, offs[:0], 4, m, ids)
