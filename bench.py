@@ -182,6 +182,9 @@ SETTLE_PAUSE_S = 15.0
 SETTLE = {}
 
 
+COPY_SHAPE = ""  # --copy-shape, applied to every store the bench creates
+
+
 def make_store(P, *args, **kw):
     t0 = time.perf_counter()
     store = P.PrefixStore(*args, **kw)
@@ -195,6 +198,8 @@ def make_store(P, *args, **kw):
         t0 = time.perf_counter()
         store = P.PrefixStore(*args, **kw)
         SETTLE.update({"reallocated": True, "second_alloc_s": round(time.perf_counter() - t0, 3)})
+    if COPY_SHAPE:
+        store.set_copy_shape(*(int(x) for x in COPY_SHAPE.split(",")))
     return store
 
 
@@ -291,8 +296,6 @@ def run_passage(args, torch, P, synth, dev):
                          sh.layer_chunk_bytes)
     pool_blocks = len(w.stored) * w.passage_blocks
     store = make_store(P, shape, pool_blocks, flags=P.PTSTORE_FLAG_TIMING)
-    if args.copy_shape:
-        store.set_copy_shape(*(int(x) for x in args.copy_shape.split(",")))
     t0 = time.time()
     batch = max(1, (16 << 30) // (w.passage_blocks * sh.block_bytes))
     pre = prefill(store, w, dev, torch, batch_passages=min(64, batch))
@@ -751,6 +754,8 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding of "
                                    "the store is a design, not code (--gpus 1)"}))
         sys.exit(2)
+    global COPY_SHAPE
+    COPY_SHAPE = args.copy_shape
     import torch
     from paper_2607_22648_amd import ptstore as P
     from workloads import synth

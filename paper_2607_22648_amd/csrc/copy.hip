@@ -212,11 +212,12 @@ struct CopyArgs {
 };
 
 // The (descriptor, chunk group) units are visited grid-stride. The host
-// picks the grid: a gather launches one workgroup per possible unit, so the
-// dense front of the list runs in hardware dispatch order (neighbouring
-// workgroups copy neighbouring chunks, the few workgroups past the end exit
-// at once); a scatter, whose created blocks are sparse, launches a few
-// workgroups per compute unit that loop.
+// picks the grid: a gather launches one workgroup per possible unit, up to
+// 2048 times what the device holds at once, so the dense front of the list
+// runs in hardware dispatch order (neighbouring workgroups copy neighbouring
+// chunks; past the cap a workgroup also takes the unit one grid further on,
+// and workgroups past the end exit at once); a scatter, whose created blocks
+// are sparse, launches 16 times what the device holds, looping.
 // Uniform slabs: a unit is (descriptor, group of chunks_per_group slabs).
 template <bool GATHER>
 __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
@@ -379,7 +380,7 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     }
     const int64_t bound = (int64_t)R * max_blocks * a.groups;  // units if every entry moves
     const int64_t cap = (1ll << 31) / p.threads;                 // launch limit on work-items
-    int64_t grid = p.grid ? p.grid : (GATHER ? bound : (int64_t)p.loop_grid);
+    int64_t grid = p.grid ? p.grid : (GATHER ? (int64_t)p.gather_grid : (int64_t)p.loop_grid);
     if (grid > bound) grid = bound;
     if (grid > cap) grid = cap;
     if (grid < 1) return hipSuccess;

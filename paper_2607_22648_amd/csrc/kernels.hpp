@@ -94,6 +94,7 @@ struct CopyPlan {
     int32_t chunks_per_group;  // chunks one copy unit moves
     int32_t threads;           // workgroup size of the copy kernel
     int32_t grid;              // workgroups of the copy kernel, 0 = chosen per call
+    int32_t gather_grid;       // most workgroups of a gather (one per unit below that)
     int32_t loop_grid;         // workgroups of a looping (sparse) copy
     DevState* state;
     TierView tier;
