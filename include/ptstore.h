@@ -326,10 +326,11 @@ int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64
  * current value. chunks_per_group: (layer, K|V) chunks one unit moves (by
  * default the smallest divisor of 2 * num_layers that leaves at most 64
  * units per block); threads: workgroup size, 64..1024, a multiple of 64
- * (default 1024); grid: workgroups of
- * the copy kernels (by default a gather launches one per possible unit and
- * a scatter four times what every compute unit holds). For tuning sweeps;
- * results never depend on it. */
+ * (default 1024); grid: workgroups of the copy kernels (by default a
+ * gather launches one per possible unit, up to 2048 times the workgroups
+ * the device holds at once, and a scatter 16 times the workgroups the
+ * device holds, looping; a grid once set replaces both until set again).
+ * For tuning sweeps; results never depend on it. */
 int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t threads,
                            int32_t grid);
 
