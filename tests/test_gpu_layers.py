@@ -192,3 +192,43 @@ def test_prepared_per_layer_gather(chunks):
     with pytest.raises(P.PTStoreError):
         t.gpu.gather_prepared(dst, (0, 1))
     t.close()
+
+
+def test_large_variable_slabs_span_several_units():
+    """Blocks of per-layer slabs larger than one span-copy unit (256 KiB), with
+    layer boundaries inside units, gathered whole and by layer ranges, and
+    scattered by layer ranges."""
+    chunks = [32 << 10, 8 << 10, 96 << 10, 16, 48 << 10, 112]  # blocks of 368.3 KiB
+    rng = np.random.default_rng(31)
+    t = Twin(len(chunks), 1, 1, 2, 40, layer_chunk_bytes=chunks)
+    atoms = _atoms(rng, 4, 2, 50)
+    for i in range(3):
+        toks, offs = random_block_batch(rng, 6, atoms, 5, tail_p=0.2)
+        R = len(offs) - 1
+        (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, 5)
+        t.scatter_random(ids, cr, rids, rcr, block_table_identity(R, 5), seed=70 + i,
+                         layers=(0, 3) if i == 1 else None)
+        if i == 1:
+            t.scatter_random(ids, cr, rids, rcr, block_table_identity(R, 5), seed=80, layers=(3, 6))
+    t.check_pool()
+    toks, offs = random_block_batch(rng, 8, atoms, 5, tail_p=0.3)
+    R = len(offs) - 1
+    (m, ids, _), (rm, rids, _) = t.lookup_gather(toks, offs, 5, block_table_identity(R, 5), R * 5)
+    for layers in ((0, 6), (2, 3), (1, 5), (5, 6)):
+        t.gather_layers(m, ids, rm, rids, block_table_identity(R, 5), R * 5, layers)
+    t.close()
+
+
+def test_variable_slabs_beyond_the_gather_grid_cap():
+    """More span units than the gather launches workgroups (20,000 requests x
+    64 blocks, one unit each): workgroups take a second unit one grid on."""
+    rng = np.random.default_rng(14)
+    R, maxb = 20_000, 64
+    toks = rng.integers(0, 32000, size=R * maxb * 2, dtype=np.int32)
+    offs = np.arange(R + 1, dtype=np.int64) * (maxb * 2)
+    t = Twin(2, 1, 1, 2, R * maxb, layer_chunk_bytes=[16, 32])
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, maxb)
+    t.scatter_random(ids, cr, rids, rcr, block_table_identity(R, maxb), seed=19)
+    t.check_pool()
+    t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
+    t.close()
