@@ -50,7 +50,8 @@ struct ptstore {
     TierView tier;  // owned = capacity and no host rows for a device-only store
     void* tier_mem; // replica map and replicate scratch
     void* host_mem; // the host tier as allocated (tier.host is its device address)
-    void* layer_tab; // per-layer slab sizes [L] then bases [L + 1], int64; null if uniform
+    void* layer_tab; // per-layer slab bases [L + 1], int64 (layer l's slabs are half of
+                     // base[l+1] - base[l] each); null if every layer has chunk_bytes
     std::vector<int64_t> lbase_host;  // the bases, for launch shapes
     // the block list of ptstore_gather_prepare, while it is valid
     bool prep_valid;
@@ -150,8 +151,7 @@ CopyPlan copy_plan(ptstore_t* s) {
     p.loop_grid = resident * 16;
     p.state = s->state;
     p.tier = s->tier;
-    p.lchunk = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) : nullptr;
-    p.lbase = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) + s->cfg.num_layers : nullptr;
+    p.lbase = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) : nullptr;
     p.lbase_host = s->layer_tab ? s->lbase_host.data() : nullptr;
     return p;
 }
@@ -419,12 +419,10 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         return fail(PTSTORE_ERR_NOMEM, "ptstore_create: hipMalloc", e);
     }
     if (!lchunk.empty()) {
-        const size_t n = (size_t)c.num_layers * sizeof(int64_t);
+        const size_t n = ((size_t)c.num_layers + 1) * sizeof(int64_t);
         s->lbase_host = lbase;
-        if ((e = hipMalloc(&s->layer_tab, 2 * n + sizeof(int64_t))) != hipSuccess ||
-            (e = hipMemcpy(s->layer_tab, lchunk.data(), n, hipMemcpyHostToDevice)) != hipSuccess ||
-            (e = hipMemcpy(static_cast<int64_t*>(s->layer_tab) + c.num_layers, lbase.data(),
-                           n + sizeof(int64_t), hipMemcpyHostToDevice)) != hipSuccess) {
+        if ((e = hipMalloc(&s->layer_tab, n)) != hipSuccess ||
+            (e = hipMemcpy(s->layer_tab, lbase.data(), n, hipMemcpyHostToDevice)) != hipSuccess) {
             ptstore_destroy(s);
             (void)hipGetLastError();
             return fail(PTSTORE_ERR_NOMEM, "ptstore_create: layer tables", e);

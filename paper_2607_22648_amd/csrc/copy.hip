@@ -207,8 +207,7 @@ struct CopyArgs {
     int32_t chunks_per_group;
     int32_t groups;            // ceil((c_hi - c_lo) / chunks_per_group)
     int32_t c_lo, c_hi;        // chunks moved: 2*l0 .. 2*l1-1
-    const int64_t* lchunk;     // per-layer slab sizes (VAR only)
-    const int64_t* lbase;
+    const int64_t* lbase;      // per-layer slab bases (null when uniform)
 };
 
 // The (descriptor, chunk group) units are visited grid-stride. The host
@@ -370,9 +369,8 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     a.chunks_per_group = p.chunks_per_group;
     a.c_lo = 2 * l0;
     a.c_hi = 2 * l1;
-    a.lchunk = p.lchunk;
     a.lbase = p.lbase;
-    if (p.lchunk) {  // units are kSpanBytes spans of the layer range
+    if (p.lbase) {  // units are kSpanBytes spans of the layer range
         const int64_t lo = p.lbase_host[l0], hi = p.lbase_host[l1];
         a.groups = (int32_t)((hi - lo + kSpanBytes - 1) / kSpanBytes);
     } else {
@@ -384,7 +382,7 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     if (grid > bound) grid = bound;
     if (grid > cap) grid = cap;
     if (grid < 1) return hipSuccess;
-    if (p.lchunk)
+    if (p.lbase)
         hipLaunchKernelGGL(k_copy_spans<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     else
         hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);

@@ -98,10 +98,9 @@ struct CopyPlan {
     int32_t loop_grid;         // workgroups of a looping (sparse) copy
     DevState* state;
     TierView tier;
-    // per-layer slab sizes (null when every layer has chunk_bytes): device
-    // tables lchunk[l] (L entries) and lbase[l] = 2 * sum of lchunk[0..l-1]
-    // (L + 1 entries), and the host's copy of lbase
-    const int64_t* lchunk;
+    // per-layer slab sizes (null when every layer has chunk_bytes): the
+    // device table lbase[l] = 2 * (sum of the slab sizes of layers 0..l-1),
+    // L + 1 entries, and the host's copy of it
     const int64_t* lbase;
     const int64_t* lbase_host;
 };
