@@ -39,6 +39,14 @@
  *  - Return codes: PTSTORE_OK, or an error found on the host before any
  *    work is enqueued. Conditions only the device can see (a full store,
  *    out-of-range entries) are counted and reported by ptstore_stats().
+ *  - HIP graphs: once a call has grown the store's scratch to a batch size,
+ *    lookup, gather, gather_layers, lookup_gather, scatter, scatter_layers
+ *    and (without PTSTORE_FLAG_EVICT) insert of that size or smaller only
+ *    launch kernels: no allocation, no wait, no memset. They may be
+ *    captured and replayed; a replay works on the store as it is then. A
+ *    later call with a larger batch regrows the scratch, after which
+ *    earlier captures must not be replayed. An evicting insert keeps a
+ *    per-call value on the host and is not to be replayed.
  */
 #ifndef PTSTORE_H
 #define PTSTORE_H

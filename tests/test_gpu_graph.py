@@ -1,0 +1,83 @@
+"""The hot path under HIP graph capture.
+
+A lookup + gather captured once replays bit-exact against the oracle, three
+times, with eager work of the program between the replays: inserts and
+scatters that grow the store (so each replay must see the store as it is
+then, not as it was at capture), sentinel fills of the outputs and
+synchronisations. The calls allocate nothing and wait for nothing once the
+store's scratch has grown to the batch size, which a first eager call does;
+later calls on the store must not need a larger copy scratch than the
+captured one (a larger batch regrows it).
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from tests.helpers import random_block_batch, block_table_identity
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from tests.twin import Twin, host, to_dev
+
+
+def _atoms(rng, n, bt, vocab):
+    while True:
+        a = rng.integers(0, vocab, size=(n, bt), dtype=np.int32)
+        if len({r.tobytes() for r in a}) == n:
+            return a
+
+
+def _grow(t, rng, atoms, R, maxb, seed):
+    toks, offs = random_block_batch(rng, R, atoms, maxb, tail_p=0.2)
+    Ri = len(offs) - 1
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(toks, offs, maxb)
+    t.scatter_random(ids, cr, rids, rcr, block_table_identity(Ri, maxb), seed=seed)
+
+
+@pytest.mark.parametrize("chunks", [None, [32, 96, 16]])
+def test_captured_lookup_gather_replays(chunks):
+    rng = np.random.default_rng(41)
+    bt_ = 4
+    if chunks is None:
+        t = Twin(3, 2, 8, bt_, 2000)
+    else:
+        t = Twin(len(chunks), 1, 1, bt_, 2000, layer_chunk_bytes=chunks)
+    atoms = _atoms(rng, 5, bt_, 200)
+    R, maxb = 16, 8
+    _grow(t, rng, atoms, 8, maxb, seed=1)
+    toks, offs = random_block_batch(rng, R, atoms, maxb + 2, tail_p=0.3)
+    tt, oo = to_dev(toks), to_dev(offs)
+    bt_np = block_table_identity(R, maxb)
+    bt = to_dev(bt_np)
+    m = torch.empty(R, dtype=torch.int32, device="cuda")
+    ids = torch.empty((R, maxb), dtype=torch.int32, device="cuda")
+    n = R * maxb * t.shape.block_bytes
+    cache = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")
+    t.gpu.lookup_gather(tt, oo, maxb, bt, cache, m=m, ids=ids)  # grows the scratch
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        t.gpu.lookup_gather(tt, oo, maxb, bt, cache, m=m, ids=ids)
+    torch.cuda.synchronize()
+    seen = set()
+    for rep in range(3):
+        cache.fill_(0xA5)
+        m.fill_(-7)
+        ids.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        rm, rids = t.ref.lookup(toks, offs, maxb)
+        rdst = np.full(n, 0xA5, dtype=np.uint8)
+        t.ref.gather(rids, rm, bt_np, rdst, R * maxb)
+        np.testing.assert_array_equal(host(m), rm, err_msg=f"replay {rep}: m")
+        np.testing.assert_array_equal(host(ids), rids, err_msg=f"replay {rep}: ids")
+        np.testing.assert_array_equal(host(cache), rdst, err_msg=f"replay {rep}: gathered bytes")
+        seen.add(int(rm.sum()))
+        # eager work between replays: the store grows (batches no larger
+        # than the captured one, so the copy scratch stays where it was)
+        _grow(t, rng, atoms, 8, maxb, seed=10 + rep)
+    assert len(seen) > 1, "the replays should have seen the store grow"
+    t.close()
