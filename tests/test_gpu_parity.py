@@ -376,3 +376,56 @@ def test_copy_grid_beyond_launch_limit():
     t.check_pool()
     t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
     t.close()
+
+
+def test_batch_at_the_size_limit():
+    """R x max_blocks at its limit, 2^29 (8192 requests x 65,536 blocks of
+    room): lookup, insert and gather agree with the oracle on every request,
+    all room past a request's blocks reads -1, and one entry more is refused
+    before any work."""
+    R, maxb = 1 << 13, 1 << 16
+    rng = np.random.default_rng(23)
+    bt_ = 16
+    stored = [rng.integers(0, 32000, size=bt_ * k, dtype=np.int32) for k in (1, 2, 3, 4)]
+    t = Twin(1, 1, 8, bt_, 64)
+    st_toks, st_offs = synth.concat_requests(stored[1:3])
+    (m, ids, cr), (rc, rm, rids, rcr) = t.insert(st_toks, st_offs, 4)
+    t.scatter_random(ids, cr, rids, rcr, block_table_identity(2, 4), seed=5)
+    # every request is one of the four sequences, some of them extended
+    pick = rng.integers(0, 4, size=R)
+    seqs = [stored[p] if i % 3 else np.concatenate([stored[p], stored[0]]) for i, p in enumerate(pick)]
+    toks, offs = synth.concat_requests(seqs)
+    tt, oo = to_dev(toks), to_dev(offs)
+    s = t.gpu
+    m = torch.empty(R, dtype=torch.int32, device=DEV)
+    ids = torch.empty((R, maxb), dtype=torch.int32, device=DEV)
+    s.lookup(tt, oo, maxb, m=m, ids=ids)
+    om, oids = t.ref.lookup(toks, offs, 8)  # no request has more than 5 blocks
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(m), om)
+    np.testing.assert_array_equal(host(ids[:, :8]), oids)
+    assert bool((ids[:, 8:] == -1).all())
+    # gather: destinations for the first 8 columns only, the rest -1
+    bt = torch.full((R, maxb), -1, dtype=torch.int32, device=DEV)
+    bt[:, :8] = torch.arange(R * 8, dtype=torch.int32, device=DEV).view(R, 8)
+    n = R * 8 * t.shape.block_bytes
+    cache = torch.full((n,), 0xA5, dtype=torch.uint8, device=DEV)
+    s.gather(ids, m, bt, cache)
+    rdst = np.full(n, 0xA5, dtype=np.uint8)
+    t.ref.gather(oids, om, block_table_identity(R, 8), rdst, R * 8)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(cache), rdst)
+    # insert of the same batch: the new blocks, each created once
+    im, iids, icr = s.insert(tt, oo, maxb)
+    orc = t.ref.insert(toks, offs, 8)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(im), orc[1])
+    np.testing.assert_array_equal(host(iids[:, :8]), orc[2])
+    np.testing.assert_array_equal(host(icr[:, :8]).astype(bool), orc[3].astype(bool))
+    assert bool((iids[:, 8:] == -1).all()) and int(icr[:, 8:].sum()) == 0
+    # one entry over the limit is refused on the host
+    lib = P.lib()
+    rc = lib.ptstore_lookup(s.h, tt.data_ptr(), oo.data_ptr(), tt.numel(), R, maxb + 1,
+                            m.data_ptr(), ids.data_ptr(), None)
+    assert rc == P.PTSTORE_ERR_INVALID
+    t.close()
