@@ -54,7 +54,7 @@ def test_golden_example(case):
     t.close()
 
 
-@pytest.mark.parametrize("bt", [16, 2, 5])
+@pytest.mark.parametrize("bt", [16, 2, 5, 1, 63, 64])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_random_tries(seed, bt):
     rng = np.random.default_rng(100 + seed)
