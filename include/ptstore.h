@@ -36,6 +36,8 @@
  *    the stream has reached that point. Calls on one store must be ordered
  *    on one stream (a store is not safe for concurrent calls); a lookup sees
  *    exactly the inserts enqueued before it.
+ *  - A call takes at most 2^29 (request, block) entries: R * max_blocks
+ *    <= 2^29, else INVALID.
  *  - Return codes: PTSTORE_OK, or an error found on the host before any
  *    work is enqueued. Conditions only the device can see (a full store,
  *    out-of-range entries) are counted and reported by ptstore_stats().
@@ -188,8 +190,8 @@ int ptstore_destroy(ptstore_t *store);
  * and ids[r][b] = the id of the stored block at depth b for b < m[r], -1
  * beyond. Outputs: m [R] int32, ids [R][max_blocks] int32. With
  * PTSTORE_FLAG_EVICT every matched block of every request counts one access.
- * Errors: INVALID (store NULL, R < 0, max_blocks < 1, n_tokens < 0 or
- * >= 2^32, a NULL pointer with R > 0).
+ * Errors: INVALID (store NULL, R < 0, max_blocks < 1, R * max_blocks >
+ * 2^29, n_tokens < 0 or >= 2^32, a NULL pointer with R > 0), HIP.
  */
 int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
                    int64_t n_tokens, int32_t R, int32_t max_blocks,
@@ -205,7 +207,10 @@ int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * naming the same cache block race). `cache` must be 16-byte aligned.
  * The call first builds a dense list of the blocks to copy in store-owned
  * scratch of 8 bytes per (request, block), grown on demand (growing waits
- * for `stream`), then copies only those blocks.
+ * for `stream`), then copies only those blocks. Errors: INVALID (store
+ * NULL, R < 0, max_blocks < 1, R * max_blocks > 2^29, cache_blocks < 0, a
+ * NULL pointer with R > 0, `cache` not 16-byte aligned), NOMEM (scratch),
+ * HIP.
  */
 int ptstore_gather(ptstore_t *store, const int32_t *ids, const int32_t *m,
                    const int32_t *block_table, int32_t R, int32_t max_blocks,
@@ -214,7 +219,7 @@ int ptstore_gather(ptstore_t *store, const int32_t *ids, const int32_t *m,
 /*
  * ptstore_lookup followed by ptstore_gather of its result, enqueued
  * back to back on `stream` (the measured hot path). m and ids are written
- * as by ptstore_lookup.
+ * as by ptstore_lookup. Errors: those of either call.
  */
 int ptstore_lookup_gather(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
                           int64_t n_tokens, int32_t R, int32_t max_blocks,
@@ -278,6 +283,7 @@ int ptstore_insert(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * and block_table[r][b] >= 0, copy each chunk of
  * cache[layer][K|V][block_table[r][b]] into pool block ids[r][b].
  * Out-of-range ids / cache blocks are skipped and counted in bad_entries.
+ * Errors as ptstore_gather.
  */
 int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created,
                     const int32_t *block_table, int32_t R, int32_t max_blocks,
@@ -307,15 +313,17 @@ int ptstore_scatter_layers(ptstore_t *store, const int32_t *ids, const uint8_t *
                            int32_t layer_begin, int32_t layer_end, const void *cache,
                            int64_t cache_blocks, void *stream);
 
-/* Wait for the device and read the store's counters into *stats. */
+/* Wait for the device and read the store's counters into *stats.
+ * Errors: INVALID (a NULL argument), HIP. */
 int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);
 
 /* Zero the event counters (probes, compares, CAS, full_events, bad_entries,
  * insert_fallbacks, index_rebuilds); blocks_stored, evictions and the clock
- * are state and stay. */
+ * are state and stay. Waits for the device. Errors: INVALID (NULL), HIP. */
 int ptstore_reset_counters(ptstore_t *store);
 
-/* Device buffers of the store (see ptstore_buffers_t). */
+/* Device buffers of the store (see ptstore_buffers_t); no device work.
+ * Errors: INVALID (a NULL argument). */
 int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
 
 /*

@@ -195,12 +195,15 @@ struct Timed {
     }
 };
 
+// Most (request, block) entries one call takes.
+constexpr int64_t kMaxEntries = 1ll << 29;
+
 bool check_batch(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, int64_t n_tokens,
                  int32_t R, int32_t max_blocks) {
     (void)s;
     if (R < 0 || max_blocks < 1) return false;
     if (n_tokens < 0 || n_tokens >= (int64_t)0xFFFFFFFFll) return false;
-    if ((int64_t)R * max_blocks > (1ll << 29)) return false;
+    if ((int64_t)R * max_blocks > kMaxEntries) return false;
     if (R > 0 && (!offsets || (!tokens && n_tokens > 0))) return false;
     return true;
 }
@@ -540,7 +543,7 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
                           const int32_t* block_table, int32_t R, int32_t max_blocks,
                           int32_t layer_begin, int32_t layer_end, void* cache, int64_t cache_blocks,
                           void* stream) {
-    if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
+    if (!s || R < 0 || max_blocks < 1 || (int64_t)R * max_blocks > kMaxEntries || cache_blocks < 0 ||
         (R > 0 && (!ids || !m || !block_table || !cache)) ||
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0 || layer_begin < 0 ||
         layer_end > s->cfg.num_layers || layer_begin >= layer_end)
@@ -573,7 +576,7 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
 int ptstore_gather_prepare(ptstore_t* s, const int32_t* ids, const int32_t* m,
                            const int32_t* block_table, int32_t R, int32_t max_blocks,
                            int64_t cache_blocks, void* stream) {
-    if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
+    if (!s || R < 0 || max_blocks < 1 || (int64_t)R * max_blocks > kMaxEntries || cache_blocks < 0 ||
         (R > 0 && (!ids || !m || !block_table)))
         return fail(PTSTORE_ERR_INVALID, "ptstore_gather_prepare: bad argument");
     s->prep_valid = false;
@@ -683,7 +686,7 @@ int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* crea
                            const int32_t* block_table, int32_t R, int32_t max_blocks,
                            int32_t layer_begin, int32_t layer_end, const void* cache,
                            int64_t cache_blocks, void* stream) {
-    if (!s || R < 0 || max_blocks < 1 || cache_blocks < 0 ||
+    if (!s || R < 0 || max_blocks < 1 || (int64_t)R * max_blocks > kMaxEntries || cache_blocks < 0 ||
         (R > 0 && (!ids || !created || !block_table || !cache)) ||
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0 || layer_begin < 0 ||
         layer_end > s->cfg.num_layers || layer_begin >= layer_end)

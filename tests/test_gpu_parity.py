@@ -423,9 +423,19 @@ def test_batch_at_the_size_limit():
     np.testing.assert_array_equal(host(iids[:, :8]), orc[2])
     np.testing.assert_array_equal(host(icr[:, :8]).astype(bool), orc[3].astype(bool))
     assert bool((iids[:, 8:] == -1).all()) and int(icr[:, 8:].sum()) == 0
-    # one entry over the limit is refused on the host
+    # one more request over the limit is refused on the host, by every call
     lib = P.lib()
-    rc = lib.ptstore_lookup(s.h, tt.data_ptr(), oo.data_ptr(), tt.numel(), R, maxb + 1,
-                            m.data_ptr(), ids.data_ptr(), None)
-    assert rc == P.PTSTORE_ERR_INVALID
+    over = [
+        lib.ptstore_lookup(s.h, tt.data_ptr(), oo.data_ptr(), tt.numel(), R + 1, maxb,
+                           m.data_ptr(), ids.data_ptr(), None),
+        lib.ptstore_gather(s.h, ids.data_ptr(), m.data_ptr(), bt.data_ptr(), R + 1, maxb,
+                           cache.data_ptr(), R * 8, None),
+        lib.ptstore_gather_prepare(s.h, ids.data_ptr(), m.data_ptr(), bt.data_ptr(), R + 1, maxb,
+                                   R * 8, None),
+        lib.ptstore_scatter(s.h, iids.data_ptr(), icr.data_ptr(), bt.data_ptr(), R + 1, maxb,
+                            cache.data_ptr(), R * 8, None),
+        lib.ptstore_insert(s.h, tt.data_ptr(), oo.data_ptr(), tt.numel(), R + 1, maxb,
+                           im.data_ptr(), iids.data_ptr(), icr.data_ptr(), None),
+    ]
+    assert all(rc == P.PTSTORE_ERR_INVALID for rc in over), over
     t.close()
