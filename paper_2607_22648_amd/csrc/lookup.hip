@@ -13,7 +13,9 @@
 //      with the right tokens but the wrong parent (two prefixes whose keys
 //      collide), it keeps probing for one with the right parent before the
 //      window is decided, so the answer never depends on the hash.
-// Windows are walked in order and the walk stops at the first miss.
+// Windows are walked in order and the walk stops at the first miss; for
+// requests with room for more than one window, k_lookup_wide gives each
+// window of a round its own wave instead.
 // With eviction on, every matched block counts one access: its frequency F
 // grows by one and its priority becomes max(H, L + F), which is L + F for
 // the final F whatever order the atomics land in.
@@ -206,6 +208,123 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
     }
 }
 
+// Long requests: one workgroup of W waves per request, each wave on its
+// own window, W windows per round instead of one after another. Within a
+// round each wave scans its window's key chain from a zero carry; the affine
+// chain makes window w's carry P^64 * (carry of window w-1) + (its offset),
+// folded over the round's earlier windows from LDS, so every lane then has
+// its key and probes at once. A position's parent check needs the candidate
+// of the position before it, across a wave boundary through LDS. The round's
+// first failing position decides; only when it found the right tokens under
+// another parent (a key collision) does that lane probe on, and the round is
+// checked again.
+template <int BT, bool TOUCH, int W>
+__global__ __launch_bounds__(W * kWave) void k_lookup_wide(IndexView ix, Batch bat,
+                                                           int32_t* __restrict__ m_out,
+                                                           int32_t* __restrict__ ids_out) {
+    __shared__ uint64_t sh_off[W];   // each window's chain offset (zero carry)
+    __shared__ int32_t sh_last[W];   // candidate of each window's last lane
+    __shared__ int32_t sh_fail[W];   // first failing lane per window (kWave: none)
+    __shared__ int32_t sh_retry[W];  // 1: that lane found the tokens under another parent
+    __shared__ uint64_t sh_klast;    // key of the round's last position
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x / kWave;
+    const int64_t r = blockIdx.x;
+    if (r >= bat.R) return;  // uniform over the workgroup
+    const int bt = BT ? BT : ix.block_tokens;
+    const HashTables* __restrict__ ht = ix.ht;
+    int64_t o0;
+    const int32_t n = request_blocks(bat, r, bt, wv == 0 ? lane : 1, ix.state, &o0);
+    const int32_t* __restrict__ seq = bat.tokens + o0;
+    int32_t* __restrict__ row = ids_out + r * bat.max_blocks;
+    const uint64_t clock = TOUCH ? ix.state->clock : 0;
+    const uint64_t p64 = ht->pow_lane[kWave - 1];  // P^64
+    uint64_t carry_key = ht->root_key;
+    int32_t carry_id = -1;  // the root
+    int32_t m = n;
+    unsigned long long probes = 0, cmps = 0;
+    int r0 = 0;  // first block of the round
+    for (; r0 < n; r0 += W * kWave) {
+        const int b = r0 + wv * kWave + lane;
+        const bool active = b < n;
+        BlockTokens<BT> bk;
+        uint64_t c = 0;
+        if (active) {
+            bk.load(seq + (int64_t)b * bt);
+            c = bk.hash(ht->content_seed, bt);
+        }
+        const uint64_t sl = window_chain(c, 0, ht, lane);  // zero-carry chain
+        if (lane == kWave - 1) sh_off[wv] = sl;
+        __syncthreads();
+        uint64_t carry = carry_key;
+        for (int i = 0; i < wv; ++i) carry = addmod61(mulmod61(p64, carry), sh_off[i]);
+        const uint64_t k = addmod61(mulmod61(ht->pow_lane[lane], carry), sl);
+        const uint64_t ik = index_key(k, *ht);
+        int32_t cand = -1, cpar = -2;
+        uint64_t pos = 0;
+        if (active)
+            cand = probe<BT>(ix, ik, slot_of(ik, ht->slot_seed, ix.slot_mask), bk, false, 0, &pos,
+                             &cpar, &probes, &cmps);
+        if (wv == W - 1 && lane == kWave - 1) sh_klast = k;
+        int fail = W * kWave;  // first failing position of the round, relative to r0
+        while (true) {
+            if (lane == kWave - 1) sh_last[wv] = cand;
+            __syncthreads();
+            int32_t prev = __shfl_up(cand, 1, kWave);
+            if (lane == 0) prev = wv == 0 ? carry_id : sh_last[wv - 1];
+            const int32_t par = cand >= 0 ? cpar : -2;
+            const bool ok = active && cand >= 0 && par == prev;
+            const unsigned long long bad = ballot64(!ok);
+            const int f = bad ? __ffsll((long long)bad) - 1 : kWave;
+            const int rt = f < kWave ? __shfl((active && cand >= 0 && par != prev) ? 1 : 0, f, kWave) : 0;
+            if (lane == 0) {
+                sh_fail[wv] = f;
+                sh_retry[wv] = rt;
+            }
+            __syncthreads();
+            int fw = -1;
+            for (int i = 0; i < W; ++i)
+                if (sh_fail[i] < kWave) {
+                    fw = i;
+                    break;
+                }
+            const int fl = fw >= 0 ? sh_fail[fw] : kWave;
+            const bool again = fw >= 0 && sh_retry[fw];
+            if (fw >= 0) fail = fw * kWave + fl;
+            __syncthreads();  // every wave has read the round's flags
+            if (!again) break;
+            // keys of two different prefixes collided: that lane looks
+            // further along its probe sequence for the block with the
+            // right parent, then the round is checked again
+            if (wv == fw && lane == fl)
+                cand = probe<BT>(ix, ik, (pos + 1) & ix.slot_mask, bk, true, prev, &pos, &cpar,
+                                 &probes, &cmps);
+        }
+        const int rel = wv * kWave + lane;
+        if (active) row[b] = rel < fail ? cand : -1;
+        if (TOUCH && active && rel < fail) {
+            const uint64_t fq = atomicAdd((unsigned long long*)&ix.freq[cand], 1ull) + 1ull;
+            atomicMax((unsigned long long*)&ix.prio[cand], (unsigned long long)(clock + fq));
+        }
+        if (fail < W * kWave) {
+            m = r0 + fail < n ? r0 + fail : n;
+            r0 += W * kWave;
+            break;
+        }
+        carry_key = sh_klast;
+        carry_id = sh_last[W - 1];
+        __syncthreads();  // sh_klast and sh_last read before the next round writes them
+    }
+    const int fill_from = r0 < n ? r0 : n;
+    for (int b = fill_from + (int)threadIdx.x; b < bat.max_blocks; b += W * kWave) row[b] = -1;
+    if (threadIdx.x == 0) m_out[r] = m;
+    if (ix.counters) {
+        CounterSlot* cs = counter_slot(ix.state);
+        wave_count(&cs->probes, probes, lane);
+        wave_count(&cs->token_compares, cmps, lane);
+    }
+}
+
 // Chained keys of every whole block of every request (no probing).
 template <int BT>
 __global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, uint64_t* __restrict__ keys) {
@@ -242,7 +361,38 @@ __global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, 
 
 }  // namespace
 
+namespace {
+template <int W>
+void launch_wide(const IndexView& ix, const Batch& b, int32_t* m, int32_t* ids, hipStream_t s) {
+    const dim3 grid((unsigned)b.R), block(W * kWave);
+    const bool touch = ix.freq != nullptr;
+    if (ix.block_tokens == 16) {
+        if (touch)
+            hipLaunchKernelGGL((k_lookup_wide<16, true, W>), grid, block, 0, s, ix, b, m, ids);
+        else
+            hipLaunchKernelGGL((k_lookup_wide<16, false, W>), grid, block, 0, s, ix, b, m, ids);
+    } else {
+        if (touch)
+            hipLaunchKernelGGL((k_lookup_wide<0, true, W>), grid, block, 0, s, ix, b, m, ids);
+        else
+            hipLaunchKernelGGL((k_lookup_wide<0, false, W>), grid, block, 0, s, ix, b, m, ids);
+    }
+}
+
+}  // namespace
+
 hipError_t launch_lookup(const IndexView& ix, const Batch& b, int32_t* m, int32_t* ids, hipStream_t s) {
+    // requests of more than one window: a workgroup per request, windows in
+    // parallel (4 waves up to 256 blocks, 8 up to 512, 16 beyond)
+    if (b.max_blocks > kWave) {
+        if (b.max_blocks <= 4 * kWave)
+            launch_wide<4>(ix, b, m, ids, s);
+        else if (b.max_blocks <= 8 * kWave)
+            launch_wide<8>(ix, b, m, ids, s);
+        else
+            launch_wide<16>(ix, b, m, ids, s);
+        return hipGetLastError();
+    }
     const unsigned grid = (unsigned)((b.R + kWavesPerGroup - 1) / kWavesPerGroup);
     const bool touch = ix.freq != nullptr;
     if (ix.block_tokens == 16) {

@@ -88,6 +88,31 @@ def test_weak_hash_gives_same_results():
     t.close()
 
 
+@pytest.mark.parametrize("maxb", [130, 300, 700])
+def test_weak_hash_long_requests(maxb):
+    """Key collisions in requests of several windows, looked up a workgroup
+    per request with windows in parallel (4, 8 and 16 waves). Three 4-token
+    blocks make up every request, so equal blocks under different parents
+    abound, and 8-bit index keys make them collide often: a lane that finds
+    the right tokens under another parent probes on, at any lane of a
+    window, and the result is the sequential one."""
+    rng = np.random.default_rng(maxb)
+    atoms = _atoms(rng, 3, 4, 3)
+    t = Twin(1, 1, 8, 4, 100_000, flags=P.PTSTORE_FLAG_WEAK_HASH | P.PTSTORE_FLAG_COUNTERS)
+    for _ in range(3):
+        toks, offs = random_block_batch(rng, 24, atoms, maxb + 20)
+        t.insert(toks, offs, maxb)
+        toks, offs = random_block_batch(rng, 24, atoms, maxb + 20)
+        t.lookup(toks, offs, maxb)
+    # lookups of stored sequences themselves: full matches through every window
+    toks, offs = random_block_batch(rng, 12, atoms, maxb, tail_p=0.0)
+    t.insert(toks, offs, maxb)
+    (m, ids), (rm, rids) = t.lookup(toks, offs, maxb)
+    assert (rm == np.diff(offs) // 4).all()
+    t.check_meta()
+    t.close()
+
+
 def test_hash_seed_does_not_change_results():
     rng = np.random.default_rng(6)
     atoms = _atoms(rng, 3, 16, 5)
