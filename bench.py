@@ -298,7 +298,8 @@ def run_passage(args, torch, P, synth, dev):
     store = make_store(P, shape, pool_blocks, flags=P.PTSTORE_FLAG_TIMING)
     # one paged cache shared by the sub-batches, allocated before the
     # prefill's temporary caches: allocated after them (right after their
-    # free) its gathers ran 13 % slower on hybrid8b (no change on llama8b)
+    # free) its gathers ran 13 % slower on hybrid8b, and on llama8b 9 %
+    # slower when another process had just freed a large allocation
     subs = w.sub_batches()
     maxb = w.max_blocks
     max_R = max(hi - lo for lo, hi in subs)
