@@ -5,7 +5,7 @@ in a dict and a list, not trie nodes.
 
 - ``lcp_blocks``: the longest common prefix, in whole blocks, of a request
   with every stored object, taken as a maximum over all of them (Section 4.1:
-  the LCP is sought "among all previously stored objects").
+  the LCP is taken over every object stored so far).
 - ``BruteStore.insert``: each distinct block-prefix is stored once (Section 1,
   redundancy-free growth) and gets the next id the first time it is seen in
   request order; a request inherits the ids of what is already stored and

@@ -10,8 +10,8 @@
  *
  *   - Stored objects are sequences of fixed-size token blocks. The store
  *     keeps each distinct block-prefix exactly once, as a node of a trie
- *     whose root is the empty prefix: prefixes "grow redundancy-free ...
- *     in divergent directions, similar to a trie" (Section 1).
+ *     whose root is the empty prefix: prefixes that branch apart share what
+ *     they have in common and nothing is stored twice (Section 1).
  *   - Every node has a dense unique id and a KV payload of block_bytes in
  *     a pool indexed by that id. An object's metadata is the flat list of
  *     the ids on its root path: it inherits the ids of its longest common
