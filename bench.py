@@ -755,8 +755,8 @@ def run_stream(args, torch, P, synth, dev):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU sharding of "
-                                   "the store is a design, not code (--gpus 1)"}))
+        print(json.dumps({"error": "the store runs on one GPU only; sharding it over several "
+                                   "GPUs is a design, not code (--gpus 1)"}))
         sys.exit(2)
     global COPY_SHAPE
     COPY_SHAPE = args.copy_shape

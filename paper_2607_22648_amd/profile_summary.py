@@ -122,7 +122,7 @@ def main():
         json.dump(rec, f, indent=1)
         f.write("\n")
 
-    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the GPU box):", "",
+    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the MI355X host):", "",
              "```", a.cmd.strip(), "```", "",
              "| kernel | calls | avg ms | % of GPU time |", "|---|---|---|---|"]
     for name, calls, avg, pct in stats[:12]:
@@ -139,7 +139,7 @@ def main():
     with open(os.path.join(a.out, f"{a.name}_kernel_trace.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
-    lines = [f"# HBM traffic: {a.name}", "", "Commands (repository root, GPU box):", "", "```",
+    lines = [f"# HBM traffic: {a.name}", "", "Commands (repository root, on the MI355X host):", "", "```",
              a.cmd.strip(), "```", "",
              "| quantity | value |", "|---|---|",
              f"| gather FETCH_SIZE per dispatch | {g_fetch:,.0f} KiB ({len(fetch[GATHER])} dispatches) |",
@@ -174,7 +174,7 @@ def store_counters(a):
             vals[short_name(r["Kernel_Name"])][c].append(float(r["Counter_Value"]))
     hit = "TCC_HIT_sum" in order and "TCC_MISS_sum" in order
     head = ["kernel", "dispatches"] + [f"{c} / dispatch" for c in order] + (["L2 hit rate"] if hit else [])
-    lines = [f"# Counters: {a.name}", "", "Commands (run from the repository root on the GPU box):",
+    lines = [f"# Counters: {a.name}", "", "Commands (run from the repository root on the MI355X host):",
              "", "```", a.cmd.strip(), "```", "",
              "Averages per dispatch over every dispatch of the runs (FETCH_SIZE in KiB, "
              "unscaled).", "",
@@ -207,7 +207,7 @@ def store_kernels_only(a):
     """Per-kernel table of every store kernel in a trace run, plus the
     per-round kernel times bench.py measured with HIP events in that run."""
     stats = kernel_stats(a.trace)
-    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the GPU box):", "",
+    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the MI355X host):", "",
              "```", a.cmd.strip(), "```", "",
              "| kernel | calls | avg us | % of GPU time |", "|---|---|---|---|"]
     for name, calls, avg, pct in stats:
