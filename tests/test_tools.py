@@ -1,0 +1,86 @@
+"""Host-side tools: bench.py's argument contract and the rocprofv3 summariser (no GPU)."""
+from __future__ import annotations
+
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert p.returncode == 2
+    line = json.loads(p.stdout.strip().splitlines()[-1])
+    assert "one GPU" in line["error"]
+
+
+def _write_trace(d, rows):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_kernel_stats.csv"), "w") as f:
+        f.write('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n')
+        for name, calls, avg, pct in rows:
+            f.write(f'"{name}",{calls},{calls * avg},{avg},{pct},{avg},{avg},0\n')
+
+
+def _write_pmc(d, rows):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_counter_collection.csv"), "w") as f:
+        f.write('"Kernel_Name","Counter_Name","Counter_Value"\n')
+        for k, c, v in rows:
+            f.write(f'"{k}","{c}",{v}\n')
+
+
+def test_profile_summary_traffic(tmp_path):
+    """Traffic = FETCH_SIZE and WRITE_SIZE scaled by what a plain copy of
+    known size reads for them, against the bench's algorithmic bytes."""
+    gather = "void ptsd::(anonymous namespace)::k_copy_pairs<true>(ptsd::(anonymous namespace)::CopyArgs)"
+    copy = "__amd_rocclr_copyBuffer"
+    tr, fe, wr = tmp_path / "trace", tmp_path / "fetch", tmp_path / "write"
+    _write_trace(str(tr), [(gather, 4, 10_000_000, 90.0), (copy, 2, 1_000_000, 5.0)])
+    gib = 1 << 30
+    # the plain 1 GiB copy reads FETCH_SIZE = half its KiB (factor 2) and
+    # WRITE_SIZE = its KiB (factor 1); the gather 3 GiB read, 3 GiB written
+    _write_pmc(str(fe), [(copy, "FETCH_SIZE", gib / 1024 / 2), (gather, "FETCH_SIZE", 3 * gib / 1024 / 2)])
+    _write_pmc(str(wr), [(copy, "WRITE_SIZE", gib / 1024), (gather, "WRITE_SIZE", 3 * gib / 1024)])
+    bench = tmp_path / "bench.json"
+    bench.write_text(json.dumps({"roofline": {"bytes_per_launch": 6 * gib, "avg_launch_ms": 10.0,
+                                              "launches": 4, "achieved": 644.2, "frac": 0.08},
+                                 "hbm_ceiling": {"bytes": gib},
+                                 "config": {"workload": "synthetic"}}) + "\n")
+    out = tmp_path / "profiles"
+    p = subprocess.run([sys.executable, "-m", "paper_2607_22648_amd.profile_summary",
+                        "--trace", str(tr), "--fetch", str(fe), "--write", str(wr),
+                        "--bench", str(bench), "--trace-bench", str(bench), "--out", str(out),
+                        "--name", "t", "--cmd", "cmd"], capture_output=True, text=True, cwd=ROOT,
+                       timeout=120)
+    assert p.returncode == 0, p.stderr
+    rec = json.loads((out / "t_traffic.json").read_text())
+    assert rec["fetch_factor"] == 2.0 and rec["write_factor"] == 1.0
+    assert rec["traffic_bytes_per_launch"] == 6 * gib
+    assert rec["traffic_over_algorithmic"] == 1.0
+    trace = (out / "t_kernel_trace.md").read_text()
+    assert "10.0000 ms" in trace and "cmd" in trace
+
+
+def test_profile_summary_counters(tmp_path):
+    """Per-kernel averages of any counters, and the L2 hit rate."""
+    k = "void ptsd::(anonymous namespace)::k_lookup<16, false>(ptsd::IndexView, ptsd::Batch, int*, int*)"
+    d = tmp_path / "pmc"
+    _write_pmc(str(d), [(k, "TCC_HIT_sum", 30), (k, "TCC_MISS_sum", 10),
+                        (k, "TCC_HIT_sum", 50), (k, "TCC_MISS_sum", 10),
+                        ("void at::native::other", "TCC_HIT_sum", 1)])
+    out = tmp_path / "profiles"
+    p = subprocess.run([sys.executable, "-m", "paper_2607_22648_amd.profile_summary", "--trace", "x",
+                        "--pmc", str(d), "--out", str(out), "--name", "c", "--cmd", "cmd"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert p.returncode == 0, p.stderr
+    text = (out / "c_counters.md").read_text()
+    row = [l for l in text.splitlines() if "k_lookup<16, false>" in l][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[1] == "2"                      # dispatches
+    assert cells[2] == "40.0" and cells[3] == "10.0"  # averages of HIT and MISS
+    assert cells[4] == "0.800"                  # 80 hits of 100
+    assert "at::native" not in text
