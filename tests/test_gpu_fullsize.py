@@ -183,6 +183,22 @@ def test_llama8b_full():
         expect = np.where(np.isin(w.req_passage[lo:hi], w.stored), w.passage_blocks, 0)
         np.testing.assert_array_equal(m_h, expect)
     assert seen > 0
+    # the per-layer load as bench.py --per-layer runs it: the block list once,
+    # then one prepared copy per layer; the same bytes as the fused gather
+    lo, hi = w.sub_batches()[0]
+    toks, offs = w.request_slice(lo, hi)
+    R = hi - lo
+    bt_h = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
+    m, ids = store.lookup(to_dev(toks), to_dev(offs), maxb)
+    cache.fill_(SENTINEL)
+    store.gather_prepare(ids, m, to_dev(bt_h), cache)
+    for l in range(kv.layers):
+        store.gather_prepared(cache, (l, l + 1))
+    rm, rids = ref.lookup(toks, offs, maxb)
+    m_h, ids_h = host(m), host(ids)
+    np.testing.assert_array_equal(m_h, rm)
+    np.testing.assert_array_equal(ids_h, rids)
+    assert check_gather(store, kv, cache, m_h, ids_h, bt_h, rec) > 0
     del cache
     _free(store, ref)
 
