@@ -4,7 +4,8 @@ A lookup + gather captured once replays bit-exact against the oracle, three
 times, with eager work of the program between the replays: inserts and
 scatters that grow the store (so each replay must see the store as it is
 then, not as it was at capture), sentinel fills of the outputs and
-synchronisations. The calls allocate nothing and wait for nothing once the
+synchronisations. An insert + scatter captured once stores, replay after
+replay, the new batch written into its captured buffers. The calls allocate nothing and wait for nothing once the
 store's scratch has grown to the batch size, which a first eager call does;
 later calls on the store must not need a larger copy scratch than the
 captured one (a larger batch regrows it).
@@ -20,7 +21,8 @@ from tests.helpers import random_block_batch, block_table_identity
 pytestmark = pytest.mark.gpu
 
 if torch.cuda.is_available():
-    from tests.twin import Twin, host, to_dev
+    from paper_2607_22648_amd import ptstore as P
+    from tests.twin import Twin, host, to_dev, random_bytes
 
 
 def _atoms(rng, n, bt, vocab):
@@ -80,4 +82,64 @@ def test_captured_lookup_gather_replays(chunks):
         # than the captured one, so the copy scratch stays where it was)
         _grow(t, rng, atoms, 8, maxb, seed=10 + rep)
     assert len(seen) > 1, "the replays should have seen the store grow"
+    t.close()
+
+
+def test_captured_insert_and_scatter_replays():
+    """An insert and a scatter captured once, replayed with new token contents
+    and new KV bytes written into the captured buffers between replays: each
+    replay stores exactly what the oracle stores for that batch (ids,
+    created flags, block metadata, pool bytes)."""
+    rng = np.random.default_rng(43)
+    bt_, R, maxb = 4, 8, 6
+    t = Twin(2, 1, 8, bt_, 5000)
+    atoms = _atoms(rng, 4, bt_, 300)
+
+    def batch():  # every request exactly maxb blocks: the offsets stay the same
+        return atoms[rng.integers(0, 4, size=(R, maxb))].reshape(-1).astype(np.int32)
+
+    offs = (np.arange(R + 1, dtype=np.int64) * maxb * bt_)
+    oo = to_dev(offs)
+    tt = to_dev(batch())
+    bt_np = block_table_identity(R, maxb)
+    bt = to_dev(bt_np)
+    n = R * maxb * t.shape.block_bytes
+    cache = torch.empty(n, dtype=torch.uint8, device="cuda")
+    m = torch.empty(R, dtype=torch.int32, device="cuda")
+    ids = torch.empty((R, maxb), dtype=torch.int32, device="cuda")
+    cr = torch.empty((R, maxb), dtype=torch.uint8, device="cuda")
+
+    def eager_twin_step(toks, seed):
+        cache.copy_(random_bytes(n, seed))
+        rc, rm, rids, rcr = t.ref.insert(toks, offs, maxb)
+        t.ref.scatter(rids, rcr, bt_np, host(cache), R * maxb)
+        return rm, rids, rcr
+
+    # warm-up: an eager insert + scatter of this size grows the scratch
+    toks0 = host(tt)
+    rm, rids, rcr = eager_twin_step(toks0, 100)
+    P.ptstore_insert(t.gpu.h, tt, oo, maxb, m, ids, cr)
+    P.ptstore_scatter(t.gpu.h, ids, cr, bt, cache, R * maxb)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(ids), rids)
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        P.ptstore_insert(t.gpu.h, tt, oo, maxb, m, ids, cr)
+        P.ptstore_scatter(t.gpu.h, ids, cr, bt, cache, R * maxb)
+    torch.cuda.synchronize()  # capture only records; nothing has run
+    created_total = 0
+    for rep in range(3):
+        toks = batch()
+        tt.copy_(to_dev(toks))
+        rm, rids, rcr = eager_twin_step(toks, 200 + rep)
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(m), rm, err_msg=f"replay {rep}: m")
+        np.testing.assert_array_equal(host(ids), rids, err_msg=f"replay {rep}: ids")
+        np.testing.assert_array_equal(host(cr), rcr, err_msg=f"replay {rep}: created")
+        created_total += int(rcr.sum())
+    assert created_total > 0
+    t.check_meta()
+    t.check_pool()
     t.close()
