@@ -178,18 +178,34 @@ __device__ inline uint64_t window_chain(uint64_t c, uint64_t carry, const HashTa
 
 __device__ inline unsigned long long ballot64(bool p) { return __ballot(p); }
 
+// Sum of a per-lane count over the wave, the same in every lane. Counts
+// are mostly 0, 1 or 2 (probes, comparisons, CAS attempts), so the sum is
+// first taken as the number of lanes whose count reaches k, for k = 1..4:
+// one ballot each and no lane shuffles. What larger counts hold beyond 4
+// goes through a shuffle tree, only when some lane has such a count.
+__device__ inline unsigned long long wave_sum(unsigned long long v, int lane) {
+    unsigned long long sum = 0;
+#pragma unroll
+    for (unsigned k = 1; k <= 4; ++k) sum += __popcll(ballot64(v >= k));
+    if (ballot64(v > 4)) {
+        unsigned long long x = v > 4 ? v - 4 : 0;
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) x += (unsigned long long)shfl_u64(x, lane ^ d);
+        sum += x;
+    }
+    return sum;
+}
+
 // Sum of a per-lane count over the wave, added once to a device counter.
 __device__ inline void wave_count(unsigned long long* ctr, unsigned long long v, int lane) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) v += (unsigned long long)shfl_u64(v, lane ^ d);
-    if (lane == 0 && v) atomicAdd(ctr, v);
+    const unsigned long long t = wave_sum(v, lane);
+    if (lane == 0 && t) atomicAdd(ctr, t);
 }
 
 // Sum of a per-lane count over the wave, taken once from a device counter.
 __device__ inline void wave_sub(unsigned long long* ctr, unsigned long long v, int lane) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) v += (unsigned long long)shfl_u64(v, lane ^ d);
-    if (lane == 0 && v) atomicSub(ctr, v);
+    const unsigned long long t = wave_sum(v, lane);
+    if (lane == 0 && t) atomicSub(ctr, t);
 }
 
 // The counter slot a wave adds to.

@@ -27,72 +27,164 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWavesPerGroup = kThreads / kWave;
 
-// A request's block of BT tokens (BT = 0: the block size is a run-time
-// value). Only a pointer is kept: the tokens are read for hashing and read
-// again, next to the stored row, when a candidate is compared, which keeps
-// the lookup's register count (and so its occupancy) down.
-template <int BT>
-struct BlockTokens {
-    const int32_t* p;
-    __device__ inline void load(const int32_t* __restrict__ q) { p = q; }
-    __device__ inline bool aligned() const { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
-    __device__ inline uint64_t hash(uint64_t seed, int) const {
-        if (aligned()) {
-            int32_t t[BT];
-#pragma unroll
-            for (int i = 0; i < BT; i += 4) {
-                int4 v = *reinterpret_cast<const int4*>(p + i);
-                t[i] = v.x; t[i + 1] = v.y; t[i + 2] = v.z; t[i + 3] = v.w;
-            }
-            return content_hash_regs<BT>(t, seed);
-        }
-        return content_hash_mem(p, BT, seed);
+// Makes a wave's LDS writes visible to its other lanes and keeps the
+// compiler from moving LDS accesses across this point. A wave's LDS
+// operations are performed in the order it issues them, so no other wave
+// takes part.
+__device__ inline void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// All four bits of each 4-bit group of b set -> one bit per group (16 bits).
+__device__ inline uint64_t quads_all(uint64_t b) {
+    uint64_t t = b & (b >> 1);
+    t = t & (t >> 2) & 0x1111111111111111ull;
+    t = (t | (t >> 3)) & 0x0303030303030303ull;
+    t = (t | (t >> 6)) & 0x000F000F000F000Full;
+    t = (t | (t >> 12)) & 0x000000FF000000FFull;
+    return (t | (t >> 24)) & 0xFFFFull;
+}
+
+constexpr int kQuads = 4;  // 16-byte pieces of a block of 16 tokens
+
+// A window of up to 64 blocks of 16 tokens of one request, staged in the
+// wave's own LDS area. The request is read with coalesced 16-byte loads
+// (consecutive lanes, consecutive bytes: a 4 KiB window costs 64 requests to
+// the L2 instead of 256 when each lane read its own block), and each lane
+// then hashes and compares its block from LDS. Stored rows are compared four
+// lanes to a row, so one load instruction reads 16 whole 64-byte rows.
+struct Window16 {
+    int4* sh;  // [kWave][kQuads], this wave's area
+    int lane;
+
+    // area: the workgroup's LDS, kWave * kQuads int4 per wave
+    __device__ inline void init(int4* area, int wave, int l) {
+        sh = area + wave * (kWave * kQuads);
+        lane = l;
     }
-    // stored rows are BT*4 = 64-byte aligned; compared 32 bytes at a time
+
+    __device__ inline void stage(const int32_t* __restrict__ seq, int w0, int n, int) {
+        wave_lds_sync();  // the previous window's reads are issued
+        const int nq = (n - w0 < kWave ? n - w0 : kWave) * kQuads;
+        const int32_t* base = seq + (int64_t)w0 * 16;
+        if ((reinterpret_cast<uintptr_t>(base) & 15) == 0) {
+#pragma unroll
+            for (int i = 0; i < kQuads; ++i) {
+                const int q = i * kWave + lane;
+                if (q < nq) sh[q] = *reinterpret_cast<const int4*>(base + 4 * q);
+            }
+        } else {
+            int32_t* d = reinterpret_cast<int32_t*>(sh);
+            for (int q = lane; q < 4 * nq; q += kWave) d[q] = base[q];
+        }
+        wave_lds_sync();
+    }
+    __device__ inline uint64_t hash(uint64_t seed, int) const {
+        int32_t t[16];
+#pragma unroll
+        for (int i = 0; i < kQuads; ++i) {
+            const int4 v = sh[lane * kQuads + i];
+            t[4 * i] = v.x; t[4 * i + 1] = v.y; t[4 * i + 2] = v.z; t[4 * i + 3] = v.w;
+        }
+        return content_hash_regs<16>(t, seed);
+    }
+    // This lane's block against one stored row (64-byte aligned). Only the
+    // rare paths (a key hit with other tokens, a key collision between
+    // prefixes) compare one lane at a time, so this takes one piece per step
+    // to keep the kernel's register count down.
     __device__ inline bool equals(const int32_t* __restrict__ s, int) const {
         bool eq = true;
-        const bool al = aligned();
 #pragma unroll 1
-        for (int i = 0; i < BT; i += 8) {
-            const int4 v0 = *reinterpret_cast<const int4*>(s + i);
-            const int4 v1 = *reinterpret_cast<const int4*>(s + i + 4);
-            int4 w0, w1;
-            if (al) {
-                w0 = *reinterpret_cast<const int4*>(p + i);
-                w1 = *reinterpret_cast<const int4*>(p + i + 4);
-            } else {
-                w0 = make_int4(p[i], p[i + 1], p[i + 2], p[i + 3]);
-                w1 = make_int4(p[i + 4], p[i + 5], p[i + 6], p[i + 7]);
-            }
-            eq &= (v0.x == w0.x) & (v0.y == w0.y) & (v0.z == w0.z) & (v0.w == w0.w) &
-                  (v1.x == w1.x) & (v1.y == w1.y) & (v1.z == w1.z) & (v1.w == w1.w);
+        for (int i = 0; i < kQuads; ++i) {
+            const int4 v = *reinterpret_cast<const int4*>(s + 4 * i);
+            const int4 w = sh[lane * kQuads + i];
+            eq &= (v.x == w.x) & (v.y == w.y) & (v.z == w.z) & (v.w == w.w);
         }
         return eq;
     }
+    // Token check of every lane's candidate (-1: none); called by the whole
+    // wave. Returns whether this lane's candidate row holds its tokens.
+    __device__ inline bool verify(const int32_t* __restrict__ tokens, int32_t cand, int) const {
+        uint64_t ok = 0;  // bit j: block j's candidate row holds block j's tokens
+#pragma unroll 1
+        for (int g = 0; g < kWave / 16; ++g) {
+            const int j = g * 16 + (lane >> 2);
+            const int32_t id = __shfl(cand, j, kWave);
+            bool eq = false;
+            if (id >= 0) {
+                const int4 v = *reinterpret_cast<const int4*>(tokens + (int64_t)id * 16 + 4 * (lane & 3));
+                const int4 w = sh[j * kQuads + (lane & 3)];
+                eq = (v.x == w.x) & (v.y == w.y) & (v.z == w.z) & (v.w == w.w);
+            }
+            ok |= quads_all(ballot64(eq)) << (16 * g);
+        }
+        return (ok >> lane) & 1;
+    }
 };
 
-template <>
-struct BlockTokens<0> {
-    const int32_t* p;
-    __device__ inline void load(const int32_t* __restrict__ q) { p = q; }
+// Any block size: each lane reads its own block from the request.
+struct WindowAny {
+    const int32_t* p;  // this lane's block (meaningful for lanes inside the request)
+    int lane;
+
+    __device__ inline void init(int4*, int, int l) { lane = l; }
+
+    __device__ inline void stage(const int32_t* __restrict__ seq, int w0, int, int bt) {
+        p = seq + (int64_t)(w0 + lane) * bt;
+    }
     __device__ inline uint64_t hash(uint64_t seed, int bt) const { return content_hash_mem(p, bt, seed); }
     __device__ inline bool equals(const int32_t* __restrict__ s, int bt) const {
         for (int i = 0; i < bt; ++i)
             if (s[i] != p[i]) return false;
         return true;
     }
+    __device__ inline bool verify(const int32_t* __restrict__ tokens, int32_t cand, int bt) const {
+        return cand >= 0 && equals(tokens + (int64_t)cand * bt, bt);
+    }
 };
 
-// Linear probing from `pos` for a slot holding `ikey` whose block has the
-// lane's tokens (and, if need_parent, parent id `want_parent`).
-// Returns the block id or -1 at the first empty slot; *pos_out is the slot
-// and *parent_out the block's parent id.
+// The window type for a compile-time block size (0: a run-time one).
 template <int BT>
-__device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos,
-                                const BlockTokens<BT>& bk, bool need_parent, int32_t want_parent,
-                                uint64_t* pos_out, int32_t* parent_out, unsigned long long* probes,
-                                unsigned long long* cmps) {
-    const int bt = BT ? BT : ix.block_tokens;
+struct WindowOf {
+    static_assert(BT == 0 || BT == 16, "block sizes: 16, or any at run time");
+    typedef WindowAny type;
+};
+template <>
+struct WindowOf<16> {
+    typedef Window16 type;
+};
+
+// First slot along the probe sequence from `pos` that holds `ikey`, its
+// tokens not yet compared; -1 at the first empty slot. *pos_out is the slot
+// and *parent_out the block's parent id.
+__device__ inline int32_t probe_key(const IndexView& ix, uint64_t ikey, uint64_t pos, uint64_t* pos_out,
+                                    int32_t* parent_out, unsigned* probes) {
+    while (true) {
+        const Slot s = ix.slots[pos];
+        ++*probes;
+        if (s.key == kEmptyKey) {
+            *pos_out = pos;
+            return -1;
+        }
+        if (s.key == ikey) {
+            *pos_out = pos;
+            *parent_out = s.parent;
+            return s.id;
+        }
+        pos = (pos + 1) & ix.slot_mask;
+    }
+}
+
+// Linear probing from `pos` for a slot holding `ikey` whose block has the
+// lane's tokens (and, if need_parent, parent id `want_parent`), comparing as
+// it goes. Returns the block id or -1 at the first empty slot.
+template <class Win>
+__device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos, const Win& win,
+                                bool need_parent, int32_t want_parent, uint64_t* pos_out,
+                                int32_t* parent_out, unsigned* probes, unsigned* cmps) {
+    const int bt = ix.block_tokens;
     while (true) {
         const Slot s = ix.slots[pos];
         ++*probes;
@@ -102,7 +194,7 @@ __device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos
         }
         if (s.key == ikey && (!need_parent || s.parent == want_parent)) {
             ++*cmps;
-            if (bk.equals(ix.tokens + (int64_t)s.id * bt, bt)) {
+            if (win.equals(ix.tokens + (int64_t)s.id * bt, bt)) {
                 *pos_out = pos;
                 *parent_out = s.parent;
                 return s.id;
@@ -110,6 +202,24 @@ __device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos
         }
         pos = (pos + 1) & ix.slot_mask;
     }
+}
+
+// Every lane's first block along its key's probe sequence that holds its
+// tokens (-1: none); called by the whole wave. All lanes find their first
+// key hit, the hits' tokens are compared together, and a lane whose hit
+// holds other tokens (a content-hash collision) probes on alone.
+template <class Win>
+__device__ inline int32_t find_block(const IndexView& ix, const Win& win, bool active, uint64_t ik,
+                                     uint64_t* pos, int32_t* par, unsigned* probes, unsigned* cmps) {
+    int32_t cand = -1;
+    if (active) {
+        cand = probe_key(ix, ik, slot_of(ik, ix.ht->slot_seed, ix.slot_mask), pos, par, probes);
+        if (cand >= 0) ++*cmps;
+    }
+    const bool same = win.verify(ix.tokens, cand, ix.block_tokens);
+    if (cand >= 0 && !same)
+        cand = probe(ix, ik, (*pos + 1) & ix.slot_mask, win, false, 0, pos, par, probes, cmps);
+    return cand;
 }
 
 // Request bounds; a malformed request is empty and counted.
@@ -140,30 +250,27 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
     const int32_t n = request_blocks(bat, r, bt, lane, ix.state, &o0);
     const int32_t* __restrict__ seq = bat.tokens + o0;
     int32_t* __restrict__ row = ids_out + r * bat.max_blocks;
+    __shared__ int4 sh_tok[BT == 16 ? kThreads * kQuads : 1];
+    typename WindowOf<BT>::type win;
+    win.init(sh_tok, threadIdx.x / kWave, lane);
 
     const uint64_t clock = TOUCH ? ix.state->clock : 0;
     uint64_t carry_key = ht->root_key;
     int32_t carry_id = -1;  // the root
     int32_t m = 0;
-    unsigned long long probes = 0, cmps = 0;
+    unsigned probes = 0, cmps = 0;
     int w0 = 0;
     bool done = false;
     for (; w0 < n && !done; w0 += kWave) {
         const int b = w0 + lane;
         const bool active = b < n;
-        BlockTokens<BT> bk;
-        uint64_t c = 0;
-        if (active) {
-            bk.load(seq + (int64_t)b * bt);
-            c = bk.hash(ht->content_seed, bt);
-        }
+        win.stage(seq, w0, n, bt);
+        const uint64_t c = active ? win.hash(ht->content_seed, bt) : 0;
         const uint64_t k = window_chain(c, carry_key, ht, lane);
         const uint64_t ik = index_key(k, *ht);
-        int32_t cand = -1, cpar = -2;
+        int32_t cpar = -2;
         uint64_t pos = 0;
-        if (active)
-            cand = probe<BT>(ix, ik, slot_of(ik, ht->slot_seed, ix.slot_mask), bk, false, 0, &pos,
-                             &cpar, &probes, &cmps);
+        int32_t cand = find_block(ix, win, active, ik, &pos, &cpar, &probes, &cmps);
         int first_bad = kWave;
         while (true) {
             int32_t prev = __shfl_up(cand, 1, kWave);
@@ -181,8 +288,8 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
             // keys of two different prefixes collided: lane f looks further
             // along its probe sequence for the block with the right parent
             if (lane == f)
-                cand = probe<BT>(ix, ik, (pos + 1) & ix.slot_mask, bk, true, prev, &pos, &cpar,
-                                 &probes, &cmps);
+                cand = probe(ix, ik, (pos + 1) & ix.slot_mask, win, true, prev, &pos, &cpar,
+                             &probes, &cmps);
         }
         if (active) row[b] = lane < first_bad ? cand : -1;
         if (TOUCH && active && lane < first_bad) {
@@ -239,20 +346,19 @@ __global__ __launch_bounds__(W * kWave) void k_lookup_wide(IndexView ix, Batch b
     int32_t* __restrict__ row = ids_out + r * bat.max_blocks;
     const uint64_t clock = TOUCH ? ix.state->clock : 0;
     const uint64_t p64 = ht->pow_lane[kWave - 1];  // P^64
+    __shared__ int4 sh_tok[BT == 16 ? W * kWave * kQuads : 1];
+    typename WindowOf<BT>::type win;
+    win.init(sh_tok, wv, lane);
     uint64_t carry_key = ht->root_key;
     int32_t carry_id = -1;  // the root
     int32_t m = n;
-    unsigned long long probes = 0, cmps = 0;
+    unsigned probes = 0, cmps = 0;
     int r0 = 0;  // first block of the round
     for (; r0 < n; r0 += W * kWave) {
         const int b = r0 + wv * kWave + lane;
         const bool active = b < n;
-        BlockTokens<BT> bk;
-        uint64_t c = 0;
-        if (active) {
-            bk.load(seq + (int64_t)b * bt);
-            c = bk.hash(ht->content_seed, bt);
-        }
+        win.stage(seq, r0 + wv * kWave, n, bt);
+        const uint64_t c = active ? win.hash(ht->content_seed, bt) : 0;
         const uint64_t sl = window_chain(c, 0, ht, lane);  // zero-carry chain
         if (lane == kWave - 1) sh_off[wv] = sl;
         __syncthreads();
@@ -260,11 +366,9 @@ __global__ __launch_bounds__(W * kWave) void k_lookup_wide(IndexView ix, Batch b
         for (int i = 0; i < wv; ++i) carry = addmod61(mulmod61(p64, carry), sh_off[i]);
         const uint64_t k = addmod61(mulmod61(ht->pow_lane[lane], carry), sl);
         const uint64_t ik = index_key(k, *ht);
-        int32_t cand = -1, cpar = -2;
+        int32_t cpar = -2;
         uint64_t pos = 0;
-        if (active)
-            cand = probe<BT>(ix, ik, slot_of(ik, ht->slot_seed, ix.slot_mask), bk, false, 0, &pos,
-                             &cpar, &probes, &cmps);
+        int32_t cand = find_block(ix, win, active, ik, &pos, &cpar, &probes, &cmps);
         if (wv == W - 1 && lane == kWave - 1) sh_klast = k;
         int fail = W * kWave;  // first failing position of the round, relative to r0
         while (true) {
@@ -297,8 +401,8 @@ __global__ __launch_bounds__(W * kWave) void k_lookup_wide(IndexView ix, Batch b
             // further along its probe sequence for the block with the
             // right parent, then the round is checked again
             if (wv == fw && lane == fl)
-                cand = probe<BT>(ix, ik, (pos + 1) & ix.slot_mask, bk, true, prev, &pos, &cpar,
-                                 &probes, &cmps);
+                cand = probe(ix, ik, (pos + 1) & ix.slot_mask, win, true, prev, &pos, &cpar,
+                             &probes, &cmps);
         }
         const int rel = wv * kWave + lane;
         if (active) row[b] = rel < fail ? cand : -1;
@@ -344,15 +448,14 @@ __global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, 
         n = (int32_t)(nb < bat.max_blocks ? nb : bat.max_blocks);
     }
     const int32_t* __restrict__ seq = bat.tokens + o0;
+    __shared__ int4 sh_tok[BT == 16 ? kThreads * kQuads : 1];
+    typename WindowOf<BT>::type win;
+    win.init(sh_tok, threadIdx.x / kWave, lane);
     uint64_t carry = ht->root_key;
     for (int w0 = 0; w0 < n; w0 += kWave) {
         const int b = w0 + lane;
-        uint64_t c = 0;
-        if (b < n) {
-            BlockTokens<BT> bk;
-            bk.load(seq + (int64_t)b * bt);
-            c = bk.hash(ht->content_seed, bt);
-        }
+        win.stage(seq, w0, n, bt);
+        const uint64_t c = b < n ? win.hash(ht->content_seed, bt) : 0;
         const uint64_t k = window_chain(c, carry, ht, lane);
         if (b < n) keys[r * bat.max_blocks + b] = k;
         carry = shfl_u64(k, kWave - 1);
