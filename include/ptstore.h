@@ -322,6 +322,15 @@ int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);
  * are state and stay. Waits for the device. Errors: INVALID (NULL), HIP. */
 int ptstore_reset_counters(ptstore_t *store);
 
+/* Turn the event counters (probes, token compares, CAS attempts and
+ * failures) on (on != 0) or off for the calls enqueued after this one;
+ * PTSTORE_FLAG_COUNTERS sets the state a store starts in. Counting costs
+ * about a tenth of a lookup's kernel time when the lookup is bound by
+ * probe latency, so a caller can measure with it off and count in a
+ * separate pass. Host only: no device work, no wait. Errors: INVALID (NULL
+ * store). */
+int ptstore_set_counters(ptstore_t *store, int on);
+
 /* Device buffers of the store (see ptstore_buffers_t); no device work.
  * Errors: INVALID (a NULL argument). */
 int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);

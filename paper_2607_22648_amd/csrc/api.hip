@@ -776,6 +776,15 @@ int ptstore_stats(ptstore_t* s, ptstore_stats_t* out) {
     return PTSTORE_OK;
 }
 
+int ptstore_set_counters(ptstore_t* s, int on) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_set_counters: null store");
+    if (on)
+        s->cfg.flags |= PTSTORE_FLAG_COUNTERS;
+    else
+        s->cfg.flags &= ~(uint32_t)PTSTORE_FLAG_COUNTERS;
+    return PTSTORE_OK;
+}
+
 int ptstore_reset_counters(ptstore_t* s) {
     if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_reset_counters: null store");
     DeviceScope dev(s);

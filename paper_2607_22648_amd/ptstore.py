@@ -59,7 +59,8 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_reset_counters", "ptstore_get_buffers", "ptstore_kernel_times",
            "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
            "ptstore_bandwidth_probe", "ptstore_replicate", "ptstore_gather_layers",
-           "ptstore_scatter_layers", "ptstore_gather_prepare", "ptstore_gather_prepared")
+           "ptstore_scatter_layers", "ptstore_gather_prepare", "ptstore_gather_prepared",
+           "ptstore_set_counters")
 
 
 def _load() -> C.CDLL:
@@ -78,6 +79,7 @@ def _load() -> C.CDLL:
         "ptstore_scatter": [p, p, p, p, i32, i32, p, i64, p],
         "ptstore_stats": [p, C.POINTER(ptstore_stats_t)],
         "ptstore_reset_counters": [p],
+        "ptstore_set_counters": [p, C.c_int],
         "ptstore_get_buffers": [p, C.POINTER(ptstore_buffers_t)],
         "ptstore_kernel_times": [p, i32, C.POINTER(d), C.POINTER(i64)],
         "ptstore_set_copy_shape": [p, i32, i32, i32],
@@ -279,6 +281,10 @@ def ptstore_reset_counters(h) -> None:
     _check("ptstore_reset_counters", _lib.ptstore_reset_counters(h))
 
 
+def ptstore_set_counters(h, on: bool) -> None:
+    _check("ptstore_set_counters", _lib.ptstore_set_counters(h, 1 if on else 0))
+
+
 def ptstore_get_buffers(h) -> ptstore_buffers_t:
     b = ptstore_buffers_t()
     _check("ptstore_get_buffers", _lib.ptstore_get_buffers(h, C.byref(b)))
@@ -431,6 +437,9 @@ class PrefixStore:
 
     def reset_counters(self):
         ptstore_reset_counters(self.h)
+
+    def set_counters(self, on: bool):
+        ptstore_set_counters(self.h, on)
 
     def kernel_times(self, kind: int) -> Tuple[float, int]:
         return ptstore_kernel_times(self.h, kind)

@@ -88,17 +88,21 @@ def test_weak_hash_gives_same_results():
     t.close()
 
 
+@pytest.mark.parametrize("bt", [4, 16])
 @pytest.mark.parametrize("maxb", [130, 300, 700])
-def test_weak_hash_long_requests(maxb):
+def test_weak_hash_long_requests(maxb, bt):
     """Key collisions in requests of several windows, looked up a workgroup
-    per request with windows in parallel (4, 8 and 16 waves). Three 4-token
+    per request with windows in parallel (4, 8 and 16 waves). Three distinct
     blocks make up every request, so equal blocks under different parents
-    abound, and 8-bit index keys make them collide often: a lane that finds
-    the right tokens under another parent probes on, at any lane of a
-    window, and the result is the sequential one."""
-    rng = np.random.default_rng(maxb)
-    atoms = _atoms(rng, 3, 4, 3)
-    t = Twin(1, 1, 8, 4, 100_000, flags=P.PTSTORE_FLAG_WEAK_HASH | P.PTSTORE_FLAG_COUNTERS)
+    abound, and 8-bit index keys make them collide often: a key hit may hold
+    other tokens, or the right tokens under another parent; either way the
+    lane probes on, at any lane of a window, and the result is the
+    sequential one. 16-token blocks take the kernels' LDS-staged path, with
+    stored rows compared four lanes to a row; 4-token blocks the generic
+    one."""
+    rng = np.random.default_rng(maxb + bt)
+    atoms = _atoms(rng, 3, bt, 3)
+    t = Twin(1, 1, 8, bt, 100_000, flags=P.PTSTORE_FLAG_WEAK_HASH | P.PTSTORE_FLAG_COUNTERS)
     for _ in range(3):
         toks, offs = random_block_batch(rng, 24, atoms, maxb + 20)
         t.insert(toks, offs, maxb)
@@ -108,9 +112,36 @@ def test_weak_hash_long_requests(maxb):
     toks, offs = random_block_batch(rng, 12, atoms, maxb, tail_p=0.0)
     t.insert(toks, offs, maxb)
     (m, ids), (rm, rids) = t.lookup(toks, offs, maxb)
-    assert (rm == np.diff(offs) // 4).all()
+    assert (rm == np.diff(offs) // bt).all()
     t.check_meta()
     t.close()
+
+
+def test_counters_switch_at_run_time():
+    """ptstore_set_counters turns counting on and off between calls; the
+    outputs do not change, and a lookup counts one probe or more per examined
+    block only while counting is on."""
+    rng = np.random.default_rng(8)
+    atoms = _atoms(rng, 3, 16, 5)
+    s = P.PrefixStore(P.StoreShape(1, 1, 8, 16), 5000)
+    toks, offs = random_block_batch(rng, 40, atoms, 90)
+    s.insert(to_dev(toks), to_dev(offs), 90)
+    lk = [to_dev(a) for a in random_block_batch(rng, 60, atoms, 100)]
+    outs, probes = [], []
+    for on in (False, True, False):
+        s.set_counters(on)
+        s.reset_counters()
+        m, ids = s.lookup(lk[0], lk[1], 100)
+        outs.append((host(m), host(ids)))
+        st = s.stats()
+        probes.append((st["probes"], st["token_compares"]))
+    s.close()
+    examined = int(np.minimum(np.diff(host(lk[1])) // 16, 100).sum())
+    assert probes[0] == (0, 0) and probes[2] == (0, 0)
+    assert probes[1][0] >= examined and probes[1][1] >= int(outs[1][0].sum())
+    for m, ids in outs[1:]:
+        np.testing.assert_array_equal(m, outs[0][0])
+        np.testing.assert_array_equal(ids, outs[0][1])
 
 
 def test_hash_seed_does_not_change_results():
