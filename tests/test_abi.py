@@ -31,6 +31,24 @@ def test_library_exports_every_declared_symbol():
     assert not missing, missing
 
 
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """Importing the binding from a copy of the package that has no built
+    library raises at import: there is no fallback path."""
+    import shutil
+    pkg = tmp_path / "paper_2607_22648_amd"
+    pkg.mkdir()
+    for f in ("__init__.py", "ptstore.py"):
+        shutil.copy(os.path.join(ROOT, "paper_2607_22648_amd", f), pkg / f)
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "try:\n    from paper_2607_22648_amd import ptstore\n"
+            "except ImportError as e:\n    print('ImportError', e)\n"
+            "else:\n    print('loaded')\n") % str(tmp_path)
+    out = subprocess.run(["python", "-c", code], capture_output=True, text=True, timeout=300,
+                         cwd=str(tmp_path))
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.startswith("ImportError") and "libptstore.so is missing" in out.stdout
+
+
 def test_binding_names_match_header():
     from paper_2607_22648_amd import ptstore as P
     assert sorted(P.EXPORTS) == declared_functions()
