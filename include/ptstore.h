@@ -48,7 +48,8 @@
  *    captured and replayed; a replay works on the store as it is then. A
  *    later call with a larger batch regrows the scratch, after which
  *    earlier captures must not be replayed. An evicting insert keeps a
- *    per-call value on the host and is not to be replayed.
+ *    per-call value on the host and is not to be replayed. A capture keeps
+ *    the counting state (ptstore_set_counters) it was made with.
  */
 #ifndef PTSTORE_H
 #define PTSTORE_H
