@@ -161,19 +161,46 @@ __device__ inline uint64_t shfl_up_u64(uint64_t v, int d) {
     return ((uint64_t)hi << 32) | lo;
 }
 
+// The constants of the key chain a lane uses, read from HashTables once per
+// kernel and then held in registers, so that no table read sits between a
+// window's tokens and its probes.
+struct ChainConsts {
+    uint64_t lane_pow;  // P^(lane+1)
+    uint64_t step[6];   // P^(2^t)
+    uint64_t root_key;
+    uint64_t content_seed;
+    uint64_t slot_seed;
+    uint32_t weak;
+};
+
+__device__ inline ChainConsts chain_consts(const HashTables* __restrict__ ht, int lane) {
+    ChainConsts c;
+    c.lane_pow = ht->pow_lane[lane];
+#pragma unroll
+    for (int t = 0; t < 6; ++t) c.step[t] = ht->pow_step[t];
+    c.root_key = ht->root_key;
+    c.content_seed = ht->content_seed;
+    c.slot_seed = ht->slot_seed;
+    c.weak = ht->weak;
+    return c;
+}
+
+__device__ inline uint64_t index_key(uint64_t k, const ChainConsts& c) {
+    return c.weak ? (k & 0xFFull) : k;
+}
+
 // Inclusive scan of the affine key chain over one 64-block window.
 // c: this lane's content hash (0 for lanes past the request's end);
 // carry: k_{w0-1}. Returns this lane's chained key k_{w0+lane}.
-__device__ inline uint64_t window_chain(uint64_t c, uint64_t carry, const HashTables* __restrict__ ht,
-                                        int lane) {
+__device__ inline uint64_t window_chain(uint64_t c, uint64_t carry, const ChainConsts& cc, int lane) {
     uint64_t s = c;
 #pragma unroll
     for (int t = 0; t < 6; ++t) {
         const int d = 1 << t;
         uint64_t sp = shfl_up_u64(s, d);
-        if (lane >= d) s = addmod61(s, mulmod61(ht->pow_step[t], sp));
+        if (lane >= d) s = addmod61(s, mulmod61(cc.step[t], sp));
     }
-    return addmod61(mulmod61(ht->pow_lane[lane], carry), s);
+    return addmod61(mulmod61(cc.lane_pow, carry), s);
 }
 
 __device__ inline unsigned long long ballot64(bool p) { return __ballot(p); }

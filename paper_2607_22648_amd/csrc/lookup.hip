@@ -210,10 +210,11 @@ __device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos
 // holds other tokens (a content-hash collision) probes on alone.
 template <class Win>
 __device__ inline int32_t find_block(const IndexView& ix, const Win& win, bool active, uint64_t ik,
-                                     uint64_t* pos, int32_t* par, unsigned* probes, unsigned* cmps) {
+                                     uint64_t slot_seed, uint64_t* pos, int32_t* par, unsigned* probes,
+                                     unsigned* cmps) {
     int32_t cand = -1;
     if (active) {
-        cand = probe_key(ix, ik, slot_of(ik, ix.ht->slot_seed, ix.slot_mask), pos, par, probes);
+        cand = probe_key(ix, ik, slot_of(ik, slot_seed, ix.slot_mask), pos, par, probes);
         if (cand >= 0) ++*cmps;
     }
     const bool same = win.verify(ix.tokens, cand, ix.block_tokens);
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
     const int64_t r = (int64_t)blockIdx.x * kWavesPerGroup + (threadIdx.x / kWave);
     if (r >= bat.R) return;  // uniform per wave
     const int bt = BT ? BT : ix.block_tokens;
-    const HashTables* __restrict__ ht = ix.ht;
+    const ChainConsts cc = chain_consts(ix.ht, lane);
     int64_t o0;
     const int32_t n = request_blocks(bat, r, bt, lane, ix.state, &o0);
     const int32_t* __restrict__ seq = bat.tokens + o0;
@@ -255,7 +256,7 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
     win.init(sh_tok, threadIdx.x / kWave, lane);
 
     const uint64_t clock = TOUCH ? ix.state->clock : 0;
-    uint64_t carry_key = ht->root_key;
+    uint64_t carry_key = cc.root_key;
     int32_t carry_id = -1;  // the root
     int32_t m = 0;
     unsigned probes = 0, cmps = 0;
@@ -265,12 +266,12 @@ __global__ __launch_bounds__(kThreads) void k_lookup(IndexView ix, Batch bat, in
         const int b = w0 + lane;
         const bool active = b < n;
         win.stage(seq, w0, n, bt);
-        const uint64_t c = active ? win.hash(ht->content_seed, bt) : 0;
-        const uint64_t k = window_chain(c, carry_key, ht, lane);
-        const uint64_t ik = index_key(k, *ht);
+        const uint64_t c = active ? win.hash(cc.content_seed, bt) : 0;
+        const uint64_t k = window_chain(c, carry_key, cc, lane);
+        const uint64_t ik = index_key(k, cc);
         int32_t cpar = -2;
         uint64_t pos = 0;
-        int32_t cand = find_block(ix, win, active, ik, &pos, &cpar, &probes, &cmps);
+        int32_t cand = find_block(ix, win, active, ik, cc.slot_seed, &pos, &cpar, &probes, &cmps);
         int first_bad = kWave;
         while (true) {
             int32_t prev = __shfl_up(cand, 1, kWave);
@@ -339,17 +340,17 @@ __global__ __launch_bounds__(W * kWave) void k_lookup_wide(IndexView ix, Batch b
     const int64_t r = blockIdx.x;
     if (r >= bat.R) return;  // uniform over the workgroup
     const int bt = BT ? BT : ix.block_tokens;
-    const HashTables* __restrict__ ht = ix.ht;
+    const ChainConsts cc = chain_consts(ix.ht, lane);
     int64_t o0;
     const int32_t n = request_blocks(bat, r, bt, wv == 0 ? lane : 1, ix.state, &o0);
     const int32_t* __restrict__ seq = bat.tokens + o0;
     int32_t* __restrict__ row = ids_out + r * bat.max_blocks;
     const uint64_t clock = TOUCH ? ix.state->clock : 0;
-    const uint64_t p64 = ht->pow_lane[kWave - 1];  // P^64
+    const uint64_t p64 = ix.ht->pow_lane[kWave - 1];  // P^64
     __shared__ int4 sh_tok[BT == 16 ? W * kWave * kQuads : 1];
     typename WindowOf<BT>::type win;
     win.init(sh_tok, wv, lane);
-    uint64_t carry_key = ht->root_key;
+    uint64_t carry_key = cc.root_key;
     int32_t carry_id = -1;  // the root
     int32_t m = n;
     unsigned probes = 0, cmps = 0;
@@ -358,17 +359,17 @@ __global__ __launch_bounds__(W * kWave) void k_lookup_wide(IndexView ix, Batch b
         const int b = r0 + wv * kWave + lane;
         const bool active = b < n;
         win.stage(seq, r0 + wv * kWave, n, bt);
-        const uint64_t c = active ? win.hash(ht->content_seed, bt) : 0;
-        const uint64_t sl = window_chain(c, 0, ht, lane);  // zero-carry chain
+        const uint64_t c = active ? win.hash(cc.content_seed, bt) : 0;
+        const uint64_t sl = window_chain(c, 0, cc, lane);  // zero-carry chain
         if (lane == kWave - 1) sh_off[wv] = sl;
         __syncthreads();
         uint64_t carry = carry_key;
         for (int i = 0; i < wv; ++i) carry = addmod61(mulmod61(p64, carry), sh_off[i]);
-        const uint64_t k = addmod61(mulmod61(ht->pow_lane[lane], carry), sl);
-        const uint64_t ik = index_key(k, *ht);
+        const uint64_t k = addmod61(mulmod61(cc.lane_pow, carry), sl);
+        const uint64_t ik = index_key(k, cc);
         int32_t cpar = -2;
         uint64_t pos = 0;
-        int32_t cand = find_block(ix, win, active, ik, &pos, &cpar, &probes, &cmps);
+        int32_t cand = find_block(ix, win, active, ik, cc.slot_seed, &pos, &cpar, &probes, &cmps);
         if (wv == W - 1 && lane == kWave - 1) sh_klast = k;
         int fail = W * kWave;  // first failing position of the round, relative to r0
         while (true) {
@@ -436,7 +437,7 @@ __global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, 
     const int64_t r = (int64_t)blockIdx.x * kWavesPerGroup + (threadIdx.x / kWave);
     if (r >= bat.R) return;
     const int bt = BT ? BT : ix.block_tokens;
-    const HashTables* __restrict__ ht = ix.ht;
+    const ChainConsts cc = chain_consts(ix.ht, lane);
     int64_t o0;
     // malformed requests were already counted by the lookup of the same batch
     int64_t a = bat.offsets[r], e = bat.offsets[r + 1];
@@ -451,12 +452,12 @@ __global__ __launch_bounds__(kThreads) void k_hash_all(IndexView ix, Batch bat, 
     __shared__ int4 sh_tok[BT == 16 ? kThreads * kQuads : 1];
     typename WindowOf<BT>::type win;
     win.init(sh_tok, threadIdx.x / kWave, lane);
-    uint64_t carry = ht->root_key;
+    uint64_t carry = cc.root_key;
     for (int w0 = 0; w0 < n; w0 += kWave) {
         const int b = w0 + lane;
         win.stage(seq, w0, n, bt);
-        const uint64_t c = b < n ? win.hash(ht->content_seed, bt) : 0;
-        const uint64_t k = window_chain(c, carry, ht, lane);
+        const uint64_t c = b < n ? win.hash(cc.content_seed, bt) : 0;
+        const uint64_t k = window_chain(c, carry, cc, lane);
         if (b < n) keys[r * bat.max_blocks + b] = k;
         carry = shfl_u64(k, kWave - 1);
     }
