@@ -14,7 +14,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ptstore_oracle.c")
-_LIB = os.path.join(_HERE, "libptstore_oracle.so")
+# PTSTORE_ORACLE_LIB names another build of the same source (the sanitized
+# build a CPU test runs the pins against); the default is built on demand.
+_LIB = os.environ.get("PTSTORE_ORACLE_LIB") or os.path.join(_HERE, "libptstore_oracle.so")
 # library OracleStore loads when no path is given (the mutation tests swap it)
 DEFAULT_LIB = _LIB
 
