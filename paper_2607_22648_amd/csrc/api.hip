@@ -5,7 +5,7 @@
 //           the home of ids below `owned`, then the replica slots
 //   host    [host rows][...] pinned host tier, the home of ids owned..
 //   parent  [capacity] int32, tokens [capacity][block_tokens] int32   block metadata
-//   slots   [index_slots] {key, id}                  open-addressing block index
+//   slots   [index_slots] {key, id, parent}          open-addressing block index
 //   ht      key-chain constants, state: counters and the block count
 //   evs     with eviction on: per-block access counts, priorities, child
 //           counts, depths, index keys and slots, and the victim-selection
