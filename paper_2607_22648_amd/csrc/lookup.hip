@@ -2,10 +2,13 @@
 // the longest prefix of a request that is stored, and the ids along it).
 //
 // One wavefront per request, lane j owns block w0+j of a 64-block window:
-//   1. each lane reads its block's tokens and hashes them;
+//   1. the wave copies the window's tokens into LDS with coalesced loads and
+//      each lane hashes its block from there;
 //   2. a wave prefix scan chains the hashes into per-block prefix keys;
-//   3. each lane probes the open-addressing index for its key and accepts the
-//      first slot whose stored block has the same tokens;
+//   3. each lane probes the open-addressing index for its key up to the
+//      first key hit; the hits' stored tokens are compared by four lanes per
+//      row, and a lane whose hit holds other tokens probes on, so it accepts
+//      the first slot whose stored block has the same tokens;
 //   4. the candidate of lane j must have as parent the id accepted by lane
 //      j-1 (the root, -1, for block 0; the slot carries the parent id, so this
 //      costs no extra load); a ballot finds the first lane that
