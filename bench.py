@@ -87,10 +87,7 @@ def prefill(store, w, dev, torch, batch_passages: int):
     nb = w.passage_blocks
     Rs = len(st_offs) - 1
     g = torch.Generator(device=dev)
-    t_ins = t_sc = 0.0
-    n_ins = n_sc = 0
     bytes_sc = 0
-    ids_all = []
     cache = None
     for lo in range(0, Rs, batch_passages):
         hi = min(Rs, lo + batch_passages)
@@ -105,7 +102,6 @@ def prefill(store, w, dev, torch, batch_passages: int):
         bt = torch.arange(R * nb, dtype=torch.int32, device=dev).view(R, nb)
         m, ids, created = store.insert(toks, offs, nb)
         store.scatter(ids, created, bt, cache)
-        ids_all.append(ids)
         bytes_sc += int(created.sum().item()) * 2 * sh.block_bytes
     torch.cuda.synchronize()
     t_ins, n_ins = store.kernel_times(P.KIND_INSERT)
@@ -694,12 +690,11 @@ def run_stream(args, torch, P, synth, dev):
                torch.from_numpy(r.insert_tokens).to(dev), torch.from_numpy(r.insert_offsets).to(dev))
               for r in sw.rounds]
     n_timed = min(args.steps, len(rounds) - args.warmup)
-    stats = {"matched": 0, "created": 0}
 
     def one_round(i, count):
         lt, lo, it, io = rounds[i]
         store.lookup_gather(lt, lo, maxb, bt, cache, m=m, ids=ids)
-        im, iids, icr = store.insert(it, io, maxb)
+        _, iids, icr = store.insert(it, io, maxb)
         store.scatter(iids, icr, bt[:io.numel() - 1], cache)
         if count:
             return m, icr

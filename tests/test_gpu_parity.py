@@ -12,7 +12,6 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import OracleStore
 from workloads import synth
 from tests.helpers import load_golden, spell_batch, random_block_batch, block_table_identity
 
@@ -20,7 +19,7 @@ pytestmark = pytest.mark.gpu
 
 if torch.cuda.is_available():
     from paper_2607_22648_amd import ptstore as P
-    from tests.twin import Twin, to_dev, host, random_bytes, DEV
+    from tests.twin import Twin, to_dev, host, DEV
 
 
 def _atoms(rng, n, bt, vocab, shared_head=False):

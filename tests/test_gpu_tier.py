@@ -19,7 +19,7 @@ pytestmark = pytest.mark.gpu
 
 if torch.cuda.is_available():
     from paper_2607_22648_amd import ptstore as P
-    from tests.twin import Twin, host, to_dev, random_bytes
+    from tests.twin import Twin
 
     EVICT = P.PTSTORE_FLAG_EVICT
 

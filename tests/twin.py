@@ -7,7 +7,7 @@ the bar is bit-exact).
 """
 from __future__ import annotations
 
-from typing import Optional, Tuple
+from typing import Optional
 
 import numpy as np
 import torch

@@ -12,7 +12,7 @@ All arrays are numpy. Token sequences of a batch are packed as CSR:
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
