@@ -94,7 +94,13 @@ enum {
      * never-used ids first, then the freed ids from the smallest up; blocks
      * still without an id are refused as without this flag. Costs 44 bytes
      * of device memory per pool block. */
-    PTSTORE_FLAG_EVICT = 8u
+    PTSTORE_FLAG_EVICT = 8u,
+    /* Name a new block in an insert's batch table by its key and only the
+     * parity of its depth, so that blocks of one request at different
+     * depths share entries: used to test that such sharing is detected and
+     * the insert takes its exact path, with the same results. Slow; for
+     * tests only. */
+    PTSTORE_FLAG_WEAK_TAGS = 16u
 };
 
 typedef struct {

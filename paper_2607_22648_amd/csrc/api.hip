@@ -95,7 +95,7 @@ uint64_t host_mulmod61(uint64_t a, uint64_t b) {
     return mod61(lo + hi);
 }
 
-void make_hash_tables(uint64_t seed, bool weak, HashTables* h) {
+void make_hash_tables(uint64_t seed, bool weak, bool weak_tag, HashTables* h) {
     memset(h, 0, sizeof *h);
     const uint64_t P = mod61(mix64(seed ^ 0x2545F4914F6CDD1Dull)) % (kM61 - 2) + 2;
     uint64_t x = P;
@@ -112,6 +112,7 @@ void make_hash_tables(uint64_t seed, bool weak, HashTables* h) {
     h->content_seed = mix64(seed ^ 0xD6E8FEB86659FD93ull);
     h->slot_seed = mix64(seed ^ 0xA0761D6478BD642Full);
     h->weak = weak ? 1u : 0u;
+    h->weak_tag = weak_tag ? 1u : 0u;
 }
 
 IndexView index_view(ptstore_t* s) {
@@ -482,7 +483,8 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     }
     s->evs.tier = s->tier;
     HashTables h;
-    make_hash_tables(c.hash_seed, (c.flags & PTSTORE_FLAG_WEAK_HASH) != 0, &h);
+    make_hash_tables(c.hash_seed, (c.flags & PTSTORE_FLAG_WEAK_HASH) != 0,
+                     (c.flags & PTSTORE_FLAG_WEAK_TAGS) != 0, &h);
     DevState st;
     memset(&st, 0, sizeof st);
     if ((e = hipMemcpy(s->ht, &h, sizeof h, hipMemcpyHostToDevice)) != hipSuccess ||

@@ -36,7 +36,7 @@ struct HashTables {
     uint64_t content_seed;
     uint64_t slot_seed;
     uint32_t weak;             // 1: index keys masked to 8 bits
-    uint32_t pad;
+    uint32_t weak_tag;         // 1: insert batch-table tags keep only the depth's parity
 };
 
 // Event counters a lookup adds to are spread over this many slots, each on

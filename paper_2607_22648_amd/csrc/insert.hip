@@ -13,13 +13,17 @@
 //              of the whole prefix up to b)
 //   claim      wave per request, lane per missing block b >= m0: the block
 //              claims or joins the batch-table entry named by (key, depth)
-//              and records in it the smallest request that needs it
-//   verify     wave per request, lane per block: the entry's smallest request
-//              o must hold the same prefix. It does if block b's tokens are
+//              and records in it the smallest request that needs it; the
+//              block that claims an entry also records its depth there
+//   verify     wave per request, lane per block: the entry must hold the
+//              block's depth (else blocks of two depths, possibly of one
+//              request, share it), and the entry's smallest request o must
+//              hold the same prefix. It does if block b's tokens are
 //              equal and either b is both requests' first missing block under
 //              the same stored parent, or both requests' blocks b-1 sit in
 //              the same entry (by induction, equal prefixes). Any failure --
-//              a key collision between different prefixes -- raises a flag.
+//              a collision of names between different prefixes -- raises a
+//              flag.
 //   exact      only when the flag is up: the table is cleared and rebuilt one
 //              block after another per request, each block named exactly by
 //              (entry of its parent, its tokens); slower, same result
@@ -46,7 +50,8 @@ namespace ptsd {
 struct alignas(16) BatchEntry {
     unsigned long long word;  // claim: tag of (key, depth); exact: (parent label << 32) | token position
     int32_t owner;            // smallest request that needs this block
-    int32_t node_id;          // id assigned, -1 if refused
+    int32_t node_id;          // claim to verify: depth of the claiming block (exact path: -1);
+                              // from assign on: id assigned, -1 if refused
 };
 
 namespace {
@@ -93,10 +98,12 @@ __device__ inline int32_t n_blocks(const Batch& bat, int64_t r, int bt, int64_t*
     return (int32_t)(n < bat.max_blocks ? n : bat.max_blocks);
 }
 
-// Name of a new block in the batch table: its chained key and its depth.
-// The top bit is clear, so a tag never equals the empty marker.
+// Name of a new block in the batch table: its chained key and its depth
+// (only the depth's parity with the weak test tags). The top bit is clear,
+// so a tag never equals the empty marker.
 __device__ inline unsigned long long tag_of(uint64_t key, int32_t b, const HashTables& ht) {
-    return mix64(index_key(key, ht) ^ (0x9E3779B97F4A7C15ull * (uint64_t)(b + 1)) ^ ~ht.slot_seed) &
+    const uint64_t d = ht.weak_tag ? (uint64_t)(b & 1) : (uint64_t)b;
+    return mix64(index_key(key, ht) ^ (0x9E3779B97F4A7C15ull * (d + 1)) ^ ~ht.slot_seed) &
            0x7FFFFFFFFFFFFFFFull;
 }
 
@@ -137,7 +144,11 @@ __global__ __launch_bounds__(kThreads) void k_claim(InsertArgs a) {
         while (true) {
             const unsigned long long prev = atomicCAS(&tab[pos].word, kEmptyKey, tag);
             ++cas;
-            if (prev == kEmptyKey || prev == tag) break;
+            if (prev == kEmptyKey) {
+                tab[pos].node_id = b;  // read by verify, kernels later
+                break;
+            }
+            if (prev == tag) break;
             ++fails;
             pos = (pos + 1) & a.sc.table_mask;
         }
@@ -161,7 +172,12 @@ __global__ __launch_bounds__(kThreads) void k_verify(InsertArgs a) {
     for (int32_t w0 = m0; w0 < n; w0 += kWave) {
         const int32_t b = w0 + lane;
         if (b >= n) continue;
-        const int64_t o = tab[a.sc.label[r * maxb + b]].owner;
+        const BatchEntry te = tab[a.sc.label[r * maxb + b]];
+        if (te.node_id != b) {  // the entry was claimed at another depth
+            ok = false;
+            continue;
+        }
+        const int64_t o = te.owner;
         if (o == r) continue;
         int64_t oo0;
         const int32_t on = n_blocks(a.bat, o, bt, &oo0);

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libptstore.so")
 PTSTORE_OK, PTSTORE_ERR_INVALID, PTSTORE_ERR_FULL, PTSTORE_ERR_HIP, PTSTORE_ERR_NOMEM = 0, 1, 2, 3, 4
 PTSTORE_FLAG_WEAK_HASH, PTSTORE_FLAG_COUNTERS, PTSTORE_FLAG_TIMING = 1, 2, 4
 PTSTORE_FLAG_EVICT = 8
+PTSTORE_FLAG_WEAK_TAGS = 16
 KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT, KIND_SELECT, KIND_EVICT = 0, 1, 2, 3, 4, 5
 KIND_REPLICATE = 6
 

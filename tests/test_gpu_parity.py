@@ -87,6 +87,44 @@ def test_weak_hash_gives_same_results():
     t.close()
 
 
+@pytest.mark.parametrize("weak_hash", [False, True])
+def test_one_request_blocks_sharing_a_batch_entry(weak_hash):
+    """An insert names each new block in its batch table by chained key and
+    depth. The weak test tags keep only the depth's parity; with 8-bit index
+    keys on top, blocks of a single request at different depths then share
+    entries. The claim records each entry's depth, verification finds the
+    sharing and the insert takes its exact path, with the sequential
+    results. One request per call, so no other request can be what raises
+    the flag. With full keys the weak tags alone share nothing: the parallel
+    claim holds."""
+    rng = np.random.default_rng(23)
+    flags = P.PTSTORE_FLAG_WEAK_TAGS | (P.PTSTORE_FLAG_WEAK_HASH if weak_hash else 0)
+    t = Twin(1, 1, 8, 16, 5000, flags=flags)
+    seqs = []
+    for i in range(8):
+        if i % 2 == 0 or not seqs:  # fresh tokens: 48 new blocks
+            s = rng.integers(0, 32000, size=48 * 16, dtype=np.int32)
+        else:  # an earlier sequence cut at a block boundary, then new blocks
+            base = seqs[int(rng.integers(0, len(seqs)))]
+            cut = int(rng.integers(1, 40)) * 16
+            s = np.concatenate([base[:cut], rng.integers(0, 32000, size=24 * 16, dtype=np.int32)])
+        seqs.append(s)
+        offs = np.array([0, s.size], dtype=np.int64)
+        t.insert(s, offs, 64)
+        t.lookup(s, offs, 64)
+    toks = np.concatenate(seqs)
+    offs = np.concatenate([[0], np.cumsum([x.size for x in seqs])]).astype(np.int64)
+    (m, _), (rm, _) = t.lookup(toks, offs, 64)
+    assert (rm == offs[1:] // 16 - offs[:-1] // 16).all()  # every sequence stored whole
+    t.check_meta()
+    fb = t.gpu.stats()["insert_fallbacks"]
+    if weak_hash:
+        assert fb >= 1  # single-request inserts shared entries across depths
+    else:
+        assert fb == 0
+    t.close()
+
+
 @pytest.mark.parametrize("bt", [4, 16])
 @pytest.mark.parametrize("maxb", [130, 300, 700])
 def test_weak_hash_long_requests(maxb, bt):
