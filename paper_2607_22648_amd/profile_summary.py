@@ -7,6 +7,11 @@ Inputs (directories written by rocprofv3 ``--output-format csv``):
   --fetch DIR   a ``--pmc FETCH_SIZE`` run (uses *_counter_collection.csv)
   --write DIR   a ``--pmc WRITE_SIZE`` run
   --bench FILE  the JSON line bench.py printed in the counter runs
+  --window NAME:FIRST:COUNT  (repeatable, with --trace alone) the average
+                duration of dispatches FIRST .. FIRST+COUNT-1, in start order,
+                of the kernel whose name contains NAME (*_kernel_trace.csv):
+                the launches a bench phase timed, apart from other launches
+                of the same kernel in the run
   --pmc DIR     (repeatable, instead of --fetch/--write) any ``--pmc`` runs:
                 the average per dispatch of every counter collected, for
                 every store kernel, plus the L2 hit rate where TCC_HIT and
@@ -54,6 +59,20 @@ def kernel_stats(trace_dir: str):
             for r in rows]
 
 
+def dispatch_window(trace_dir: str, spec: str):
+    """(name, first, count, average ms) over a slice of one kernel's dispatches."""
+    name, first, count = spec.rsplit(":", 2)
+    first, count = int(first), int(count)
+    rows = [r for r in csv.DictReader(open(_one(os.path.join(trace_dir, "*kernel_trace.csv"))))
+            if name in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    sel = rows[first:first + count]
+    if len(sel) != count:
+        raise ValueError(f"{spec}: the trace holds {len(rows)} dispatches of {name}")
+    ms = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6 for r in sel]
+    return name, first, count, sum(ms) / count
+
+
 def counter_per_dispatch(pmc_dir: str, counter: str):
     """{kernel short name: [value per dispatch]} for the gather, scatter and plain copy."""
     out = defaultdict(list)
@@ -84,6 +103,8 @@ def main():
     ap.add_argument("--name", default="gather_llama8b")
     ap.add_argument("--cmd", required=True, help="the command that produced the inputs")
     ap.add_argument("--pmc", action="append", default=[], help="a --pmc run directory")
+    ap.add_argument("--window", action="append", default=[],
+                    help="NAME:FIRST:COUNT, the average over a slice of one kernel's dispatches")
     a = ap.parse_args()
     if a.pmc:
         return store_counters(a)
@@ -224,6 +245,18 @@ def store_kernels_only(a):
         if "evictions" in tb:
             lines.append(f"- evictions in the warm-up and timed steps: {tb['evictions']}; "
                          f"index rebuilds in the timed steps: {tb['index_rebuilds']}")
+        if "lookup_only" in tb:
+            lo = tb["lookup_only"]
+            lines.append(f"- lookup only (counters off): {lo['kernel_avg_ms']} ms per call, "
+                         f"{lo['lookups_per_s_kernel']:,.0f} lookups/s at the kernel")
+        if "roofline" in tb and not tb.get("kernel_ms_per_round"):
+            rf = tb["roofline"]
+            lines.append(f"- gather: {rf['avg_launch_ms']} ms per launch over {rf['launches']} "
+                         f"timed launches ({rf['achieved']} GB/s)")
+    for spec in a.window:
+        name, first, count, avg = dispatch_window(a.trace, spec)
+        lines += ["", f"`{name}` dispatches {first}-{first + count - 1} (start order) in the trace: "
+                  f"**{avg:.4f} ms** average."]
     os.makedirs(a.out, exist_ok=True)
     with open(os.path.join(a.out, f"{a.name}_kernel_trace.md"), "w") as f:
         f.write("\n".join(lines) + "\n")

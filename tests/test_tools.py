@@ -84,3 +84,31 @@ def test_profile_summary_counters(tmp_path):
     assert cells[2] == "40.0" and cells[3] == "10.0"  # averages of HIT and MISS
     assert cells[4] == "0.800"                  # 80 hits of 100
     assert "at::native" not in text
+
+
+def test_profile_summary_dispatch_window(tmp_path):
+    """--window averages one slice of a kernel's dispatches, in start order,
+    from the per-dispatch trace; the other kernels and dispatches stay out."""
+    look = "void ptsd::(anonymous namespace)::k_lookup<16, false>(ptsd::IndexView, ptsd::Batch, int*, int*)"
+    other = "void ptsd::(anonymous namespace)::k_publish(ptsd::(anonymous namespace)::InsertArgs)"
+    tr = tmp_path / "trace"
+    _write_trace(str(tr), [(look, 6, 30_000, 80.0), (other, 2, 5_000, 20.0)])
+    # dispatches in shuffled file order: start times 0..5 ms, durations 100, 10, 20, 30, 40, 100 us
+    rows = [(look, 5, 100), (other, 1, 7), (look, 0, 100), (look, 3, 30), (look, 1, 10), (look, 4, 40),
+            (look, 2, 20), (other, 2, 9)]
+    with open(tr / "run_kernel_trace.csv", "w") as f:
+        f.write('"Kernel_Name","Start_Timestamp","End_Timestamp"\n')
+        for k, start_ms, dur_us in rows:
+            s0 = start_ms * 1_000_000 + (500_000 if k == other else 0)
+            f.write(f'"{k}",{s0},{s0 + dur_us * 1000}\n')
+    out = tmp_path / "profiles"
+    p = subprocess.run([sys.executable, "-m", "paper_2607_22648_amd.profile_summary", "--trace", str(tr),
+                        "--window", "k_lookup<16, false>:1:4", "--out", str(out), "--name", "w",
+                        "--cmd", "cmd"], capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert p.returncode == 0, p.stderr
+    text = (out / "w_kernel_trace.md").read_text()
+    assert "dispatches 1-4" in text and "**0.0250 ms** average" in text  # (10+20+30+40)/4 us
+    p = subprocess.run([sys.executable, "-m", "paper_2607_22648_amd.profile_summary", "--trace", str(tr),
+                        "--window", "k_lookup<16, false>:3:4", "--out", str(out), "--name", "w",
+                        "--cmd", "cmd"], capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert p.returncode != 0 and "holds 6 dispatches" in p.stderr  # a slice past the end is refused
