@@ -591,17 +591,31 @@ def run_trie(args, torch, P, synth, dev):
     cache = torch.full((sh.layers * 2 * R * w.depth * sh.chunk_bytes,), 0xA5, dtype=torch.uint8,
                        device=dev)
     # lookup only (the probe-bound headline of this workload), timed with the
-    # event counters off; one more lookup with them on counts its probes
+    # event counters off. First back to back, with the library's per-launch
+    # events off too and one event pair around all K calls on the stream
+    # they run on (two events around every launch add microseconds to a
+    # 25-microsecond kernel); then K more, each bracketed by the library's
+    # own events. One more lookup with the counters on counts its probes.
     store.set_counters(False)
+    store.set_timing(False)
     for _ in range(args.warmup):
         store.lookup(toks, offs, w.depth, m=m, ids=ids)
     torch.cuda.synchronize()
     store.kernel_times(P.KIND_LOOKUP)
+    cur = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    ev0.record(cur)
+    for _ in range(args.steps):
+        store.lookup(toks, offs, w.depth, m=m, ids=ids)
+    ev1.record(cur)
+    torch.cuda.synchronize()
+    lk_elapsed = time.perf_counter() - t0
+    lk_stream = ev0.elapsed_time(ev1) / args.steps
+    store.set_timing(True)
     for _ in range(args.steps):
         store.lookup(toks, offs, w.depth, m=m, ids=ids)
     torch.cuda.synchronize()
-    lk_elapsed = time.perf_counter() - t0
     lk_ms, lk_n = store.kernel_times(P.KIND_LOOKUP)
     store.set_counters(True)
     store.reset_counters()
@@ -648,8 +662,13 @@ def run_trie(args, torch, P, synth, dev):
         "stored_blocks": int(stt["blocks_stored"]), "block_bytes": sh.block_bytes})
     out.update({
         "lookup_only": {"lookups_per_s": round(R * args.steps / lk_elapsed, 1),
+                        "stream_ms_per_call": round(lk_stream, 4),
+                        "lookups_per_s_stream": round(R / (lk_stream / 1e3), 1),
                         "kernel_avg_ms": round(lk_avg, 4),
                         "lookups_per_s_kernel": round(R / (lk_avg / 1e3), 1),
+                        "timing": "lookups_per_s (wall) and *_stream: K calls back to back, the "
+                                  "library's per-launch events off, one event pair around them; "
+                                  "kernel_*: K more calls, each between the library's own events",
                         "counters": "off in the timed lookups; probes and compares from one "
                                     "more lookup with them on",
                         "probes_per_call": int(probes), "token_compares_per_call": int(compares),

@@ -338,6 +338,15 @@ int ptstore_reset_counters(ptstore_t *store);
  * store). */
 int ptstore_set_counters(ptstore_t *store, int on);
 
+/* Turn the HIP events around kernels (what ptstore_kernel_times() reports)
+ * on (on != 0) or off for the calls enqueued after this one; pairs already
+ * recorded stay until read. PTSTORE_FLAG_TIMING sets the state a store
+ * starts in. Two events around each launch add a few microseconds to a
+ * short call, so a caller can time back-to-back short calls with them off
+ * and one event pair of its own around all of them. Host only: no device
+ * work, no wait. Errors: INVALID (NULL store). */
+int ptstore_set_timing(ptstore_t *store, int on);
+
 /* Device buffers of the store (see ptstore_buffers_t); no device work.
  * Errors: INVALID (a NULL argument). */
 int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);

@@ -787,6 +787,15 @@ int ptstore_set_counters(ptstore_t* s, int on) {
     return PTSTORE_OK;
 }
 
+int ptstore_set_timing(ptstore_t* s, int on) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_set_timing: null store");
+    if (on)
+        s->cfg.flags |= PTSTORE_FLAG_TIMING;
+    else
+        s->cfg.flags &= ~(uint32_t)PTSTORE_FLAG_TIMING;
+    return PTSTORE_OK;
+}
+
 int ptstore_reset_counters(ptstore_t* s) {
     if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_reset_counters: null store");
     DeviceScope dev(s);

@@ -181,6 +181,32 @@ def test_counters_switch_at_run_time():
         np.testing.assert_array_equal(ids, outs[0][1])
 
 
+def test_timing_switch_at_run_time():
+    """ptstore_set_timing turns the per-kernel events on and off between
+    calls: only the calls made while it is on are reported, pairs recorded
+    before a switch-off stay until read, and the outputs do not change."""
+    rng = np.random.default_rng(9)
+    atoms = _atoms(rng, 3, 16, 5)
+    s = P.PrefixStore(P.StoreShape(1, 1, 8, 16), 5000)  # starts with timing off
+    toks, offs = random_block_batch(rng, 40, atoms, 90)
+    s.insert(to_dev(toks), to_dev(offs), 90)
+    lk = [to_dev(a) for a in random_block_batch(rng, 60, atoms, 100)]
+    ref = [host(a) for a in s.lookup(lk[0], lk[1], 100)]
+    assert s.kernel_times(P.KIND_LOOKUP)[1] == 0
+    s.set_timing(True)
+    for _ in range(3):
+        s.lookup(lk[0], lk[1], 100)
+    s.set_timing(False)
+    for _ in range(2):
+        m, ids = s.lookup(lk[0], lk[1], 100)
+    ms, n = s.kernel_times(P.KIND_LOOKUP)
+    assert n == 3 and ms > 0
+    assert s.kernel_times(P.KIND_LOOKUP)[1] == 0  # read once
+    np.testing.assert_array_equal(host(m), ref[0])
+    np.testing.assert_array_equal(host(ids), ref[1])
+    s.close()
+
+
 def test_hash_seed_does_not_change_results():
     rng = np.random.default_rng(6)
     atoms = _atoms(rng, 3, 16, 5)
