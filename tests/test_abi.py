@@ -156,3 +156,17 @@ def test_binding_checks_array_sizes_without_gpu():
         P.ptstore_lookup_gather(None, toks, offs, 4, m, ids, ids.view(-1)[:2], None, 0)
     with pytest.raises(ValueError, match="offsets"):
         P.ptstore_lookup(None, toks, offs[:0], 4, m, ids)
+
+
+def test_binding_constants_match_header():
+    """Every PTSTORE_* enum constant of the header (error codes, flags) has
+    the same value in the binding, and the binding defines none the header
+    lacks."""
+    from paper_2607_22648_amd import ptstore as P
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    header = {n: int(v) for n, v in re.findall(r"\b(PTSTORE_[A-Z_]+)\s*=\s*(\d+)u?\b", text)}
+    assert "PTSTORE_FLAG_WEAK_TAGS" in header and "PTSTORE_ERR_NOMEM" in header
+    for n, v in header.items():
+        assert getattr(P, n, None) == v, n
+    binding = {n for n in dir(P) if re.fullmatch(r"PTSTORE_(ERR|FLAG|OK)[A-Z_]*", n)}
+    assert binding == set(header), binding ^ set(header)
