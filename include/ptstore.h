@@ -386,6 +386,30 @@ int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t t
  */
 int ptstore_bandwidth_probe(int32_t kind, const void *a, void *b, int64_t bytes, void *stream);
 
+/*
+ * Allocation-free lookup + gather
+ * -------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, kernels and results as ptstore_lookup_gather, but the
+ * gather's descriptor list lives in a static device array of the library
+ * (about 20 MiB per device, held until the process ends) instead of
+ * store-owned scratch. The call allocates nothing, frees nothing, creates
+ * no event and never waits; it records no ptstore_kernel_times() entries
+ * and leaves a list made by ptstore_gather_prepare intact.
+ * Limit: R * max_blocks <= PTSTORE_NOALLOC_MAX_ENTRIES, else INVALID before
+ * any work is enqueued. Every such call on one device shares that device's
+ * array, whichever store it names: calls that overlap in time on one device
+ * (other streams, other threads) race and must be ordered by the caller.
+ * Errors: those of ptstore_lookup_gather (NOMEM excepted), plus INVALID for
+ * a batch over the limit or a device index of 64 or more.
+ */
+enum { PTSTORE_NOALLOC_MAX_ENTRIES = 1048576 /* 2^20 (request, block) entries */ };
+int ptstore_lookup_gather_noalloc(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                                  int64_t n_tokens, int32_t R, int32_t max_blocks,
+                                  int32_t *m, int32_t *ids, const int32_t *block_table,
+                                  void *cache, int64_t cache_blocks, void *stream);
+
 /* Human-readable text for a return code. */
 const char *ptstore_strerror(int code);
 

@@ -10,7 +10,7 @@
 //   evs     with eviction on: per-block access counts, priorities, child
 //           counts, depths, index keys and slots, and the victim-selection
 //           scratch (all sized by the capacity, allocated here once)
-//   scratch insert work space; copy_scratch gather/scatter descriptor lists
+//   insert_scratch insert work space; copy_scratch gather/scatter descriptor lists
 //           (both grown on demand, so the hot path allocates only when a
 //           batch is larger than every earlier one)
 // Calls check their arguments, enqueue kernels on the caller's stream and
@@ -19,14 +19,24 @@
 
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
-#include <string>
 #include <vector>
 
 #include "ptstore.h"
 #include "kernels.hpp"
 
 using namespace ptsd;
+
+// Descriptor-list scratch of ptstore_lookup_gather_noalloc, for callers that
+// cannot allocate: one copy per device, held until the process ends, shared
+// by every such call on that device (calls that overlap on one device race).
+// Its size is the gather's list for PTSTORE_NOALLOC_MAX_ENTRIES (request,
+// block) entries: 8 bytes per entry, 4 + 8 per request (at most one request
+// per entry), the 8-byte total, each part rounded up to 256 bytes.
+constexpr size_t kNoAllocScratchBytes =
+    (size_t)PTSTORE_NOALLOC_MAX_ENTRIES * (8 + 4 + 8) + 256;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 
 struct ptstore {
     ptstore_config_t cfg;
@@ -39,8 +49,8 @@ struct ptstore {
     Slot* slots;
     HashTables* ht;
     DevState* state;
-    void* scratch;
-    size_t scratch_bytes;
+    void* insert_scratch;
+    size_t insert_scratch_size;
     void* copy_scratch;
     size_t copy_scratch_bytes;
     int32_t chunks_per_group, threads, grid;
@@ -64,15 +74,14 @@ struct ptstore {
 
 namespace {
 
-thread_local std::string g_last_error;
+// A fixed buffer, so that no error path allocates host memory either.
+thread_local char g_last_error[512];
 
 int fail(int code, const char* what, hipError_t e = hipSuccess) {
-    char buf[512];
     if (e != hipSuccess)
-        snprintf(buf, sizeof buf, "%s: %s", what, hipGetErrorString(e));
+        snprintf(g_last_error, sizeof g_last_error, "%s: %s", what, hipGetErrorString(e));
     else
-        snprintf(buf, sizeof buf, "%s", what);
-    g_last_error = buf;
+        snprintf(g_last_error, sizeof g_last_error, "%s", what);
     return code;
 }
 
@@ -113,6 +122,30 @@ void make_hash_tables(uint64_t seed, bool weak, bool weak_tag, HashTables* h) {
     h->slot_seed = mix64(seed ^ 0xA0761D6478BD642Full);
     h->weak = weak ? 1u : 0u;
     h->weak_tag = weak_tag ? 1u : 0u;
+}
+
+// Device address of `scratch` per device, taken once with the device
+// current (each device holds its own copy of the array at its own address).
+// Host code uses only these addresses, never the array's name.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int bind_static_scratch(int device) {
+    if (device < 0 || device >= kMaxDevices) return PTSTORE_OK;  // the no-alloc call refuses
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[device]) return PTSTORE_OK;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(PTSTORE_ERR_HIP, "ptstore_create: static scratch address", e);
+    g_scratch_ptr[device] = p;
+    return PTSTORE_OK;
+}
+
+void* static_scratch(int device) {
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_ptr[device];
 }
 
 IndexView index_view(ptstore_t* s) {
@@ -313,7 +346,7 @@ const char* ptstore_strerror(int code) {
     }
 }
 
-const char* ptstore_last_error(void) { return g_last_error.c_str(); }
+const char* ptstore_last_error(void) { return g_last_error; }
 
 int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     if (!cfg || !out) return fail(PTSTORE_ERR_INVALID, "ptstore_create: null argument");
@@ -409,6 +442,13 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     if (e != hipSuccess) {
         delete s;
         return fail(PTSTORE_ERR_HIP, "ptstore_create: device query", e);
+    }
+    {  // the device's copy of the no-alloc call's scratch, with the device current
+        const int rc = bind_static_scratch(s->device);
+        if (rc) {
+            delete s;
+            return rc;
+        }
     }
     const size_t pool_bytes = (size_t)(s->tier.dev_rows > 0 ? s->tier.dev_rows : 1) * (size_t)s->block_bytes;
     const size_t cap1 = (size_t)(s->capacity > 0 ? s->capacity : 1);
@@ -514,7 +554,7 @@ int ptstore_destroy(ptstore_t* s) {
     (void)hipFree(s->slots);
     (void)hipFree(s->ht);
     (void)hipFree(s->state);
-    (void)hipFree(s->scratch);
+    (void)hipFree(s->insert_scratch);
     (void)hipFree(s->copy_scratch);
     (void)hipFree(s->ev_mem);
     (void)hipFree(s->tier_mem);
@@ -647,6 +687,41 @@ int ptstore_lookup_gather(ptstore_t* s, const int32_t* tokens, const int64_t* of
     return ptstore_gather(s, ids, m, block_table, R, max_blocks, cache, cache_blocks, stream);
 }
 
+int ptstore_lookup_gather_noalloc(ptstore_t* s, const int32_t* tokens, const int64_t* offsets,
+                                  int64_t n_tokens, int32_t R, int32_t max_blocks, int32_t* m,
+                                  int32_t* ids, const int32_t* block_table, void* cache,
+                                  int64_t cache_blocks, void* stream) {
+    if (!s || !check_batch(s, tokens, offsets, n_tokens, R, max_blocks) ||
+        (R > 0 && (!m || !ids || !block_table || !cache)) || cache_blocks < 0 ||
+        (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_lookup_gather_noalloc: bad argument");
+    if ((int64_t)R * max_blocks > PTSTORE_NOALLOC_MAX_ENTRIES ||
+        copy_scratch_bytes(R, max_blocks) > kNoAllocScratchBytes)
+        return fail(PTSTORE_ERR_INVALID,
+                    "ptstore_lookup_gather_noalloc: R * max_blocks exceeds PTSTORE_NOALLOC_MAX_ENTRIES");
+    if (R == 0) return PTSTORE_OK;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
+    void* sp = static_scratch(s->device);
+    if (!sp)
+        return fail(PTSTORE_ERR_INVALID, "ptstore_lookup_gather_noalloc: no static scratch on this device");
+    hipStream_t st = (hipStream_t)stream;
+    Batch b{tokens, offsets, n_tokens, R, max_blocks};
+    // the same kernels as ptstore_lookup_gather; no events are recorded, so
+    // nothing is created on the way either
+    hipError_t e = launch_lookup(index_view(s), b, m, ids, st);
+    CopyScratch sc;
+    copy_scratch_carve(sp, R, max_blocks, &sc);
+    const CopyPlan plan = copy_plan(s);
+    if (e == hipSuccess)
+        e = launch_gather_select(plan, sc, ids, m, block_table, R, max_blocks, cache_blocks, st);
+    if (e == hipSuccess)
+        e = launch_gather_copy(plan, sc, static_cast<uint8_t*>(cache), cache_blocks, R, max_blocks, 0,
+                               s->cfg.num_layers, st);
+    return e == hipSuccess ? PTSTORE_OK
+                           : fail(PTSTORE_ERR_HIP, "ptstore_lookup_gather_noalloc: launch", e);
+}
+
 int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, int64_t n_tokens,
                    int32_t R, int32_t max_blocks, int32_t* m_out, int32_t* ids, uint8_t* created,
                    void* stream) {
@@ -661,10 +736,10 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     uint64_t tn;
     const size_t need = insert_scratch_bytes(R, max_blocks, &tn);
     hipError_t e;
-    int rc2 = ensure_scratch(&s->scratch, &s->scratch_bytes, need, st, "ptstore_insert: scratch");
+    int rc2 = ensure_scratch(&s->insert_scratch, &s->insert_scratch_size, need, st, "ptstore_insert: scratch");
     if (rc2) return rc2;
     InsertScratch sc;
-    insert_scratch_carve(s->scratch, R, max_blocks, &sc);
+    insert_scratch_carve(s->insert_scratch, R, max_blocks, &sc);
     InsertTarget tgt{s->slots, s->parent, s->tokens, s->capacity};
     Batch b{tokens, offsets, n_tokens, R, max_blocks};
     if (s->evs.on) {

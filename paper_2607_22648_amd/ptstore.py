@@ -21,6 +21,7 @@ PTSTORE_OK, PTSTORE_ERR_INVALID, PTSTORE_ERR_FULL, PTSTORE_ERR_HIP, PTSTORE_ERR_
 PTSTORE_FLAG_WEAK_HASH, PTSTORE_FLAG_COUNTERS, PTSTORE_FLAG_TIMING = 1, 2, 4
 PTSTORE_FLAG_EVICT = 8
 PTSTORE_FLAG_WEAK_TAGS = 16
+PTSTORE_NOALLOC_MAX_ENTRIES = 1 << 20
 KIND_GATHER, KIND_LOOKUP, KIND_SCATTER, KIND_INSERT, KIND_SELECT, KIND_EVICT = 0, 1, 2, 3, 4, 5
 KIND_REPLICATE = 6
 
@@ -61,7 +62,7 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
            "ptstore_bandwidth_probe", "ptstore_replicate", "ptstore_gather_layers",
            "ptstore_scatter_layers", "ptstore_gather_prepare", "ptstore_gather_prepared",
-           "ptstore_set_counters", "ptstore_set_timing")
+           "ptstore_set_counters", "ptstore_set_timing", "ptstore_lookup_gather_noalloc")
 
 
 def _load() -> C.CDLL:
@@ -76,6 +77,7 @@ def _load() -> C.CDLL:
         "ptstore_lookup": [p, p, p, i64, i32, i32, p, p, p],
         "ptstore_gather": [p, p, p, p, i32, i32, p, i64, p],
         "ptstore_lookup_gather": [p, p, p, i64, i32, i32, p, p, p, p, i64, p],
+        "ptstore_lookup_gather_noalloc": [p, p, p, i64, i32, i32, p, p, p, p, i64, p],
         "ptstore_insert": [p, p, p, i64, i32, i32, p, p, p, p],
         "ptstore_scatter": [p, p, p, p, i32, i32, p, i64, p],
         "ptstore_stats": [p, C.POINTER(ptstore_stats_t)],
@@ -248,6 +250,19 @@ def ptstore_lookup_gather(h, tokens, offsets, max_blocks, m, ids, block_table, c
         _stream(stream)))
 
 
+def ptstore_lookup_gather_noalloc(h, tokens, offsets, max_blocks, m, ids, block_table, cache,
+                                  cache_blocks, stream=None) -> None:
+    R = _requests(offsets)
+    _need(m, R, "m")
+    _need(ids, R * max_blocks, "ids")
+    _need(block_table, R * max_blocks, "block_table")
+    _check("ptstore_lookup_gather_noalloc", _lib.ptstore_lookup_gather_noalloc(
+        h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
+        tokens.numel(), R, max_blocks, _dev(m, torch.int32, "m"), _dev(ids, torch.int32, "ids"),
+        _dev(block_table, torch.int32, "block_table"), _dev(cache, None, "cache"), cache_blocks,
+        _stream(stream)))
+
+
 def ptstore_insert(h, tokens, offsets, max_blocks, m_out, ids, created, stream=None) -> None:
     R = _requests(offsets)
     _need(m_out, R, "m_out")
@@ -407,6 +422,13 @@ class PrefixStore:
         ids = torch.empty((R, max_blocks), dtype=torch.int32, device=dev) if ids is None else ids
         ptstore_lookup_gather(self.h, tokens, offsets, max_blocks, m, ids, block_table, cache,
                               self.cache_blocks(cache), stream)
+        return m, ids
+
+    def lookup_gather_noalloc(self, tokens, offsets, max_blocks, block_table, cache, m, ids,
+                              stream=None):
+        """ptstore_lookup_gather_noalloc: the caller brings every output buffer."""
+        ptstore_lookup_gather_noalloc(self.h, tokens, offsets, max_blocks, m, ids, block_table,
+                                      cache, self.cache_blocks(cache), stream)
         return m, ids
 
     def insert(self, tokens, offsets, max_blocks, stream=None):

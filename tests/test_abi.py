@@ -168,5 +168,5 @@ def test_binding_constants_match_header():
     assert "PTSTORE_FLAG_WEAK_TAGS" in header and "PTSTORE_ERR_NOMEM" in header
     for n, v in header.items():
         assert getattr(P, n, None) == v, n
-    binding = {n for n in dir(P) if re.fullmatch(r"PTSTORE_(ERR|FLAG|OK)[A-Z_]*", n)}
+    binding = {n for n in dir(P) if re.fullmatch(r"PTSTORE_(ERR|FLAG|OK|NOALLOC)[A-Z_]*", n)}
     assert binding == set(header), binding ^ set(header)
