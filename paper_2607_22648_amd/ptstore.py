@@ -505,11 +505,14 @@ class PrefixStore:
         b = self.buffers()
         ids = torch.as_tensor(ids, dtype=torch.int64)
         dev = self.pool_tensor()
-        out = torch.empty((ids.numel(), self.shape.block_bytes), dtype=torch.uint8, device=dev.device)
         on_dev = ids < b.device_blocks
+        if bool(on_dev.all()):
+            return dev[ids.to(dev.device)]
+        out = torch.empty((ids.numel(), self.shape.block_bytes), dtype=torch.uint8, device=dev.device)
         if bool(on_dev.any()):
             out[on_dev.to(dev.device)] = dev[ids[on_dev].to(dev.device)]
         if bool((~on_dev).any()):
+            torch.cuda.synchronize()  # host-tier rows are written by device kernels
             host = self.host_tensor()
             out[(~on_dev).to(dev.device)] = host[ids[~on_dev] - b.device_blocks].to(dev.device)
         return out

@@ -1,12 +1,18 @@
 """Parity at the workloads' full sizes, in the launch configuration bench.py times.
 
-At these sizes the oracle runs without payload (its trie alone), so:
-- m, ids and created are compared with the oracle for every request, exactly;
-- every gathered block is compared with pool[id] on the device (a property
-  that holds at any size), and every cache block the gather must not touch
-  still holds the sentinel;
-- pool blocks whose input bytes were recorded when they were scattered are
-  compared byte for byte through the gather (sampled outputs).
+At these sizes the oracle runs without payload (its trie alone). Every
+copied byte is still checked, through this chain:
+1. m, ids and created of every insert and lookup equal the oracle's, exactly;
+2. right after each scatter, every block it created holds, in its home row
+   (device pool or host tier), exactly the bytes of its cache block;
+3. after the prefill, the whole pool is checked once more against its
+   inputs: each scatter's seeded cache is drawn again and every block holds
+   the bytes of the scatter that last wrote it (a later scatter writing
+   outside its own blocks fails here);
+4. every gathered block equals its home row, and every cache block or
+   layer the gather must not touch still holds the sentinel.
+Bytes recorded from sampled blocks at scatter time are compared with what
+the gathers return as an end-to-end check of the same chain.
 """
 from __future__ import annotations
 
@@ -37,10 +43,12 @@ if torch.cuda.is_available():
     from tests.twin import to_dev, host, DEV
 
 SENTINEL = 0xA5
+CMP_BYTES = 512 << 20  # bytes of blocks compared per step
 
 
 def _shape(kv):
-    return P.StoreShape(kv.layers, kv.kv_heads, kv.head_dim, kv.block_tokens, kv.elem_bytes)
+    return P.StoreShape(kv.layers, kv.kv_heads, kv.head_dim, kv.block_tokens, kv.elem_bytes,
+                        kv.layer_chunk_bytes)
 
 
 def _free(*objs):
@@ -49,6 +57,78 @@ def _free(*objs):
             o.close()
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def seeded_cache(kv, nb_cache: int, seed: int) -> torch.Tensor:
+    """A flat paged cache of nb_cache blocks filled with seeded random bytes
+    (the same bytes every time for the same seed and size)."""
+    cache = torch.empty(nb_cache * kv.block_bytes, dtype=torch.uint8, device=DEV)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    cache.random_(0, 256, generator=g)
+    return cache
+
+
+def cache_block_bytes(kv, cache: torch.Tensor, nb_cache: int, cbs: torch.Tensor) -> torch.Tensor:
+    """[n, block_bytes]: cache blocks cbs in pool-block order (layer after layer,
+    K then V). Layer l of the cache takes the next 2 * nb_cache * slab_l bytes."""
+    n = cbs.numel()
+    if kv.layer_chunk_bytes is None:
+        cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
+        return cv[:, :, cbs].permute(2, 0, 1, 3).reshape(n, kv.block_bytes)
+    pieces, off = [], 0
+    for ch in kv.layer_chunk_bytes:
+        v = cache[off:off + 2 * nb_cache * ch].view(2, nb_cache, ch)
+        pieces.append(v[:, cbs].permute(1, 0, 2).reshape(n, 2 * ch))
+        off += 2 * nb_cache * ch
+    return torch.cat(pieces, dim=1)
+
+
+def compare_blocks(store, kv, cache, nb_cache, ids: np.ndarray, cbs: np.ndarray, what: str,
+                   cols=None):
+    """Home bytes of block ids[k] == bytes of cache block cbs[k], for every k
+    (only byte columns cols[0]:cols[1] of the block when given)."""
+    per = max(1, CMP_BYTES // kv.block_bytes)
+    a, e = cols if cols is not None else (0, kv.block_bytes)
+    for s in range(0, len(ids), per):
+        got = store.block_bytes_of(ids[s:s + per])[:, a:e]
+        exp = cache_block_bytes(kv, cache, nb_cache, to_dev(cbs[s:s + per].astype(np.int64)))[:, a:e]
+        if not torch.equal(got, exp):
+            k = int(torch.nonzero((got != exp).any(dim=1))[0])
+            raise AssertionError(f"{what}: block id {ids[s + k]} differs from cache block "
+                                 f"{cbs[s + k]} ({len(ids)} blocks compared in all)")
+
+
+class Ledger:
+    """Which scatter last wrote each block id, from which cache block; a
+    scatter's cache is kept as (seed, size) and drawn again to re-check."""
+
+    def __init__(self, kv, capacity: int):
+        self.kv = kv
+        self.calls = []  # (seed, nb_cache)
+        self.writer = np.full(capacity, -1, dtype=np.int64)
+        self.block = np.full(capacity, -1, dtype=np.int64)
+
+    def record(self, seed: int, nb_cache: int, ids: np.ndarray, cbs: np.ndarray):
+        self.calls.append((seed, nb_cache))
+        self.writer[ids] = len(self.calls) - 1
+        self.block[ids] = cbs
+
+    def verify(self, store, count: int):
+        """Every block id < count holds the bytes of the scatter that last wrote it."""
+        assert (self.writer[:count] >= 0).all(), "a stored block was never scattered"
+        checked = 0
+        for k, (seed, nb) in enumerate(self.calls):
+            ids = np.flatnonzero(self.writer[:count] == k)
+            if len(ids) == 0:
+                continue
+            cache = seeded_cache(self.kv, nb, seed)
+            compare_blocks(store, self.kv, cache, nb, ids, self.block[ids],
+                           f"pool re-check, scatter {k}")
+            checked += len(ids)
+            del cache
+        assert checked == count
+        return checked
 
 
 class Recorder:
@@ -64,14 +144,15 @@ class Recorder:
         cand = np.argwhere((created != 0) & (bt >= 0))
         if len(cand) == 0 or len(self.bytes) >= self.want:
             return
-        cv = cache.view(self.kv.layers, 2, nb_cache, self.kv.chunk_bytes)
         for r, b in cand[self.rng.choice(len(cand), size=min(k, len(cand)), replace=False)]:
-            self.bytes[int(ids[r, b])] = host(cv[:, :, int(bt[r, b])])
+            sel = torch.tensor([int(bt[r, b])], dtype=torch.int64, device=DEV)
+            self.bytes[int(ids[r, b])] = host(cache_block_bytes(self.kv, cache, nb_cache, sel)[0])
 
 
-def insert_scatter(store, ref, kv, toks, offs, maxb, seed, rec: Recorder = None, k=4,
-                   compact=False):
-    """Insert on both sides (outputs compared), scatter seeded random KV on the GPU.
+def insert_scatter(store, ref, kv, toks, offs, maxb, seed, ledger: Ledger, rec: Recorder = None,
+                   k=4, compact=False):
+    """Insert on both sides (outputs compared), scatter seeded random KV on the
+    GPU, then compare every created block with its cache block.
 
     With compact=True only created blocks get a cache slot (block table -1 elsewhere)."""
     m, ids, cr = store.insert(to_dev(toks), to_dev(offs), maxb)
@@ -88,11 +169,11 @@ def insert_scatter(store, ref, kv, toks, offs, maxb, seed, rec: Recorder = None,
     else:
         bt = np.arange(R * maxb, dtype=np.int32).reshape(R, maxb)
         nb_cache = R * maxb
-    cache = torch.empty(kv.layers * 2 * nb_cache * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
-    g = torch.Generator(device=DEV)
-    g.manual_seed(seed)
-    cache.random_(0, 256, generator=g)
+    cache = seeded_cache(kv, nb_cache, seed)
     store.scatter(ids, cr, to_dev(bt), cache)
+    made = (cr_h != 0) & (bt >= 0)
+    compare_blocks(store, kv, cache, nb_cache, ids_h[made], bt[made], f"scatter seed {seed}")
+    ledger.record(seed, nb_cache, ids_h[made], bt[made])
     if rec is not None:
         rec.take(cache, nb_cache, ids_h, cr_h, bt, k)
     torch.cuda.synchronize()
@@ -100,34 +181,43 @@ def insert_scatter(store, ref, kv, toks, offs, maxb, seed, rec: Recorder = None,
     return ids_h, cr_h
 
 
-def check_gather(store, kv, cache, m_h, ids_h, bt_h, rec: Recorder = None, chunk=128):
-    """Every gathered block == pool[id]; untouched blocks keep the sentinel; recorded bytes."""
-    cap = store.stats()["capacity"]
-    nb_cache = cache.numel() // (kv.layers * 2 * kv.chunk_bytes)
-    cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
-    pv = store.pool_tensor().view(cap, kv.layers, 2, kv.chunk_bytes)
-    R, maxb = ids_h.shape
-    hit = (np.arange(maxb)[None, :] < m_h[:, None]) & (bt_h >= 0)
-    sel_ids = to_dev(ids_h[hit].astype(np.int64))
-    sel_bt = to_dev(bt_h[hit].astype(np.int64))
-    for s in range(0, sel_ids.numel(), chunk):
-        a = cv[:, :, sel_bt[s:s + chunk]]
-        b = pv[sel_ids[s:s + chunk]].permute(1, 2, 0, 3)
-        assert torch.equal(a, b), f"gathered blocks {s}..{s + chunk} differ from the pool"
+def check_gather(store, kv, cache, m_h, ids_h, bt_h, rec: Recorder = None, layers=None):
+    """Every gathered block equals its home row (within the layer range when
+    given: the rest of every block keeps the sentinel); every cache block the
+    gather must not touch keeps the sentinel; recorded bytes where seen."""
+    nb_cache = cache.numel() // kv.block_bytes
+    hit = (np.arange(ids_h.shape[1])[None, :] < m_h[:, None]) & (bt_h >= 0)
+    cols = None
+    if layers is not None:
+        lb = np.concatenate([[0], np.cumsum([2 * c for c in (kv.layer_chunk_bytes or
+                                                             [kv.chunk_bytes] * kv.layers)])])
+        cols = (int(lb[layers[0]]), int(lb[layers[1]]))
+    compare_blocks(store, kv, cache, nb_cache, ids_h[hit].astype(np.int64),
+                   bt_h[hit].astype(np.int64), "gather", cols=cols)
+    per = max(1, CMP_BYTES // kv.block_bytes)
+    if cols is not None:  # the other layers of the gathered blocks are untouched
+        sel = bt_h[hit].astype(np.int64)
+        for s in range(0, len(sel), per):
+            got = cache_block_bytes(kv, cache, nb_cache, to_dev(sel[s:s + per]))
+            assert bool((got[:, :cols[0]] == SENTINEL).all()) and \
+                bool((got[:, cols[1]:] == SENTINEL).all()), "gather wrote outside its layers"
     untouched = np.ones(nb_cache, dtype=bool)
     untouched[bt_h[hit]] = False
-    un = to_dev(np.flatnonzero(untouched))
-    for s in range(0, un.numel(), chunk):
-        assert bool((cv[:, :, un[s:s + chunk]] == SENTINEL).all()), "gather wrote outside its blocks"
+    un = np.flatnonzero(untouched)
+    for s in range(0, len(un), per):
+        got = cache_block_bytes(kv, cache, nb_cache, to_dev(un[s:s + per]))
+        assert bool((got == SENTINEL).all()), "gather wrote outside its blocks"
+    seen = 0
     if rec is not None:
-        seen = 0
         for (r, b) in np.argwhere(hit):
             i = int(ids_h[r, b])
             if i in rec.bytes:
-                np.testing.assert_array_equal(host(cv[:, :, int(bt_h[r, b])]), rec.bytes[i])
+                sel = torch.tensor([int(bt_h[r, b])], dtype=torch.int64, device=DEV)
+                got = host(cache_block_bytes(kv, cache, nb_cache, sel)[0])
+                a, e = cols if cols is not None else (0, kv.block_bytes)
+                np.testing.assert_array_equal(got[a:e], rec.bytes[i][a:e])
                 seen += 1
-        return seen
-    return 0
+    return seen
 
 
 def lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec=None):
@@ -140,7 +230,7 @@ def lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec=None):
     np.testing.assert_array_equal(m_h, rm)
     np.testing.assert_array_equal(ids_h, rids)
     seen = check_gather(store, kv, cache, m_h, ids_h, bt_h, rec)
-    return m_h, seen
+    return m_h, ids_h, seen
 
 
 def check_access_counts(store, ref):
@@ -156,29 +246,31 @@ def check_access_counts(store, ref):
 def _passage_store(w, capacity, batch, rec, evict=False):
     kv = w.shape
     store = P.PrefixStore(_shape(kv), capacity, flags=P.PTSTORE_FLAG_EVICT if evict else 0)
-    ref = OracleStore.for_shape(kv, capacity, with_payload=False, evict=evict)
+    cap = store.stats()["capacity"]
+    ref = OracleStore.for_shape(kv, cap, with_payload=False, evict=evict)
+    ledger = Ledger(kv, cap)
     st, so = w.store_batch()
     Rs = len(so) - 1
     for lo in range(0, Rs, batch):
         hi = min(Rs, lo + batch)
         insert_scatter(store, ref, kv, st[so[lo]:so[hi]], (so[lo:hi + 1] - so[lo]).astype(np.int64),
-                       w.passage_blocks, seed=lo, rec=rec, k=8)
+                       w.passage_blocks, seed=lo, ledger=ledger, rec=rec, k=8)
     assert store.stats()["blocks_stored"] == ref.count == len(w.stored) * w.passage_blocks
-    return store, ref
+    assert ledger.verify(store, ref.count) == ref.count
+    return store, ref, ledger
 
 
 def test_llama8b_full():
     w = synth.build("llama8b")
     kv = w.shape
     rec = Recorder(kv, 64, 1)
-    store, ref = _passage_store(w, len(w.stored) * w.passage_blocks, 32, rec)
+    store, ref, _ = _passage_store(w, len(w.stored) * w.passage_blocks, 32, rec)
     maxb = w.max_blocks
-    cache = torch.empty(kv.layers * 2 * w.sub_batch * maxb * kv.chunk_bytes, dtype=torch.uint8,
-                        device=DEV)
+    cache = torch.empty(w.sub_batch * maxb * kv.block_bytes, dtype=torch.uint8, device=DEV)
     seen = 0
     for lo, hi in w.sub_batches():
         toks, offs = w.request_slice(lo, hi)
-        m_h, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
+        m_h, _, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
         seen += s
         expect = np.where(np.isin(w.req_passage[lo:hi], w.stored), w.passage_blocks, 0)
         np.testing.assert_array_equal(m_h, expect)
@@ -207,14 +299,13 @@ def test_llama70b_shard_full():
     w = synth.build("llama70b_shard")
     kv = w.shape
     rec = Recorder(kv, 32, 2)
-    store, ref = _passage_store(w, len(w.stored) * w.passage_blocks, 2, rec)
+    store, ref, _ = _passage_store(w, len(w.stored) * w.passage_blocks, 2, rec)
     maxb = w.max_blocks
-    cache = torch.empty(kv.layers * 2 * w.sub_batch * maxb * kv.chunk_bytes, dtype=torch.uint8,
-                        device=DEV)
+    cache = torch.empty(w.sub_batch * maxb * kv.block_bytes, dtype=torch.uint8, device=DEV)
     seen = 0
     for lo, hi in w.sub_batches():
         toks, offs = w.request_slice(lo, hi)
-        m_h, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
+        m_h, _, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
         seen += s
         expect = np.where(np.isin(w.req_passage[lo:hi], w.stored), w.passage_blocks, 0)
         np.testing.assert_array_equal(m_h, expect)
@@ -228,6 +319,7 @@ def test_trie_full():
     kv = w.shape
     store = P.PrefixStore(_shape(kv), w.capacity, flags=P.PTSTORE_FLAG_COUNTERS)
     ref = OracleStore.for_shape(kv, w.capacity, with_payload=False)
+    ledger = Ledger(kv, w.capacity)
     rec = Recorder(kv, 256, 3)
     W = len(w.store_offsets) - 1
     batch = 32768
@@ -235,12 +327,14 @@ def test_trie_full():
         hi = min(W, lo + batch)
         toks = w.store_tokens[w.store_offsets[lo]:w.store_offsets[hi]]
         offs = (w.store_offsets[lo:hi + 1] - w.store_offsets[lo]).astype(np.int64)
-        insert_scatter(store, ref, kv, toks, offs, w.depth, seed=lo, rec=rec, k=16, compact=True)
+        insert_scatter(store, ref, kv, toks, offs, w.depth, seed=lo, ledger=ledger, rec=rec, k=16,
+                       compact=True)
     st = store.stats()
     assert st["blocks_stored"] == ref.count == w.capacity and st["full_events"] >= 1
+    assert ledger.verify(store, ref.count) == w.capacity
     R = w.n_requests
-    cache = torch.empty(kv.layers * 2 * R * w.depth * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
-    m_h, seen = lookup_gather_checked(store, ref, kv, w.tokens, w.offsets, w.depth, cache, rec)
+    cache = torch.empty(R * w.depth * kv.block_bytes, dtype=torch.uint8, device=DEV)
+    m_h, _, seen = lookup_gather_checked(store, ref, kv, w.tokens, w.offsets, w.depth, cache, rec)
     assert seen > 0 and m_h.mean() > 60
     del cache
     _free(store, ref)
@@ -249,29 +343,32 @@ def test_trie_full():
 @pytest.mark.parametrize("name,rounds", [("stream", None), ("stream_evict", 14)])
 def test_stream_full(name, rounds):
     """100 rounds of the stream on the 160 GB pool; with eviction, 14 rounds (the
-    pool fills in the sixth; the oracle's one-leaf-at-a-time eviction is slow)."""
+    pool fills in the sixth; the oracle's one-leaf-at-a-time eviction is slow).
+    Each round's lookup cache is re-filled with seeded bytes for its inserts'
+    scatter; at the end the whole pool is re-checked against those draws."""
     over = {} if rounds is None else {"n_rounds": rounds}
     sw = synth.build(name, **over)
     evict = name == "stream_evict"
     base = sw.base
     kv = base.shape
     rec = Recorder(kv, 64, 4)
-    store, ref = _passage_store(base, sw.pool_blocks, 32, rec, evict=evict)
+    store, ref, ledger = _passage_store(base, sw.pool_blocks, 32, rec, evict=evict)
     maxb = base.max_blocks
     per = len(sw.rounds[0].lookup_offsets) - 1
-    cache = torch.empty(kv.layers * 2 * per * maxb * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
     nb_cache = per * maxb
+    cache = torch.empty(nb_cache * kv.block_bytes, dtype=torch.uint8, device=DEV)
     g = torch.Generator(device=DEV)
     seen = 0
     for i, rd in enumerate(sw.rounds):
-        _, s = lookup_gather_checked(store, ref, kv, rd.lookup_tokens, rd.lookup_offsets, maxb,
-                                     cache, rec)
+        _, _, s = lookup_gather_checked(store, ref, kv, rd.lookup_tokens, rd.lookup_offsets, maxb,
+                                        cache, rec)
         seen += s
         # inserts: KV of the new blocks is fresh in the cache, then scattered
         Ri = len(rd.insert_offsets) - 1
         bt_h = np.arange(Ri * maxb, dtype=np.int32).reshape(Ri, maxb)
-        g.manual_seed(10_000 + i)
-        cache.random_(0, 256, generator=g)
+        seed = 10_000 + i
+        g.manual_seed(seed)
+        cache.random_(0, 256, generator=g)  # the bytes seeded_cache(kv, nb_cache, seed) draws
         m, ids, cr = store.insert(to_dev(rd.insert_tokens), to_dev(rd.insert_offsets), maxb)
         rc, rm, rids, rcr = ref.insert(rd.insert_tokens, rd.insert_offsets, maxb)
         ids_h, cr_h = host(ids), host(cr)
@@ -279,15 +376,11 @@ def test_stream_full(name, rounds):
         np.testing.assert_array_equal(ids_h, rids)
         np.testing.assert_array_equal(cr_h, rcr)
         store.scatter(ids, cr, to_dev(bt_h), cache)
-        # every created block now holds its cache block's bytes
-        made = np.argwhere(cr_h != 0)
-        if len(made):
-            cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
-            pv = store.pool_tensor().view(-1, kv.layers, 2, kv.chunk_bytes)
-            sel_ids = to_dev(ids_h[cr_h != 0].astype(np.int64))
-            sel_bt = to_dev(bt_h[cr_h != 0].astype(np.int64))
-            assert torch.equal(cv[:, :, sel_bt], pv[sel_ids].permute(1, 2, 0, 3))
-            for reused in ids_h[cr_h != 0].tolist():  # an evicted id now holds another block
+        made = cr_h != 0
+        if made.any():
+            compare_blocks(store, kv, cache, nb_cache, ids_h[made], bt_h[made], f"round {i} scatter")
+            ledger.record(seed, nb_cache, ids_h[made], bt_h[made])
+            for reused in ids_h[made].tolist():  # an evicted id now holds another block
                 rec.bytes.pop(int(reused), None)
             rec.take(cache, nb_cache, ids_h, cr_h, bt_h, 1)
         if evict and (i % 4 == 3 or i == len(sw.rounds) - 1):
@@ -299,40 +392,17 @@ def test_stream_full(name, rounds):
         st = store.stats()
         assert st["evictions"] == ref.evictions > 0 and st["clock"] == ref.clock
     del cache
+    torch.cuda.empty_cache()
+    assert ledger.verify(store, ref.count) == ref.count
     _free(store, ref)
-
-
-def _check_gather_tiered(store, kv, cache, m_h, ids_h, bt_h, rng, rec=None, per_row=8):
-    """Sampled gathered blocks equal their home bytes (device or host tier);
-    sampled unmatched blocks keep the sentinel; recorded bytes where seen."""
-    nb_cache = cache.numel() // (kv.layers * 2 * kv.chunk_bytes)
-    cv = cache.view(kv.layers, 2, nb_cache, kv.chunk_bytes)
-    seen = 0
-    for r in range(len(m_h)):
-        if m_h[r]:
-            bs = rng.choice(m_h[r], size=min(per_row, m_h[r]), replace=False)
-            got = cv[:, :, torch.from_numpy(bt_h[r, bs].astype(np.int64)).to(DEV)].permute(2, 0, 1, 3)
-            exp = store.block_bytes_of(ids_h[r, bs]).view(len(bs), kv.layers, 2, kv.chunk_bytes)
-            assert torch.equal(got, exp), f"request {r}: gathered blocks differ from their home"
-        rest = np.arange(m_h[r], ids_h.shape[1])
-        if len(rest):
-            bs = rng.choice(rest, size=min(per_row, len(rest)), replace=False)
-            sel = torch.from_numpy(bt_h[r, bs].astype(np.int64)).to(DEV)
-            assert bool((cv[:, :, sel] == SENTINEL).all()), "gather wrote outside its blocks"
-        if rec is not None:
-            for b in range(m_h[r]):
-                i = int(ids_h[r, b])
-                if i in rec.bytes:
-                    np.testing.assert_array_equal(host(cv[:, :, int(bt_h[r, b])]), rec.bytes[i])
-                    seen += 1
-    return seen
 
 
 def test_llama70b_full_tiered():
     """All 32 passages (322 GB) on one GPU: HBM, HBM replicas and the pinned
-    host tier. Metadata against the oracle everywhere; payload by sampled
-    home-byte checks and recorded scatter bytes; replicas against the
-    oracle's hot set."""
+    host tier. Metadata against the oracle everywhere; every scattered and
+    every gathered block against its home bytes (host-tier rows read back
+    from pinned memory); replicas against the oracle's hot set and their
+    home bytes."""
     w = synth.build("llama70b_full")
     kv, tiers = w.shape, w.tiers
     store = P.PrefixStore(_shape(kv), tiers["device_blocks"] + tiers["replica_blocks"],
@@ -341,32 +411,27 @@ def test_llama70b_full_tiered():
     cap = store.stats()["capacity"]
     assert cap == len(w.stored) * w.passage_blocks
     ref = OracleStore.for_shape(kv, cap, with_payload=False, evict=True)
+    ledger = Ledger(kv, cap)
     rec = Recorder(kv, 96, 9)
     st_, so = w.store_batch()
     for k in range(len(so) - 1):
         insert_scatter(store, ref, kv, st_[so[k]:so[k + 1]], (so[k:k + 2] - so[k]).astype(np.int64),
-                       w.passage_blocks, seed=k, rec=rec, k=3)
+                       w.passage_blocks, seed=k, ledger=ledger, rec=rec, k=3)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     assert store.stats()["blocks_stored"] == ref.count == cap
+    assert ledger.verify(store, cap) == cap
     owned = store.stats()["device_blocks"]
     maxb = w.max_blocks
-    cache = torch.empty(kv.layers * 2 * maxb * kv.chunk_bytes, dtype=torch.uint8, device=DEV)
-    rng = np.random.default_rng(3)
+    cache = torch.empty(maxb * kv.block_bytes, dtype=torch.uint8, device=DEV)
     seen = 0
     host_hits = 0
     for rnd in range(2):
         for lo, hi in w.sub_batches():
             toks, offs = w.request_slice(lo, hi)
-            bt_h = np.arange((hi - lo) * maxb, dtype=np.int32).reshape(hi - lo, maxb)
-            cache.fill_(SENTINEL)
-            m, ids = store.lookup_gather(to_dev(toks), to_dev(offs), maxb, to_dev(bt_h), cache)
-            rm, rids = ref.lookup(toks, offs, maxb)
-            m_h, ids_h = host(m), host(ids)
-            np.testing.assert_array_equal(m_h, rm)
-            np.testing.assert_array_equal(ids_h, rids)
+            m_h, ids_h, s = lookup_gather_checked(store, ref, kv, toks, offs, maxb, cache, rec)
             host_hits += int((ids_h[0, :m_h[0]] >= owned).sum())
-            seen += _check_gather_tiered(store, kv, cache, m_h, ids_h, bt_h, rng, rec)
+            seen += s
         check_access_counts(store, ref)
         if rnd == 0:  # replicate the host tier's hot set, then read through it
             store.replicate()
@@ -374,64 +439,39 @@ def test_llama70b_full_tiered():
             rep = host(store.replica_map())
             have = np.flatnonzero(rep >= 0)
             np.testing.assert_array_equal(owned + have, ref.hot_set(owned, ref.count, tiers["replica_blocks"]))
-            sample = rng.choice(have, size=min(64, len(have)), replace=False)
-            dev_rows = store.pool_tensor()[torch.from_numpy(owned + rep[sample].astype(np.int64)).to(DEV)]
-            assert torch.equal(dev_rows, store.block_bytes_of(owned + sample))
+            per = max(1, CMP_BYTES // kv.block_bytes)
+            for s in range(0, len(have), per):  # every replica row holds its home bytes
+                h = have[s:s + per]
+                dev_rows = store.pool_tensor()[torch.from_numpy(owned + rep[h].astype(np.int64)).to(DEV)]
+                assert torch.equal(dev_rows, store.block_bytes_of(owned + h)), "replica bytes"
     assert host_hits > 0 and seen > 0
     del cache
     _free(store, ref)
 
 
-def _block_of(cache: torch.Tensor, nb: int, chunks, cb: int) -> torch.Tensor:
-    """Bytes of cache block cb in pool-block order (layer after layer, K then V):
-    layer l of the cache takes the next 2 * nb * chunks[l] bytes."""
-    out, off = [], 0
-    for ch in chunks:
-        v = cache[off:off + 2 * nb * ch].view(2, nb, ch)
-        out.append(v[:, cb].reshape(-1))
-        off += 2 * nb * ch
-    return torch.cat(out)
-
-
 def test_hybrid8b_full():
     """Per-layer slab sizes (32 KiB / 8 KiB alternating) at the 8B-shaped
-    workload's full size: metadata against the oracle, sampled blocks against
-    the pool and the bytes recorded at scatter, and a layer-range gather."""
+    workload's full size: metadata against the oracle, every scattered and
+    gathered block against its home row, and a layer-range gather."""
     w = synth.build("hybrid8b")
     kv = w.shape
-    chunks = kv.layer_chunk_bytes
     cap = len(w.stored) * w.passage_blocks
-    shape = P.StoreShape(kv.layers, kv.kv_heads, kv.head_dim, kv.block_tokens, kv.elem_bytes, chunks)
-    store = P.PrefixStore(shape, cap)
+    store = P.PrefixStore(_shape(kv), cap)
     ref = OracleStore.for_shape(kv, cap, with_payload=False)
-    rng = np.random.default_rng(8)
-    recorded = {}
+    ledger = Ledger(kv, cap)
+    rec = Recorder(kv, 64, 8)
     st_, so = w.store_batch()
-    g = torch.Generator(device=DEV)
     for lo in range(0, len(so) - 1, 16):
         hi = min(len(so) - 1, lo + 16)
-        toks, offs = st_[so[lo]:so[hi]], (so[lo:hi + 1] - so[lo]).astype(np.int64)
-        m, ids, cr = store.insert(to_dev(toks), to_dev(offs), w.passage_blocks)
-        rc, rm, rids, rcr = ref.insert(toks, offs, w.passage_blocks)
-        ids_h, cr_h = host(ids), host(cr)
-        np.testing.assert_array_equal(ids_h, rids)
-        np.testing.assert_array_equal(cr_h, rcr)
-        nb = (hi - lo) * w.passage_blocks
-        cache = torch.empty(nb * kv.block_bytes, dtype=torch.uint8, device=DEV)
-        g.manual_seed(lo)
-        cache.random_(0, 256, generator=g)
-        bt_h = np.arange(nb, dtype=np.int32).reshape(hi - lo, w.passage_blocks)
-        store.scatter(ids, cr, to_dev(bt_h), cache)
-        for r, b in np.argwhere(cr_h != 0)[rng.choice(int((cr_h != 0).sum()), 4, replace=False)]:
-            recorded[int(ids_h[r, b])] = host(_block_of(cache, nb, chunks, int(bt_h[r, b])))
-        del cache
+        insert_scatter(store, ref, kv, st_[so[lo]:so[hi]], (so[lo:hi + 1] - so[lo]).astype(np.int64),
+                       w.passage_blocks, seed=lo, ledger=ledger, rec=rec, k=4)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    assert store.stats()["block_bytes"] == kv.block_bytes == 2 * sum(chunks)
-    pool = store.pool_tensor()
+    assert store.stats()["block_bytes"] == kv.block_bytes == 2 * sum(kv.layer_chunk_bytes)
+    assert store.stats()["blocks_stored"] == ref.count == cap
+    assert ledger.verify(store, cap) == cap
     maxb = w.max_blocks
-    nbc = w.sub_batch * maxb
-    cache = torch.empty(nbc * kv.block_bytes, dtype=torch.uint8, device=DEV)
+    cache = torch.empty(w.sub_batch * maxb * kv.block_bytes, dtype=torch.uint8, device=DEV)
     seen = 0
     for k, (lo, hi) in enumerate(w.sub_batches()):
         toks, offs = w.request_slice(lo, hi)
@@ -445,26 +485,7 @@ def test_hybrid8b_full():
         m_h, ids_h = host(m), host(ids)
         np.testing.assert_array_equal(m_h, rm)
         np.testing.assert_array_equal(ids_h, rids)
-        lb = np.concatenate([[0], np.cumsum([2 * c for c in chunks])])
-        for r in rng.choice(R, 12, replace=False):
-            for b in rng.choice(maxb, 6, replace=False):
-                got = _block_of(cache, nbc, chunks, int(bt_h[r, b]))
-                if b >= m_h[r]:
-                    assert bool((got == SENTINEL).all())
-                    continue
-                row = pool[int(ids_h[r, b])]
-                if layers is None:
-                    assert torch.equal(got, row)
-                    if int(ids_h[r, b]) in recorded:
-                        np.testing.assert_array_equal(host(got), recorded[int(ids_h[r, b])])
-                        seen += 1
-                else:
-                    a, e = int(lb[layers[0]]), int(lb[layers[1]])
-                    assert torch.equal(got[a:e], row[a:e])
-                    assert bool((got[:a] == SENTINEL).all()) and bool((got[e:] == SENTINEL).all())
-        for i, want in recorded.items():  # the pool keeps what was scattered
-            np.testing.assert_array_equal(host(pool[i]), want)
-            seen += 1
+        seen += check_gather(store, kv, cache, m_h, ids_h, bt_h, rec, layers=layers)
     assert seen > 0
     del cache
     _free(store, ref)
