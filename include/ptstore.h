@@ -40,16 +40,20 @@
  *    <= 2^29, else INVALID.
  *  - Return codes: PTSTORE_OK, or an error found on the host before any
  *    work is enqueued. Conditions only the device can see (a full store,
- *    out-of-range entries) are counted and reported by ptstore_stats().
+ *    out-of-range entries) are counted and reported by ptstore_stats();
+ *    ptstore_insert_sync waits for its stream and returns PTSTORE_ERR_FULL
+ *    when that insert refused blocks. Without waiting, a caller sees a cut
+ *    in the outputs: request r was cut exactly when m_out[r] is below its
+ *    number of whole blocks (at most max_blocks).
  *  - HIP graphs: once a call has grown the store's scratch to a batch size,
- *    lookup, gather, gather_layers, lookup_gather, scatter, scatter_layers
- *    and (without PTSTORE_FLAG_EVICT) insert of that size or smaller only
- *    launch kernels: no allocation, no wait, no memset. They may be
- *    captured and replayed; a replay works on the store as it is then. A
- *    later call with a larger batch regrows the scratch, after which
- *    earlier captures must not be replayed. An evicting insert keeps a
- *    per-call value on the host and is not to be replayed. A capture keeps
- *    the counting state (ptstore_set_counters) it was made with.
+ *    lookup, gather, gather_layers, lookup_gather, insert (with or without
+ *    PTSTORE_FLAG_EVICT), scatter and scatter_layers of that size or
+ *    smaller only launch kernels: no allocation, no wait, no memset. They
+ *    may be captured and replayed; a replay works on the store as it is
+ *    then. A later call with a larger batch regrows the scratch, after which
+ *    earlier captures must not be replayed. A capture keeps the counting
+ *    state (ptstore_set_counters) it was made with. ptstore_lookup_gather_noalloc
+ *    never allocates, whatever the batch (up to its limit).
  */
 #ifndef PTSTORE_H
 #define PTSTORE_H
@@ -65,7 +69,7 @@ typedef struct ptstore ptstore_t;
 enum {
     PTSTORE_OK = 0,
     PTSTORE_ERR_INVALID = 1, /* bad argument (null pointer, negative size, misaligned, ...) */
-    PTSTORE_ERR_FULL = 2,    /* reserved: a full store is reported through ptstore_stats */
+    PTSTORE_ERR_FULL = 2,    /* ptstore_insert_sync: the insert refused blocks for lack of room */
     PTSTORE_ERR_HIP = 3,     /* a HIP runtime call failed (see ptstore_last_error) */
     PTSTORE_ERR_NOMEM = 4    /* device or host allocation failed */
 };
@@ -178,6 +182,10 @@ typedef struct {
                                   (its bytes are pool row device_blocks + slot), or -1 */
 } ptstore_buffers_t;
 
+/* ======================================================================
+ * Store lifetime
+ * ====================================================================== */
+
 /*
  * Create a store on the current HIP device: allocates the pool, the block
  * metadata and the hash index, and waits until they are initialised.
@@ -190,6 +198,10 @@ int ptstore_create(const ptstore_config_t *cfg, ptstore_t **out);
 
 /* Wait for the device, then free everything the store owns. NULL is a no-op. */
 int ptstore_destroy(ptstore_t *store);
+
+/* ======================================================================
+ * The prefix query and the load (Section 4.1; Section 5)
+ * ====================================================================== */
 
 /*
  * LCP query (Section 4.1): for each request r, m[r] = the largest k such that
@@ -224,14 +236,77 @@ int ptstore_gather(ptstore_t *store, const int32_t *ids, const int32_t *m,
                    void *cache, int64_t cache_blocks, void *stream);
 
 /*
- * ptstore_lookup followed by ptstore_gather of its result, enqueued
- * back to back on `stream` (the measured hot path). m and ids are written
- * as by ptstore_lookup. Errors: those of either call.
+ * The hot path of a prefix-cache hit: the LCP query, then the load of the
+ * matched prefix's tensors into the caller's paged cache (Section 4.1: a
+ * load finds the longest stored prefix and iterates over its ids; Section 5:
+ * the client issues an LCP query, then reads the tensors it names).
+ * ptstore_lookup followed by ptstore_gather of its result, enqueued back to
+ * back on `stream`. m and ids are written as by ptstore_lookup.
+ * Errors: those of either call.
  */
 int ptstore_lookup_gather(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
                           int64_t n_tokens, int32_t R, int32_t max_blocks,
                           int32_t *m, int32_t *ids, const int32_t *block_table,
                           void *cache, int64_t cache_blocks, void *stream);
+
+/* ======================================================================
+ * The store of an increment (Sections 1 and 4; Section 4.1)
+ * ====================================================================== */
+
+/*
+ * Store (Sections 1 and 4): with the same result as taking the requests one
+ * after another, each request reuses the stored blocks of its longest
+ * common prefix (including blocks created by earlier requests of this
+ * batch) and creates one new block per missing block, ids handed out
+ * densely in (request, block) order. Once the store holds `capacity`
+ * blocks nothing more is created (with PTSTORE_FLAG_EVICT: once no block can
+ * be evicted, see there); a request then keeps only the blocks it
+ * could reuse or create (the cut is always a prefix), full_events is
+ * incremented and ptstore_insert_sync would return PTSTORE_ERR_FULL. With
+ * PTSTORE_FLAG_EVICT, after the evictions every block on each request's
+ * resident path counts one access. Outputs: m_out [R] = blocks of r
+ * resident after the call;
+ * ids [R][max_blocks] their ids (-1 beyond m_out); created [R][max_blocks]
+ * = 1 exactly where request r created the block (a block shared by several
+ * requests of the batch is created by the first of them).
+ * Uses store-owned scratch sized for R * max_blocks, grown on demand (the
+ * growth waits for `stream`). Errors as ptstore_lookup, plus NOMEM.
+ */
+int ptstore_insert(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                   int64_t n_tokens, int32_t R, int32_t max_blocks,
+                   int32_t *m_out, int32_t *ids, uint8_t *created, void *stream);
+
+/*
+ * ptstore_insert, then wait for `stream` and report whether that insert
+ * refused blocks for lack of room (the capacity cut of ptstore_insert;
+ * with PTSTORE_FLAG_EVICT, blocks left after every possible eviction).
+ * Returns PTSTORE_ERR_FULL in that case, with every output written as
+ * ptstore_insert writes it (the cut is a prefix of each request, the same
+ * as the one-after-another insert gives), else PTSTORE_OK.
+ * Errors: those of ptstore_insert, HIP.
+ */
+int ptstore_insert_sync(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                        int64_t n_tokens, int32_t R, int32_t max_blocks,
+                        int32_t *m_out, int32_t *ids, uint8_t *created, void *stream);
+
+/*
+ * Store the tensors of new blocks (Section 4: a store saves only the
+ * increment beyond the longest common prefix; Section 4.1: the application
+ * supplies pointers to the GPU memory holding the tensors of the object to
+ * store): for every (r, b) with created[r][b] != 0 and block_table[r][b] >= 0,
+ * copy each chunk of cache[layer][K|V][block_table[r][b]] into pool block
+ * ids[r][b] (its home row: device pool or host tier). Out-of-range ids /
+ * cache blocks are skipped and counted in bad_entries. Uses the same
+ * store-owned descriptor scratch as ptstore_gather. Errors as ptstore_gather.
+ */
+int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created,
+                    const int32_t *block_table, int32_t R, int32_t max_blocks,
+                    const void *cache, int64_t cache_blocks, void *stream);
+
+/* ======================================================================
+ * Layer granularity (Section 4.1: transfers overlap computation;
+ * Section 5: subsets of tensors, tensors of variable sizes)
+ * ====================================================================== */
 
 /*
  * Load of a range of layers (Section 4.1: transfers overlap computation;
@@ -265,36 +340,20 @@ int ptstore_gather_prepared(ptstore_t *store, int32_t layer_begin, int32_t layer
                             int64_t cache_blocks, void *stream);
 
 /*
- * Store (Sections 1 and 4): with the same result as taking the requests one
- * after another, each request reuses the stored blocks of its longest
- * common prefix (including blocks created by earlier requests of this
- * batch) and creates one new block per missing block, ids handed out
- * densely in (request, block) order. Once the store holds `capacity`
- * blocks nothing more is created (with PTSTORE_FLAG_EVICT: once no block can
- * be evicted, see there); a request then keeps only the blocks it
- * could reuse or create (the cut is always a prefix) and full_events is
- * incremented. With PTSTORE_FLAG_EVICT, after the evictions every block on
- * each request's resident path counts one access. Outputs: m_out [R] = blocks of r resident after the call;
- * ids [R][max_blocks] their ids (-1 beyond m_out); created [R][max_blocks]
- * = 1 exactly where request r created the block (a block shared by several
- * requests of the batch is created by the first of them).
- * Uses store-owned scratch sized for R * max_blocks, grown on demand (the
- * growth waits for `stream`). Errors as ptstore_lookup, plus NOMEM.
+ * Store the tensors of a range of layers of new blocks (a prefill can hand
+ * each layer's KV to the store as soon as it is computed): as
+ * ptstore_scatter, but only layers layer_begin .. layer_end-1. Errors as
+ * ptstore_scatter, plus INVALID for a bad range. A block's replica, if any,
+ * is dropped as by ptstore_scatter.
  */
-int ptstore_insert(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
-                   int64_t n_tokens, int32_t R, int32_t max_blocks,
-                   int32_t *m_out, int32_t *ids, uint8_t *created, void *stream);
+int ptstore_scatter_layers(ptstore_t *store, const int32_t *ids, const uint8_t *created,
+                           const int32_t *block_table, int32_t R, int32_t max_blocks,
+                           int32_t layer_begin, int32_t layer_end, const void *cache,
+                           int64_t cache_blocks, void *stream);
 
-/*
- * Store the tensors of new blocks: for every (r, b) with created[r][b] != 0
- * and block_table[r][b] >= 0, copy each chunk of
- * cache[layer][K|V][block_table[r][b]] into pool block ids[r][b].
- * Out-of-range ids / cache blocks are skipped and counted in bad_entries.
- * Errors as ptstore_gather.
- */
-int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created,
-                    const int32_t *block_table, int32_t R, int32_t max_blocks,
-                    const void *cache, int64_t cache_blocks, void *stream);
+/* ======================================================================
+ * Tiers and replication (Section 4.1)
+ * ====================================================================== */
 
 /*
  * Replication of popular prefixes (Section 4.1): make the device replica
@@ -308,21 +367,56 @@ int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created
  */
 int ptstore_replicate(ptstore_t *store, void *stream);
 
-/*
- * Store the tensors of a range of layers of new blocks (a prefill can hand
- * each layer's KV to the store as soon as it is computed): as
- * ptstore_scatter, but only layers layer_begin .. layer_end-1. Errors as
- * ptstore_scatter, plus INVALID for a bad range. A block's replica, if any,
- * is dropped as by ptstore_scatter.
- */
-int ptstore_scatter_layers(ptstore_t *store, const int32_t *ids, const uint8_t *created,
-                           const int32_t *block_table, int32_t R, int32_t max_blocks,
-                           int32_t layer_begin, int32_t layer_end, const void *cache,
-                           int64_t cache_blocks, void *stream);
+/* ======================================================================
+ * Status
+ * ====================================================================== */
 
-/* Wait for the device and read the store's counters into *stats.
- * Errors: INVALID (a NULL argument), HIP. */
+/*
+ * Wait for the device and read the store's counters into *stats: what it
+ * holds, and the conditions only the device sees while running the calls
+ * above (blocks refused for lack of room, the Section 4.1 capacity limit;
+ * skipped malformed entries; evictions and the eviction clock of Section 4.1's
+ * access-pattern-aware policy; replicas). Errors: INVALID (a NULL argument),
+ * HIP.
+ */
 int ptstore_stats(ptstore_t *store, ptstore_stats_t *stats);
+
+/* Human-readable text for a return code. */
+const char *ptstore_strerror(int code);
+
+/* Text of the last error on this host thread ("" if none). */
+const char *ptstore_last_error(void);
+
+/* ======================================================================
+ * Allocation-free variant (for callers that cannot allocate)
+ * ====================================================================== */
+
+/*
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, kernels and results as ptstore_lookup_gather, but the
+ * gather's descriptor list lives in a static device array of the library
+ * (about 20 MiB per device, held until the process ends) instead of
+ * store-owned scratch. The call allocates nothing, frees nothing, creates
+ * no event and never waits; it records no ptstore_kernel_times() entries
+ * and leaves a list made by ptstore_gather_prepare intact.
+ * Limit: R * max_blocks <= PTSTORE_NOALLOC_MAX_ENTRIES, else INVALID before
+ * any work is enqueued. Every such call on one device shares that device's
+ * array, whichever store it names: calls that overlap in time on one device
+ * (other streams, other threads) race and must be ordered by the caller.
+ * Errors: those of ptstore_lookup_gather (NOMEM excepted), plus INVALID for
+ * a batch over the limit or a device index of 64 or more.
+ */
+enum { PTSTORE_NOALLOC_MAX_ENTRIES = 1048576 /* 2^20 (request, block) entries */ };
+int ptstore_lookup_gather_noalloc(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
+                                  int64_t n_tokens, int32_t R, int32_t max_blocks,
+                                  int32_t *m, int32_t *ids, const int32_t *block_table,
+                                  void *cache, int64_t cache_blocks, void *stream);
+
+/* ======================================================================
+ * Tuning and diagnostics: not store operations. Counters, timing, the
+ * store's buffers for tests, copy launch shapes, and a bandwidth probe.
+ * ====================================================================== */
 
 /* Zero the event counters (probes, compares, CAS, full_events, bad_entries,
  * insert_fallbacks, index_rebuilds); blocks_stored, evictions and the clock
@@ -385,36 +479,6 @@ int ptstore_set_copy_shape(ptstore_t *store, int32_t chunks_per_group, int32_t t
  * multiple of 16, at most 32 GiB. Errors: INVALID, HIP.
  */
 int ptstore_bandwidth_probe(int32_t kind, const void *a, void *b, int64_t bytes, void *stream);
-
-/*
- * Allocation-free lookup + gather
- * -------------------------------
- * For callers that cannot allocate device memory: code under HIP graph
- * capture, tight serving loops, harnesses that forbid hipMalloc.
- * Same arguments, kernels and results as ptstore_lookup_gather, but the
- * gather's descriptor list lives in a static device array of the library
- * (about 20 MiB per device, held until the process ends) instead of
- * store-owned scratch. The call allocates nothing, frees nothing, creates
- * no event and never waits; it records no ptstore_kernel_times() entries
- * and leaves a list made by ptstore_gather_prepare intact.
- * Limit: R * max_blocks <= PTSTORE_NOALLOC_MAX_ENTRIES, else INVALID before
- * any work is enqueued. Every such call on one device shares that device's
- * array, whichever store it names: calls that overlap in time on one device
- * (other streams, other threads) race and must be ordered by the caller.
- * Errors: those of ptstore_lookup_gather (NOMEM excepted), plus INVALID for
- * a batch over the limit or a device index of 64 or more.
- */
-enum { PTSTORE_NOALLOC_MAX_ENTRIES = 1048576 /* 2^20 (request, block) entries */ };
-int ptstore_lookup_gather_noalloc(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
-                                  int64_t n_tokens, int32_t R, int32_t max_blocks,
-                                  int32_t *m, int32_t *ids, const int32_t *block_table,
-                                  void *cache, int64_t cache_blocks, void *stream);
-
-/* Human-readable text for a return code. */
-const char *ptstore_strerror(int code);
-
-/* Text of the last error on this host thread ("" if none). */
-const char *ptstore_last_error(void);
 
 #ifdef __cplusplus
 }

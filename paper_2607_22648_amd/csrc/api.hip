@@ -519,7 +519,6 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
         }
         carve_evict(s->ev_mem, s->capacity, &s->evs);
         s->evs.on = 1;
-        s->evs.epoch = 0;
     }
     s->evs.tier = s->tier;
     HashTables h;
@@ -742,10 +741,6 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     insert_scratch_carve(s->insert_scratch, R, max_blocks, &sc);
     InsertTarget tgt{s->slots, s->parent, s->tokens, s->capacity};
     Batch b{tokens, offsets, n_tokens, R, max_blocks};
-    if (s->evs.on) {
-        // protection marks are compared with the epoch; 0 marks nothing
-        if (++s->evs.epoch == 0x7FFFFFFF) s->evs.epoch = 1;
-    }
     {
         Timed t(s, 3, st);
         const IndexView ix = index_view(s);
@@ -757,6 +752,23 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
         if (e == hipSuccess) e = launch_insert_commit(ix, tgt, s->evs, b, sc, m_out, ids, created, st);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_insert: launch", e);
+}
+
+int ptstore_insert_sync(ptstore_t* s, const int32_t* tokens, const int64_t* offsets,
+                        int64_t n_tokens, int32_t R, int32_t max_blocks, int32_t* m_out,
+                        int32_t* ids, uint8_t* created, void* stream) {
+    const int rc = ptstore_insert(s, tokens, offsets, n_tokens, R, max_blocks, m_out, ids, created,
+                                  stream);
+    if (rc || R == 0) return rc;
+    DeviceScope dev(s);
+    if (dev.rc) return dev.rc;
+    hipStream_t st = (hipStream_t)stream;
+    unsigned long long full = 0;
+    hipError_t e = hipMemcpyAsync(&full, &s->state->insert_full, sizeof full, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, "ptstore_insert_sync: status", e);
+    return full ? fail(PTSTORE_ERR_FULL, "ptstore_insert_sync: blocks refused for lack of room")
+                : PTSTORE_OK;
 }
 
 int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* created,
@@ -887,6 +899,8 @@ int ptstore_reset_counters(ptstore_t* s) {
         keep.tombstones = st.tombstones;
         keep.rep_count = st.rep_count;
         keep.rep_copies = st.rep_copies;
+        keep.ev_epoch = st.ev_epoch;  // protection marks are compared with it
+        keep.insert_full = st.insert_full;
         e = hipMemcpy(s->state, &keep, sizeof keep, hipMemcpyHostToDevice);
     }
     return e == hipSuccess ? PTSTORE_OK : fail(PTSTORE_ERR_HIP, "ptstore_reset_counters", e);

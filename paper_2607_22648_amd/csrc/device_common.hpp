@@ -70,6 +70,9 @@ struct DevState {
     unsigned long long evictions;
     unsigned long long tombstones;    // upper bound on deleted index slots
     unsigned long long rebuilds;
+    unsigned long long ev_epoch;      // protection mark of the running insert (>= 1),
+                                      // advanced by the insert's first kernel
+    unsigned long long insert_full;   // 1: the last insert refused blocks for lack of room
     // eviction (scratch of the running insert)
     unsigned long long ev_new;        // distinct new blocks the batch needs
     unsigned long long ev_want;       // blocks to evict

@@ -43,7 +43,7 @@ __device__ inline unsigned bit_width(uint64_t x) { return x ? 64u - (unsigned)__
 
 // Is `id` ranked by the running search? (sel_lo_id <= id < sel_hi_id holds.)
 __device__ inline bool sel_candidate(const EvictView& ev, const DevState* st, int64_t id) {
-    return st->sel_hot || ev.prot[id] != ev.epoch;
+    return st->sel_hot || ev.prot[id] != (int32_t)st->ev_epoch;
 }
 
 // The candidate's compressed key, left-aligned in 128 bits (state written by
@@ -221,11 +221,12 @@ __global__ __launch_bounds__(kThreads) void k_ev_mark(EvictView ev, DevState* st
     const u128 thr = ((u128)st->sel_hi << 64) | (u128)st->sel_lo;
     const int64_t old = (int64_t)st->insert_old_count;
     const int64_t span = ev.words * kWave;
+    const int32_t epoch = (int32_t)st->ev_epoch;
     uint64_t maxp = 0;
     for (int64_t base = (int64_t)blockIdx.x * kThreads; base < span; base += (int64_t)gridDim.x * kThreads) {
         const int64_t id = base + threadIdx.x;
         bool sel = false;
-        if (id < old && ev.prot[id] != ev.epoch) {
+        if (id < old && ev.prot[id] != epoch) {
             sel = all || sel_key(ev, st, id) <= thr;
             if (sel) {
                 const uint64_t hp = ev.prio[id];
@@ -291,7 +292,10 @@ __global__ __launch_bounds__(1024) void k_ev_scan(EvictView ev, DevState* st, in
         const unsigned long long fresh = (unsigned long long)capacity - st->insert_old_count;
         st->ev_nv = nv;
         st->evictions += nv;
-        if (st->ev_new > fresh + nv) st->full_events += 1;
+        if (st->ev_new > fresh + nv) {
+            st->full_events += 1;
+            st->insert_full = 1;
+        }
         const unsigned long long tomb = st->tombstones + nv;
         if (tomb * 4 > slots_n) {
             st->ev_rebuild = 1;

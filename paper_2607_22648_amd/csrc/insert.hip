@@ -66,10 +66,18 @@ __device__ inline unsigned long long lanes_below(int lane) {
 
 // Clears the batch table. The first clear of an insert (only_if_collision =
 // 0) also lowers the collision flag; the second runs only if it was raised.
+// The insert's first kernel (only_if_collision = 0) also advances the
+// eviction epoch, so that a replayed capture marks its own matches.
 __global__ void k_table_clear(BatchEntry* __restrict__ t, uint64_t n, unsigned int* collision,
-                              int only_if_collision) {
+                              int only_if_collision, DevState* st, int ev_on) {
     if (only_if_collision && *collision == 0) return;
-    if (!only_if_collision && blockIdx.x == 0 && threadIdx.x == 0) *collision = 0;
+    if (!only_if_collision && blockIdx.x == 0 && threadIdx.x == 0) {
+        *collision = 0;
+        if (ev_on) {  // protection marks are compared with it; 0 marks nothing
+            const unsigned long long e = st->ev_epoch + 1;
+            st->ev_epoch = e >= 0x7FFFFFFFull ? 1ull : e;
+        }
+    }
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (uint64_t)gridDim.x * blockDim.x) {
         BatchEntry e;
@@ -236,8 +244,10 @@ __global__ __launch_bounds__(kThreads) void k_count(InsertArgs a) {
     int64_t o0;
     const int32_t n = n_blocks(a.bat, r, a.ix.block_tokens, &o0);
     const BatchEntry* __restrict__ tab = reinterpret_cast<const BatchEntry*>(a.sc.table);
-    if (a.ev.on)  // the blocks this request matched cannot be evicted by this insert
-        for (int32_t b = lane; b < a.sc.m0[r]; b += kWave) a.ev.prot[a.ids[r * maxb + b]] = a.ev.epoch;
+    if (a.ev.on) {  // the blocks this request matched cannot be evicted by this insert
+        const int32_t epoch = (int32_t)a.ix.state->ev_epoch;
+        for (int32_t b = lane; b < a.sc.m0[r]; b += kWave) a.ev.prot[a.ids[r * maxb + b]] = epoch;
+    }
     int32_t c = 0;
     for (int32_t w0 = a.sc.m0[r]; w0 < n; w0 += kWave) {
         const int32_t b = w0 + lane;
@@ -277,8 +287,12 @@ __global__ __launch_bounds__(1024) void k_scan(InsertArgs a) {
         const long long old = (long long)st->count;
         const long long cap = a.tgt.capacity;
         st->insert_old_count = (unsigned long long)old;
+        st->insert_full = 0;
         if (old + total > cap) {
-            if (!a.ev.on) st->full_events += 1;  // with eviction: decided once victims are known
+            if (!a.ev.on) {  // with eviction: decided once victims are known
+                st->full_events += 1;
+                st->insert_full = 1;
+            }
             st->count = (unsigned long long)cap;
         } else {
             st->count = (unsigned long long)(old + total);
@@ -471,13 +485,15 @@ hipError_t launch_insert_match(const IndexView& ix, const InsertTarget& tgt, con
     InsertArgs a{quiet, tgt, ev, b, sc, m_out, ids, created};
     const unsigned wgrid = (unsigned)((b.R + kWaves - 1) / kWaves);      // wave per request
     const unsigned tgrid = (unsigned)((b.R + kThreads - 1) / kThreads);  // thread per request
-    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 0);
+    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 0,
+                       ix.state, ev.on);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_claim, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_verify, dim3(wgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 1);
+    hipLaunchKernelGGL(k_table_clear, dim3(cgrid), dim3(kThreads), 0, s, table, tn, sc.collision, 1,
+                       ix.state, 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_claim_exact, dim3(tgrid), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -56,7 +56,8 @@ struct EvictView {
     uint64_t* freq;     // [capacity] F
     uint64_t* prio;     // [capacity] H
     int32_t* live;      // [capacity] children that hold an id
-    int32_t* prot;      // [capacity] last insert epoch whose batch matched the block
+    int32_t* prot;      // [capacity] last insert epoch (DevState::ev_epoch) whose batch
+                        // matched the block
     int32_t* depth;     // [capacity] 0 for a child of the root
     uint64_t* nkey;     // [capacity] index key, to rebuild the index
     uint32_t* spos;     // [capacity] index slot, to delete the entry
@@ -67,7 +68,6 @@ struct EvictView {
     uint32_t* hist;     // [kSelPasses][kSelBins] digit histograms
     uint64_t* part;     // [kSelGroups][8] per-workgroup partials of the range pass
     int64_t words;      // ceil(capacity / 64)
-    int32_t epoch;      // of the running insert, >= 1
     int32_t on;         // 0: eviction disabled, nothing here is touched
     TierView tier;      // an evicted host-tier block loses its replica
 };

@@ -62,7 +62,8 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_set_copy_shape", "ptstore_strerror", "ptstore_last_error",
            "ptstore_bandwidth_probe", "ptstore_replicate", "ptstore_gather_layers",
            "ptstore_scatter_layers", "ptstore_gather_prepare", "ptstore_gather_prepared",
-           "ptstore_set_counters", "ptstore_set_timing", "ptstore_lookup_gather_noalloc")
+           "ptstore_set_counters", "ptstore_set_timing", "ptstore_lookup_gather_noalloc",
+           "ptstore_insert_sync")
 
 
 def _load() -> C.CDLL:
@@ -79,6 +80,7 @@ def _load() -> C.CDLL:
         "ptstore_lookup_gather": [p, p, p, i64, i32, i32, p, p, p, p, i64, p],
         "ptstore_lookup_gather_noalloc": [p, p, p, i64, i32, i32, p, p, p, p, i64, p],
         "ptstore_insert": [p, p, p, i64, i32, i32, p, p, p, p],
+        "ptstore_insert_sync": [p, p, p, i64, i32, i32, p, p, p, p],
         "ptstore_scatter": [p, p, p, p, i32, i32, p, i64, p],
         "ptstore_stats": [p, C.POINTER(ptstore_stats_t)],
         "ptstore_reset_counters": [p],
@@ -274,6 +276,22 @@ def ptstore_insert(h, tokens, offsets, max_blocks, m_out, ids, created, stream=N
         _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"), _stream(stream)))
 
 
+def ptstore_insert_sync(h, tokens, offsets, max_blocks, m_out, ids, created, stream=None) -> int:
+    """Returns PTSTORE_OK, or PTSTORE_ERR_FULL when the insert refused blocks
+    (its outputs are written either way); raises on any other error."""
+    R = _requests(offsets)
+    _need(m_out, R, "m_out")
+    _need(ids, R * max_blocks, "ids")
+    _need(created, R * max_blocks, "created")
+    rc = _lib.ptstore_insert_sync(
+        h, _dev(tokens, torch.int32, "tokens"), _dev(offsets, torch.int64, "offsets"),
+        tokens.numel(), R, max_blocks, _dev(m_out, torch.int32, "m_out"),
+        _dev(ids, torch.int32, "ids"), _dev(created, torch.uint8, "created"), _stream(stream))
+    if rc != PTSTORE_ERR_FULL:
+        _check("ptstore_insert_sync", rc)
+    return rc
+
+
 def ptstore_scatter(h, ids, created, block_table, cache, cache_blocks, stream=None) -> None:
     R, maxb = _rows(ids)
     _need(created, R * maxb, "created")
@@ -439,6 +457,16 @@ class PrefixStore:
         created = torch.empty((R, max_blocks), dtype=torch.uint8, device=dev)
         ptstore_insert(self.h, tokens, offsets, max_blocks, m, ids, created, stream)
         return m, ids, created
+
+    def insert_sync(self, tokens, offsets, max_blocks, stream=None):
+        """(rc, m, ids, created): rc is PTSTORE_OK or PTSTORE_ERR_FULL."""
+        R = offsets.numel() - 1
+        dev = offsets.device
+        m = torch.empty(R, dtype=torch.int32, device=dev)
+        ids = torch.empty((R, max_blocks), dtype=torch.int32, device=dev)
+        created = torch.empty((R, max_blocks), dtype=torch.uint8, device=dev)
+        rc = ptstore_insert_sync(self.h, tokens, offsets, max_blocks, m, ids, created, stream)
+        return rc, m, ids, created
 
     def gather_prepare(self, ids, m, block_table, cache, stream=None):
         """List once the blocks a gather of (ids, m, block_table) into `cache` moves."""

@@ -7,7 +7,10 @@
  *   insert  AB, ABC, ABD  -> ids A=0 B=1 C=2 D=3, 4 blocks stored
  *   lookup  ABD+CC        -> m=3, ids 0 1 3     (ABDC is not stored)
  *           BA            -> m=0                 (no root child B)
- * Every gathered byte must equal the byte scattered for that block.
+ * Every gathered byte must equal the byte scattered for that block. The
+ * allocation-free lookup + gather must give the same m, ids and bytes.
+ * A second store of 3 blocks refuses D: ptstore_insert_sync returns
+ * PTSTORE_ERR_FULL with m = 2 3 2, then PTSTORE_OK for AB alone.
  * Exit status 0 and "abi_demo ok" on success.
  */
 #include <hip/hip_runtime_api.h>
@@ -106,9 +109,42 @@ int main(void) {
                 for (int i = 0; i < CHUNK; ++i) CHECK(got[i] == 0xA5, "untouched bytes");
             }
         }
+    /* the allocation-free call on the same inputs, into a second cache */
+    void *dout2, *dqm2, *dqids2;
+    unsigned char *fill = malloc((size_t)QR * QMB * BLOCK);
+    memset(fill, 0xA5, (size_t)QR * QMB * BLOCK);
+    CHECK(!to_dev(&dout2, fill, (size_t)QR * QMB * BLOCK), "noalloc cache in");
+    CHECK(hipMalloc(&dqm2, QR * 4) == hipSuccess && hipMalloc(&dqids2, QR * QMB * 4) == hipSuccess,
+          "alloc noalloc outputs");
+    CHECK(ptstore_lookup_gather_noalloc(s, dq, dqo, 14, QR, QMB, dqm2, dqids2, dqbt, dout2, QR * QMB,
+                                        NULL) == PTSTORE_OK, "lookup_gather_noalloc");
+    CHECK(hipDeviceSynchronize() == hipSuccess, "sync 3");
+    int32_t qm2[2], qids2[10];
+    hipMemcpy(qm2, dqm2, sizeof qm2, hipMemcpyDeviceToHost);
+    hipMemcpy(qids2, dqids2, sizeof qids2, hipMemcpyDeviceToHost);
+    hipMemcpy(fill, dout2, (size_t)QR * QMB * BLOCK, hipMemcpyDeviceToHost);
+    CHECK(!memcmp(qm, qm2, sizeof qm) && !memcmp(qids, qids2, sizeof qids) &&
+          !memcmp(out, fill, (size_t)QR * QMB * BLOCK), "noalloc differs from lookup_gather");
+    CHECK(ptstore_lookup_gather_noalloc(s, dq, dqo, 14, QR, PTSTORE_NOALLOC_MAX_ENTRIES, dqm2, dqids2,
+                                        dqbt, dout2, QR * QMB, NULL) == PTSTORE_ERR_INVALID,
+          "noalloc over its limit");
+
     ptstore_stats_t st;
     CHECK(ptstore_stats(s, &st) == PTSTORE_OK && st.blocks_stored == 4 && st.bad_entries == 0, "stats");
     CHECK(ptstore_destroy(s) == PTSTORE_OK, "destroy");
+
+    /* a store of 3 blocks: D does not fit */
+    cfg.pool_blocks = 3;
+    CHECK(ptstore_create(&cfg, &s) == PTSTORE_OK, "create small");
+    CHECK(ptstore_insert_sync(s, dtok, doff, 16, R, MB, dm, dids, dcr, NULL) == PTSTORE_ERR_FULL,
+          "insert_sync on a full store");
+    hipMemcpy(m, dm, sizeof m, hipMemcpyDeviceToHost);
+    CHECK(m[0] == 2 && m[1] == 3 && m[2] == 2, "insert_sync m after the cut");
+    CHECK(ptstore_insert_sync(s, dtok, doff, 4, 1, MB, dm, dids, dcr, NULL) == PTSTORE_OK,
+          "insert_sync with nothing refused");
+    CHECK(ptstore_stats(s, &st) == PTSTORE_OK && st.blocks_stored == 3 && st.full_events == 1,
+          "stats of the small store");
+    CHECK(ptstore_destroy(s) == PTSTORE_OK, "destroy small");
     printf("abi_demo ok\n");
     return 0;
 }

@@ -29,7 +29,7 @@ def test_header_compiles_as_c_and_links():
 
 @pytest.mark.gpu
 def test_demo_runs_on_gpu():
-    exe = build_demo() if not os.path.exists(EXE) else EXE
+    exe = build_demo()  # always against the current header and library
     p = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert p.returncode == 0, p.stderr
     assert "abi_demo ok" in p.stdout

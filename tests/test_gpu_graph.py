@@ -143,3 +143,65 @@ def test_captured_insert_and_scatter_replays():
     t.check_meta()
     t.check_pool()
     t.close()
+
+
+def test_captured_evicting_insert_replays():
+    """With PTSTORE_FLAG_EVICT: an insert and a scatter captured once, replayed
+    on new batches with eager lookups (accesses) between the replays. Each
+    replay protects its own batch's matches (the epoch advances on the
+    device), so victims, ids, access counts, the clock and the pool follow
+    the oracle replay after replay."""
+    rng = np.random.default_rng(47)
+    bt_, R, maxb = 4, 8, 6
+    t = Twin(2, 1, 8, bt_, 60, flags=P.PTSTORE_FLAG_EVICT)
+    atoms = _atoms(rng, 6, bt_, 300)
+
+    def batch():
+        return atoms[rng.integers(0, 6, size=(R, maxb))].reshape(-1).astype(np.int32)
+
+    offs = (np.arange(R + 1, dtype=np.int64) * maxb * bt_)
+    oo = to_dev(offs)
+    tt = to_dev(batch())
+    bt_np = block_table_identity(R, maxb)
+    bt = to_dev(bt_np)
+    n = R * maxb * t.shape.block_bytes
+    cache = torch.empty(n, dtype=torch.uint8, device="cuda")
+    m = torch.empty(R, dtype=torch.int32, device="cuda")
+    ids = torch.empty((R, maxb), dtype=torch.int32, device="cuda")
+    cr = torch.empty((R, maxb), dtype=torch.uint8, device="cuda")
+
+    def eager_twin_step(toks, seed):
+        cache.copy_(random_bytes(n, seed))
+        rc, rm, rids, rcr = t.ref.insert(toks, offs, maxb)
+        t.ref.scatter(rids, rcr, bt_np, host(cache), R * maxb)
+        return rm, rids, rcr
+
+    toks0 = host(tt)
+    rm, rids, rcr = eager_twin_step(toks0, 300)
+    P.ptstore_insert(t.gpu.h, tt, oo, maxb, m, ids, cr)
+    P.ptstore_scatter(t.gpu.h, ids, cr, bt, cache, R * maxb)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(ids), rids)
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        P.ptstore_insert(t.gpu.h, tt, oo, maxb, m, ids, cr)
+        P.ptstore_scatter(t.gpu.h, ids, cr, bt, cache, R * maxb)
+    torch.cuda.synchronize()
+    for rep in range(6):
+        # eager lookups between replays count accesses on both sides
+        lt, lo = random_block_batch(rng, 6, atoms, maxb, tail_p=0.2)
+        t.lookup(lt, lo, maxb)
+        toks = batch()
+        tt.copy_(to_dev(toks))
+        rm, rids, rcr = eager_twin_step(toks, 400 + rep)
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(m), rm, err_msg=f"replay {rep}: m")
+        np.testing.assert_array_equal(host(ids), rids, err_msg=f"replay {rep}: ids")
+        np.testing.assert_array_equal(host(cr), rcr, err_msg=f"replay {rep}: created")
+        t.check_evict()
+    assert t.gpu.stats()["evictions"] > 0
+    t.check_meta()
+    t.check_pool()
+    t.close()

@@ -558,3 +558,26 @@ def test_batch_at_the_size_limit():
     ]
     assert all(rc == P.PTSTORE_ERR_INVALID for rc in over), over
     t.close()
+
+
+@pytest.mark.parametrize("evict", [False, True])
+def test_insert_sync_reports_refused_blocks(evict):
+    """ptstore_insert_sync returns PTSTORE_ERR_FULL exactly when the oracle's
+    insert refused blocks, with the same outputs either way."""
+    from oracle import ORC_ERR_FULL
+    rng = np.random.default_rng(71 + evict)
+    atoms = _atoms(rng, 5, 4, 50)
+    t = Twin(1, 1, 8, 4, 30, flags=P.PTSTORE_FLAG_EVICT if evict else 0)
+    codes = set()
+    for i in range(10):  # small and large batches taking turns
+        toks, offs = random_block_batch(rng, 10 if i % 2 else 2, atoms, 9)
+        rc, m, ids, cr = t.gpu.insert_sync(to_dev(toks), to_dev(offs), 9)
+        orc, rm, rids, rcr = t.ref.insert(toks, offs, 9)
+        assert (rc == P.PTSTORE_ERR_FULL) == (orc == ORC_ERR_FULL), (rc, orc)
+        np.testing.assert_array_equal(host(m), rm)
+        np.testing.assert_array_equal(host(ids), rids)
+        np.testing.assert_array_equal(host(cr), rcr)
+        codes.add(rc)
+    assert codes == {P.PTSTORE_OK, P.PTSTORE_ERR_FULL}
+    assert t.gpu.stats()["blocks_stored"] == t.ref.count
+    t.close()
