@@ -66,9 +66,11 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def recorded_traffic(config: str):
-    """HBM bytes per gather launch from the committed rocprofv3 counter record,
-    or None if there is none for this workload or the copy kernel changed since."""
+def recorded_traffic(config: str, bytes_per_launch: float):
+    """HBM bytes per gather launch from the committed rocprofv3 counter record
+    (its measured traffic over algorithmic bytes, times this run's
+    algorithmic bytes per launch), or None if there is none for this workload
+    or the copy kernel changed since."""
     from paper_2607_22648_amd.profile_summary import copy_source_sha
     path = os.path.join(ROOT, "profiles", f"gather_{config}_traffic.json")
     if not os.path.exists(path):
@@ -76,7 +78,7 @@ def recorded_traffic(config: str):
     rec = json.load(open(path))
     if rec.get("copy_hip_sha256") != copy_source_sha():
         return None
-    return rec["traffic_bytes_per_launch"]
+    return int(round(rec["traffic_over_algorithmic"] * bytes_per_launch))
 
 
 def prefill(store, w, dev, torch, batch_passages: int):
@@ -405,9 +407,16 @@ def run_passage(args, torch, P, synth, dev):
                              else "k_copy_spans<true> (gather)",
                              gather_bytes_step * args.steps / max(g_n, 1),
                              g_ms / max(g_n, 1), g_n,
-                             None if args.per_layer else recorded_traffic(args.config), ceiling),
+                             None if args.per_layer else
+                             recorded_traffic(args.config, gather_bytes_step * args.steps / max(g_n, 1)),
+                             ceiling),
         "lookup_kernel_avg_ms": round(l_ms / max(l_n, 1), 4),
         "gather_after_cache_flush": flushed,
+        # every gather dispatch of this process (warm-up, timed and flushed
+        # steps, each step the same blocks), for the rocprofv3 traffic record
+        "gather_all": None if args.per_layer else {
+            "dispatches": (args.warmup + args.steps + (args.steps if flushed else 0)) * len(subs),
+            "bytes": (args.warmup + args.steps + (args.steps if flushed else 0)) * gather_bytes_step},
         "hbm_ceiling": ceiling,
         "prefill": pre,
         "cpu_baseline": cpu,
@@ -638,6 +647,8 @@ def run_trie(args, torch, P, synth, dev):
     torch.cuda.synchronize()
     fu_elapsed = time.perf_counter() - t0
     g_ms, g_n = store.kernel_times(P.KIND_GATHER)
+    nb = min(cache.numel(), int(stt["blocks_stored"]) * sh.block_bytes, 16 << 30) // 16 * 16
+    ceiling = hbm_ceiling(torch, P, store.pool_tensor(), cache, nb)
     store.close()
     del cache
     torch.cuda.empty_cache()
@@ -678,7 +689,10 @@ def run_trie(args, torch, P, synth, dev):
                                                   / (lk_avg * 1e6), 1)},
         "matched_blocks": matched,
         "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
-                             g_n, recorded_traffic("trie")),
+                             g_n, recorded_traffic("trie", matched * 2 * sh.block_bytes), ceiling),
+        "hbm_ceiling": ceiling,
+        "gather_all": {"dispatches": args.warmup + args.steps,
+                       "bytes": (args.warmup + args.steps) * matched * 2 * sh.block_bytes},
         "prefill": {"insert_ms": round(ins_ms, 3), "insert_calls": ins_n,
                     "scatter_ms": round(sc_ms, 3), "blocks": created_total},
         "cpu_baseline": cpu,
@@ -710,18 +724,16 @@ def run_stream(args, torch, P, synth, dev):
               for r in sw.rounds]
     n_timed = min(args.steps, len(rounds) - args.warmup)
 
-    def one_round(i, count):
+    def one_round(i):
         lt, lo, it, io = rounds[i]
         store.lookup_gather(lt, lo, maxb, bt, cache, m=m, ids=ids)
         _, iids, icr = store.insert(it, io, maxb)
         store.scatter(iids, icr, bt[:io.numel() - 1], cache)
-        if count:
-            return m, icr
-        return None
+        return m.sum(), icr
 
-    for i in range(args.warmup):
-        one_round(i, False)
+    warm = [one_round(i)[0] for i in range(args.warmup)]
     torch.cuda.synchronize()
+    matched_warm = int(sum(int(x.item()) for x in warm))
     for k in (P.KIND_GATHER, P.KIND_LOOKUP, P.KIND_INSERT, P.KIND_SCATTER, P.KIND_EVICT):
         store.kernel_times(k)
     blocks0 = store.stats()["blocks_stored"]
@@ -730,8 +742,8 @@ def run_stream(args, torch, P, synth, dev):
     keep = []
     t0 = time.perf_counter()
     for i in range(args.warmup, args.warmup + n_timed):
-        mm, cr = one_round(i, True)
-        keep.append((mm.sum(), cr.to(torch.int64).sum()))
+        ms, cr = one_round(i)
+        keep.append((ms, cr.to(torch.int64).sum()))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     matched = int(sum(int(a.item()) for a, _ in keep))
@@ -740,6 +752,8 @@ def run_stream(args, torch, P, synth, dev):
              ("scatter", P.KIND_SCATTER)] + ([("evict (part of insert)", P.KIND_EVICT)] if evict else [])
     t = {k: store.kernel_times(v) for k, v in kinds}
     st = store.stats()
+    nb = min(cache.numel(), st["blocks_stored"] * sh.block_bytes, 16 << 30) // 16 * 16
+    ceiling = hbm_ceiling(torch, P, store.pool_tensor(), cache, nb)
     store.close()
     del cache
     torch.cuda.empty_cache()
@@ -754,7 +768,12 @@ def run_stream(args, torch, P, synth, dev):
         "matched_blocks": matched, "created_blocks": created,
         "blocks_stored": {"before": blocks0, "after": st["blocks_stored"]},
         "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
-                             g_ms / max(g_n, 1), g_n, recorded_traffic(args.config)),
+                             g_ms / max(g_n, 1), g_n,
+                             recorded_traffic(args.config, matched * 2 * sh.block_bytes / max(g_n, 1)),
+                             ceiling),
+        "hbm_ceiling": ceiling,
+        "gather_all": {"dispatches": args.warmup + n_timed,
+                       "bytes": (matched_warm + matched) * 2 * sh.block_bytes},
         "evictions": st["evictions"], "index_rebuilds": st["index_rebuilds"],
         "full_events": st["full_events"],
         "library_counters": {

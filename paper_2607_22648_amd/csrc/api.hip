@@ -112,11 +112,20 @@ void make_hash_tables(uint64_t seed, bool weak, bool weak_tag, HashTables* h) {
         h->pow_lane[j] = x;  // P^(j+1)
         x = host_mulmod61(x, P);
     }
-    uint64_t y = P;
-    for (int t = 0; t < 6; ++t) {
-        h->pow_step[t] = y;  // P^(2^t)
-        y = host_mulmod61(y, y);
+    // P^-1 = P^(p-2) (Fermat; p = 2^61-1 is prime)
+    uint64_t pinv = 1, base = P;
+    for (uint64_t e = kM61 - 2; e; e >>= 1) {
+        if (e & 1) pinv = host_mulmod61(pinv, base);
+        base = host_mulmod61(base, base);
     }
+    uint64_t a = 1, b = 1;
+    for (int j = 0; j < kWave; ++j) {
+        h->pow0[j] = a;     // P^j
+        h->inv_pow[j] = b;  // P^-j
+        a = host_mulmod61(a, P);
+        b = host_mulmod61(b, pinv);
+    }
+    h->p = P;
     h->root_key = mod61(mix64(seed ^ 0x9E3779B97F4A7C15ull));
     h->content_seed = mix64(seed ^ 0xD6E8FEB86659FD93ull);
     h->slot_seed = mix64(seed ^ 0xA0761D6478BD642Full);

@@ -31,7 +31,9 @@ struct alignas(16) Slot {
 // Per-store constants of the key chain, in device memory.
 struct HashTables {
     uint64_t pow_lane[kWave];  // P^(j+1), j = 0..63
-    uint64_t pow_step[6];      // P^(2^t), t = 0..5
+    uint64_t pow0[kWave];      // P^j
+    uint64_t inv_pow[kWave];   // P^-j (mod 2^61-1)
+    uint64_t p;                // P
     uint64_t root_key;         // k_{-1}
     uint64_t content_seed;
     uint64_t slot_seed;
@@ -120,27 +122,36 @@ __device__ inline uint64_t mulmod61(uint64_t a, uint64_t b) {
 
 __device__ inline uint64_t addmod61(uint64_t a, uint64_t b) { return mod61(a + b); }
 
-// Content hash of one block of BT tokens (BT words read from `blk`).
-template <int BT>
-__device__ inline uint64_t content_hash_regs(const int32_t (&t)[BT], uint64_t seed) {
-    uint64_t h = seed ^ (0x9E3779B97F4A7C15ull * BT);
-#pragma unroll
-    for (int i = 0; i < BT; i += 2) {
-        uint64_t w = (uint64_t)(uint32_t)t[i];
-        if (i + 1 < BT) w |= (uint64_t)(uint32_t)t[i + 1] << 32;
-        h = mix64(h ^ (w + 0x632BE59BD9B4E019ull * (uint64_t)(i + 1)));
-    }
-    return mod61(mix64(h));
+// Content hash of one block of bt tokens: tokens are taken in pairs (i, i+1)
+// (the last one alone when bt is odd), each pair mixed into the state; the
+// result is reduced mod 2^61-1. The three steps below are the only
+// definition, so every caller (whole block in registers, streamed from LDS,
+// read from memory) gets the same value.
+__device__ inline uint64_t content_hash_init(uint64_t seed, int bt) {
+    return seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)bt);
 }
+__device__ inline uint64_t content_hash_pair(uint64_t h, int32_t lo, int32_t hi, int i) {
+    const uint64_t w = (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32);
+    return mix64(h ^ (w + 0x632BE59BD9B4E019ull * (uint64_t)(i + 1)));
+}
+__device__ inline uint64_t content_hash_final(uint64_t h) { return mod61(mix64(h)); }
 
 __device__ inline uint64_t content_hash_mem(const int32_t* __restrict__ blk, int bt, uint64_t seed) {
-    uint64_t h = seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)bt);
-    for (int i = 0; i < bt; i += 2) {
-        uint64_t w = (uint64_t)(uint32_t)blk[i];
-        if (i + 1 < bt) w |= (uint64_t)(uint32_t)blk[i + 1] << 32;
-        h = mix64(h ^ (w + 0x632BE59BD9B4E019ull * (uint64_t)(i + 1)));
-    }
-    return mod61(mix64(h));
+    uint64_t h = content_hash_init(seed, bt);
+    for (int i = 0; i < bt; i += 2) h = content_hash_pair(h, blk[i], i + 1 < bt ? blk[i + 1] : 0, i);
+    return content_hash_final(h);
+}
+
+// One index slot in one 16-byte load: a probe learns the key, the id and the
+// parent of a slot at once, with no second dependent load.
+__device__ inline Slot load_slot(const Slot* p) {
+    typedef unsigned int v4u_t __attribute__((ext_vector_type(4)));
+    const v4u_t v = *reinterpret_cast<const v4u_t*>(p);
+    Slot s;
+    s.key = ((uint64_t)v.y << 32) | (uint64_t)v.x;
+    s.id = (int32_t)v.z;
+    s.parent = (int32_t)v.w;
+    return s;
 }
 
 __device__ inline uint64_t index_key(uint64_t k, const HashTables& ht) {
@@ -169,7 +180,9 @@ __device__ inline uint64_t shfl_up_u64(uint64_t v, int d) {
 // window's tokens and its probes.
 struct ChainConsts {
     uint64_t lane_pow;  // P^(lane+1)
-    uint64_t step[6];   // P^(2^t)
+    uint64_t pow0;      // P^lane
+    uint64_t inv;       // P^-lane
+    uint64_t p;         // P
     uint64_t root_key;
     uint64_t content_seed;
     uint64_t slot_seed;
@@ -179,8 +192,9 @@ struct ChainConsts {
 __device__ inline ChainConsts chain_consts(const HashTables* __restrict__ ht, int lane) {
     ChainConsts c;
     c.lane_pow = ht->pow_lane[lane];
-#pragma unroll
-    for (int t = 0; t < 6; ++t) c.step[t] = ht->pow_step[t];
+    c.pow0 = ht->pow0[lane];
+    c.inv = ht->inv_pow[lane];
+    c.p = ht->p;
     c.root_key = ht->root_key;
     c.content_seed = ht->content_seed;
     c.slot_seed = ht->slot_seed;
@@ -192,18 +206,23 @@ __device__ inline uint64_t index_key(uint64_t k, const ChainConsts& c) {
     return c.weak ? (k & 0xFFull) : k;
 }
 
-// Inclusive scan of the affine key chain over one 64-block window.
-// c: this lane's content hash (0 for lanes past the request's end);
-// carry: k_{w0-1}. Returns this lane's chained key k_{w0+lane}.
+// The affine key chain over one 64-block window. With c_i the content hash
+// of block w0+i (0 past the request's end) and carry = k_{w0-1}, lane j's key
+//   k_{w0+j} = P^(j+1) carry + sum_{i<=j} P^(j-i) c_i
+//            = P^j (P carry + sum_{i<=j} P^-i c_i)          (mod 2^61-1),
+// so one product per lane turns the hashes into terms P^-i c_i, a wave
+// prefix sum of plain modular additions adds them up, and one more product
+// (P carry is the same in every lane) gives the key: the same values as
+// folding the chain block by block, with 2 products per lane instead of 7.
 __device__ inline uint64_t window_chain(uint64_t c, uint64_t carry, const ChainConsts& cc, int lane) {
-    uint64_t s = c;
+    uint64_t s = mulmod61(c, cc.inv);
 #pragma unroll
     for (int t = 0; t < 6; ++t) {
         const int d = 1 << t;
-        uint64_t sp = shfl_up_u64(s, d);
-        if (lane >= d) s = addmod61(s, mulmod61(cc.step[t], sp));
+        const uint64_t sp = shfl_up_u64(s, d);
+        if (lane >= d) s = addmod61(s, sp);
     }
-    return addmod61(mulmod61(cc.lane_pow, carry), s);
+    return mulmod61(cc.pow0, addmod61(mulmod61(cc.p, carry), s));
 }
 
 __device__ inline unsigned long long ballot64(bool p) { return __ballot(p); }

@@ -68,30 +68,39 @@ struct Window16 {
         lane = l;
     }
 
+    // n > w0. All of a lane's loads are issued before any is waited for:
+    // pieces past the window's end re-read its last piece (always inside the
+    // request) and land in LDS rows no lane reads.
     __device__ inline void stage(const int32_t* __restrict__ seq, int w0, int n, int) {
         wave_lds_sync();  // the previous window's reads are issued
         const int nq = (n - w0 < kWave ? n - w0 : kWave) * kQuads;
         const int32_t* base = seq + (int64_t)w0 * 16;
         if ((reinterpret_cast<uintptr_t>(base) & 15) == 0) {
-#pragma unroll
-            for (int i = 0; i < kQuads; ++i) {
-                const int q = i * kWave + lane;
-                if (q < nq) sh[q] = *reinterpret_cast<const int4*>(base + 4 * q);
-            }
+            const int q0 = lane, q1 = kWave + lane, q2 = 2 * kWave + lane, q3 = 3 * kWave + lane;
+            const int4 v0 = *reinterpret_cast<const int4*>(base + 4 * (q0 < nq ? q0 : nq - 1));
+            const int4 v1 = *reinterpret_cast<const int4*>(base + 4 * (q1 < nq ? q1 : nq - 1));
+            const int4 v2 = *reinterpret_cast<const int4*>(base + 4 * (q2 < nq ? q2 : nq - 1));
+            const int4 v3 = *reinterpret_cast<const int4*>(base + 4 * (q3 < nq ? q3 : nq - 1));
+            sh[q0] = v0;
+            sh[q1] = v1;
+            sh[q2] = v2;
+            sh[q3] = v3;
         } else {
             int32_t* d = reinterpret_cast<int32_t*>(sh);
             for (int q = lane; q < 4 * nq; q += kWave) d[q] = base[q];
         }
         wave_lds_sync();
     }
+    // streamed from LDS a piece at a time (four tokens live, not sixteen)
     __device__ inline uint64_t hash(uint64_t seed, int) const {
-        int32_t t[16];
+        uint64_t h = content_hash_init(seed, 16);
 #pragma unroll
         for (int i = 0; i < kQuads; ++i) {
             const int4 v = sh[lane * kQuads + i];
-            t[4 * i] = v.x; t[4 * i + 1] = v.y; t[4 * i + 2] = v.z; t[4 * i + 3] = v.w;
+            h = content_hash_pair(h, v.x, v.y, 4 * i);
+            h = content_hash_pair(h, v.z, v.w, 4 * i + 2);
         }
-        return content_hash_regs<16>(t, seed);
+        return content_hash_final(h);
     }
     // This lane's block against one stored row (64-byte aligned). Only the
     // rare paths (a key hit with other tokens, a key collision between
@@ -108,19 +117,25 @@ struct Window16 {
         return eq;
     }
     // Token check of every lane's candidate (-1: none); called by the whole
-    // wave. Returns whether this lane's candidate row holds its tokens.
+    // wave. Returns whether this lane's candidate row holds its tokens. The
+    // four row loads are issued together; a lane of a block without a
+    // candidate reads row 0 (always allocated) and ignores it.
     __device__ inline bool verify(const int32_t* __restrict__ tokens, int32_t cand, int) const {
+        constexpr int G = kWave / 16;
+        int32_t id[G];
+        int4 v[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            id[g] = __shfl(cand, g * 16 + (lane >> 2), kWave);
+            const int64_t row = id[g] >= 0 ? id[g] : 0;
+            v[g] = *reinterpret_cast<const int4*>(tokens + row * 16 + 4 * (lane & 3));
+        }
         uint64_t ok = 0;  // bit j: block j's candidate row holds block j's tokens
-#pragma unroll 1
-        for (int g = 0; g < kWave / 16; ++g) {
-            const int j = g * 16 + (lane >> 2);
-            const int32_t id = __shfl(cand, j, kWave);
-            bool eq = false;
-            if (id >= 0) {
-                const int4 v = *reinterpret_cast<const int4*>(tokens + (int64_t)id * 16 + 4 * (lane & 3));
-                const int4 w = sh[j * kQuads + (lane & 3)];
-                eq = (v.x == w.x) & (v.y == w.y) & (v.z == w.z) & (v.w == w.w);
-            }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int4 w = sh[(g * 16 + (lane >> 2)) * kQuads + (lane & 3)];
+            const bool eq = (id[g] >= 0) & (v[g].x == w.x) & (v[g].y == w.y) & (v[g].z == w.z) &
+                            (v[g].w == w.w);
             ok |= quads_all(ballot64(eq)) << (16 * g);
         }
         return (ok >> lane) & 1;
@@ -165,7 +180,7 @@ struct WindowOf<16> {
 __device__ inline int32_t probe_key(const IndexView& ix, uint64_t ikey, uint64_t pos, uint64_t* pos_out,
                                     int32_t* parent_out, unsigned* probes) {
     while (true) {
-        const Slot s = ix.slots[pos];
+        const Slot s = load_slot(ix.slots + pos);
         ++*probes;
         if (s.key == kEmptyKey) {
             *pos_out = pos;
@@ -189,7 +204,7 @@ __device__ inline int32_t probe(const IndexView& ix, uint64_t ikey, uint64_t pos
                                 int32_t* parent_out, unsigned* probes, unsigned* cmps) {
     const int bt = ix.block_tokens;
     while (true) {
-        const Slot s = ix.slots[pos];
+        const Slot s = load_slot(ix.slots + pos);
         ++*probes;
         if (s.key == kEmptyKey) {
             *pos_out = pos;

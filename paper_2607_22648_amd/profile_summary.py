@@ -1,29 +1,39 @@
 """Summarise rocprofv3 output of bench.py into short text notes under profiles/.
 
 Inputs (directories written by rocprofv3 ``--output-format csv``):
-  --trace DIR   a ``--kernel-trace --stats`` run (uses *_kernel_stats.csv);
-                alone (with --trace-bench), only the per-kernel table of the
-                store's own kernels is written
-  --fetch DIR   a ``--pmc FETCH_SIZE`` run (uses *_counter_collection.csv)
-  --write DIR   a ``--pmc WRITE_SIZE`` run
-  --bench FILE  the JSON line bench.py printed in the counter runs
-  --window NAME:FIRST:COUNT  (repeatable, with --trace alone) the average
+  --trace DIR   a ``--kernel-trace --stats`` run (uses *_kernel_stats.csv):
+                the per-kernel table of the store's own kernels
+  --window NAME:FIRST:COUNT  (repeatable, with --trace) the average
                 duration of dispatches FIRST .. FIRST+COUNT-1, in start order,
                 of the kernel whose name contains NAME (*_kernel_trace.csv):
                 the launches a bench phase timed, apart from other launches
                 of the same kernel in the run
-  --pmc DIR     (repeatable, instead of --fetch/--write) any ``--pmc`` runs:
-                the average per dispatch of every counter collected, for
-                every store kernel, plus the L2 hit rate where TCC_HIT and
-                TCC_MISS were both collected
+  --fetch DIR, --write DIR  ``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE`` runs,
+                with --bench FILE, the JSON line bench.py printed in them:
+                the gather's HBM traffic record (below)
+  --reqs DIR    (optional, with --fetch) a ``--pmc TCC_EA0_RDREQ
+                TCC_EA0_RDREQ_32B TCC_EA0_RDREQ_64B TCC_EA0_RDREQ_128B`` run,
+  --wreqs DIR   and a ``--pmc TCC_EA0_WRREQ TCC_EA0_WRREQ_64B ...`` run: the
+                same traffic counted from memory requests times their sizes
+  --pmc DIR     (repeatable, instead of the above) any ``--pmc`` runs: the
+                average per dispatch of every counter collected, for every
+                store kernel, plus the L2 hit rate where TCC_HIT and TCC_MISS
+                were both collected
 
-HBM traffic of a kernel = FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
-scaled by the factor that maps the same counter onto the known byte count of
-a plain device-to-device copy in the same run (the copy bench.py times for
-its ceiling, a ``__amd_rocclr_copyBuffer`` dispatch of ``hbm_ceiling.bytes``
-bytes as that run's JSON line states). The record
-carries the SHA-256 of the copy kernel's source; bench.py reports the traffic
-only while that source is unchanged.
+HBM traffic of the gather. FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are
+each scaled by the factor that maps the same counter onto the known byte
+count of the bench's own bandwidth probes in the same run: a pure read
+stream (ptstore_bandwidth_probe kind 0, ``k_read``) and a pure write stream
+(kind 1, ``k_write``) of ``hbm_ceiling.bytes`` each, as the run's JSON line
+states. The raw counts, the factors and, for comparison, the factors a plain
+device-to-device copy (``__amd_rocclr_copyBuffer``) gives are all recorded.
+Independently of any factor, the request counters give bytes as requests x
+request size (32, 64 or 128 bytes; a write request is 64 bytes if counted as
+such, else 32), checked against the probes' known bytes as well. Traffic
+is compared with the algorithmic bytes summed over every gather dispatch of
+the run (the JSON line's ``gather_all``). The record carries the SHA-256 of
+the copy kernel's source; bench.py reports the traffic only while that
+source is unchanged.
 """
 from __future__ import annotations
 
@@ -73,30 +83,57 @@ def dispatch_window(trace_dir: str, spec: str):
     return name, first, count, sum(ms) / count
 
 
-def counter_per_dispatch(pmc_dir: str, counter: str):
-    """{kernel short name: [value per dispatch]} for the gather, scatter and plain copy."""
-    out = defaultdict(list)
+PROBE_READ = "k_read("
+PROBE_WRITE = "k_write("
+
+
+def kernel_key(name: str):
+    """The short key of a kernel this summary tracks, or None."""
+    for key in (GATHER, "k_copy_spans<true>", SCATTER, PROBE_READ, PROBE_WRITE, PLAIN_COPY):
+        if key in name:
+            return key
+    return None
+
+
+def counters_by_kernel(pmc_dir: str):
+    """{kernel key: {counter: [value per dispatch, in file order]}}."""
+    out = defaultdict(lambda: defaultdict(list))
     for r in csv.DictReader(open(_one(os.path.join(pmc_dir, "*counter_collection.csv")))):
-        if r["Counter_Name"] != counter:
-            continue
-        name = r["Kernel_Name"]
-        for key in (GATHER, SCATTER, PLAIN_COPY):
-            if key in name:
-                out[key].append(float(r["Counter_Value"]))
+        key = kernel_key(r["Kernel_Name"])
+        if key:
+            c = r["Counter_Name"].replace("_sum", "")
+            out[key][c].append(float(r["Counter_Value"]))
     return out
 
 
 def plain_copy_value(vals):
-    """The 8 GiB copy dispatches (the largest plain-copy dispatches of the run)."""
+    """The large plain-copy dispatches (the largest of the run)."""
     top = max(vals)
     return [v for v in vals if v > 0.9 * top]
 
 
+def mean(v):
+    return sum(v) / len(v)
+
+
+def read_bytes(cs, k):
+    """Read bytes of dispatch k from the request counters: requests x size."""
+    r32, r64, r128 = (cs[c][k] for c in ("TCC_EA0_RDREQ_32B", "TCC_EA0_RDREQ_64B", "TCC_EA0_RDREQ_128B"))
+    return 32 * r32 + 64 * r64 + 128 * r128
+
+
+def write_bytes(cs, k):
+    w, w64 = cs["TCC_EA0_WRREQ"][k], cs["TCC_EA0_WRREQ_64B"][k]
+    return 64 * w64 + 32 * (w - w64)
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--trace", required=True)
+    ap.add_argument("--trace", default=None)
     ap.add_argument("--fetch", default=None)
     ap.add_argument("--write", default=None)
+    ap.add_argument("--reqs", default=None, help="a --pmc run of the read request counters")
+    ap.add_argument("--wreqs", default=None, help="a --pmc run of the write request counters")
     ap.add_argument("--bench", default=None, help="bench.py JSON line of a counter run")
     ap.add_argument("--trace-bench", default=None, help="bench.py JSON line of the trace run")
     ap.add_argument("--out", default=os.path.join(os.path.dirname(HERE), "profiles"))
@@ -108,69 +145,107 @@ def main():
     a = ap.parse_args()
     if a.pmc:
         return store_counters(a)
-    if not (a.fetch and a.write and a.bench):
-        return store_kernels_only(a)
+    if a.fetch and a.write and a.bench:
+        return gather_traffic(a)
+    return store_kernels_only(a)
 
+
+def gather_traffic(a):
     bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
-    algo = bench["roofline"]["bytes_per_launch"]
-    fetch = counter_per_dispatch(a.fetch, "FETCH_SIZE")
-    write = counter_per_dispatch(a.write, "WRITE_SIZE")
-    pf = plain_copy_value(fetch[PLAIN_COPY])
-    pw = plain_copy_value(write[PLAIN_COPY])
-    known_kib = bench["hbm_ceiling"]["bytes"] / 1024  # the plain copy's size in that run
-    f_factor = known_kib / (sum(pf) / len(pf))
-    w_factor = known_kib / (sum(pw) / len(pw))
-    g_fetch = sum(fetch[GATHER]) / len(fetch[GATHER])
-    g_write = sum(write[GATHER]) / len(write[GATHER])
-    traffic = (g_fetch * f_factor + g_write * w_factor) * 1024
-    stats = kernel_stats(a.trace)
-
-    os.makedirs(a.out, exist_ok=True)
+    known = bench["hbm_ceiling"]["bytes"]  # bytes of each probe dispatch
+    fe, wr = counters_by_kernel(a.fetch), counters_by_kernel(a.write)
+    gk = GATHER if GATHER in fe else "k_copy_spans<true>"
+    f_factor = known / 1024 / mean(fe[PROBE_READ]["FETCH_SIZE"])
+    w_factor = known / 1024 / mean(wr[PROBE_WRITE]["WRITE_SIZE"])
+    cf = cw = None
+    if PLAIN_COPY in fe and PLAIN_COPY in wr:
+        cf = known / 1024 / mean(plain_copy_value(fe[PLAIN_COPY]["FETCH_SIZE"]))
+        cw = known / 1024 / mean(plain_copy_value(wr[PLAIN_COPY]["WRITE_SIZE"]))
+    g_fetch, g_write = fe[gk]["FETCH_SIZE"], wr[gk]["WRITE_SIZE"]
+    n = len(g_fetch)
+    ga = bench.get("gather_all")
+    if ga:  # algorithmic bytes over every gather dispatch of the run
+        if ga["dispatches"] != n:
+            raise ValueError(f"the run holds {n} gather dispatches, bench.py counted {ga['dispatches']}")
+        algo_total = ga["bytes"]
+    else:
+        algo_total = bench["roofline"]["bytes_per_launch"] * n
+    traffic_total = (sum(g_fetch) * f_factor + sum(g_write) * w_factor) * 1024
+    ratio = traffic_total / algo_total
+    per_launch = bench["roofline"]["bytes_per_launch"]
     rec = {
-        "kernel": GATHER,
+        "kernel": gk,
         "workload": bench["config"]["workload"],
         "copy_hip_sha256": copy_source_sha(),
-        "fetch_kib_per_dispatch": round(g_fetch, 1),
-        "write_kib_per_dispatch": round(g_write, 1),
+        "dispatches": n,
+        "raw_fetch_kib_per_dispatch": round(mean(g_fetch), 1),
+        "raw_write_kib_per_dispatch": round(mean(g_write), 1),
         "fetch_factor": round(f_factor, 4),
         "write_factor": round(w_factor, 4),
-        "traffic_bytes_per_launch": int(traffic),
-        "algorithmic_bytes_per_launch": int(algo),
-        "traffic_over_algorithmic": round(traffic / algo, 4),
-        "dispatches": len(fetch[GATHER]),
+        "factor_source": f"bandwidth probes of {known} bytes (read kind 0, write kind 1) in the same runs",
+        "plain_copy_factors": [round(cf, 4), round(cw, 4)] if cf else None,
+        "algorithmic_bytes_all_dispatches": int(algo_total),
+        "traffic_bytes_all_dispatches": int(traffic_total),
+        "traffic_over_algorithmic": round(ratio, 4),
+        "algorithmic_bytes_per_launch": int(per_launch),
+        "traffic_bytes_per_launch": int(round(ratio * per_launch)),
     }
+    lines_req = []
+    if a.reqs and a.wreqs:
+        rq, wq = counters_by_kernel(a.reqs), counters_by_kernel(a.wreqs)
+        if len(rq[gk]["TCC_EA0_RDREQ_32B"]) != n or len(wq[gk]["TCC_EA0_WRREQ"]) != n:
+            raise ValueError("the request runs hold another number of gather dispatches")
+        rd = sum(read_bytes(rq[gk], k) for k in range(n))
+        wb = sum(write_bytes(wq[gk], k) for k in range(n))
+        probe_rd = mean([read_bytes(rq[PROBE_READ], k) for k in range(len(rq[PROBE_READ]["TCC_EA0_RDREQ_32B"]))])
+        probe_wr = mean([write_bytes(wq[PROBE_WRITE], k) for k in range(len(wq[PROBE_WRITE]["TCC_EA0_WRREQ"]))])
+        cover = sum(rq[gk]["TCC_EA0_RDREQ_32B"][k] + rq[gk]["TCC_EA0_RDREQ_64B"][k] +
+                    rq[gk]["TCC_EA0_RDREQ_128B"][k] for k in range(n)) / sum(rq[gk]["TCC_EA0_RDREQ"])
+        rec.update({
+            "request_read_bytes_all_dispatches": int(rd),
+            "request_write_bytes_all_dispatches": int(wb),
+            "request_traffic_over_algorithmic": round((rd + wb) / algo_total, 4),
+            "request_read_over_algorithmic_read": round(rd / (algo_total / 2), 4),
+            "request_write_over_algorithmic_write": round(wb / (algo_total / 2), 4),
+            "probe_check": {"read_probe_bytes_from_requests_over_known": round(probe_rd / known, 4),
+                            "write_probe_bytes_from_requests_over_known": round(probe_wr / known, 4),
+                            "read_requests_covered_by_size_classes": round(cover, 4)},
+        })
+        if "TCC_EA0_WRREQ_DRAM_CREDIT_STALL" in wq[gk]:
+            w_all = sum(wq[gk]["TCC_EA0_WRREQ"])
+            rec["dram_credit_stalls_per_write_request"] = {
+                "read": round(sum(wq[gk]["TCC_EA0_RDREQ_DRAM_CREDIT_STALL"]) / w_all, 4),
+                "write": round(sum(wq[gk]["TCC_EA0_WRREQ_DRAM_CREDIT_STALL"]) / w_all, 4)}
+        lines_req = [
+            f"| gather read bytes from requests (32/64/128 B classes) | {rd / n / 1e9:.3f} GB per dispatch |",
+            f"| gather write bytes from requests (64 B, else 32 B) | {wb / n / 1e9:.3f} GB per dispatch |",
+            f"| request bytes / algorithmic | {(rd + wb) / algo_total:.4f} (read {rd / (algo_total / 2):.4f}, "
+            f"write {wb / (algo_total / 2):.4f}) |",
+            f"| check: read probe bytes from requests / known | {probe_rd / known:.4f} |",
+            f"| check: write probe bytes from requests / known | {probe_wr / known:.4f} |",
+            f"| read requests counted in a size class | {cover:.4f} |"]
+        if "dram_credit_stalls_per_write_request" in rec:
+            st = rec["dram_credit_stalls_per_write_request"]
+            lines_req.append(f"| DRAM credit stalls per write request (read, write) | "
+                             f"{st['read']:.4f}, {st['write']:.4f} |")
+    os.makedirs(a.out, exist_ok=True)
     with open(os.path.join(a.out, f"{a.name}_traffic.json"), "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
-
-    lines = [f"# Kernel trace: {a.name}", "", "Command (run from the repository root on the MI355X host):", "",
-             "```", a.cmd.strip(), "```", "",
-             "| kernel | calls | avg ms | % of GPU time |", "|---|---|---|---|"]
-    for name, calls, avg, pct in stats[:12]:
-        short = name if len(name) < 70 else name[:67] + "..."
-        lines.append(f"| `{short}` | {calls} | {avg:.4f} | {pct:.2f} |")
-    g = [s for s in stats if GATHER in s[0]]
-    if g:
-        lines += ["", f"Gather kernel average over {g[0][1]} dispatches: **{g[0][2]:.4f} ms**."]
-    if a.trace_bench:
-        tb = json.loads(open(a.trace_bench).read().strip().splitlines()[-1])["roofline"]
-        lines += [f"bench.py's own HIP-event average in the same run: **{tb['avg_launch_ms']:.4f} ms** "
-                  f"over {tb['launches']} timed launches ({tb['achieved']:.1f} GB/s, "
-                  f"{100 * tb['frac']:.1f}% of 8 TB/s)."]
-    with open(os.path.join(a.out, f"{a.name}_kernel_trace.md"), "w") as f:
-        f.write("\n".join(lines) + "\n")
-
     lines = [f"# HBM traffic: {a.name}", "", "Commands (repository root, on the MI355X host):", "", "```",
              a.cmd.strip(), "```", "",
              "| quantity | value |", "|---|---|",
-             f"| gather FETCH_SIZE per dispatch | {g_fetch:,.0f} KiB ({len(fetch[GATHER])} dispatches) |",
-             f"| gather WRITE_SIZE per dispatch | {g_write:,.0f} KiB |",
-             f"| plain {known_kib / 2**20:.0f} GiB copy FETCH_SIZE | {sum(pf) / len(pf):,.0f} KiB -> factor {f_factor:.4f} |",
-             f"| plain {known_kib / 2**20:.0f} GiB copy WRITE_SIZE | {sum(pw) / len(pw):,.0f} KiB -> factor {w_factor:.4f} |",
-             f"| traffic per gather launch (scaled) | {traffic / 1e9:.3f} GB |",
-             f"| algorithmic bytes per launch | {algo / 1e9:.3f} GB |",
-             f"| traffic / algorithmic | {traffic / algo:.4f} |",
-             "", f"Copy kernel source SHA-256: `{rec['copy_hip_sha256']}`."]
+             f"| gather dispatches in the run | {n} |",
+             f"| gather FETCH_SIZE, raw | {mean(g_fetch):,.0f} KiB per dispatch |",
+             f"| gather WRITE_SIZE, raw | {mean(g_write):,.0f} KiB per dispatch |",
+             f"| read probe ({known / 2**30:.0f} GiB) FETCH_SIZE | {mean(fe[PROBE_READ]['FETCH_SIZE']):,.0f} KiB -> factor {f_factor:.4f} |",
+             f"| write probe ({known / 2**30:.0f} GiB) WRITE_SIZE | {mean(wr[PROBE_WRITE]['WRITE_SIZE']):,.0f} KiB -> factor {w_factor:.4f} |"]
+    if cf:
+        lines.append(f"| plain copy factors, for comparison | FETCH {cf:.4f}, WRITE {cw:.4f} |")
+    lines += [f"| traffic, all gather dispatches (scaled) | {traffic_total / 1e9:.3f} GB |",
+              f"| algorithmic bytes, all gather dispatches | {algo_total / 1e9:.3f} GB |",
+              f"| traffic / algorithmic | {ratio:.4f} |"] + lines_req + [
+              "", f"Copy kernel source SHA-256: `{rec['copy_hip_sha256']}`."]
     with open(os.path.join(a.out, f"{a.name}_hbm_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(rec))
@@ -183,7 +258,7 @@ def short_name(name: str) -> str:
 
 def store_counters(a):
     """Per-kernel averages of the counters of one or more --pmc runs."""
-    vals = defaultdict(lambda: defaultdict(list))  # kernel -> counter -> values
+    vals = defaultdict(lambda: defaultdict(list))  # (kernel, grid) -> counter -> values
     order = []
     for d in a.pmc:
         for r in csv.DictReader(open(_one(os.path.join(d, "*counter_collection.csv")))):
@@ -192,7 +267,14 @@ def store_counters(a):
             c = r["Counter_Name"]
             if c not in order:
                 order.append(c)
-            vals[short_name(r["Kernel_Name"])][c].append(float(r["Counter_Value"]))
+            vals[(short_name(r["Kernel_Name"]), int(r.get("Grid_Size") or 0))][c].append(
+                float(r["Counter_Value"]))
+    # a kernel launched at several grid sizes (say a lookup of a timed batch and
+    # the lookups inside the prefill's inserts) gets a row per grid size
+    grids = defaultdict(set)
+    for k, g in vals:
+        grids[k].add(g)
+    vals = {(f"{k} (grid {g:,})" if len(grids[k]) > 1 else k): v for (k, g), v in vals.items()}
     hit = "TCC_HIT_sum" in order and "TCC_MISS_sum" in order
     head = ["kernel", "dispatches"] + [f"{c} / dispatch" for c in order] + (["L2 hit rate"] if hit else [])
     lines = [f"# Counters: {a.name}", "", "Commands (run from the repository root on the MI355X host):",

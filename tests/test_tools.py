@@ -34,35 +34,58 @@ def _write_pmc(d, rows):
 
 
 def test_profile_summary_traffic(tmp_path):
-    """Traffic = FETCH_SIZE and WRITE_SIZE scaled by what a plain copy of
-    known size reads for them, against the bench's algorithmic bytes."""
-    gather = "void ptsd::(anonymous namespace)::k_copy_pairs<true>(ptsd::(anonymous namespace)::CopyArgs)"
-    copy = "__amd_rocclr_copyBuffer"
-    tr, fe, wr = tmp_path / "trace", tmp_path / "fetch", tmp_path / "write"
-    _write_trace(str(tr), [(gather, 4, 10_000_000, 90.0), (copy, 2, 1_000_000, 5.0)])
+    """Traffic = FETCH_SIZE and WRITE_SIZE scaled by what the bench's read and
+    write probes of known size read for them in the same runs, against the
+    algorithmic bytes summed over every gather dispatch; and, independently,
+    memory requests times their sizes, checked on the probes too."""
+    ns = "void ptsd::(anonymous namespace)::"
+    gather = ns + "k_copy_pairs<true>(ptsd::(anonymous namespace)::CopyArgs)"
+    rd = ns + "k_read(unsigned int __vector(4) const*, long, unsigned int __vector(4)*)"
+    wrk = ns + "k_write(unsigned int __vector(4)*, long)"
     gib = 1 << 30
-    # the plain 1 GiB copy reads FETCH_SIZE = half its KiB (factor 2) and
-    # WRITE_SIZE = its KiB (factor 1); the gather 3 GiB read, 3 GiB written
-    _write_pmc(str(fe), [(copy, "FETCH_SIZE", gib / 1024 / 2), (gather, "FETCH_SIZE", 3 * gib / 1024 / 2)])
-    _write_pmc(str(wr), [(copy, "WRITE_SIZE", gib / 1024), (gather, "WRITE_SIZE", 3 * gib / 1024)])
+    fe, wr, rq, wq = (tmp_path / n for n in ("fetch", "write", "reqs", "wreqs"))
+    # FETCH_SIZE reads half the KiB of a pure read (factor 2), WRITE_SIZE all of a
+    # pure write (factor 1); four gathers of 3 GiB read + 3 GiB written, then a
+    # fifth dispatch of 1 GiB + 1 GiB: 26 GiB algorithmic in all
+    g_r = [3 * gib] * 4 + [gib]
+    _write_pmc(str(fe), [(rd, "FETCH_SIZE", gib / 1024 / 2)] * 2 +
+               [(gather, "FETCH_SIZE", b / 1024 / 2) for b in g_r])
+    _write_pmc(str(wr), [(wrk, "WRITE_SIZE", gib / 1024)] * 2 +
+               [(gather, "WRITE_SIZE", b / 1024) for b in g_r])
+    # reads in 128-byte requests (a few 64 and 32 byte ones), writes in 64-byte ones
+    req = []
+    for k, b in [(rd, gib)] + [(gather, b) for b in g_r]:
+        req += [(k, "TCC_EA0_RDREQ_sum", (b - 96) / 128 + 2), (k, "TCC_EA0_RDREQ_32B_sum", 1),
+                (k, "TCC_EA0_RDREQ_64B_sum", 1), (k, "TCC_EA0_RDREQ_128B_sum", (b - 96) / 128)]
+    _write_pmc(str(rq), req)
+    _write_pmc(str(wq), [(k, c, v) for k, b in [(wrk, gib)] + [(gather, b) for b in g_r]
+                         for c, v in (("TCC_EA0_WRREQ_sum", b / 64), ("TCC_EA0_WRREQ_64B_sum", b / 64))])
     bench = tmp_path / "bench.json"
-    bench.write_text(json.dumps({"roofline": {"bytes_per_launch": 6 * gib, "avg_launch_ms": 10.0,
-                                              "launches": 4, "achieved": 644.2, "frac": 0.08},
+    bench.write_text(json.dumps({"roofline": {"bytes_per_launch": 26 * gib / 5},
+                                 "gather_all": {"dispatches": 5, "bytes": 26 * gib},
                                  "hbm_ceiling": {"bytes": gib},
                                  "config": {"workload": "synthetic"}}) + "\n")
     out = tmp_path / "profiles"
-    p = subprocess.run([sys.executable, "-m", "paper_2607_22648_amd.profile_summary",
-                        "--trace", str(tr), "--fetch", str(fe), "--write", str(wr),
-                        "--bench", str(bench), "--trace-bench", str(bench), "--out", str(out),
-                        "--name", "t", "--cmd", "cmd"], capture_output=True, text=True, cwd=ROOT,
-                       timeout=120)
+    args = [sys.executable, "-m", "paper_2607_22648_amd.profile_summary", "--fetch", str(fe),
+            "--write", str(wr), "--reqs", str(rq), "--wreqs", str(wq), "--bench", str(bench),
+            "--out", str(out), "--name", "t", "--cmd", "cmd"]
+    p = subprocess.run(args, capture_output=True, text=True, cwd=ROOT, timeout=120)
     assert p.returncode == 0, p.stderr
     rec = json.loads((out / "t_traffic.json").read_text())
     assert rec["fetch_factor"] == 2.0 and rec["write_factor"] == 1.0
-    assert rec["traffic_bytes_per_launch"] == 6 * gib
-    assert rec["traffic_over_algorithmic"] == 1.0
-    trace = (out / "t_kernel_trace.md").read_text()
-    assert "10.0000 ms" in trace and "cmd" in trace
+    assert rec["dispatches"] == 5 and rec["traffic_over_algorithmic"] == 1.0
+    assert rec["traffic_bytes_per_launch"] == round(26 * gib / 5)
+    assert rec["raw_fetch_kib_per_dispatch"] == round(26 * gib / 2 / 1024 / 2 / 5, 1)
+    assert rec["request_traffic_over_algorithmic"] == 1.0
+    assert rec["probe_check"]["read_probe_bytes_from_requests_over_known"] == 1.0
+    assert rec["probe_check"]["write_probe_bytes_from_requests_over_known"] == 1.0
+    assert rec["probe_check"]["read_requests_covered_by_size_classes"] == 1.0
+    assert "cmd" in (out / "t_hbm_counters.md").read_text()
+    # a run whose gather dispatches differ from what bench.py counted is refused
+    bench.write_text(json.dumps({"roofline": {"bytes_per_launch": 1}, "gather_all": {"dispatches": 4, "bytes": 1},
+                                 "hbm_ceiling": {"bytes": gib}, "config": {"workload": "x"}}) + "\n")
+    p = subprocess.run(args, capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert p.returncode != 0 and "gather dispatches" in p.stderr
 
 
 def test_profile_summary_counters(tmp_path):
