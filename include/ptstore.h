@@ -33,9 +33,15 @@
  *  - Every pointer argument except `cfg`/`out`/`stats` is a DEVICE pointer
  *    owned by the caller. `stream` is a hipStream_t (NULL = default stream).
  *    Calls only enqueue work on `stream` and return; outputs are valid once
- *    the stream has reached that point. Calls on one store must be ordered
- *    on one stream (a store is not safe for concurrent calls); a lookup sees
- *    exactly the inserts enqueued before it.
+ *    the stream has reached that point.
+ *  - Streams: lookups and loads (lookup, gather, gather_layers,
+ *    lookup_gather) may run on several streams of one store at once, up to
+ *    16 streams per store: each stream has its own descriptor scratch. Every
+ *    other call (insert, scatter, scatter_layers, replicate, gather_prepare,
+ *    gather_prepared) must be ordered by the caller with respect to all
+ *    other calls on the store (one stream, or events across streams); a
+ *    lookup sees exactly the inserts ordered before it. Calls on one store
+ *    come from one host thread at a time.
  *  - A call takes at most 2^29 (request, block) entries: R * max_blocks
  *    <= 2^29, else INVALID.
  *  - Return codes: PTSTORE_OK, or an error found on the host before any
@@ -45,14 +51,18 @@
  *    when that insert refused blocks. Without waiting, a caller sees a cut
  *    in the outputs: request r was cut exactly when m_out[r] is below its
  *    number of whole blocks (at most max_blocks).
- *  - HIP graphs: once a call has grown the store's scratch to a batch size,
+ *  - HIP graphs: once a call has grown the store's scratch to a batch size
+ *    (for a load: the scratch of the capture's stream, or, for a capture
+ *    stream that has made no call, that of the first stream that did),
  *    lookup, gather, gather_layers, lookup_gather, insert (with or without
  *    PTSTORE_FLAG_EVICT), scatter and scatter_layers of that size or
  *    smaller only launch kernels: no allocation, no wait, no memset. They
  *    may be captured and replayed; a replay works on the store as it is
  *    then. A later call with a larger batch regrows the scratch, after which
- *    earlier captures must not be replayed. A capture keeps the counting
- *    state (ptstore_set_counters) it was made with. ptstore_lookup_gather_noalloc
+ *    earlier captures must not be replayed; a captured call that would need
+ *    a larger scratch returns INVALID and allocates nothing. A capture keeps
+ *    the counting state (ptstore_set_counters) it was made with.
+ *    ptstore_lookup_gather_noalloc
  *    never allocates, whatever the batch (up to its limit).
  */
 #ifndef PTSTORE_H
@@ -225,8 +235,12 @@ int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * and counted in bad_entries. Destinations must be distinct (two entries
  * naming the same cache block race). `cache` must be 16-byte aligned.
  * The call first builds a dense list of the blocks to copy in store-owned
- * scratch of 8 bytes per (request, block), grown on demand (growing waits
- * for `stream`), then copies only those blocks. Errors: INVALID (store
+ * scratch of `stream` (8 bytes per (request, block) plus 24 per request,
+ * grown on demand; growing waits for `stream`), then copies only those
+ * blocks: blocks read from device memory on the full device, blocks read
+ * from the host tier by a quarter of the compute units (they move at the
+ * host link's rate whatever the grid, and the rest of the device stays free
+ * for device-memory copies, of this call or of loads on other streams). Errors: INVALID (store
  * NULL, R < 0, max_blocks < 1, R * max_blocks > 2^29, cache_blocks < 0, a
  * NULL pointer with R > 0, `cache` not 16-byte aligned), NOMEM (scratch),
  * HIP.
@@ -327,7 +341,8 @@ int ptstore_gather_layers(ptstore_t *store, const int32_t *ids, const int32_t *m
  * block_table) moves (bad entries are counted here); each
  * ptstore_gather_prepared then copies layers layer_begin .. layer_end-1 of
  * those blocks into `cache`, exactly as ptstore_gather_layers with the
- * prepare's arguments would. The list lives in store-owned scratch; any
+ * prepare's arguments would. The list lives in the scratch of the prepare's
+ * stream (a prepared copy on another stream must be ordered after it); any
  * other call on the store except lookups (gather, gather_layers,
  * lookup_gather, scatter, scatter_layers, insert, replicate) discards it.
  * ptstore_gather_prepared returns INVALID when there is no list, or when
@@ -396,7 +411,7 @@ const char *ptstore_last_error(void);
  * capture, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, kernels and results as ptstore_lookup_gather, but the
  * gather's descriptor list lives in a static device array of the library
- * (about 20 MiB per device, held until the process ends) instead of
+ * (about 32 MiB per device, held until the process ends) instead of
  * store-owned scratch. The call allocates nothing, frees nothing, creates
  * no event and never waits; it records no ptstore_kernel_times() entries
  * and leaves a list made by ptstore_gather_prepare intact.

@@ -10,9 +10,10 @@
 //   evs     with eviction on: per-block access counts, priorities, child
 //           counts, depths, index keys and slots, and the victim-selection
 //           scratch (all sized by the capacity, allocated here once)
-//   insert_scratch insert work space; copy_scratch gather/scatter descriptor lists
-//           (both grown on demand, so the hot path allocates only when a
-//           batch is larger than every earlier one)
+//   insert_scratch insert work space; copy_scratch gather/scatter descriptor lists,
+//           one per stream the store's calls are enqueued on (both grown on
+//           demand, so the hot path allocates only when a batch is larger
+//           than every earlier one on that stream)
 // Calls check their arguments, enqueue kernels on the caller's stream and
 // return; nothing on the lookup / gather path allocates or synchronises.
 #include <hip/hip_runtime.h>
@@ -32,10 +33,11 @@ using namespace ptsd;
 // cannot allocate: one copy per device, held until the process ends, shared
 // by every such call on that device (calls that overlap on one device race).
 // Its size is the gather's list for PTSTORE_NOALLOC_MAX_ENTRIES (request,
-// block) entries: 8 bytes per entry, 4 + 8 per request (at most one request
-// per entry), the 8-byte total, each part rounded up to 256 bytes.
+// block) entries: 8 bytes per entry, 2 x (4 + 8) per request (at most one
+// request per entry), the two 8-byte totals, each part rounded up to 256
+// bytes.
 constexpr size_t kNoAllocScratchBytes =
-    (size_t)PTSTORE_NOALLOC_MAX_ENTRIES * (8 + 4 + 8) + 256;
+    (size_t)PTSTORE_NOALLOC_MAX_ENTRIES * (8 + 2 * (4 + 8)) + 256;
 static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 
 struct ptstore {
@@ -51,8 +53,14 @@ struct ptstore {
     DevState* state;
     void* insert_scratch;
     size_t insert_scratch_size;
-    void* copy_scratch;
-    size_t copy_scratch_bytes;
+    // descriptor-list scratch per stream, so that lookups and gathers on
+    // different streams may run at the same time
+    struct StreamScratch {
+        hipStream_t stream;
+        void* p;
+        size_t bytes;
+    };
+    std::vector<StreamScratch> copy_scratch;
     int32_t chunks_per_group, threads, grid;
     int32_t cus;  // compute units of the device
     EvictView evs;  // evs.on = 0 without PTSTORE_FLAG_EVICT
@@ -65,6 +73,7 @@ struct ptstore {
     std::vector<int64_t> lbase_host;  // the bases, for launch shapes
     // the block list of ptstore_gather_prepare, while it is valid
     bool prep_valid;
+    void* prep_list;  // the copy scratch holding it
     int32_t prep_R, prep_max_blocks;
     int64_t prep_cache_blocks;
     // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
@@ -192,6 +201,9 @@ CopyPlan copy_plan(ptstore_t* s) {
     const int resident = s->cus * (2048 / s->threads);
     p.gather_grid = resident * 2048;
     p.loop_grid = resident * 16;
+    // host-tier rows move over the host link whatever the grid: a quarter of
+    // the compute units carry one workgroup each, the rest stay free
+    p.host_grid = s->cus / 4 > 0 ? s->cus / 4 : 1;
     p.state = s->state;
     p.tier = s->tier;
     p.lbase = s->layer_tab ? static_cast<const int64_t*>(s->layer_tab) : nullptr;
@@ -286,6 +298,49 @@ int ensure_scratch(void** buf, size_t* have, size_t need, hipStream_t st, const 
     }
     *have = grow;
     return PTSTORE_OK;
+}
+
+// Most streams a store keeps a descriptor scratch for.
+constexpr size_t kMaxStreams = 16;
+
+// Is work on `st` being captured into a graph? No allocation or wait may
+// happen then.
+bool capturing(hipStream_t st) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(st, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
+// The descriptor scratch of `st`, grown to `need` bytes (waiting for `st`
+// when it grows); made on the first call on a stream. Under graph capture
+// nothing is allocated: a stream that has a scratch must already have one of
+// this size, and a stream that has made no call yet (such as a capture
+// stream of its own) uses the scratch of the store's first stream.
+int copy_scratch_for(ptstore_t* s, hipStream_t st, size_t need, void** out, const char* who) {
+    const bool cap = capturing(st);
+    for (auto& e : s->copy_scratch)
+        if (e.stream == st) {
+            if (cap && need > e.bytes)
+                return fail(PTSTORE_ERR_INVALID, "a captured call needs a larger scratch than its "
+                            "stream has: run a call of that size on the stream before capturing");
+            const int rc = ensure_scratch(&e.p, &e.bytes, need, st, who);
+            *out = e.p;
+            return rc;
+        }
+    if (cap) {
+        if (!s->copy_scratch.empty() && s->copy_scratch[0].bytes >= need) {
+            *out = s->copy_scratch[0].p;
+            return PTSTORE_OK;
+        }
+        return fail(PTSTORE_ERR_INVALID, "a captured call needs a scratch no earlier call made: "
+                    "run a call of that size before capturing");
+    }
+    if (s->copy_scratch.size() >= kMaxStreams)
+        return fail(PTSTORE_ERR_INVALID, "calls on more than 16 streams of one store");
+    s->copy_scratch.push_back({st, nullptr, 0});
+    auto& e = s->copy_scratch.back();
+    const int rc = ensure_scratch(&e.p, &e.bytes, need, st, who);
+    *out = e.p;
+    return rc;
 }
 
 // Carves the eviction arrays out of one block of device memory; returns the
@@ -563,7 +618,7 @@ int ptstore_destroy(ptstore_t* s) {
     (void)hipFree(s->ht);
     (void)hipFree(s->state);
     (void)hipFree(s->insert_scratch);
-    (void)hipFree(s->copy_scratch);
+    for (auto& e : s->copy_scratch) (void)hipFree(e.p);
     (void)hipFree(s->ev_mem);
     (void)hipFree(s->tier_mem);
     (void)hipFree(s->layer_tab);
@@ -604,11 +659,11 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
     if (dev.rc) return dev.rc;
     int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes, copy_scratch_bytes(R, max_blocks),
-                        st, "ptstore_gather: scratch");
+    void* scr = nullptr;
+    rc = copy_scratch_for(s, st, copy_scratch_bytes(R, max_blocks), &scr, "ptstore_gather: scratch");
     if (rc) return rc;
     CopyScratch sc;
-    copy_scratch_carve(s->copy_scratch, R, max_blocks, &sc);
+    copy_scratch_carve(scr, R, max_blocks, &sc);
     const CopyPlan plan = copy_plan(s);
     hipError_t e;
     {
@@ -635,11 +690,13 @@ int ptstore_gather_prepare(ptstore_t* s, const int32_t* ids, const int32_t* m,
     int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
     if (R > 0) {
-        rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes,
-                            copy_scratch_bytes(R, max_blocks), st, "ptstore_gather_prepare: scratch");
+        void* scr = nullptr;
+        rc = copy_scratch_for(s, st, copy_scratch_bytes(R, max_blocks), &scr,
+                              "ptstore_gather_prepare: scratch");
         if (rc) return rc;
+        s->prep_list = scr;
         CopyScratch sc;
-        copy_scratch_carve(s->copy_scratch, R, max_blocks, &sc);
+        copy_scratch_carve(scr, R, max_blocks, &sc);
         hipError_t e;
         {
             Timed t(s, 4, st);
@@ -666,7 +723,7 @@ int ptstore_gather_prepared(ptstore_t* s, int32_t layer_begin, int32_t layer_end
     if (dev.rc) return dev.rc;
     hipStream_t st = (hipStream_t)stream;
     CopyScratch sc;
-    copy_scratch_carve(s->copy_scratch, s->prep_R, s->prep_max_blocks, &sc);
+    copy_scratch_carve(s->prep_list, s->prep_R, s->prep_max_blocks, &sc);
     hipError_t e;
     {
         Timed t(s, 0, st);
@@ -744,6 +801,9 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
     uint64_t tn;
     const size_t need = insert_scratch_bytes(R, max_blocks, &tn);
     hipError_t e;
+    if (need > s->insert_scratch_size && capturing(st))
+        return fail(PTSTORE_ERR_INVALID, "a captured insert needs a larger scratch than the store "
+                    "has: run an insert of that size before capturing");
     int rc2 = ensure_scratch(&s->insert_scratch, &s->insert_scratch_size, need, st, "ptstore_insert: scratch");
     if (rc2) return rc2;
     InsertScratch sc;
@@ -795,11 +855,11 @@ int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* crea
     if (dev.rc) return dev.rc;
     int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_scratch(&s->copy_scratch, &s->copy_scratch_bytes, copy_scratch_bytes(R, max_blocks),
-                        st, "ptstore_scatter: scratch");
+    void* scr = nullptr;
+    rc = copy_scratch_for(s, st, copy_scratch_bytes(R, max_blocks), &scr, "ptstore_scatter: scratch");
     if (rc) return rc;
     CopyScratch sc;
-    copy_scratch_carve(s->copy_scratch, R, max_blocks, &sc);
+    copy_scratch_carve(scr, R, max_blocks, &sc);
     const CopyPlan plan = copy_plan(s);
     hipError_t e;
     {

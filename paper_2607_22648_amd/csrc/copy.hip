@@ -125,44 +125,58 @@ __global__ __launch_bounds__(kSelThreads) void k_select_count(SelectArgs a) {
     if (r >= a.R) return;
     const int32_t n = row_len<GATHER>(a, r);
     const unsigned long long count = a.state->count;
-    int32_t cnt = 0, bad = 0;
+    int32_t cnt = 0, cnt_h = 0, bad = 0;
     for (int32_t b0 = 0; b0 < n; b0 += kWave) {
         const int32_t b = b0 + lane;
         Pair p;
         bool isbad = false;
         const bool sel = b < n && selected<GATHER>(a, r * a.max_blocks + b, count, &p, &isbad);
-        cnt += __popcll(ballot64(sel));
+        cnt += __popcll(ballot64(sel && p.row < a.tier.dev_rows));
+        cnt_h += __popcll(ballot64(sel && p.row >= a.tier.dev_rows));
         bad += __popcll(ballot64(isbad));
     }
     if (lane == 0) {
         a.sc.row_cnt[r] = cnt;
+        a.sc.row_cnt_h[r] = cnt_h;
         if (bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
     }
 }
 
-// One workgroup: exclusive scan of row_cnt into row_base, total into *total.
+// One workgroup: exclusive scans of row_cnt and row_cnt_h into row_base and
+// row_base_h, their totals into *total and *total_h.
 __global__ __launch_bounds__(1024) void k_select_scan(SelectArgs a) {
-    __shared__ long long part[1024];
+    __shared__ long long part[1024], part_h[1024];
     const int R = a.R;
     const int t = threadIdx.x, nt = blockDim.x;
     const int per = (R + nt - 1) / nt;
     const int lo = min(R, t * per), hi = min(R, lo + per);
-    long long s = 0;
-    for (int i = lo; i < hi; ++i) s += a.sc.row_cnt[i];
+    long long s = 0, s_h = 0;
+    for (int i = lo; i < hi; ++i) {
+        s += a.sc.row_cnt[i];
+        s_h += a.sc.row_cnt_h[i];
+    }
     part[t] = s;
+    part_h[t] = s_h;
     __syncthreads();
     for (int d = 1; d < nt; d <<= 1) {
-        long long v = t >= d ? part[t - d] : 0;
+        const long long v = t >= d ? part[t - d] : 0;
+        const long long v_h = t >= d ? part_h[t - d] : 0;
         __syncthreads();
         part[t] += v;
+        part_h[t] += v_h;
         __syncthreads();
     }
-    long long run = part[t] - s;
+    long long run = part[t] - s, run_h = part_h[t] - s_h;
     for (int i = lo; i < hi; ++i) {
         a.sc.row_base[i] = run;
+        a.sc.row_base_h[i] = run_h;
         run += a.sc.row_cnt[i];
+        run_h += a.sc.row_cnt_h[i];
     }
-    if (t == nt - 1) *a.sc.total = (unsigned long long)part[nt - 1];
+    if (t == nt - 1) {
+        *a.sc.total = (unsigned long long)part[nt - 1];
+        *a.sc.total_h = (unsigned long long)part_h[nt - 1];
+    }
 }
 
 template <bool GATHER>
@@ -173,14 +187,19 @@ __global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
     const int32_t n = row_len<GATHER>(a, r);
     const unsigned long long count = a.state->count;
     int64_t pos = a.sc.row_base[r];
+    int64_t pos_h = (int64_t)*a.sc.total + a.sc.row_base_h[r];  // host rows after all device rows
     for (int32_t b0 = 0; b0 < n; b0 += kWave) {
         const int32_t b = b0 + lane;
         Pair p;
         bool isbad = false;
         const bool sel = b < n && selected<GATHER>(a, r * a.max_blocks + b, count, &p, &isbad);
-        const unsigned long long mask = ballot64(sel);
-        if (sel) a.sc.pairs[pos + __popcll(mask & lanes_below(lane))] = p;
+        const bool dev = sel && p.row < a.tier.dev_rows;
+        const unsigned long long mask = ballot64(dev);
+        const unsigned long long mask_h = ballot64(sel && !dev);
+        if (dev) a.sc.pairs[pos + __popcll(mask & lanes_below(lane))] = p;
+        if (sel && !dev) a.sc.pairs[pos_h + __popcll(mask_h & lanes_below(lane))] = p;
         pos += __popcll(mask);
+        pos_h += __popcll(mask_h);
         // new bytes for a host-tier block: its device replica is stale, drop it
         if (!GATHER && sel && a.tier.rep_of && p.row >= a.tier.dev_rows) {
             const int64_t h = p.row - a.tier.dev_rows;
@@ -199,7 +218,8 @@ struct CopyArgs {
     int64_t dev_rows;
     uint8_t* cache;
     const Pair* pairs;
-    const unsigned long long* total;
+    const unsigned long long* first;  // the first descriptor (null: 0)
+    const unsigned long long* total;  // descriptors from there
     int64_t block_bytes;
     int64_t chunk_bytes;
     int64_t cache_blocks;
@@ -221,11 +241,12 @@ struct CopyArgs {
 template <bool GATHER>
 __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
     const unsigned long long units = *a.total * (unsigned long long)a.groups;
+    const Pair* pairs = a.pairs + (a.first ? *a.first : 0ull);
     const int n16 = (int)(a.chunk_bytes >> 4);
     for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const unsigned long long d = unit / (unsigned)a.groups;
         const int g = (int)(unit - d * (unsigned)a.groups);
-        const Pair p = a.pairs[d];
+        const Pair p = pairs[d];
         const int c0 = a.c_lo + g * a.chunks_per_group;
         const int c1 = min(c0 + a.chunks_per_group, a.c_hi);
         uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
@@ -280,6 +301,7 @@ __global__ __launch_bounds__(1024) void k_copy_spans(CopyArgs a) {
     __shared__ int64_t lb[kMaxVarLayers + 1];
     const unsigned long long spans = (unsigned)a.groups;  // kSpanBytes units per descriptor
     const unsigned long long units = *a.total * spans;
+    const Pair* pairs = a.pairs + (a.first ? *a.first : 0ull);
     if (blockIdx.x >= units) return;  // the whole workgroup: nothing to move
     const int l0 = a.c_lo >> 1, l1 = a.c_hi >> 1, n = l1 - l0;
     for (int l = l0 + (int)threadIdx.x; l <= l1; l += blockDim.x) lb[l - l0] = a.lbase[l];
@@ -290,7 +312,7 @@ __global__ __launch_bounds__(1024) void k_copy_spans(CopyArgs a) {
         const unsigned long long d = unit / spans;
         const int64_t s0 = b0 + (int64_t)(unit - d * spans) * kSpanBytes;
         const int64_t s1 = min(s0 + (int64_t)kSpanBytes, b1);
-        const Pair p = a.pairs[d];
+        const Pair p = pairs[d];
         uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
                                           : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
         // two vectors per thread in flight: both loaded before either is stored
@@ -386,6 +408,21 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
         hipLaunchKernelGGL(k_copy_spans<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     else
         hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.tier.host_blocks == 0) return e;
+    // host-tier rows: bound by the host link, so a small looping grid moves
+    // them and the device's other compute units stay free for device rows
+    // (of this call or of calls on other streams)
+    CopyArgs h = a;
+    h.first = sc.total;
+    h.total = sc.total_h;
+    int64_t hg = p.host_grid;
+    if (hg > bound) hg = bound;
+    if (hg > cap) hg = cap;
+    if (p.lbase)
+        hipLaunchKernelGGL(k_copy_spans<GATHER>, dim3((unsigned)hg), dim3(p.threads), 0, s, h);
+    else
+        hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)hg), dim3(p.threads), 0, s, h);
     return hipGetLastError();
 }
 
@@ -412,7 +449,7 @@ hipError_t launch_copy_rows(const CopyPlan& p, const Pair* pairs, const unsigned
 
 size_t copy_scratch_bytes(int32_t R, int32_t max_blocks) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return up((size_t)R * max_blocks * sizeof(Pair)) + up((size_t)R * 4) + up((size_t)R * 8) + 256;
+    return up((size_t)R * max_blocks * sizeof(Pair)) + 2 * up((size_t)R * 4) + 2 * up((size_t)R * 8) + 256;
 }
 
 void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* out) {
@@ -422,9 +459,14 @@ void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* 
     q += up((size_t)R * max_blocks * sizeof(Pair));
     out->row_cnt = reinterpret_cast<int32_t*>(q);
     q += up((size_t)R * 4);
+    out->row_cnt_h = reinterpret_cast<int32_t*>(q);
+    q += up((size_t)R * 4);
     out->row_base = reinterpret_cast<int64_t*>(q);
     q += up((size_t)R * 8);
+    out->row_base_h = reinterpret_cast<int64_t*>(q);
+    q += up((size_t)R * 8);
     out->total = reinterpret_cast<unsigned long long*>(q);
+    out->total_h = out->total + 1;
 }
 
 hipError_t launch_gather_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,

@@ -96,6 +96,7 @@ struct CopyPlan {
     int32_t grid;              // workgroups of the copy kernel, 0 = chosen per call
     int32_t gather_grid;       // most workgroups of a gather (one per unit below that)
     int32_t loop_grid;         // workgroups of a looping (sparse) copy
+    int32_t host_grid;         // workgroups of the looping copy of host-tier rows
     DevState* state;
     TierView tier;
     // per-layer slab sizes (null when every layer has chunk_bytes): the
@@ -109,12 +110,17 @@ struct CopyPlan {
 constexpr int kMaxVarLayers = 1024;
 
 
-// Descriptor list of one gather / scatter call.
+// Descriptor list of one gather / scatter call: the blocks whose row is in
+// device memory first (*total of them), then those whose row is in the host
+// tier (*total_h), each part in (request, block) order.
 struct CopyScratch {
-    Pair* pairs;               // [R * max_blocks] (dense prefix of *total entries)
-    int32_t* row_cnt;          // [R]
-    int64_t* row_base;         // [R]
-    unsigned long long* total; // number of pairs
+    Pair* pairs;                 // [R * max_blocks]
+    int32_t* row_cnt;            // [R] device-row blocks of each request
+    int32_t* row_cnt_h;          // [R] host-row blocks of each request
+    int64_t* row_base;           // [R] exclusive scan of row_cnt
+    int64_t* row_base_h;         // [R] exclusive scan of row_cnt_h
+    unsigned long long* total;   // device-row pairs
+    unsigned long long* total_h; // host-row pairs (after the device-row ones)
 };
 size_t copy_scratch_bytes(int32_t R, int32_t max_blocks);
 void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* out);

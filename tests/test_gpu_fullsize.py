@@ -433,6 +433,40 @@ def test_llama70b_full_tiered():
             host_hits += int((ids_h[0, :m_h[0]] >= owned).sum())
             seen += s
         check_access_counts(store, ref)
+        if rnd == 1:
+            # all requests looked up at once, then loads of requests that read
+            # the host tier on one stream and of the others on a second, two
+            # caches, pairs in flight together; every byte checked per pair
+            toks, offs = w.request_slice(0, w.n_requests)
+            m, ids = store.lookup(to_dev(toks), to_dev(offs), maxb)
+            rm, rids = ref.lookup(toks, offs, maxb)
+            m_h, ids_h = host(m), host(ids)
+            np.testing.assert_array_equal(m_h, rm)
+            np.testing.assert_array_equal(ids_h, rids)
+            rep = host(store.replica_map())
+            on_host = [bool(((ids_h[r, :m_h[r]] >= owned) &
+                             (rep[np.maximum(ids_h[r, :m_h[r]] - owned, 0)] < 0)).any())
+                       for r in range(len(m_h))]
+            hr = [r for r in range(len(m_h)) if on_host[r]]
+            dr = [r for r in range(len(m_h)) if not on_host[r]]
+            assert hr and dr
+            cache2 = torch.empty_like(cache)
+            s_h, s_d = torch.cuda.Stream(), torch.cuda.Stream()
+            bt1 = np.arange(maxb, dtype=np.int32).reshape(1, maxb)
+            for k in range(max(len(hr), len(dr))):
+                pair = [(s_h, hr[k], cache2)] if k < len(hr) else []
+                pair += [(s_d, dr[k], cache)] if k < len(dr) else []
+                torch.cuda.synchronize()
+                for st_, r, c in pair:
+                    c.fill_(SENTINEL)
+                torch.cuda.synchronize()
+                for st_, r, c in pair:
+                    store.gather(ids[r:r + 1], m[r:r + 1], to_dev(bt1), c, stream=st_)
+                torch.cuda.synchronize()
+                for st_, r, c in pair:
+                    seen += check_gather(store, kv, c, m_h[r:r + 1], ids_h[r:r + 1], bt1, rec)
+            del cache2
+            check_access_counts(store, ref)  # the one lookup of this phase, on both sides
         if rnd == 0:  # replicate the host tier's hot set, then read through it
             store.replicate()
             torch.cuda.synchronize()
