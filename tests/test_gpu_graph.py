@@ -205,3 +205,40 @@ def test_captured_evicting_insert_replays():
     t.check_meta()
     t.check_pool()
     t.close()
+
+
+def test_capture_that_needs_more_scratch_is_refused():
+    """A captured load or insert larger than any earlier call on the store
+    would have to grow a scratch: the call returns INVALID and allocates
+    nothing (the capture is not broken by an allocation or a wait), and the
+    store works as before afterwards."""
+    rng = np.random.default_rng(53)
+    t = Twin(1, 1, 8, 4, 3000)
+    atoms = _atoms(rng, 4, 4, 300)
+    _grow(t, rng, atoms, 4, 6, seed=1)  # scratch for 4 requests x 6 blocks
+    R, maxb = 64, 12
+    toks, offs = random_block_batch(rng, R, atoms, maxb)
+    tt, oo = to_dev(toks), to_dev(offs)
+    bt = to_dev(block_table_identity(R, maxb))
+    cache = torch.zeros(R * maxb * t.shape.block_bytes, dtype=torch.uint8, device="cuda")
+    m = torch.empty(R, dtype=torch.int32, device="cuda")
+    ids = torch.empty((R, maxb), dtype=torch.int32, device="cuda")
+    cr = torch.empty((R, maxb), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    for call in ("gather", "insert"):
+        g = torch.cuda.CUDAGraph()
+        with pytest.raises(P.PTStoreError) as ei:
+            with torch.cuda.graph(g):
+                m.fill_(0)  # the graph is not empty when the refused call ends it
+                if call == "gather":
+                    P.ptstore_gather(t.gpu.h, ids, m, bt, cache, R * maxb)
+                else:
+                    P.ptstore_insert(t.gpu.h, tt, oo, maxb, m, ids, cr)
+        assert ei.value.code == P.PTSTORE_ERR_INVALID
+        assert "captur" in P.ptstore_last_error()
+        torch.cuda.synchronize()
+    # eagerly the same calls grow the scratch and match the oracle
+    t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
+    (_, ids2, cr2), (_, _, rids, rcr) = t.insert(toks, offs, maxb)
+    t.check_meta()
+    t.close()
