@@ -297,7 +297,8 @@ int ptstore_insert(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * Returns PTSTORE_ERR_FULL in that case, with every output written as
  * ptstore_insert writes it (the cut is a prefix of each request, the same
  * as the one-after-another insert gives), else PTSTORE_OK.
- * Errors: those of ptstore_insert, HIP.
+ * Errors: those of ptstore_insert, HIP; INVALID when `stream` is being
+ * captured into a graph (nothing is enqueued; capture ptstore_insert).
  */
 int ptstore_insert_sync(ptstore_t *store, const int32_t *tokens, const int64_t *offsets,
                         int64_t n_tokens, int32_t R, int32_t max_blocks,

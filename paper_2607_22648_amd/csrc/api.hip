@@ -826,6 +826,9 @@ int ptstore_insert(ptstore_t* s, const int32_t* tokens, const int64_t* offsets, 
 int ptstore_insert_sync(ptstore_t* s, const int32_t* tokens, const int64_t* offsets,
                         int64_t n_tokens, int32_t R, int32_t max_blocks, int32_t* m_out,
                         int32_t* ids, uint8_t* created, void* stream) {
+    if (s && capturing((hipStream_t)stream))
+        return fail(PTSTORE_ERR_INVALID, "ptstore_insert_sync waits for its stream: it cannot be "
+                    "captured (capture ptstore_insert)");
     const int rc = ptstore_insert(s, tokens, offsets, n_tokens, R, max_blocks, m_out, ids, created,
                                   stream);
     if (rc || R == 0) return rc;

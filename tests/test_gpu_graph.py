@@ -237,6 +237,16 @@ def test_capture_that_needs_more_scratch_is_refused():
         assert ei.value.code == P.PTSTORE_ERR_INVALID
         assert "captur" in P.ptstore_last_error()
         torch.cuda.synchronize()
+    # the waiting insert is refused under capture whatever its size
+    one = torch.tensor([0, 16], dtype=torch.int64, device="cuda")  # a request of 4 blocks
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with pytest.raises(P.PTStoreError) as ei:
+        with torch.cuda.graph(g):
+            m.fill_(0)
+            P.ptstore_insert_sync(t.gpu.h, tt[:16], one, 4, m, ids, cr)
+    assert ei.value.code == P.PTSTORE_ERR_INVALID and "captured" in P.ptstore_last_error()
+    torch.cuda.synchronize()
     # eagerly the same calls grow the scratch and match the oracle
     t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
     (_, ids2, cr2), (_, _, rids, rcr) = t.insert(toks, offs, maxb)
