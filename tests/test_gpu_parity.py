@@ -581,3 +581,43 @@ def test_insert_sync_reports_refused_blocks(evict):
     assert codes == {P.PTSTORE_OK, P.PTSTORE_ERR_FULL}
     assert t.gpu.stats()["blocks_stored"] == t.ref.count
     t.close()
+
+
+@pytest.mark.parametrize("fill", [0.25, 0.4, 0.5])
+def test_index_load_factors(fill):
+    """A 4096-slot index filled to 25, 40 and 50 % of its slots (50 % is the
+    most a store holds): lookups of stored, extended and fresh sequences
+    match the oracle at every fill, and probing stays short."""
+    rng = np.random.default_rng(int(fill * 100))
+    slots = 4096
+    t = Twin(1, 1, 8, 4, 10_000, index_slots=slots, flags=P.PTSTORE_FLAG_COUNTERS)
+    assert t.gpu.stats()["capacity"] == slots // 2
+    want = int(fill * slots)
+    seqs = []
+    while t.ref.count < want:
+        n = int(rng.integers(1, 9))
+        need = min(8, want - t.ref.count)  # fill to the exact count
+        s = rng.integers(0, 50, size=4 * min(n, need), dtype=np.int32)
+        toks, offs = synth.concat_requests([s])
+        t.insert(toks, offs, 8)
+        seqs.append(s)
+    assert t.gpu.stats()["blocks_stored"] == t.ref.count == want
+    looks = []
+    for _ in range(300):
+        u = rng.random()
+        s = seqs[int(rng.integers(len(seqs)))]
+        if u < 0.4:
+            looks.append(s)  # stored
+        elif u < 0.7:
+            looks.append(np.concatenate([s, rng.integers(0, 50, size=8, dtype=np.int32)]))  # extended
+        else:
+            looks.append(rng.integers(0, 50, size=4 * int(rng.integers(1, 9)), dtype=np.int32))  # fresh
+    toks, offs = synth.concat_requests(looks)
+    t.gpu.reset_counters()
+    (m, ids), (rm, rids) = t.lookup(toks, offs, 12)
+    st = t.gpu.stats()
+    examined = int(np.minimum(np.diff(offs) // 4, 12).sum())
+    assert st["probes"] <= 3 * examined  # linear probing at load <= 0.5 stays short
+    assert rm.sum() > 0
+    t.check_meta()
+    t.close()
