@@ -60,8 +60,10 @@
  *    may be captured and replayed; a replay works on the store as it is
  *    then. A later call with a larger batch regrows the scratch, after which
  *    earlier captures must not be replayed; a captured call that would need
- *    a larger scratch returns INVALID and allocates nothing. A capture keeps
- *    the counting state (ptstore_set_counters) it was made with.
+ *    a larger scratch returns INVALID and allocates nothing. A load captured
+ *    on a stream that had made no call shares the first stream's scratch:
+ *    its replays must not overlap loads enqueued on that stream. A capture
+ *    keeps the counting state (ptstore_set_counters) it was made with.
  *    ptstore_lookup_gather_noalloc
  *    never allocates, whatever the batch (up to its limit).
  */
