@@ -336,11 +336,15 @@ def run_passage(args, torch, P, synth, dev):
                 store.lookup_gather(s["toks"], s["offs"], maxb, s["bt"], cache, m=s["m"],
                                     ids=s["ids"])
 
+    # in the timed steps the library records events around its copy kernel
+    # alone: events around the lookup and the list build too would add
+    # microseconds to every call (a fifth of a step at the tiny shape); the
+    # lookups are timed in a pass of their own afterwards
+    store.set_timing_kinds(1 << P.KIND_GATHER)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     store.kernel_times(P.KIND_GATHER)
-    store.kernel_times(P.KIND_LOOKUP)
     matched = sum(int(s["m"].sum().item()) for s in sub_inputs)
     blocks_examined = sum(int(np.minimum(np.diff(w.request_slice(lo, hi)[1]) // sh.block_tokens,
                                          maxb).sum()) for lo, hi in subs)
@@ -359,7 +363,20 @@ def run_passage(args, torch, P, synth, dev):
     elapsed = time.perf_counter() - t0
     per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
     g_ms, g_n = store.kernel_times(P.KIND_GATHER)
-    l_ms, l_n = store.kernel_times(P.KIND_LOOKUP)
+    # the lookups of the same sub-batches back to back, the library's events
+    # off, one event pair around them (an event pair around each short
+    # launch would add its launch latency)
+    store.set_timing_kinds(0)
+    lk_reps = min(args.steps, 10)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(cur)
+    for _ in range(lk_reps):
+        for s in sub_inputs:
+            store.lookup(s["toks"], s["offs"], maxb, m=s["m"], ids=s["ids"])
+    ev1.record(cur)
+    torch.cuda.synchronize()
+    lookup_ms = ev0.elapsed_time(ev1) / (lk_reps * len(sub_inputs))
+    store.set_timing_kinds(1 << P.KIND_GATHER)
 
     ms_per_step = elapsed * 1e3 / args.steps
     gather_bytes_step = matched * 2 * sh.block_bytes
@@ -414,7 +431,7 @@ def run_passage(args, torch, P, synth, dev):
                              None if args.per_layer else
                              recorded_traffic(args.config, gather_bytes_step * args.steps / max(g_n, 1)),
                              ceiling),
-        "lookup_kernel_avg_ms": round(l_ms / max(l_n, 1), 4),
+        "lookup_ms_per_call": round(lookup_ms, 4),
         "gather_after_cache_flush": flushed,
         # every gather dispatch of this process (warm-up, timed and flushed
         # steps, each step the same blocks), for the rocprofv3 traffic record
@@ -700,7 +717,8 @@ def run_trie(args, torch, P, synth, dev):
     store.kernel_times(P.KIND_LOOKUP)
     store.set_counters(False)
     matched = int(m.sum().item())
-    # fused lookup + gather
+    # fused lookup + gather, with events around the copy kernel alone
+    store.set_timing_kinds(1 << P.KIND_GATHER)
     for _ in range(args.warmup):
         store.lookup_gather(toks, offs, w.depth, bt, cache, m=m, ids=ids)
     torch.cuda.synchronize()

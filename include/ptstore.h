@@ -456,15 +456,26 @@ int ptstore_set_counters(ptstore_t *store, int on);
  * starts in. Two events around each launch add a few microseconds to a
  * short call, so a caller can time back-to-back short calls with them off
  * and one event pair of its own around all of them. Host only: no device
- * work, no wait. Errors: INVALID (NULL store). */
+ * work, no wait. Errors: INVALID (NULL store). The same as
+ * ptstore_set_timing_kinds with every kind (0x7F) or none. */
 int ptstore_set_timing(ptstore_t *store, int on);
+
+/* The events of some kinds only: bit k of `kinds` turns on those around
+ * the kernels of kind k (the kinds of ptstore_kernel_times), and a clear
+ * bit turns them off, for the calls enqueued after this one. A caller that
+ * times short calls back to back can so keep the events around the copy
+ * kernel alone (kinds = 1) and leave the lookup and the descriptor-list
+ * build without them. Host only. Errors: INVALID (NULL store, a bit above
+ * 6). */
+int ptstore_set_timing_kinds(ptstore_t *store, uint32_t kinds);
 
 /* Device buffers of the store (see ptstore_buffers_t); no device work.
  * Errors: INVALID (a NULL argument). */
 int ptstore_get_buffers(ptstore_t *store, ptstore_buffers_t *out);
 
 /*
- * With PTSTORE_FLAG_TIMING: wait for the device, then return the summed
+ * With events on (PTSTORE_FLAG_TIMING, ptstore_set_timing or
+ * ptstore_set_timing_kinds): wait for the device, then return the summed
  * durations (ms) and launch counts of the kernels recorded since the last
  * call, for kind 0 = gather copy kernel, 1 = lookup, 2 = scatter copy
  * kernel, 3 = insert (all its kernels), 4 = descriptor-list build of gather

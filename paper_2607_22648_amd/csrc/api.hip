@@ -76,7 +76,8 @@ struct ptstore {
     void* prep_list;  // the copy scratch holding it
     int32_t prep_R, prep_max_blocks;
     int64_t prep_cache_blocks;
-    // HIP events around kernels (PTSTORE_FLAG_TIMING), per kind
+    // HIP events around kernels, per kind; bit k of timing_kinds records kind k
+    uint32_t timing_kinds;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[7];
     std::vector<hipEvent_t> free_ev;
 };
@@ -222,6 +223,9 @@ hipEvent_t take_event(ptstore_t* s) {
     return e;
 }
 
+// Every kind of kernel ptstore_kernel_times() reports (0..6).
+constexpr uint32_t kAllKinds = 0x7Fu;
+
 // Most event pairs kept per kind between two ptstore_kernel_times() calls;
 // beyond that, launches are no longer recorded (the sum stays consistent).
 constexpr size_t kMaxTimed = 1 << 16;
@@ -233,7 +237,7 @@ struct Timed {
     hipStream_t st;
     hipEvent_t a = nullptr;
     Timed(ptstore_t* s_, int k, hipStream_t st_) : s(s_), kind(k), st(st_) {
-        if ((s->cfg.flags & PTSTORE_FLAG_TIMING) && s->ev[kind].size() < kMaxTimed) {
+        if (((s->timing_kinds >> kind) & 1u) && s->ev[kind].size() < kMaxTimed) {
             a = take_event(s);
             if (a) (void)hipEventRecord(a, st);
         }
@@ -500,6 +504,7 @@ int ptstore_create(const ptstore_config_t* cfg, ptstore_t** out) {
     }
     s->threads = 1024;
     s->grid = 0;
+    s->timing_kinds = (c.flags & PTSTORE_FLAG_TIMING) ? kAllKinds : 0u;
     hipError_t e = hipGetDevice(&s->device);
     if (e == hipSuccess)
         e = hipDeviceGetAttribute(&s->cus, hipDeviceAttributeMultiprocessorCount, s->device);
@@ -946,13 +951,19 @@ int ptstore_set_counters(ptstore_t* s, int on) {
     return PTSTORE_OK;
 }
 
-int ptstore_set_timing(ptstore_t* s, int on) {
-    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_set_timing: null store");
-    if (on)
+int ptstore_set_timing_kinds(ptstore_t* s, uint32_t kinds) {
+    if (!s || (kinds & ~kAllKinds)) return fail(PTSTORE_ERR_INVALID, "ptstore_set_timing_kinds: bad argument");
+    s->timing_kinds = kinds;
+    if (kinds)
         s->cfg.flags |= PTSTORE_FLAG_TIMING;
     else
         s->cfg.flags &= ~(uint32_t)PTSTORE_FLAG_TIMING;
     return PTSTORE_OK;
+}
+
+int ptstore_set_timing(ptstore_t* s, int on) {
+    if (!s) return fail(PTSTORE_ERR_INVALID, "ptstore_set_timing: null store");
+    return ptstore_set_timing_kinds(s, on ? kAllKinds : 0u);
 }
 
 int ptstore_reset_counters(ptstore_t* s) {

@@ -63,6 +63,7 @@ EXPORTS = ("ptstore_create", "ptstore_destroy", "ptstore_lookup", "ptstore_gathe
            "ptstore_bandwidth_probe", "ptstore_replicate", "ptstore_gather_layers",
            "ptstore_scatter_layers", "ptstore_gather_prepare", "ptstore_gather_prepared",
            "ptstore_set_counters", "ptstore_set_timing", "ptstore_lookup_gather_noalloc",
+           "ptstore_set_timing_kinds",
            "ptstore_insert_sync")
 
 
@@ -86,6 +87,7 @@ def _load() -> C.CDLL:
         "ptstore_reset_counters": [p],
         "ptstore_set_counters": [p, C.c_int],
         "ptstore_set_timing": [p, C.c_int],
+        "ptstore_set_timing_kinds": [p, C.c_uint32],
         "ptstore_get_buffers": [p, C.POINTER(ptstore_buffers_t)],
         "ptstore_kernel_times": [p, i32, C.POINTER(d), C.POINTER(i64)],
         "ptstore_set_copy_shape": [p, i32, i32, i32],
@@ -324,6 +326,10 @@ def ptstore_set_timing(h, on: bool) -> None:
     _check("ptstore_set_timing", _lib.ptstore_set_timing(h, 1 if on else 0))
 
 
+def ptstore_set_timing_kinds(h, kinds: int) -> None:
+    _check("ptstore_set_timing_kinds", _lib.ptstore_set_timing_kinds(h, kinds))
+
+
 def ptstore_get_buffers(h) -> ptstore_buffers_t:
     b = ptstore_buffers_t()
     _check("ptstore_get_buffers", _lib.ptstore_get_buffers(h, C.byref(b)))
@@ -499,6 +505,10 @@ class PrefixStore:
 
     def set_timing(self, on: bool):
         ptstore_set_timing(self.h, on)
+
+    def set_timing_kinds(self, kinds: int):
+        """Events around the kernels of the kinds whose bit is set only."""
+        ptstore_set_timing_kinds(self.h, kinds)
 
     def kernel_times(self, kind: int) -> Tuple[float, int]:
         return ptstore_kernel_times(self.h, kind)

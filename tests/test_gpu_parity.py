@@ -207,6 +207,51 @@ def test_timing_switch_at_run_time():
     s.close()
 
 
+def test_timing_of_some_kinds_only():
+    """ptstore_set_timing_kinds records the kinds whose bit is set and no
+    other: with kinds = 1 a fused lookup + gather reports its copy kernel
+    alone. A bit above the last kind is refused."""
+    rng = np.random.default_rng(19)
+    atoms = _atoms(rng, 3, 16, 5)
+    sh = P.StoreShape(2, 1, 8, 16)
+    s = P.PrefixStore(sh, 3000)
+    toks, offs = random_block_batch(rng, 30, atoms, 40)
+    m0, ids0, cr = s.insert(to_dev(toks), to_dev(offs), 40)
+    R = len(offs) - 1
+    bt = to_dev(block_table_identity(R, 40))
+    src = torch.randint(0, 256, (R * 40 * sh.block_bytes,), dtype=torch.uint8, device=DEV)
+    s.scatter(ids0, cr, bt, src)
+    cache = torch.zeros_like(src)
+    s.set_timing_kinds(1 << P.KIND_GATHER)
+    for _ in range(2):
+        m, ids = s.lookup_gather(to_dev(toks), to_dev(offs), 40, bt, cache)
+    torch.cuda.synchronize()
+    g_ms, g_n = s.kernel_times(P.KIND_GATHER)
+    assert g_n == 2 and g_ms > 0
+    for k in (P.KIND_LOOKUP, P.KIND_SELECT, P.KIND_INSERT, P.KIND_SCATTER):
+        assert s.kernel_times(k)[1] == 0
+    s.set_timing_kinds(1 << P.KIND_LOOKUP | 1 << P.KIND_SELECT)
+    s.lookup_gather(to_dev(toks), to_dev(offs), 40, bt, cache, m=m, ids=ids)
+    assert s.kernel_times(P.KIND_GATHER)[1] == 0
+    assert s.kernel_times(P.KIND_LOOKUP)[1] == 1 and s.kernel_times(P.KIND_SELECT)[1] == 1
+    with pytest.raises(P.PTStoreError) as ei:
+        s.set_timing_kinds(1 << 7)
+    assert ei.value.code == P.PTSTORE_ERR_INVALID
+    # the outputs: the ids the insert returned, and the same bytes as a load
+    # with every event off
+    s.set_timing_kinds(0)
+    cache2 = torch.zeros_like(src)
+    m2, ids2 = s.lookup_gather(to_dev(toks), to_dev(offs), 40, bt, cache2)
+    assert s.kernel_times(P.KIND_GATHER)[1] == 0
+    np.testing.assert_array_equal(host(m), host(m0))
+    np.testing.assert_array_equal(host(ids), host(ids0))
+    np.testing.assert_array_equal(host(m2), host(m0))
+    np.testing.assert_array_equal(host(ids2), host(ids0))
+    np.testing.assert_array_equal(host(cache), host(cache2))
+    assert int(host(m).sum()) > 0
+    s.close()
+
+
 def test_hash_seed_does_not_change_results():
     rng = np.random.default_rng(6)
     atoms = _atoms(rng, 3, 16, 5)
