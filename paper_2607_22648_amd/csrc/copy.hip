@@ -93,15 +93,17 @@ __device__ inline int32_t home_row(const TierView& t, int32_t id) {
 template <bool GATHER>
 __device__ inline bool selected(const SelectArgs& a, int64_t rb, unsigned long long count,
                                 Pair* out, bool* bad) {
-    *bad = false;
-    if (!GATHER && !a.created[rb]) return false;
+    // every load before any test (the three arrays are [R][max_blocks], so
+    // the loads are in bounds): with no branch between them and their use
+    // they are issued together and cost one trip instead of two or three
+    const bool made = GATHER || a.created[rb] != 0;
     const int32_t cb = a.block_table[rb];
-    if (cb < 0) return false;
     const int32_t id = a.ids[rb];
-    if ((int64_t)cb >= a.cache_blocks || id < 0 || (unsigned long long)id >= count) {
-        *bad = true;
-        return false;
-    }
+    const bool skip = !made | (cb < 0);
+    const bool out_of_range = ((int64_t)cb >= a.cache_blocks) | (id < 0) |
+                              ((unsigned long long)id >= count);
+    *bad = !skip & out_of_range;
+    if (skip | out_of_range) return false;
     out->row = GATHER ? gather_row(a.tier, id) : home_row(a.tier, id);
     out->cb = cb;
     return true;
@@ -118,76 +120,32 @@ __device__ inline unsigned long long lanes_below(int lane) {
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// Request r's blocks to move, counted by the whole wave: in device rows, in
+// host-tier rows, and entries out of range (added to *bad).
 template <bool GATHER>
-__global__ __launch_bounds__(kSelThreads) void k_select_count(SelectArgs a) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
-    if (r >= a.R) return;
+__device__ inline void count_row(const SelectArgs& a, int64_t r, int lane, unsigned long long count,
+                                 int32_t* cnt, int32_t* cnt_h, int32_t* bad) {
     const int32_t n = row_len<GATHER>(a, r);
-    const unsigned long long count = a.state->count;
-    int32_t cnt = 0, cnt_h = 0, bad = 0;
+    int32_t c = 0, ch = 0;
     for (int32_t b0 = 0; b0 < n; b0 += kWave) {
         const int32_t b = b0 + lane;
         Pair p;
         bool isbad = false;
         const bool sel = b < n && selected<GATHER>(a, r * a.max_blocks + b, count, &p, &isbad);
-        cnt += __popcll(ballot64(sel && p.row < a.tier.dev_rows));
-        cnt_h += __popcll(ballot64(sel && p.row >= a.tier.dev_rows));
-        bad += __popcll(ballot64(isbad));
+        c += __popcll(ballot64(sel && p.row < a.tier.dev_rows));
+        ch += __popcll(ballot64(sel && p.row >= a.tier.dev_rows));
+        *bad += __popcll(ballot64(isbad));
     }
-    if (lane == 0) {
-        a.sc.row_cnt[r] = cnt;
-        a.sc.row_cnt_h[r] = cnt_h;
-        if (bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
-    }
+    *cnt = c;
+    *cnt_h = ch;
 }
 
-// One workgroup: exclusive scans of row_cnt and row_cnt_h into row_base and
-// row_base_h, their totals into *total and *total_h.
-__global__ __launch_bounds__(1024) void k_select_scan(SelectArgs a) {
-    __shared__ long long part[1024], part_h[1024];
-    const int R = a.R;
-    const int t = threadIdx.x, nt = blockDim.x;
-    const int per = (R + nt - 1) / nt;
-    const int lo = min(R, t * per), hi = min(R, lo + per);
-    long long s = 0, s_h = 0;
-    for (int i = lo; i < hi; ++i) {
-        s += a.sc.row_cnt[i];
-        s_h += a.sc.row_cnt_h[i];
-    }
-    part[t] = s;
-    part_h[t] = s_h;
-    __syncthreads();
-    for (int d = 1; d < nt; d <<= 1) {
-        const long long v = t >= d ? part[t - d] : 0;
-        const long long v_h = t >= d ? part_h[t - d] : 0;
-        __syncthreads();
-        part[t] += v;
-        part_h[t] += v_h;
-        __syncthreads();
-    }
-    long long run = part[t] - s, run_h = part_h[t] - s_h;
-    for (int i = lo; i < hi; ++i) {
-        a.sc.row_base[i] = run;
-        a.sc.row_base_h[i] = run_h;
-        run += a.sc.row_cnt[i];
-        run_h += a.sc.row_cnt_h[i];
-    }
-    if (t == nt - 1) {
-        *a.sc.total = (unsigned long long)part[nt - 1];
-        *a.sc.total_h = (unsigned long long)part_h[nt - 1];
-    }
-}
-
+// Request r's descriptors, written by the whole wave from list position pos
+// (device rows) and pos_h (host-tier rows), in block order.
 template <bool GATHER>
-__global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
-    if (r >= a.R) return;
+__device__ inline void fill_row(const SelectArgs& a, int64_t r, int lane, unsigned long long count,
+                                int64_t pos, int64_t pos_h) {
     const int32_t n = row_len<GATHER>(a, r);
-    const unsigned long long count = a.state->count;
-    int64_t pos = a.sc.row_base[r];
-    int64_t pos_h = (int64_t)*a.sc.total + a.sc.row_base_h[r];  // host rows after all device rows
     for (int32_t b0 = 0; b0 < n; b0 += kWave) {
         const int32_t b = b0 + lane;
         Pair p;
@@ -210,6 +168,150 @@ __global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
             }
         }
     }
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(kSelThreads) void k_select_count(SelectArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
+    if (r >= a.R) return;
+    int32_t cnt, cnt_h, bad = 0;
+    count_row<GATHER>(a, r, lane, a.state->count, &cnt, &cnt_h, &bad);
+    if (lane == 0) {
+        a.sc.row_cnt[r] = cnt;
+        a.sc.row_cnt_h[r] = cnt_h;
+        if (bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
+    }
+}
+
+// One workgroup: exclusive scans of row_cnt and row_cnt_h into row_base and
+// row_base_h, their totals into *total and *total_h. The requests go in
+// tiles of 1024 x 4, each thread holding 4 neighbouring counts, so every
+// load instruction reads whole lines and a tile costs one wave scan and two
+// barriers. A call has at most 2^29 entries, so every sum fits in 32 bits.
+constexpr int kScanPer = 4;
+
+__global__ __launch_bounds__(1024) void k_select_scan(SelectArgs a) {
+    __shared__ int32_t wsum[1024 / kWave], wsum_h[1024 / kWave];
+    const int R = a.R;
+    const int t = threadIdx.x, lane = t & (kWave - 1), wv = t / kWave;
+    const int nw = blockDim.x / kWave;
+    int32_t carry = 0, carry_h = 0;
+    for (int base = 0; base < R; base += blockDim.x * kScanPer) {
+        const int i0 = base + t * kScanPer;
+        int32_t v[kScanPer], vh[kScanPer];
+        int32_t s = 0, sh = 0;
+#pragma unroll
+        for (int k = 0; k < kScanPer; ++k) {
+            v[k] = i0 + k < R ? a.sc.row_cnt[i0 + k] : 0;
+            vh[k] = i0 + k < R ? a.sc.row_cnt_h[i0 + k] : 0;
+            s += v[k];
+            sh += vh[k];
+        }
+        int32_t x = s, xh = sh;  // inclusive scan over the wave
+        for (int d = 1; d < kWave; d <<= 1) {
+            const int32_t y = __shfl_up(x, d, kWave), yh = __shfl_up(xh, d, kWave);
+            if (lane >= d) {
+                x += y;
+                xh += yh;
+            }
+        }
+        if (lane == kWave - 1) {
+            wsum[wv] = x;
+            wsum_h[wv] = xh;
+        }
+        __syncthreads();
+        int32_t run = carry + x - s, run_h = carry_h + xh - sh;
+        for (int w = 0; w < nw; ++w) {
+            const int32_t ws = wsum[w], wsh = wsum_h[w];
+            if (w < wv) {
+                run += ws;
+                run_h += wsh;
+            }
+            carry += ws;
+            carry_h += wsh;
+        }
+#pragma unroll
+        for (int k = 0; k < kScanPer; ++k) {
+            if (i0 + k < R) {
+                a.sc.row_base[i0 + k] = run;
+                a.sc.row_base_h[i0 + k] = run_h;
+            }
+            run += v[k];
+            run_h += vh[k];
+        }
+        __syncthreads();  // wsum is written again by the next tile
+    }
+    if (t == 0) {
+        *a.sc.total = (unsigned long long)carry;
+        *a.sc.total_h = (unsigned long long)carry_h;
+    }
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
+    if (r >= a.R) return;
+    // host rows after all device rows
+    fill_row<GATHER>(a, r, lane, a.state->count, a.sc.row_base[r],
+                     (int64_t)*a.sc.total + a.sc.row_base_h[r]);
+}
+
+// Small batches: count, scan and fill in one workgroup, the counts and
+// bases in LDS, so that building the list costs one launch instead of
+// three. Wave w takes requests w, w+16, ...; with at most 4 requests of at
+// most 2 windows per wave (the host's condition) its serial walk stays as
+// short as the three kernels' launch gaps.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / kWave;
+constexpr int32_t kSmallMaxR = 64;
+constexpr int64_t kSmallMaxEntries = 8192;
+
+template <bool GATHER>
+__global__ __launch_bounds__(kSmallThreads) void k_select_small(SelectArgs a) {
+    __shared__ int32_t base[kSmallMaxR], base_h[kSmallMaxR];
+    __shared__ int32_t total_dev;
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    const unsigned long long count = a.state->count;
+    int32_t bad = 0;
+    for (int r = wv; r < a.R; r += kSmallWaves) {
+        int32_t c, ch;
+        count_row<GATHER>(a, r, lane, count, &c, &ch, &bad);
+        if (lane == 0) {
+            base[r] = c;
+            base_h[r] = ch;
+        }
+    }
+    if (lane == 0 && bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
+    __syncthreads();
+    // exclusive scan over the requests, thread t holding request t (R <= 64:
+    // the first wave); totals of at most kSmallMaxEntries fit in 32 bits
+    const int t = threadIdx.x;
+    if (wv == 0) {
+        const int32_t v = t < a.R ? base[t] : 0, vh = t < a.R ? base_h[t] : 0;
+        int32_t s = v, sh = vh;
+        for (int d = 1; d < kWave; d <<= 1) {
+            const int32_t x = __shfl_up(s, d, kWave), xh = __shfl_up(sh, d, kWave);
+            if (lane >= d) {
+                s += x;
+                sh += xh;
+            }
+        }
+        if (t < a.R) {
+            base[t] = s - v;
+            base_h[t] = sh - vh;
+        }
+        if (lane == kWave - 1) {
+            total_dev = s;
+            *a.sc.total = (unsigned long long)s;
+            *a.sc.total_h = (unsigned long long)sh;
+        }
+    }
+    __syncthreads();
+    const int64_t total = total_dev;  // host rows after all device rows
+    for (int r = wv; r < a.R; r += kSmallWaves)
+        fill_row<GATHER>(a, r, lane, count, base[r], total + base_h[r]);
 }
 
 struct CopyArgs {
@@ -364,6 +466,10 @@ hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, 
                   const uint8_t* created, const int32_t* bt, int32_t R, int32_t max_blocks,
                   int64_t cache_blocks, hipStream_t s) {
     SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc, p.tier};
+    if (R <= kSmallMaxR && (int64_t)R * max_blocks <= kSmallMaxEntries) {
+        hipLaunchKernelGGL(k_select_small<GATHER>, dim3(1), dim3(kSmallThreads), 0, s, a);
+        return hipGetLastError();
+    }
     const unsigned grid = (unsigned)((R + kSelWaves - 1) / kSelWaves);
     hipLaunchKernelGGL(k_select_count<GATHER>, dim3(grid), dim3(kSelThreads), 0, s, a);
     hipError_t e = hipGetLastError();
