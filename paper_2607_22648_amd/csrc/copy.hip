@@ -20,8 +20,9 @@
 // consolidation):
 //   select  count the blocks each request must move (wave per request), scan
 //           the counts, then write a dense descriptor list of (id, cache
-//           block) pairs, compacted with a wave ballot. Entries with an id or
-//           cache block out of range are dropped here and counted.
+//           block) pairs, compacted with a wave ballot (three kernels; one
+//           workgroup does all three for a small batch). Entries with an id
+//           or cache block out of range are dropped here and counted.
 //   copy    workgroups walk (descriptor, group of chunks) units; the number
 //           of units is read on the device, so no host round trip separates
 //           the parts. Threads move 16-byte vectors with non-temporal loads
@@ -30,7 +31,8 @@
 // the [request][block] arrays (a few created blocks per insert, half the
 // requests missing the store). The default copy shape gives each
 // 1024-thread workgroup one chunk per unit (two vectors per thread for a
-// 32 KiB chunk). Pure HBM streaming: no LDS, no MFMA.
+// 32 KiB chunk). The copies are pure HBM streaming: no MFMA, and LDS only for
+// the per-layer kernel's table of layer bases.
 #include "kernels.hpp"
 
 namespace ptsd {
