@@ -80,7 +80,7 @@ def recorded_traffic(config: str, bytes_per_launch: float):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("copy_hip_sha256") != copy_source_sha():
+    if rec.get("copy_code_sha256") != copy_source_sha():
         return None
     return int(round(rec["traffic_over_algorithmic"] * bytes_per_launch))
 

@@ -43,6 +43,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 from collections import defaultdict
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -53,7 +54,13 @@ PLAIN_COPY = "__amd_rocclr_copyBuffer"
 
 
 def copy_source_sha() -> str:
-    return hashlib.sha256(open(COPY_SRC, "rb").read()).hexdigest()
+    """SHA-256 of the copy kernels' code in csrc/copy.hip: comments dropped and
+    whitespace runs collapsed, so that editing a comment does not void the
+    counter records taken on that code."""
+    src = open(COPY_SRC).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return hashlib.sha256(" ".join(src.split()).encode()).hexdigest()
 
 
 def _one(pattern: str) -> str:
@@ -176,7 +183,7 @@ def gather_traffic(a):
     rec = {
         "kernel": gk,
         "workload": bench["config"]["workload"],
-        "copy_hip_sha256": copy_source_sha(),
+        "copy_code_sha256": copy_source_sha(),
         "dispatches": n,
         "raw_fetch_kib_per_dispatch": round(mean(g_fetch), 1),
         "raw_write_kib_per_dispatch": round(mean(g_write), 1),
@@ -245,7 +252,7 @@ def gather_traffic(a):
     lines += [f"| traffic, all gather dispatches (scaled) | {traffic_total / 1e9:.3f} GB |",
               f"| algorithmic bytes, all gather dispatches | {algo_total / 1e9:.3f} GB |",
               f"| traffic / algorithmic | {ratio:.4f} |"] + lines_req + [
-              "", f"Copy kernel source SHA-256: `{rec['copy_hip_sha256']}`."]
+              "", f"Copy kernel code SHA-256 (csrc/copy.hip without comments and whitespace): `{rec['copy_code_sha256']}`."]
     with open(os.path.join(a.out, f"{a.name}_hbm_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(rec))
