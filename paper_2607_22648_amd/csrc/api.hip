@@ -380,6 +380,8 @@ size_t carve_evict(void* base, int64_t capacity, EvictView* ev) {
 }  // namespace
 
 namespace ptsd {
+int set_last_error(int code, const char* what) { return fail(code, what); }
+
 __global__ void k_fill_slots(Slot* slots, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {

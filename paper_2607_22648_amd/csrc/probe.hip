@@ -13,6 +13,10 @@
 
 #include "ptstore.h"
 
+namespace ptsd {
+int set_last_error(int code, const char* what);  // csrc/api.hip
+}
+
 namespace {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
@@ -57,13 +61,15 @@ extern "C" __attribute__((visibility("default"))) int ptstore_bandwidth_probe(
     int32_t kind, const void* a, void* b, int64_t bytes, void* stream) {
     if (kind < 0 || kind > 2 || bytes < 16 || bytes > (32ll << 30) || (bytes & 15) || !a || !b ||
         (reinterpret_cast<uintptr_t>(a) & 15) || (reinterpret_cast<uintptr_t>(b) & 15))
-        return PTSTORE_ERR_INVALID;
+        return ptsd::set_last_error(PTSTORE_ERR_INVALID,
+                                    "ptstore_bandwidth_probe: kind 0..2, bytes a multiple of 16 up to "
+                                    "32 GiB, 16-byte aligned buffers");
     hipStream_t s = (hipStream_t)stream;
     const long n16 = (long)(bytes >> 4);
     int cus = 0, dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return PTSTORE_ERR_HIP;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return ptsd::set_last_error(PTSTORE_ERR_HIP, "ptstore_bandwidth_probe: device query");
     if (kind == 0)
         hipLaunchKernelGGL(k_read, dim3((unsigned)(cus * 32)), dim3(256), 0, s, (const v4u*)a, n16, (v4u*)b);
     else if (kind == 1)
@@ -71,5 +77,7 @@ extern "C" __attribute__((visibility("default"))) int ptstore_bandwidth_probe(
     else
         hipLaunchKernelGGL(k_copy, dim3((unsigned)((n16 + 2047) / 2048)), dim3(1024), 0, s,
                            (const v4u*)a, (v4u*)b, n16);
-    return hipGetLastError() == hipSuccess ? PTSTORE_OK : PTSTORE_ERR_HIP;
+    return hipGetLastError() == hipSuccess
+               ? PTSTORE_OK
+               : ptsd::set_last_error(PTSTORE_ERR_HIP, "ptstore_bandwidth_probe: launch");
 }
