@@ -419,6 +419,12 @@ class PrefixStore:
         except Exception:
             pass
 
+    def __enter__(self) -> "PrefixStore":
+        return self
+
+    def __exit__(self, *exc) -> None:
+        self.close()
+
     def cache_blocks(self, cache: torch.Tensor) -> int:
         return _cache_blocks(cache, self.shape.block_bytes)
 
