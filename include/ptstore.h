@@ -314,7 +314,11 @@ int ptstore_insert_sync(ptstore_t *store, const int32_t *tokens, const int64_t *
  * copy each chunk of cache[layer][K|V][block_table[r][b]] into pool block
  * ids[r][b] (its home row: device pool or host tier). Out-of-range ids /
  * cache blocks are skipped and counted in bad_entries. Uses the same
- * store-owned descriptor scratch as ptstore_gather. Errors as ptstore_gather.
+ * store-owned descriptor scratch as ptstore_gather. The pool is not cleared
+ * when the store is made, and an evicted id keeps its old bytes: a block's
+ * tensors (or the layers of them ptstore_scatter_layers did not write) are
+ * undefined until a scatter writes them, and a gather of them copies
+ * whatever the row holds. Errors as ptstore_gather.
  */
 int ptstore_scatter(ptstore_t *store, const int32_t *ids, const uint8_t *created,
                     const int32_t *block_table, int32_t R, int32_t max_blocks,
