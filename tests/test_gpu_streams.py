@@ -37,9 +37,13 @@ def _filled(rng, atoms, t, n_batches, R, maxb):
         t.scatter_random(ids, cr, rids, rcr, block_table_identity(Ri, maxb), seed=1000 + k)
 
 
+@pytest.mark.parametrize("sizes", [(37, 11), (100, 11)])
 @pytest.mark.parametrize("host_blocks,evict", [(0, False), (300, False), (300, True)])
-def test_loads_on_two_streams(host_blocks, evict):
-    rng = np.random.default_rng(11 + host_blocks + evict)
+def test_loads_on_two_streams(host_blocks, evict, sizes):
+    """Two streams' lookups + gathers with no order between them; with
+    (100, 11) requests one stream lists its blocks in three kernels and the
+    other in one workgroup."""
+    rng = np.random.default_rng(11 + host_blocks + evict + sizes[0])
     atoms = _atoms(rng, 6, 4, 500)
     maxb = 10
     flags = P.PTSTORE_FLAG_EVICT if evict else 0
@@ -50,7 +54,7 @@ def test_loads_on_two_streams(host_blocks, evict):
         t.gpu.replicate()
         t.check_replicas()
     batches = []
-    for R in (37, 11):  # different sizes: each stream's scratch has its own size
+    for R in sizes:  # different sizes: each stream's scratch has its own size
         toks, offs = random_block_batch(rng, R, atoms, maxb + 2, tail_p=0.3)
         batches.append((toks, offs, R))
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
