@@ -135,3 +135,34 @@ def test_profile_summary_dispatch_window(tmp_path):
                         "--window", "k_lookup<16, false>:3:4", "--out", str(out), "--name", "w",
                         "--cmd", "cmd"], capture_output=True, text=True, cwd=ROOT, timeout=120)
     assert p.returncode != 0 and "holds 6 dispatches" in p.stderr  # a slice past the end is refused
+
+
+def test_copy_code_hash_ignores_comments_only(tmp_path, monkeypatch):
+    """The counter records are keyed to the copy kernels' code: editing a
+    comment or the spacing keeps the key, changing code changes it, and
+    bench.py reports the recorded traffic only under the same key."""
+    sys.path.insert(0, ROOT)
+    from paper_2607_22648_amd import profile_summary as ps
+    src = open(ps.COPY_SRC).read()
+    base = ps.copy_source_sha()
+    variants = {
+        "comment": src.replace("#include", "// a new comment line\n#include", 1),
+        "block comment": src.replace("#include", "/* a block\n   comment */ #include", 1),
+        "spacing": src.replace("\n", "\n\n", 5),
+        "code": src.replace("kUnroll = 8", "kUnroll = 4", 1),
+    }
+    keys = {}
+    for name, text in variants.items():
+        f = tmp_path / f"{name.replace(' ', '_')}.hip"
+        f.write_text(text)
+        monkeypatch.setattr(ps, "COPY_SRC", str(f))
+        keys[name] = ps.copy_source_sha()
+    assert keys["comment"] == base and keys["block comment"] == base and keys["spacing"] == base
+    assert keys["code"] != base
+    import bench
+    monkeypatch.setattr(ps, "COPY_SRC", str(tmp_path / "code.hip"))
+    assert bench.recorded_traffic("llama8b", 1e9) is None
+    monkeypatch.undo()
+    rec = json.load(open(os.path.join(ROOT, "profiles", "gather_llama8b_traffic.json")))
+    if rec.get("copy_code_sha256") == base:
+        assert bench.recorded_traffic("llama8b", 1e9) == round(rec["traffic_over_algorithmic"] * 1e9)
