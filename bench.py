@@ -15,9 +15,10 @@ popular passages (57,344 blocks, 120 GB); two sub-batches of 128 requests
 share one 68.7 GB paged cache.
 
 Prints one JSON line. ``value`` = requests/s of the whole job, inputs resident
-in HBM. ``roofline`` = the gather kernel's algorithmic bytes (pool read +
-cache write of every matched block) over its average duration, measured with
-HIP events the library records on the launch stream. ``cpu_baseline`` = the
+in HBM. ``roofline`` = the gather kernel's algorithmic bytes (one pool read of
+each distinct stored block a call needs + one cache write of every matched
+block) over its average duration, measured with HIP events the library
+records on the launch stream. ``cpu_baseline`` = the
 CPU oracle, single-threaded, on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -253,6 +254,15 @@ def base_line(args, value, unit, ms_per_step, config):
             "data": "synthetic", "config": config}
 
 
+def gather_rows(torch, ids, m):
+    """(distinct stored blocks, matched blocks) of one gather call. The copy
+    reads each distinct stored block once and writes it to every cache block
+    that needs it: (distinct + matched) blocks are its algorithmic bytes."""
+    sel = torch.arange(ids.shape[1], device=ids.device)[None, :] < m[:, None]
+    rows = ids[sel]
+    return int(torch.unique(rows).numel()), int(rows.numel())
+
+
 def roofline(kernel, bytes_per_launch, avg_ms, launches, traffic, ceiling=None):
     achieved = bytes_per_launch / (avg_ms * 1e6)
     out = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
@@ -261,7 +271,7 @@ def roofline(kernel, bytes_per_launch, avg_ms, launches, traffic, ceiling=None):
            "bytes_per_launch": int(bytes_per_launch)}
     if ceiling:
         # the practical ceiling on the same buffers: the faster of a pure read
-        # and a pure write stream (a gather moves as many bytes each way)
+        # and a pure write stream
         c = max(ceiling["read_GBps"], ceiling["write_GBps"])
         out["frac_of_measured_stream_ceiling"] = round(achieved / c, 4)
     return out
@@ -347,7 +357,9 @@ def run_passage(args, torch, P, synth, dev):
         step()
     torch.cuda.synchronize()
     store.kernel_times(P.KIND_GATHER)
-    matched = sum(int(s["m"].sum().item()) for s in sub_inputs)
+    rows = [gather_rows(torch, s["ids"], s["m"]) for s in sub_inputs]
+    distinct = sum(d for d, _ in rows)
+    matched = sum(n for _, n in rows)
     blocks_examined = sum(int(np.minimum(np.diff(w.request_slice(lo, hi)[1]) // sh.block_tokens,
                                          maxb).sum()) for lo, hi in subs)
 
@@ -381,7 +393,7 @@ def run_passage(args, torch, P, synth, dev):
     store.set_timing_kinds(1 << P.KIND_GATHER)
 
     ms_per_step = elapsed * 1e3 / args.steps
-    gather_bytes_step = matched * 2 * sh.block_bytes
+    gather_bytes_step = (distinct + matched) * sh.block_bytes
     lookup_bytes_step = blocks_examined * LOOKUP_BYTES_PER_BLOCK
     step_GBps = (gather_bytes_step + lookup_bytes_step) / (ms_per_step * 1e6)
     st = store.stats()
@@ -426,7 +438,8 @@ def run_passage(args, torch, P, synth, dev):
         "hbm_GBps": round(step_GBps, 1),
         "hbm_frac": round(step_GBps / HBM_PEAK_GBPS, 4),
         "matched_blocks_per_step": matched,
-        "roofline": roofline("k_copy_pairs<true> (gather)" if not sh.layer_chunk_bytes
+        "distinct_blocks_per_step": distinct,
+        "roofline": roofline("k_copy_slices (gather)" if not sh.layer_chunk_bytes
                              else "k_copy_spans<true> (gather)",
                              gather_bytes_step * args.steps / max(g_n, 1),
                              g_ms / max(g_n, 1), g_n,
@@ -439,7 +452,9 @@ def run_passage(args, torch, P, synth, dev):
         # steps, each step the same blocks), for the rocprofv3 traffic record
         "gather_all": None if args.per_layer else {
             "dispatches": (args.warmup + args.steps + (args.steps if flushed else 0)) * len(subs),
-            "bytes": (args.warmup + args.steps + (args.steps if flushed else 0)) * gather_bytes_step},
+            "bytes": (args.warmup + args.steps + (args.steps if flushed else 0)) * gather_bytes_step,
+            "read_bytes": (args.warmup + args.steps + (args.steps if flushed else 0)) * distinct
+            * sh.block_bytes},
         "hbm_ceiling": ceiling,
         "prefill": pre,
         "cpu_baseline": cpu,
@@ -616,6 +631,8 @@ def run_tiered(args, torch, P, synth, dev):
         del cache_h
     store.close()
     torch.cuda.empty_cache()
+    # one request per gather call, and a request's blocks are distinct: each
+    # matched block is read once and written once
     gather_bytes_step = b["_matched"] * 2 * sh.block_bytes
     out = base_line(args, w.n_requests * steps / b["_elapsed"], "requests/s",
                     b["_elapsed"] * 1e3 / steps, {
@@ -632,13 +649,13 @@ def run_tiered(args, torch, P, synth, dev):
         # the path is bound by the host link: the copy kernel's reads of
         # host-tier rows, their bytes per step over the time the link carries
         # them, against the link's published peak
-        "roofline": {"bound": "host link", "kernel": "k_copy_pairs<true> (gather, host-tier rows)",
+        "roofline": {"bound": "host link", "kernel": "k_copy_slices (gather, host-tier rows)",
                      "achieved": hl, "peak": HOST_LINK_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(hl / HOST_LINK_PEAK_GBPS, 4) if hl else None, "traffic": None,
                      "bytes_per_step": b["host_GB_per_step"] * 1e9,
                      "frac_of_measured_link_ceiling": round(hl / link["read_GBps"], 4) if hl else None},
         # every gather launch of a step (host-tier and device rows) against HBM
-        "gather_all_launches": roofline("k_copy_pairs<true> (gather)", gather_bytes_step / len(subs),
+        "gather_all_launches": roofline("k_copy_slices (gather)", gather_bytes_step / len(subs),
                                         b["_g_ms"] / max(b["gather_launches"], 1),
                                         b["gather_launches"], None),
         "host_link": {"achieved": hl, "ceiling": link["read_GBps"],
@@ -727,7 +744,8 @@ def run_trie(args, torch, P, synth, dev):
     compares = stt["token_compares"]
     store.kernel_times(P.KIND_LOOKUP)
     store.set_counters(False)
-    matched = int(m.sum().item())
+    distinct, matched = gather_rows(torch, ids, m)
+    trie_bytes = (distinct + matched) * sh.block_bytes
     # fused lookup + gather, with events around the copy kernel alone
     store.set_timing_kinds(1 << P.KIND_GATHER)
     for _ in range(args.warmup):
@@ -781,12 +799,13 @@ def run_trie(args, torch, P, synth, dev):
                         "blocks_examined": int(R * w.depth),
                         "algorithmic_GBps": round(R * w.depth * LOOKUP_BYTES_PER_BLOCK
                                                   / (lk_avg * 1e6), 1)},
-        "matched_blocks": matched,
-        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes, g_ms / max(g_n, 1),
-                             g_n, recorded_traffic("trie", matched * 2 * sh.block_bytes), ceiling),
+        "matched_blocks": matched, "distinct_blocks": distinct,
+        "roofline": roofline("k_copy_slices (gather)", trie_bytes, g_ms / max(g_n, 1),
+                             g_n, recorded_traffic("trie", trie_bytes), ceiling),
         "hbm_ceiling": ceiling,
         "gather_all": {"dispatches": args.warmup + args.steps,
-                       "bytes": (args.warmup + args.steps) * matched * 2 * sh.block_bytes},
+                       "bytes": (args.warmup + args.steps) * trie_bytes,
+                       "read_bytes": (args.warmup + args.steps) * distinct * sh.block_bytes},
         "prefill": {"insert_ms": round(ins_ms, 3), "insert_calls": ins_n,
                     "scatter_ms": round(sc_ms, 3), "blocks": created_total},
         "cpu_baseline": cpu,
@@ -819,15 +838,19 @@ def run_stream(args, torch, P, synth, dev):
     n_timed = min(args.steps, len(rounds) - args.warmup)
 
     def one_round(i):
+        """The round's gather list (ids, m; kept for its distinct blocks) and
+        the created flags of its insert."""
         lt, lo, it, io = rounds[i]
         store.lookup_gather(lt, lo, maxb, bt, cache, m=m, ids=ids)
+        got = (ids.clone(), m.clone())
         _, iids, icr = store.insert(it, io, maxb)
         store.scatter(iids, icr, bt[:io.numel() - 1], cache)
-        return m.sum(), icr
+        return got, icr
 
-    warm = [one_round(i)[0] for i in range(args.warmup)]
+    warm = [gather_rows(torch, *one_round(i)[0]) for i in range(args.warmup)]
     torch.cuda.synchronize()
-    matched_warm = int(sum(int(x.item()) for x in warm))
+    distinct_warm = sum(d for d, _ in warm)
+    matched_warm = sum(n for _, n in warm)
     for k in (P.KIND_GATHER, P.KIND_LOOKUP, P.KIND_INSERT, P.KIND_SCATTER, P.KIND_EVICT):
         store.kernel_times(k)
     blocks0 = store.stats()["blocks_stored"]
@@ -836,11 +859,13 @@ def run_stream(args, torch, P, synth, dev):
     keep = []
     t0 = time.perf_counter()
     for i in range(args.warmup, args.warmup + n_timed):
-        ms, cr = one_round(i)
-        keep.append((ms, cr.to(torch.int64).sum()))
+        got, cr = one_round(i)
+        keep.append((got, cr.to(torch.int64).sum()))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    matched = int(sum(int(a.item()) for a, _ in keep))
+    rows = [gather_rows(torch, *a) for a, _ in keep]
+    distinct = sum(d for d, _ in rows)
+    matched = sum(n for _, n in rows)
     created = int(sum(int(b.item()) for _, b in keep))
     kinds = [("gather", P.KIND_GATHER), ("lookup", P.KIND_LOOKUP), ("insert", P.KIND_INSERT),
              ("scatter", P.KIND_SCATTER)] + ([("evict (part of insert)", P.KIND_EVICT)] if evict else [])
@@ -852,6 +877,7 @@ def run_stream(args, torch, P, synth, dev):
     del cache
     torch.cuda.empty_cache()
     g_ms, g_n = t["gather"]
+    g_bytes = (distinct + matched) * sh.block_bytes
     ms_round = elapsed * 1e3 / n_timed
     out = base_line(args, per * n_timed / elapsed, "requests/s", ms_round, {
         "workload": WORKLOAD_TEXT[args.config], "lookups_per_round": per, "inserts_per_round": per,
@@ -859,15 +885,15 @@ def run_stream(args, torch, P, synth, dev):
     out["steps"] = n_timed
     out.update({
         "inserts_per_s": round(per * n_timed / elapsed, 2),
-        "matched_blocks": matched, "created_blocks": created,
+        "matched_blocks": matched, "distinct_blocks": distinct, "created_blocks": created,
         "blocks_stored": {"before": blocks0, "after": st["blocks_stored"]},
-        "roofline": roofline("k_copy_pairs<true> (gather)", matched * 2 * sh.block_bytes / max(g_n, 1),
+        "roofline": roofline("k_copy_slices (gather)", g_bytes / max(g_n, 1),
                              g_ms / max(g_n, 1), g_n,
-                             recorded_traffic(args.config, matched * 2 * sh.block_bytes / max(g_n, 1)),
-                             ceiling),
+                             recorded_traffic(args.config, g_bytes / max(g_n, 1)), ceiling),
         "hbm_ceiling": ceiling,
         "gather_all": {"dispatches": args.warmup + n_timed,
-                       "bytes": (matched_warm + matched) * 2 * sh.block_bytes},
+                       "bytes": (distinct_warm + matched_warm + distinct + matched) * sh.block_bytes,
+                       "read_bytes": (distinct_warm + distinct) * sh.block_bytes},
         "evictions": st["evictions"], "index_rebuilds": st["index_rebuilds"],
         "full_events": st["full_events"],
         "library_counters": {

@@ -60,7 +60,8 @@
  *    may be captured and replayed; a replay works on the store as it is
  *    then. A later call with a larger batch regrows the scratch, after which
  *    earlier captures must not be replayed; a captured call that would need
- *    a larger scratch returns INVALID and allocates nothing. A load captured
+ *    a larger scratch (or whose scratch a failed call left to be cleared
+ *    by the next uncaptured call) returns INVALID and allocates nothing. A load captured
  *    on a stream that had made no call shares the first stream's scratch:
  *    its replays must not overlap loads enqueued on that stream. A capture
  *    keeps the counting state (ptstore_set_counters) it was made with.
@@ -237,12 +238,15 @@ int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * and counted in bad_entries. Destinations must be distinct (two entries
  * naming the same cache block race). `cache` must be 16-byte aligned.
  * The call first builds a dense list of the blocks to copy in store-owned
- * scratch of `stream` (8 bytes per (request, block) plus 24 per request,
- * grown on demand; growing waits for `stream`), then copies only those
- * blocks: blocks read from device memory on the full device, blocks read
- * from the host tier by a quarter of the compute units (they move at the
- * host link's rate whatever the grid, and the rest of the device stays free
- * for device-memory copies, of this call or of loads on other streams). Errors: INVALID (store
+ * scratch of `stream` (about 68 bytes per (request, block) plus 24 per
+ * request, grown on demand; growing waits for `stream`), then copies only
+ * those blocks. With R >= 2 the list groups the entries by stored block, so
+ * that a block several requests need is read once per call and written to
+ * each of their cache blocks. Blocks read from device memory are copied on
+ * the full device, blocks read from the host tier by a quarter of the
+ * compute units (they move at the host link's rate whatever the grid, and
+ * the rest of the device stays free for device-memory copies, of this call
+ * or of loads on other streams). Errors: INVALID (store
  * NULL, R < 0, max_blocks < 1, R * max_blocks > 2^29, cache_blocks < 0, a
  * NULL pointer with R > 0, `cache` not 16-byte aligned), NOMEM (scratch),
  * HIP.
@@ -417,11 +421,12 @@ const char *ptstore_last_error(void);
  * For callers that cannot allocate device memory: code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, kernels and results as ptstore_lookup_gather, but the
- * gather's descriptor list lives in a static device array of the library
- * (about 32 MiB per device, held until the process ends) instead of
- * store-owned scratch. The call allocates nothing, frees nothing, creates
- * no event and never waits; it records no ptstore_kernel_times() entries
- * and leaves a list made by ptstore_gather_prepare intact.
+ * gather's descriptor list and the row table that groups its entries by
+ * stored block live in a static device array of the library (about 92 MiB
+ * per device, held until the process ends) instead of store-owned scratch.
+ * The call allocates nothing, frees nothing, creates no event and never
+ * waits; it records no ptstore_kernel_times() entries and leaves a list
+ * made by ptstore_gather_prepare intact.
  * Limit: R * max_blocks <= PTSTORE_NOALLOC_MAX_ENTRIES, else INVALID before
  * any work is enqueued. Every such call on one device shares that device's
  * array, whichever store it names: calls that overlap in time on one device

@@ -33,11 +33,14 @@ using namespace ptsd;
 // cannot allocate: one copy per device, held until the process ends, shared
 // by every such call on that device (calls that overlap on one device race).
 // Its size is the gather's list for PTSTORE_NOALLOC_MAX_ENTRIES (request,
-// block) entries: 8 bytes per entry, 2 x (4 + 8) per request (at most one
-// request per entry), the two 8-byte totals, each part rounded up to 256
-// bytes.
-constexpr size_t kNoAllocScratchBytes =
-    (size_t)PTSTORE_NOALLOC_MAX_ENTRIES * (8 + 2 * (4 + 8)) + 256;
+// block) entries: a row table of twice as many slots (16 bytes each), then
+// 36 bytes per entry (pair, slice, cache block, table slot and rank), 2 x
+// (4 + 8) per request (at most one request per entry) and the counters,
+// each part a multiple of 256 bytes. Static storage starts zeroed, so the
+// row table starts empty, as every call leaves it.
+constexpr uint64_t kNoAllocTableSlots = 2ull * PTSTORE_NOALLOC_MAX_ENTRIES;
+constexpr size_t kNoAllocScratchBytes = kNoAllocTableSlots * 16 +
+                                        (size_t)PTSTORE_NOALLOC_MAX_ENTRIES * (36 + 2 * (4 + 8)) + 256;
 static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 
 struct ptstore {
@@ -59,6 +62,8 @@ struct ptstore {
         hipStream_t stream;
         void* p;
         size_t bytes;
+        uint64_t table_cap;  // row-table slots at the start of p, kept empty between calls
+        bool dirty;          // a call failed between filling and emptying the row table
     };
     std::vector<StreamScratch> copy_scratch;
     int32_t chunks_per_group, threads, grid;
@@ -74,6 +79,7 @@ struct ptstore {
     // the block list of ptstore_gather_prepare, while it is valid
     bool prep_valid;
     void* prep_list;  // the copy scratch holding it
+    uint64_t prep_table_cap;
     int32_t prep_R, prep_max_blocks;
     int64_t prep_cache_blocks;
     // HIP events around kernels, per kind; bit k of timing_kinds records kind k
@@ -165,6 +171,15 @@ void* static_scratch(int device) {
     if (device < 0 || device >= kMaxDevices) return nullptr;
     std::lock_guard<std::mutex> lock(g_scratch_mu);
     return g_scratch_ptr[device];
+}
+
+// Whether a no-alloc call on `device` failed between filling and emptying
+// the static scratch's row table; with set, records `value` instead.
+bool g_scratch_dirty[kMaxDevices];
+bool static_dirty(int device, bool set, bool value = false) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (set) g_scratch_dirty[device] = value;
+    return g_scratch_dirty[device];
 }
 
 IndexView index_view(ptstore_t* s) {
@@ -314,37 +329,59 @@ bool capturing(hipStream_t st) {
     return hipStreamIsCapturing(st, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
 }
 
-// The descriptor scratch of `st`, grown to `need` bytes (waiting for `st`
-// when it grows); made on the first call on a stream. Under graph capture
-// nothing is allocated: a stream that has a scratch must already have one of
-// this size, and a stream that has made no call yet (such as a capture
-// stream of its own) uses the scratch of the store's first stream.
-int copy_scratch_for(ptstore_t* s, hipStream_t st, size_t need, void** out, const char* who) {
+// The descriptor scratch of `st` for a call of R x max_blocks entries; made
+// on the first call on a stream and grown when a call needs more (waiting
+// for `st` first, since work enqueued on it may still read the old buffer).
+// A new buffer's row table is emptied by a kernel on `st`, and so is the
+// table of a scratch whose last call failed half-way. Under graph capture
+// nothing is allocated or emptied: a stream that has a scratch must already
+// have one of this size, and a stream that has made no call yet (such as a
+// capture stream of its own) uses the scratch of the store's first stream.
+int copy_scratch_for(ptstore_t* s, hipStream_t st, int32_t R, int32_t max_blocks, void** out,
+                     uint64_t* table_cap, ptstore::StreamScratch** entry, const char* who) {
     const bool cap = capturing(st);
-    for (auto& e : s->copy_scratch)
-        if (e.stream == st) {
-            if (cap && need > e.bytes)
-                return fail(PTSTORE_ERR_INVALID, "a captured call needs a larger scratch than its "
-                            "stream has: run a call of that size on the stream before capturing");
-            const int rc = ensure_scratch(&e.p, &e.bytes, need, st, who);
-            *out = e.p;
-            return rc;
-        }
+    const uint64_t slots = copy_table_slots(R, max_blocks);
+    auto fits = [&](const ptstore::StreamScratch& e) {
+        return e.table_cap >= slots && e.bytes >= copy_scratch_bytes(R, max_blocks, e.table_cap);
+    };
+    ptstore::StreamScratch* e = nullptr;
+    for (auto& x : s->copy_scratch)
+        if (x.stream == st) e = &x;
     if (cap) {
-        if (!s->copy_scratch.empty() && s->copy_scratch[0].bytes >= need) {
-            *out = s->copy_scratch[0].p;
-            return PTSTORE_OK;
-        }
-        return fail(PTSTORE_ERR_INVALID, "a captured call needs a scratch no earlier call made: "
-                    "run a call of that size before capturing");
+        ptstore::StreamScratch* use = e ? e : (s->copy_scratch.empty() ? nullptr : &s->copy_scratch[0]);
+        if (!use || !fits(*use) || use->dirty)
+            return fail(PTSTORE_ERR_INVALID, "a captured call needs a larger scratch than its stream "
+                        "has: run a call of that size on the stream (or, for a new stream, on the "
+                        "store's first stream) before capturing");
+        *out = use->p;
+        *table_cap = use->table_cap;
+        *entry = use;
+        return PTSTORE_OK;
     }
-    if (s->copy_scratch.size() >= kMaxStreams)
-        return fail(PTSTORE_ERR_INVALID, "calls on more than 16 streams of one store");
-    s->copy_scratch.push_back({st, nullptr, 0});
-    auto& e = s->copy_scratch.back();
-    const int rc = ensure_scratch(&e.p, &e.bytes, need, st, who);
-    *out = e.p;
-    return rc;
+    if (!e) {
+        if (s->copy_scratch.size() >= kMaxStreams)
+            return fail(PTSTORE_ERR_INVALID, "calls on more than 16 streams of one store");
+        s->copy_scratch.push_back({st, nullptr, 0, 0, false});
+        e = &s->copy_scratch.back();
+    }
+    if (!fits(*e)) {
+        const uint64_t new_cap = slots > e->table_cap ? slots : e->table_cap;
+        size_t have = e->bytes;
+        const int rc = ensure_scratch(&e->p, &have, copy_scratch_bytes(R, max_blocks, new_cap), st, who);
+        e->bytes = have;
+        e->table_cap = e->p ? new_cap : 0;
+        if (rc) return rc;
+        e->dirty = true;  // a new buffer: its table is emptied below
+    }
+    if (e->dirty) {
+        const hipError_t z = launch_zero(e->p, copy_scratch_bytes(0, 0, e->table_cap) - 256, st);
+        if (z != hipSuccess) return fail(PTSTORE_ERR_HIP, who, z);
+        e->dirty = false;
+    }
+    *out = e->p;
+    *table_cap = e->table_cap;
+    *entry = e;
+    return PTSTORE_OK;
 }
 
 // Carves the eviction arrays out of one block of device memory; returns the
@@ -667,16 +704,19 @@ int ptstore_gather_layers(ptstore_t* s, const int32_t* ids, const int32_t* m,
     int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
     void* scr = nullptr;
-    rc = copy_scratch_for(s, st, copy_scratch_bytes(R, max_blocks), &scr, "ptstore_gather: scratch");
+    uint64_t tcap = 0;
+    ptstore::StreamScratch* ent = nullptr;
+    rc = copy_scratch_for(s, st, R, max_blocks, &scr, &tcap, &ent, "ptstore_gather: scratch");
     if (rc) return rc;
     CopyScratch sc;
-    copy_scratch_carve(scr, R, max_blocks, &sc);
+    copy_scratch_carve(scr, R, max_blocks, tcap, &sc);
     const CopyPlan plan = copy_plan(s);
     hipError_t e;
     {
         Timed t(s, 4, st);
         e = launch_gather_select(plan, sc, ids, m, block_table, R, max_blocks, cache_blocks, st);
     }
+    if (e != hipSuccess) ent->dirty = true;
     if (e == hipSuccess) {
         Timed t(s, 0, st);
         e = launch_gather_copy(plan, sc, static_cast<uint8_t*>(cache), cache_blocks, R, max_blocks,
@@ -698,19 +738,24 @@ int ptstore_gather_prepare(ptstore_t* s, const int32_t* ids, const int32_t* m,
     hipStream_t st = (hipStream_t)stream;
     if (R > 0) {
         void* scr = nullptr;
-        rc = copy_scratch_for(s, st, copy_scratch_bytes(R, max_blocks), &scr,
-                              "ptstore_gather_prepare: scratch");
+        uint64_t tcap = 0;
+        ptstore::StreamScratch* ent = nullptr;
+        rc = copy_scratch_for(s, st, R, max_blocks, &scr, &tcap, &ent, "ptstore_gather_prepare: scratch");
         if (rc) return rc;
         s->prep_list = scr;
+        s->prep_table_cap = tcap;
         CopyScratch sc;
-        copy_scratch_carve(scr, R, max_blocks, &sc);
+        copy_scratch_carve(scr, R, max_blocks, tcap, &sc);
         hipError_t e;
         {
             Timed t(s, 4, st);
             e = launch_gather_select(copy_plan(s), sc, ids, m, block_table, R, max_blocks,
                                      cache_blocks, st);
         }
-        if (e != hipSuccess) return fail(PTSTORE_ERR_HIP, "ptstore_gather_prepare: launch", e);
+        if (e != hipSuccess) {
+            ent->dirty = true;
+            return fail(PTSTORE_ERR_HIP, "ptstore_gather_prepare: launch", e);
+        }
     }
     s->prep_valid = true;
     s->prep_R = R;
@@ -730,7 +775,7 @@ int ptstore_gather_prepared(ptstore_t* s, int32_t layer_begin, int32_t layer_end
     if (dev.rc) return dev.rc;
     hipStream_t st = (hipStream_t)stream;
     CopyScratch sc;
-    copy_scratch_carve(s->prep_list, s->prep_R, s->prep_max_blocks, &sc);
+    copy_scratch_carve(s->prep_list, s->prep_R, s->prep_max_blocks, s->prep_table_cap, &sc);
     hipError_t e;
     {
         Timed t(s, 0, st);
@@ -768,7 +813,8 @@ int ptstore_lookup_gather_noalloc(ptstore_t* s, const int32_t* tokens, const int
         (reinterpret_cast<uintptr_t>(cache) & 15) != 0)
         return fail(PTSTORE_ERR_INVALID, "ptstore_lookup_gather_noalloc: bad argument");
     if ((int64_t)R * max_blocks > PTSTORE_NOALLOC_MAX_ENTRIES ||
-        copy_scratch_bytes(R, max_blocks) > kNoAllocScratchBytes)
+        copy_table_slots(R, max_blocks) > kNoAllocTableSlots ||
+        copy_scratch_bytes(R, max_blocks, kNoAllocTableSlots) > kNoAllocScratchBytes)
         return fail(PTSTORE_ERR_INVALID,
                     "ptstore_lookup_gather_noalloc: R * max_blocks exceeds PTSTORE_NOALLOC_MAX_ENTRIES");
     if (R == 0) return PTSTORE_OK;
@@ -781,12 +827,18 @@ int ptstore_lookup_gather_noalloc(ptstore_t* s, const int32_t* tokens, const int
     Batch b{tokens, offsets, n_tokens, R, max_blocks};
     // the same kernels as ptstore_lookup_gather; no events are recorded, so
     // nothing is created on the way either
-    hipError_t e = launch_lookup(index_view(s), b, m, ids, st);
+    hipError_t e = hipSuccess;
+    if (static_dirty(s->device, false))  // a call failed half-way: empty the row table first
+        e = launch_zero(sp, copy_scratch_bytes(0, 0, kNoAllocTableSlots) - 256, st);
+    if (e == hipSuccess) static_dirty(s->device, true, false);
+    if (e == hipSuccess) e = launch_lookup(index_view(s), b, m, ids, st);
     CopyScratch sc;
-    copy_scratch_carve(sp, R, max_blocks, &sc);
+    copy_scratch_carve(sp, R, max_blocks, kNoAllocTableSlots, &sc);
     const CopyPlan plan = copy_plan(s);
-    if (e == hipSuccess)
+    if (e == hipSuccess) {
         e = launch_gather_select(plan, sc, ids, m, block_table, R, max_blocks, cache_blocks, st);
+        if (e != hipSuccess) static_dirty(s->device, true, true);
+    }
     if (e == hipSuccess)
         e = launch_gather_copy(plan, sc, static_cast<uint8_t*>(cache), cache_blocks, R, max_blocks, 0,
                                s->cfg.num_layers, st);
@@ -866,10 +918,12 @@ int ptstore_scatter_layers(ptstore_t* s, const int32_t* ids, const uint8_t* crea
     int rc = PTSTORE_OK;
     hipStream_t st = (hipStream_t)stream;
     void* scr = nullptr;
-    rc = copy_scratch_for(s, st, copy_scratch_bytes(R, max_blocks), &scr, "ptstore_scatter: scratch");
+    uint64_t tcap = 0;
+    ptstore::StreamScratch* ent = nullptr;
+    rc = copy_scratch_for(s, st, R, max_blocks, &scr, &tcap, &ent, "ptstore_scatter: scratch");
     if (rc) return rc;
     CopyScratch sc;
-    copy_scratch_carve(scr, R, max_blocks, &sc);
+    copy_scratch_carve(scr, R, max_blocks, tcap, &sc);
     const CopyPlan plan = copy_plan(s);
     hipError_t e;
     {

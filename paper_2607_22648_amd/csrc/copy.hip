@@ -72,6 +72,7 @@ struct SelectArgs {
     DevState* state;
     CopyScratch sc;
     TierView tier;
+    int32_t group;             // gather: 1 = group the entries by row (R >= 2)
 };
 
 // The row a gather reads block `id` from: its device home, its replica, or
@@ -142,6 +143,70 @@ __device__ inline void count_row(const SelectArgs& a, int64_t r, int lane, unsig
     *cnt_h = ch;
 }
 
+__device__ inline int32_t ld_agent(const int32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline unsigned long long ld_agent(const unsigned long long* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Enter list entry i, which reads `row`, into the call's row table: the
+// row's slot, the entry's rank among the row's entries, and the row's first
+// entry. Table reads go to the device scope (other waves of the workgroup
+// write the table too). The table holds at least twice as many slots as
+// entries and every call leaves it empty, so an empty or matching slot is
+// always found; the probe still stops after one pass over the table, and
+// an entry that found no slot (slot -1) is skipped and counted as bad.
+__device__ inline bool table_enter(const CopyScratch& sc, int32_t row, int64_t i) {
+    const unsigned long long want = (unsigned long long)(uint32_t)(row + 1) << 32;
+    uint64_t h = mix64((uint64_t)(uint32_t)row) & sc.table_mask;
+    int32_t rank = -1;
+    for (uint64_t probe = 0; probe <= sc.table_mask; ++probe, h = (h + 1) & sc.table_mask) {
+        unsigned long long k = ld_agent(&sc.tkey[h]);
+        if (k == 0) {
+            k = atomicCAS(&sc.tkey[h], 0ull, want | 1ull);
+            if (k == 0) {
+                rank = 0;
+                break;
+            }
+        }
+        if ((k & 0xFFFFFFFF00000000ull) == want) {
+            rank = (int32_t)(atomicAdd(&sc.tkey[h], 1ull) & 0xFFFFFFFFull);
+            break;
+        }
+    }
+    if (rank < 0) {
+        sc.pslot[i] = -1;
+        return false;
+    }
+    sc.pslot[i] = (int32_t)h;
+    sc.prank[i] = rank;
+    atomicMax(&sc.tfirst[h], INT32_MAX - (int32_t)i);
+    return true;
+}
+
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;  // an entry the row table had no slot for
+
+// List entry i: a scatter's (home row, cache block) pair; a gather's entry
+// in the row table, or, when it is not grouping, a slice of its own.
+template <bool GATHER>
+__device__ inline void place(const SelectArgs& a, const Pair& p, int64_t i) {
+    if (!GATHER) {
+        a.sc.pairs[i] = p;
+    } else if (a.group) {
+        a.sc.pairs[i] = p;
+        if (!table_enter(a.sc, p.row, i)) atomicAdd(&a.state->bad_entries, 1ull);
+    } else {
+        Slice q;
+        q.row = p.row;
+        q.base = (int32_t)i;
+        q.n = 1;
+        q.pad = 0;
+        a.sc.slices[i] = q;
+        a.sc.dests[i] = p.cb;
+    }
+}
+
 // Request r's descriptors, written by the whole wave from list position pos
 // (device rows) and pos_h (host-tier rows), in block order.
 template <bool GATHER>
@@ -156,8 +221,8 @@ __device__ inline void fill_row(const SelectArgs& a, int64_t r, int lane, unsign
         const bool dev = sel && p.row < a.tier.dev_rows;
         const unsigned long long mask = ballot64(dev);
         const unsigned long long mask_h = ballot64(sel && !dev);
-        if (dev) a.sc.pairs[pos + __popcll(mask & lanes_below(lane))] = p;
-        if (sel && !dev) a.sc.pairs[pos_h + __popcll(mask_h & lanes_below(lane))] = p;
+        if (dev) place<GATHER>(a, p, pos + __popcll(mask & lanes_below(lane)));
+        if (sel && !dev) place<GATHER>(a, p, pos_h + __popcll(mask_h & lanes_below(lane)));
         pos += __popcll(mask);
         pos_h += __popcll(mask_h);
         // new bytes for a host-tier block: its device replica is stale, drop it
@@ -184,6 +249,18 @@ __global__ __launch_bounds__(kSelThreads) void k_select_count(SelectArgs a) {
         a.sc.row_cnt_h[r] = cnt_h;
         if (bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
     }
+}
+
+// The slice and cache-block counters of a call: a gather that groups hands
+// them out from zero; one that does not has one slice per list entry.
+__device__ inline void set_counters(const SelectArgs& a, unsigned long long total,
+                                    unsigned long long total_h) {
+    *a.sc.total = total;
+    *a.sc.total_h = total_h;
+    *a.sc.nslices = a.group ? 0ull : total;
+    *a.sc.nslices_h = a.group ? 0ull : total_h;
+    *a.sc.ndests = 0;
+    *a.sc.ndests_h = 0;
 }
 
 // One workgroup: exclusive scans of row_cnt and row_cnt_h into row_base and
@@ -244,10 +321,7 @@ __global__ __launch_bounds__(1024) void k_select_scan(SelectArgs a) {
         }
         __syncthreads();  // wsum is written again by the next tile
     }
-    if (t == 0) {
-        *a.sc.total = (unsigned long long)carry;
-        *a.sc.total_h = (unsigned long long)carry_h;
-    }
+    if (t == 0) set_counters(a, (unsigned long long)carry, (unsigned long long)carry_h);
 }
 
 template <bool GATHER>
@@ -260,60 +334,283 @@ __global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
                      (int64_t)*a.sc.total + a.sc.row_base_h[r]);
 }
 
-// Small batches: count, scan and fill in one workgroup, the counts and
-// bases in LDS, so that building the list costs one launch instead of
-// three. Wave w takes requests w, w+16, ...; with at most 4 requests of at
-// most 2 windows per wave (the host's condition) its serial walk stays as
-// short as the three kernels' launch gaps.
+// Slices of the list entries start .. start+count-1 (one request's part),
+// by the whole wave: each row's first entry takes slices for all of the
+// row's entries, kSliceDests cache blocks each, from the counters of its
+// part (one allocation per 64 entries, so slices keep the requests' order),
+// and records where the row's cache blocks start. off: where the part's
+// slices and cache blocks begin.
+__device__ inline void group_part(const CopyScratch& sc, int64_t start, int32_t count, int64_t off,
+                                  unsigned long long* nsl_ctr, unsigned long long* nd_ctr, int lane) {
+    for (int32_t w0 = 0; w0 < count; w0 += kWave) {
+        const int64_t i = start + w0 + lane;
+        int32_t h = 0, nsl = 0, n = 0, row = 0;
+        bool owner = false;
+        if (w0 + lane < count) {
+            h = ld_agent(&sc.pslot[i]);
+            owner = h >= 0 && INT32_MAX - ld_agent(&sc.tfirst[h]) == (int32_t)i;
+            if (owner) {
+                const unsigned long long k = ld_agent(&sc.tkey[h]);
+                n = (int32_t)(k & 0xFFFFFFFFull);
+                row = (int32_t)(k >> 32) - 1;
+                nsl = (n + kSliceDests - 1) / kSliceDests;
+            }
+        }
+        int32_t s_nsl = nsl, s_n = n;  // inclusive scans over the wave
+        for (int d = 1; d < kWave; d <<= 1) {
+            const int32_t x = __shfl_up(s_nsl, d, kWave), y = __shfl_up(s_n, d, kWave);
+            if (lane >= d) {
+                s_nsl += x;
+                s_n += y;
+            }
+        }
+        unsigned long long sb = 0, db = 0;
+        if (lane == kWave - 1) {
+            if (s_nsl) sb = atomicAdd(nsl_ctr, (unsigned long long)s_nsl);
+            if (s_n) db = atomicAdd(nd_ctr, (unsigned long long)s_n);
+        }
+        sb = shfl_u64(sb, kWave - 1);
+        db = shfl_u64(db, kWave - 1);
+        if (owner) {
+            const int64_t my_sb = off + (int64_t)sb + (s_nsl - nsl);
+            const int64_t my_db = off + (int64_t)db + (s_n - n);
+            sc.tbase[h] = (int32_t)my_db;
+            for (int j = 0; j < nsl; ++j) {
+                const int32_t left = n - j * kSliceDests;
+                Slice q;
+                q.row = row;
+                q.base = (int32_t)(my_db + j * kSliceDests);
+                q.n = left < kSliceDests ? left : kSliceDests;
+                q.pad = 0;
+                sc.slices[my_sb + j] = q;
+            }
+        }
+    }
+}
+
+// List entry i's cache block into its row's cache-block list; the row's
+// first entry then empties the row's table slot, so the table is empty again
+// when the call ends (only this step still reads the slot, and only its
+// base; a cleared first entry is never taken for another entry's).
+__device__ inline void place_dest(const CopyScratch& sc, int64_t i) {
+    const int32_t h = ld_agent(&sc.pslot[i]);
+    if (h < 0) return;  // an entry the table had no slot for
+    const int32_t rank = ld_agent(&sc.prank[i]);
+    const int32_t cb = ld_agent(&sc.pairs[i].cb);
+    sc.dests[ld_agent(&sc.tbase[h]) + rank] = cb;
+    if (INT32_MAX - ld_agent(&sc.tfirst[h]) == (int32_t)i) {
+        __hip_atomic_store(&sc.tkey[h], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&sc.tfirst[h], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_group_fill(SelectArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
+    if (r >= a.R) return;
+    const int64_t total = (int64_t)*a.sc.total;
+    group_part(a.sc, a.sc.row_base[r], a.sc.row_cnt[r], 0, a.sc.nslices, a.sc.ndests, lane);
+    group_part(a.sc, total + a.sc.row_base_h[r], a.sc.row_cnt_h[r], total, a.sc.nslices_h,
+               a.sc.ndests_h, lane);
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_group_dests(SelectArgs a) {
+    const int64_t all = (int64_t)*a.sc.total + (int64_t)*a.sc.total_h;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < all;
+         i += (int64_t)gridDim.x * blockDim.x)
+        place_dest(a.sc, i);
+}
+
+// Small batches (at most kSmallMaxEntries (request, block) slots): the whole
+// list in one workgroup, thread t holding slots s = k * 1024 + t. Every
+// slot's loads are issued together (one trip to memory for the batch, where
+// a walk over each request's windows costs a trip per window); list
+// positions come from ballots and one exclusive scan of the per-wave counts
+// in LDS. The list is the selected slots in slot order, device rows first,
+// as the three-kernel path builds it. A gather of several requests groups
+// its entries by row in an LDS table, each thread keeping its entries' table
+// slots, ranks and cache blocks in registers.
 constexpr int kSmallThreads = 1024;
 constexpr int kSmallWaves = kSmallThreads / kWave;
-constexpr int32_t kSmallMaxR = 64;
 constexpr int64_t kSmallMaxEntries = 8192;
+constexpr int kSmallPer = (int)(kSmallMaxEntries / kSmallThreads);  // slots per thread
+constexpr int kSmallCounts = kSmallPer * kSmallWaves;               // (k, wave) counts
+constexpr uint32_t kSmallSlots = 2 * kSmallMaxEntries;               // LDS row table
+
+// Enter an entry that reads `row` into the LDS row table (words (row + 1)
+// << 32 | entries so far, 0 empty); returns slot | rank << 16, or kNoSlot if
+// one pass over the table found no slot (it holds at least twice as many
+// slots as entries, so one is always found).
+__device__ inline uint32_t lds_enter(unsigned long long* tw, uint32_t slots, int32_t row) {
+    const unsigned long long want = (unsigned long long)(uint32_t)(row + 1) << 32;
+    uint32_t h = (uint32_t)(((uint64_t)(uint32_t)mix64((uint64_t)(uint32_t)row) * slots) >> 32);
+    for (uint32_t probe = 0; probe < slots; ++probe) {
+        const unsigned long long k = atomicCAS(&tw[h], 0ull, want | 1ull);
+        if (k == 0) return h;
+        if ((k & 0xFFFFFFFF00000000ull) == want)
+            return h | (uint32_t)(atomicAdd(&tw[h], 1ull) & 0xFFFFFFFFull) << 16;
+        h = h + 1 == slots ? 0 : h + 1;
+    }
+    return kNoSlot;
+}
 
 template <bool GATHER>
 __global__ __launch_bounds__(kSmallThreads) void k_select_small(SelectArgs a) {
-    __shared__ int32_t base[kSmallMaxR], base_h[kSmallMaxR];
-    __shared__ int32_t total_dev;
+    __shared__ int32_t wc[kSmallCounts], wch[kSmallCounts];  // per (k, wave); then their bases
+    __shared__ int32_t total_dev, total_host;
+    __shared__ unsigned long long alloc[2];  // per part: slices << 32 | cache blocks
+    __shared__ unsigned long long tw[GATHER ? kSmallSlots : 1];
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    const int t = threadIdx.x;
     const unsigned long long count = a.state->count;
+    const bool group = GATHER && a.group;
+    const int32_t E = a.R * a.max_blocks;  // the host's condition: E <= kSmallMaxEntries
+    uint32_t slots = 2u * (uint32_t)E;
+    if (slots < 64) slots = 64;
+    if (slots > kSmallSlots) slots = kSmallSlots;
+    if (group) {
+        for (uint32_t h = t; h < slots; h += blockDim.x) tw[h] = 0ull;
+        if (t == 0) alloc[0] = alloc[1] = 0ull;
+    }
+    // every load first, from in-bounds (clamped) slots, with no branch between
+    // them, so that they are all in flight together
+    int32_t id[kSmallPer], cb[kSmallPer], mr[kSmallPer], made[kSmallPer];
+    const int32_t last = E > 0 ? E - 1 : 0;
+#pragma unroll
+    for (int k = 0; k < kSmallPer; ++k) {
+        const int32_t s = E > 0 ? min(k * kSmallThreads + t, last) : 0;
+        id[k] = E > 0 ? a.ids[s] : -1;
+        cb[k] = E > 0 ? a.block_table[s] : -1;
+        mr[k] = GATHER && E > 0 ? a.m[s / a.max_blocks] : 0;
+        made[k] = GATHER || (E > 0 && a.created[s] != 0);
+    }
+    Pair p[kSmallPer];
+    unsigned long long dm[kSmallPer], hm[kSmallPer];  // the wave's selected slots: device, host rows
     int32_t bad = 0;
-    for (int r = wv; r < a.R; r += kSmallWaves) {
-        int32_t c, ch;
-        count_row<GATHER>(a, r, lane, count, &c, &ch, &bad);
+#pragma unroll
+    for (int k = 0; k < kSmallPer; ++k) {
+        const int32_t s = k * kSmallThreads + t;
+        const int32_t r = s / (a.max_blocks > 0 ? a.max_blocks : 1), b = s - r * a.max_blocks;
+        const int32_t n = GATHER ? (mr[k] < 0 ? 0 : (mr[k] < a.max_blocks ? mr[k] : a.max_blocks))
+                                 : a.max_blocks;
+        const bool use = (s < E) & (b < n);
+        const bool skip = !made[k] | (cb[k] < 0);
+        const bool out_of_range = ((int64_t)cb[k] >= a.cache_blocks) | (id[k] < 0) |
+                                  ((unsigned long long)(int64_t)id[k] >= count);
+        const bool sel = use & !skip & !out_of_range;
+        p[k].row = 0;
+        p[k].cb = cb[k];
+        if (sel) p[k].row = GATHER ? gather_row(a.tier, id[k]) : home_row(a.tier, id[k]);
+        const bool dev = sel && p[k].row < a.tier.dev_rows;
+        dm[k] = ballot64(dev);
+        hm[k] = ballot64(sel && !dev);
+        bad += __popcll(ballot64(use & !skip & out_of_range));
         if (lane == 0) {
-            base[r] = c;
-            base_h[r] = ch;
+            wc[k * kSmallWaves + wv] = __popcll(dm[k]);
+            wch[k * kSmallWaves + wv] = __popcll(hm[k]);
         }
     }
     if (lane == 0 && bad) atomicAdd(&a.state->bad_entries, (unsigned long long)bad);
     __syncthreads();
-    // exclusive scan over the requests, thread t holding request t (R <= 64:
-    // the first wave); totals of at most kSmallMaxEntries fit in 32 bits
-    const int t = threadIdx.x;
+    // exclusive scans of the counts in (k, wave) order by the first wave, two
+    // counts a lane (kSmallCounts = 128); totals of at most kSmallMaxEntries
+    // fit in 32 bits
     if (wv == 0) {
-        const int32_t v = t < a.R ? base[t] : 0, vh = t < a.R ? base_h[t] : 0;
-        int32_t s = v, sh = vh;
+        const int32_t c0 = wc[2 * lane], c1 = wc[2 * lane + 1];
+        const int32_t h0 = wch[2 * lane], h1 = wch[2 * lane + 1];
+        int32_t x = c0 + c1, xh = h0 + h1;
         for (int d = 1; d < kWave; d <<= 1) {
-            const int32_t x = __shfl_up(s, d, kWave), xh = __shfl_up(sh, d, kWave);
+            const int32_t y = __shfl_up(x, d, kWave), yh = __shfl_up(xh, d, kWave);
             if (lane >= d) {
-                s += x;
-                sh += xh;
+                x += y;
+                xh += yh;
             }
         }
-        if (t < a.R) {
-            base[t] = s - v;
-            base_h[t] = sh - vh;
-        }
+        const int32_t ex = x - c0 - c1, exh = xh - h0 - h1;
+        wc[2 * lane] = ex;
+        wc[2 * lane + 1] = ex + c0;
+        wch[2 * lane] = exh;
+        wch[2 * lane + 1] = exh + h0;
         if (lane == kWave - 1) {
-            total_dev = s;
-            *a.sc.total = (unsigned long long)s;
-            *a.sc.total_h = (unsigned long long)sh;
+            total_dev = x;
+            total_host = xh;
+            set_counters(a, (unsigned long long)x, (unsigned long long)xh);
         }
     }
     __syncthreads();
-    const int64_t total = total_dev;  // host rows after all device rows
-    for (int r = wv; r < a.R; r += kSmallWaves)
-        fill_row<GATHER>(a, r, lane, count, base[r], total + base_h[r]);
+    const int32_t total = total_dev;  // host rows after all device rows
+    uint32_t e[kSmallPer];
+    int32_t pos[kSmallPer];
+#pragma unroll
+    for (int k = 0; k < kSmallPer; ++k) {
+        e[k] = kNoSlot;
+        pos[k] = -1;
+        const bool dev = (dm[k] >> lane) & 1ull, host = (hm[k] >> lane) & 1ull;
+        if (!dev && !host) continue;
+        const int32_t i = dev ? wc[k * kSmallWaves + wv] + __popcll(dm[k] & lanes_below(lane))
+                              : total + wch[k * kSmallWaves + wv] + __popcll(hm[k] & lanes_below(lane));
+        pos[k] = i;
+        const Pair& q = p[k];
+        if (!GATHER) {
+            a.sc.pairs[i] = q;
+            // new bytes for a host-tier block: its device replica is stale, drop it
+            if (host && a.tier.rep_of) {
+                const int32_t slot = atomicExch(&a.tier.rep_of[q.row - a.tier.dev_rows], -1);
+                if (slot >= 0) {
+                    a.tier.rep_id[slot] = -1;
+                    atomicSub(&a.state->rep_count, 1ull);
+                }
+            }
+        } else if (group) {
+            e[k] = lds_enter(tw, slots, q.row);
+            if (e[k] == kNoSlot) atomicAdd(&a.state->bad_entries, 1ull);
+        } else {
+            Slice sl;
+            sl.row = q.row;
+            sl.base = i;
+            sl.n = 1;
+            sl.pad = 0;
+            a.sc.slices[i] = sl;
+            a.sc.dests[i] = q.cb;
+        }
+    }
+    if (!group) return;  // uniform over the workgroup
+    // every entry is in the table. Each row's rank-0 entry takes the slices
+    // and cache blocks of all of the row's entries from its part's counters
+    // (one 64-bit LDS atomic) and replaces the row's table word by where its
+    // cache blocks start; then each entry's cache block goes to its row's list
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kSmallPer; ++k) {
+        if (e[k] == kNoSlot || (e[k] >> 16) != 0) continue;
+        const int part = pos[k] >= total ? 1 : 0;
+        const int32_t off = part ? total : 0;
+        const uint32_t h = e[k] & 0xFFFFu;
+        const int32_t n = (int32_t)(tw[h] & 0xFFFFFFFFull);
+        const int32_t nsl = (n + kSliceDests - 1) / kSliceDests;
+        const unsigned long long got = atomicAdd(&alloc[part], (unsigned long long)nsl << 32 | (uint32_t)n);
+        const int32_t sb = off + (int32_t)(got >> 32), db = off + (int32_t)(got & 0xFFFFFFFFull);
+        tw[h] = (unsigned long long)(uint32_t)db;
+        for (int j = 0; j < nsl; ++j) {
+            const int32_t left = n - j * kSliceDests;
+            Slice sl;
+            sl.row = p[k].row;
+            sl.base = db + j * kSliceDests;
+            sl.n = left < kSliceDests ? left : kSliceDests;
+            sl.pad = 0;
+            a.sc.slices[sb + j] = sl;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kSmallPer; ++k)
+        if (e[k] != kNoSlot) a.sc.dests[(int32_t)tw[e[k] & 0xFFFFu] + (int32_t)(e[k] >> 16)] = p[k].cb;
+    if (t == 0) {
+        *a.sc.nslices = alloc[0] >> 32;
+        *a.sc.nslices_h = alloc[1] >> 32;
+        *a.sc.ndests = alloc[0] & 0xFFFFFFFFull;
+        *a.sc.ndests_h = alloc[1] & 0xFFFFFFFFull;
+    }
 }
 
 struct CopyArgs {
@@ -321,7 +618,9 @@ struct CopyArgs {
     uint8_t* host;      // host tier: rows dev_rows.. of the pool's row space
     int64_t dev_rows;
     uint8_t* cache;
-    const Pair* pairs;
+    const Pair* pairs;       // scatter, row copies: the descriptors
+    const Slice* slices;     // gather: the descriptors
+    const int32_t* dests;    // gather: the slices' cache blocks
     const unsigned long long* first;  // the first descriptor (null: 0)
     const unsigned long long* total;  // descriptors from there
     int64_t block_bytes;
@@ -341,8 +640,7 @@ struct CopyArgs {
 // chunks; past the cap a workgroup also takes the unit one grid further on,
 // and workgroups past the end exit at once); a scatter, whose created blocks
 // are sparse, launches 16 times what the device holds, looping.
-// Uniform slabs: a unit is (descriptor, group of chunks_per_group slabs).
-template <bool GATHER>
+// Scatter, uniform slabs: a unit is (pair, group of chunks_per_group slabs).
 __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
     const unsigned long long units = *a.total * (unsigned long long)a.groups;
     const Pair* pairs = a.pairs + (a.first ? *a.first : 0ull);
@@ -356,12 +654,44 @@ __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
         uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
                                           : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
         for (int c = c0; c < c1; ++c) {
-            uint8_t* src = blk + (int64_t)c * a.chunk_bytes;
-            uint8_t* dst = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
-            if (GATHER)
-                copy_span(reinterpret_cast<const v4u*>(src), reinterpret_cast<v4u*>(dst), n16);
-            else
-                copy_span(reinterpret_cast<const v4u*>(dst), reinterpret_cast<v4u*>(src), n16);
+            uint8_t* row_chunk = blk + (int64_t)c * a.chunk_bytes;
+            const uint8_t* cache_chunk = a.cache + ((int64_t)c * a.cache_blocks + p.cb) * a.chunk_bytes;
+            copy_span(reinterpret_cast<const v4u*>(cache_chunk), reinterpret_cast<v4u*>(row_chunk), n16);
+        }
+    }
+}
+
+// Gather, uniform slabs: a unit is (slice, group of chunks). Each chunk of
+// the slice's row is read once, two vectors per thread in flight, and
+// written to each of the slice's cache blocks: a row that several requests
+// need crosses the memory bus once per kSliceDests of them.
+__global__ __launch_bounds__(1024) void k_copy_slices(CopyArgs a) {
+    const unsigned long long units = *a.total * (unsigned long long)a.groups;
+    const Slice* slices = a.slices + (a.first ? *a.first : 0ull);
+    const int n16 = (int)(a.chunk_bytes >> 4);
+    const int nt = blockDim.x;
+    for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
+        const unsigned long long d = unit / (unsigned)a.groups;
+        const int g = (int)(unit - d * (unsigned)a.groups);
+        const Slice q = slices[d];
+        const int c0 = a.c_lo + g * a.chunks_per_group;
+        const int c1 = min(c0 + a.chunks_per_group, a.c_hi);
+        const uint8_t* blk = q.row < a.dev_rows ? a.pool + (int64_t)q.row * a.block_bytes
+                                                : a.host + (int64_t)(q.row - a.dev_rows) * a.block_bytes;
+        for (int c = c0; c < c1; ++c) {
+            const v4u* src = reinterpret_cast<const v4u*>(blk + (int64_t)c * a.chunk_bytes);
+            uint8_t* plane = a.cache + (int64_t)c * a.cache_blocks * a.chunk_bytes;
+            for (int i = threadIdx.x; i < n16; i += 2 * nt) {
+                const bool two = i + nt < n16;
+                const v4u x = ld_nt(src + i);
+                v4u y;
+                if (two) y = ld_nt(src + i + nt);
+                for (int k = 0; k < q.n; ++k) {
+                    v4u* dst = reinterpret_cast<v4u*>(plane + (int64_t)a.dests[q.base + k] * a.chunk_bytes);
+                    st_nt(dst + i, x);
+                    if (two) st_nt(dst + i + nt, y);
+                }
+            }
         }
     }
 }
@@ -388,54 +718,73 @@ __device__ inline int slab_from(const int64_t* lb, int li, int n, int64_t o) {
     return lo;
 }
 
-// Pool and cache addresses of the 16 bytes at range offset o of layer li
-// (lb relative to the first layer of the call, l0).
-__device__ inline void span_vec(const CopyArgs& a, const int64_t* lb, int li, int64_t o, int32_t cb,
-                                uint8_t* blk, v4u** pv, v4u** cv) {
+// Cache address of the 16 bytes at range offset o of layer li for cache
+// block cb (lb relative to the first layer of the call, l0); the pool row's
+// bytes are at the same offset o of the row.
+__device__ inline v4u* span_cache(const CopyArgs& a, const int64_t* lb, int li, int64_t o, int32_t cb) {
     const int64_t ch = (lb[li + 1] - lb[li]) >> 1;  // the layer's K (or V) slab
     const int64_t in = o - lb[li];
     const int kv = in >= ch ? 1 : 0;
-    *pv = reinterpret_cast<v4u*>(blk + o);
-    *cv = reinterpret_cast<v4u*>(a.cache + a.cache_blocks * lb[li] +
-                                 ((int64_t)kv * a.cache_blocks + cb) * ch + (in - kv * ch));
+    return reinterpret_cast<v4u*>(a.cache + a.cache_blocks * lb[li] +
+                                  ((int64_t)kv * a.cache_blocks + cb) * ch + (in - kv * ch));
 }
 
+// A gather's unit is (slice, span): each vector of the row is read once
+// and written to each of the slice's cache blocks; a scatter's is (pair,
+// span).
 template <bool GATHER>
 __global__ __launch_bounds__(1024) void k_copy_spans(CopyArgs a) {
     __shared__ int64_t lb[kMaxVarLayers + 1];
     const unsigned long long spans = (unsigned)a.groups;  // kSpanBytes units per descriptor
     const unsigned long long units = *a.total * spans;
-    const Pair* pairs = a.pairs + (a.first ? *a.first : 0ull);
+    const unsigned long long first = a.first ? *a.first : 0ull;
     if (blockIdx.x >= units) return;  // the whole workgroup: nothing to move
-    const int l0 = a.c_lo >> 1, l1 = a.c_hi >> 1, n = l1 - l0;
+    const int l0 = a.c_lo >> 1, l1 = a.c_hi >> 1, nl = l1 - l0;
     for (int l = l0 + (int)threadIdx.x; l <= l1; l += blockDim.x) lb[l - l0] = a.lbase[l];
     __syncthreads();
-    const int64_t b0 = lb[0], b1 = lb[n];
+    const int64_t b0 = lb[0], b1 = lb[nl];
     const int64_t step = 16 * (int64_t)blockDim.x;
     for (unsigned long long unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const unsigned long long d = unit / spans;
         const int64_t s0 = b0 + (int64_t)(unit - d * spans) * kSpanBytes;
         const int64_t s1 = min(s0 + (int64_t)kSpanBytes, b1);
-        const Pair p = pairs[d];
-        uint8_t* blk = p.row < a.dev_rows ? a.pool + (int64_t)p.row * a.block_bytes
-                                          : a.host + (int64_t)(p.row - a.dev_rows) * a.block_bytes;
+        int32_t row, n = 1, base = 0, cb0 = 0;
+        if (GATHER) {
+            const Slice q = a.slices[first + d];
+            row = q.row;
+            n = q.n;
+            base = q.base;
+        } else {
+            const Pair p = a.pairs[first + d];
+            row = p.row;
+            cb0 = p.cb;
+        }
+        uint8_t* blk = row < a.dev_rows ? a.pool + (int64_t)row * a.block_bytes
+                                        : a.host + (int64_t)(row - a.dev_rows) * a.block_bytes;
         // two vectors per thread in flight: both loaded before either is stored
         int li = 0;
         for (int64_t o = s0 + 16 * (int64_t)threadIdx.x; o < s1; o += 2 * step) {
             const bool two = o + step < s1;
-            li = slab_from(lb, li, n, o);
-            v4u *pv0, *cv0, *pv1 = nullptr, *cv1 = nullptr;
-            span_vec(a, lb, li, o, p.cb, blk, &pv0, &cv0);
-            int li1 = li;
-            if (two) {
-                li1 = slab_from(lb, li, n, o + step);
-                span_vec(a, lb, li1, o + step, p.cb, blk, &pv1, &cv1);
+            li = slab_from(lb, li, nl, o);
+            const int li1 = two ? slab_from(lb, li, nl, o + step) : li;
+            v4u* pv0 = reinterpret_cast<v4u*>(blk + o);
+            v4u* pv1 = reinterpret_cast<v4u*>(blk + o + step);
+            if (GATHER) {
+                const v4u x0 = ld_nt(pv0);
+                v4u x1;
+                if (two) x1 = ld_nt(pv1);
+                for (int k = 0; k < n; ++k) {
+                    const int32_t cb = a.dests[base + k];
+                    st_nt(span_cache(a, lb, li, o, cb), x0);
+                    if (two) st_nt(span_cache(a, lb, li1, o + step, cb), x1);
+                }
+            } else {
+                const v4u x0 = ld_nt(span_cache(a, lb, li, o, cb0));
+                v4u x1;
+                if (two) x1 = ld_nt(span_cache(a, lb, li1, o + step, cb0));
+                st_nt(pv0, x0);
+                if (two) st_nt(pv1, x1);
             }
-            const v4u x0 = ld_nt(GATHER ? pv0 : cv0);
-            v4u x1;
-            if (two) x1 = ld_nt(GATHER ? pv1 : cv1);
-            st_nt(GATHER ? cv0 : pv0, x0);
-            if (two) st_nt(GATHER ? cv1 : pv1, x1);
             li = li1;
         }
     }
@@ -467,8 +816,11 @@ template <bool GATHER>
 hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, const int32_t* m,
                   const uint8_t* created, const int32_t* bt, int32_t R, int32_t max_blocks,
                   int64_t cache_blocks, hipStream_t s) {
-    SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc, p.tier};
-    if (R <= kSmallMaxR && (int64_t)R * max_blocks <= kSmallMaxEntries) {
+    // a gather of one request lists each row once (its ids are a path), so
+    // only a gather of several requests groups its entries by row
+    SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc, p.tier,
+                 GATHER && R >= 2 ? 1 : 0};
+    if ((int64_t)R * max_blocks <= kSmallMaxEntries) {
         hipLaunchKernelGGL(k_select_small<GATHER>, dim3(1), dim3(kSmallThreads), 0, s, a);
         return hipGetLastError();
     }
@@ -479,6 +831,13 @@ hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, 
     hipLaunchKernelGGL(k_select_scan, dim3(1), dim3(1024), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_select_fill<GATHER>, dim3(grid), dim3(kSelThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess || !a.group) return e;
+    hipLaunchKernelGGL(k_group_fill, dim3(grid), dim3(kSelThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int64_t entries = (int64_t)R * max_blocks;
+    int64_t dgrid = (entries + kSelThreads - 1) / kSelThreads;
+    if (dgrid > 4096) dgrid = 4096;
+    hipLaunchKernelGGL(k_group_dests, dim3((unsigned)dgrid), dim3(kSelThreads), 0, s, a);
     return hipGetLastError();
 }
 
@@ -491,7 +850,9 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     a.dev_rows = p.tier.dev_rows;
     a.cache = cache;
     a.pairs = sc.pairs;
-    a.total = sc.total;
+    a.slices = sc.slices;
+    a.dests = sc.dests;
+    a.total = GATHER ? sc.nslices : sc.total;  // a gather has at most one slice per entry
     a.block_bytes = p.block_bytes;
     a.chunk_bytes = p.chunk_bytes;
     a.cache_blocks = cache_blocks;
@@ -514,8 +875,10 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     if (grid < 1) return hipSuccess;
     if (p.lbase)
         hipLaunchKernelGGL(k_copy_spans<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+    else if (GATHER)
+        hipLaunchKernelGGL(k_copy_slices, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     else
-        hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
+        hipLaunchKernelGGL(k_copy_pairs, dim3((unsigned)grid), dim3(p.threads), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.tier.host_blocks == 0) return e;
     // host-tier rows: bound by the host link, so a small looping grid moves
@@ -523,14 +886,16 @@ hipError_t copy(const CopyPlan& p, const CopyScratch& sc, uint8_t* cache, int64_
     // (of this call or of calls on other streams)
     CopyArgs h = a;
     h.first = sc.total;
-    h.total = sc.total_h;
+    h.total = GATHER ? sc.nslices_h : sc.total_h;
     int64_t hg = p.host_grid;
     if (hg > bound) hg = bound;
     if (hg > cap) hg = cap;
     if (p.lbase)
         hipLaunchKernelGGL(k_copy_spans<GATHER>, dim3((unsigned)hg), dim3(p.threads), 0, s, h);
+    else if (GATHER)
+        hipLaunchKernelGGL(k_copy_slices, dim3((unsigned)hg), dim3(p.threads), 0, s, h);
     else
-        hipLaunchKernelGGL(k_copy_pairs<GATHER>, dim3((unsigned)hg), dim3(p.threads), 0, s, h);
+        hipLaunchKernelGGL(k_copy_pairs, dim3((unsigned)hg), dim3(p.threads), 0, s, h);
     return hipGetLastError();
 }
 
@@ -555,26 +920,67 @@ hipError_t launch_copy_rows(const CopyPlan& p, const Pair* pairs, const unsigned
     return hipGetLastError();
 }
 
-size_t copy_scratch_bytes(int32_t R, int32_t max_blocks) {
-    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return up((size_t)R * max_blocks * sizeof(Pair)) + 2 * up((size_t)R * 4) + 2 * up((size_t)R * 8) + 256;
+uint64_t copy_table_slots(int32_t R, int32_t max_blocks) {
+    const uint64_t need = 2ull * (uint64_t)R * (uint64_t)max_blocks;
+    uint64_t h = 64;
+    while (h < need) h <<= 1;
+    return h;
 }
 
-void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* out) {
-    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+namespace {
+size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+}  // namespace
+
+size_t copy_scratch_bytes(int32_t R, int32_t max_blocks, uint64_t table_cap) {
+    const size_t E = (size_t)R * max_blocks, Rs = (size_t)R;
+    return up256(table_cap * 8) + 2 * up256(table_cap * 4) + up256(E * sizeof(Pair)) +
+           up256(E * sizeof(Slice)) + 3 * up256(E * 4) + 2 * up256(Rs * 4) + 2 * up256(Rs * 8) + 256;
+}
+
+void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, uint64_t table_cap,
+                        CopyScratch* out) {
+    const size_t E = (size_t)R * max_blocks, Rs = (size_t)R;
     uint8_t* q = static_cast<uint8_t*>(base);
-    out->pairs = reinterpret_cast<Pair*>(q);
-    q += up((size_t)R * max_blocks * sizeof(Pair));
-    out->row_cnt = reinterpret_cast<int32_t*>(q);
-    q += up((size_t)R * 4);
-    out->row_cnt_h = reinterpret_cast<int32_t*>(q);
-    q += up((size_t)R * 4);
-    out->row_base = reinterpret_cast<int64_t*>(q);
-    q += up((size_t)R * 8);
-    out->row_base_h = reinterpret_cast<int64_t*>(q);
-    q += up((size_t)R * 8);
+    auto take = [&](size_t bytes) {
+        uint8_t* r = q;
+        q += up256(bytes);
+        return r;
+    };
+    out->tkey = reinterpret_cast<unsigned long long*>(take(table_cap * 8));
+    out->tfirst = reinterpret_cast<int32_t*>(take(table_cap * 4));
+    out->tbase = reinterpret_cast<int32_t*>(take(table_cap * 4));
+    out->table_mask = copy_table_slots(R, max_blocks) - 1;
+    out->pairs = reinterpret_cast<Pair*>(take(E * sizeof(Pair)));
+    out->slices = reinterpret_cast<Slice*>(take(E * sizeof(Slice)));
+    out->dests = reinterpret_cast<int32_t*>(take(E * 4));
+    out->pslot = reinterpret_cast<int32_t*>(take(E * 4));
+    out->prank = reinterpret_cast<int32_t*>(take(E * 4));
+    out->row_cnt = reinterpret_cast<int32_t*>(take(Rs * 4));
+    out->row_cnt_h = reinterpret_cast<int32_t*>(take(Rs * 4));
+    out->row_base = reinterpret_cast<int64_t*>(take(Rs * 8));
+    out->row_base_h = reinterpret_cast<int64_t*>(take(Rs * 8));
     out->total = reinterpret_cast<unsigned long long*>(q);
     out->total_h = out->total + 1;
+    out->nslices = out->total + 2;
+    out->nslices_h = out->total + 3;
+    out->ndests = out->total + 4;
+    out->ndests_h = out->total + 5;
+}
+
+namespace {
+__global__ void k_zero(uint32_t* p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+}  // namespace
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+    const size_t n = bytes / 4;
+    if (n == 0) return hipSuccess;
+    size_t g = (n + 255) / 256;
+    if (g > 65536) g = 65536;
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)g), dim3(256), 0, s, static_cast<uint32_t*>(p), n);
+    return hipGetLastError();
 }
 
 hipError_t launch_gather_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,

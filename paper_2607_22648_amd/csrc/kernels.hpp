@@ -110,20 +110,54 @@ struct CopyPlan {
 constexpr int kMaxVarLayers = 1024;
 
 
+// A block a gather reads once, and the cache blocks it writes it to:
+// dests[base .. base + n), 1 <= n <= kSliceDests.
+struct Slice {
+    int32_t row;
+    int32_t base;
+    int32_t n;
+    int32_t pad;
+};
+constexpr int kSliceDests = 16;
+
 // Descriptor list of one gather / scatter call: the blocks whose row is in
 // device memory first (*total of them), then those whose row is in the host
-// tier (*total_h), each part in (request, block) order.
+// tier (*total_h), each part in (request, block) order. A gather turns it
+// into slices: each distinct row once, with the cache blocks that need it
+// (device-row slices from 0, host-row slices from *total, in the order of
+// the first request that needs the row). The row table groups the list's
+// entries by row; it sits at the start of the scratch, table_cap slots that
+// every call leaves empty, and a call uses its first table_mask + 1.
 struct CopyScratch {
+    unsigned long long* tkey;    // [table_cap] (row + 1) << 32 | entries so far; 0: empty
+    int32_t* tfirst;             // [table_cap] INT32_MAX - first list position of the row
+    int32_t* tbase;              // [table_cap] where the row's cache blocks start in dests
+    uint64_t table_mask;
     Pair* pairs;                 // [R * max_blocks]
+    Slice* slices;               // [R * max_blocks]
+    int32_t* dests;              // [R * max_blocks]
+    int32_t* pslot;              // [R * max_blocks] table slot of each list entry
+    int32_t* prank;              // [R * max_blocks] its place among the row's cache blocks
     int32_t* row_cnt;            // [R] device-row blocks of each request
     int32_t* row_cnt_h;          // [R] host-row blocks of each request
     int64_t* row_base;           // [R] exclusive scan of row_cnt
     int64_t* row_base_h;         // [R] exclusive scan of row_cnt_h
     unsigned long long* total;   // device-row pairs
     unsigned long long* total_h; // host-row pairs (after the device-row ones)
+    unsigned long long* nslices;   // device-row slices
+    unsigned long long* nslices_h; // host-row slices (from slices + *total)
+    unsigned long long* ndests;    // cache blocks of device-row slices handed out
+    unsigned long long* ndests_h;  // the same for host-row slices (from dests + *total)
 };
-size_t copy_scratch_bytes(int32_t R, int32_t max_blocks);
-void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, CopyScratch* out);
+// Row-table slots a call needs (a power of two >= 2 R max_blocks, at least
+// 64), and the scratch bytes of a call after a table region of table_cap
+// slots; the carve lays a call out in such a scratch.
+uint64_t copy_table_slots(int32_t R, int32_t max_blocks);
+size_t copy_scratch_bytes(int32_t R, int32_t max_blocks, uint64_t table_cap);
+void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, uint64_t table_cap,
+                        CopyScratch* out);
+// Empty row table: zeroes the first `bytes` of a new scratch.
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 
 hipError_t launch_gather_select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids,
                                 const int32_t* m, const int32_t* block_table, int32_t R,

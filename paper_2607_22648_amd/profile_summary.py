@@ -48,8 +48,8 @@ from collections import defaultdict
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 COPY_SRC = os.path.join(HERE, "csrc", "copy.hip")
-GATHER = "k_copy_pairs<true>"
-SCATTER = "k_copy_pairs<false>"
+GATHER = "k_copy_slices("
+SCATTER = "k_copy_pairs("
 PLAIN_COPY = "__amd_rocclr_copyBuffer"
 
 
@@ -175,8 +175,11 @@ def gather_traffic(a):
         if ga["dispatches"] != n:
             raise ValueError(f"the run holds {n} gather dispatches, bench.py counted {ga['dispatches']}")
         algo_total = ga["bytes"]
+        algo_read = ga.get("read_bytes", algo_total / 2)
     else:
         algo_total = bench["roofline"]["bytes_per_launch"] * n
+        algo_read = algo_total / 2
+    algo_write = algo_total - algo_read
     traffic_total = (sum(g_fetch) * f_factor + sum(g_write) * w_factor) * 1024
     ratio = traffic_total / algo_total
     per_launch = bench["roofline"]["bytes_per_launch"]
@@ -212,8 +215,8 @@ def gather_traffic(a):
             "request_read_bytes_all_dispatches": int(rd),
             "request_write_bytes_all_dispatches": int(wb),
             "request_traffic_over_algorithmic": round((rd + wb) / algo_total, 4),
-            "request_read_over_algorithmic_read": round(rd / (algo_total / 2), 4),
-            "request_write_over_algorithmic_write": round(wb / (algo_total / 2), 4),
+            "request_read_over_algorithmic_read": round(rd / algo_read, 4),
+            "request_write_over_algorithmic_write": round(wb / algo_write, 4),
             "probe_check": {"read_probe_bytes_from_requests_over_known": round(probe_rd / known, 4),
                             "write_probe_bytes_from_requests_over_known": round(probe_wr / known, 4),
                             "read_requests_covered_by_size_classes": round(cover, 4)},
@@ -226,8 +229,8 @@ def gather_traffic(a):
         lines_req = [
             f"| gather read bytes from requests (32/64/128 B classes) | {rd / n / 1e9:.3f} GB per dispatch |",
             f"| gather write bytes from requests (64 B, else 32 B) | {wb / n / 1e9:.3f} GB per dispatch |",
-            f"| request bytes / algorithmic | {(rd + wb) / algo_total:.4f} (read {rd / (algo_total / 2):.4f}, "
-            f"write {wb / (algo_total / 2):.4f}) |",
+            f"| request bytes / algorithmic | {(rd + wb) / algo_total:.4f} (read {rd / algo_read:.4f}, "
+            f"write {wb / algo_write:.4f}) |",
             f"| check: read probe bytes from requests / known | {probe_rd / known:.4f} |",
             f"| check: write probe bytes from requests / known | {probe_wr / known:.4f} |",
             f"| read requests counted in a size class | {cover:.4f} |"]

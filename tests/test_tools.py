@@ -39,7 +39,7 @@ def test_profile_summary_traffic(tmp_path):
     algorithmic bytes summed over every gather dispatch; and, independently,
     memory requests times their sizes, checked on the probes too."""
     ns = "void ptsd::(anonymous namespace)::"
-    gather = ns + "k_copy_pairs<true>(ptsd::(anonymous namespace)::CopyArgs)"
+    gather = ns + "k_copy_slices(ptsd::(anonymous namespace)::CopyArgs)"
     rd = ns + "k_read(unsigned int __vector(4) const*, long, unsigned int __vector(4)*)"
     wrk = ns + "k_write(unsigned int __vector(4)*, long)"
     gib = 1 << 30
