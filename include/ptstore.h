@@ -238,7 +238,7 @@ int ptstore_lookup(ptstore_t *store, const int32_t *tokens, const int64_t *offse
  * and counted in bad_entries. Destinations must be distinct (two entries
  * naming the same cache block race). `cache` must be 16-byte aligned.
  * The call first builds a dense list of the blocks to copy in store-owned
- * scratch of `stream` (about 68 bytes per (request, block) plus 24 per
+ * scratch of `stream` (about 60 bytes per (request, block) plus 24 per
  * request, grown on demand; growing waits for `stream`), then copies only
  * those blocks. With R >= 2 the list groups the entries by stored block, so
  * that a block several requests need is read once per call and written to
@@ -422,7 +422,7 @@ const char *ptstore_last_error(void);
  * capture, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, kernels and results as ptstore_lookup_gather, but the
  * gather's descriptor list and the row table that groups its entries by
- * stored block live in a static device array of the library (about 92 MiB
+ * stored block live in a static device array of the library (about 84 MiB
  * per device, held until the process ends) instead of store-owned scratch.
  * The call allocates nothing, frees nothing, creates no event and never
  * waits; it records no ptstore_kernel_times() entries and leaves a list

@@ -33,13 +33,13 @@ using namespace ptsd;
 // cannot allocate: one copy per device, held until the process ends, shared
 // by every such call on that device (calls that overlap on one device race).
 // Its size is the gather's list for PTSTORE_NOALLOC_MAX_ENTRIES (request,
-// block) entries: a row table of twice as many slots (16 bytes each), then
+// block) entries: a row table of twice as many slots (12 bytes each), then
 // 36 bytes per entry (pair, slice, cache block, table slot and rank), 2 x
 // (4 + 8) per request (at most one request per entry) and the counters,
 // each part a multiple of 256 bytes. Static storage starts zeroed, so the
 // row table starts empty, as every call leaves it.
 constexpr uint64_t kNoAllocTableSlots = 2ull * PTSTORE_NOALLOC_MAX_ENTRIES;
-constexpr size_t kNoAllocScratchBytes = kNoAllocTableSlots * 16 +
+constexpr size_t kNoAllocScratchBytes = kNoAllocTableSlots * 12 +
                                         (size_t)PTSTORE_NOALLOC_MAX_ENTRIES * (36 + 2 * (4 + 8)) + 256;
 static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 

@@ -150,52 +150,15 @@ __device__ inline unsigned long long ld_agent(const unsigned long long* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Enter list entry i, which reads `row`, into the call's row table: the
-// row's slot, the entry's rank among the row's entries, and the row's first
-// entry. Table reads go to the device scope (other waves of the workgroup
-// write the table too). The table holds at least twice as many slots as
-// entries and every call leaves it empty, so an empty or matching slot is
-// always found; the probe still stops after one pass over the table, and
-// an entry that found no slot (slot -1) is skipped and counted as bad.
-__device__ inline bool table_enter(const CopyScratch& sc, int32_t row, int64_t i) {
-    const unsigned long long want = (unsigned long long)(uint32_t)(row + 1) << 32;
-    uint64_t h = mix64((uint64_t)(uint32_t)row) & sc.table_mask;
-    int32_t rank = -1;
-    for (uint64_t probe = 0; probe <= sc.table_mask; ++probe, h = (h + 1) & sc.table_mask) {
-        unsigned long long k = ld_agent(&sc.tkey[h]);
-        if (k == 0) {
-            k = atomicCAS(&sc.tkey[h], 0ull, want | 1ull);
-            if (k == 0) {
-                rank = 0;
-                break;
-            }
-        }
-        if ((k & 0xFFFFFFFF00000000ull) == want) {
-            rank = (int32_t)(atomicAdd(&sc.tkey[h], 1ull) & 0xFFFFFFFFull);
-            break;
-        }
-    }
-    if (rank < 0) {
-        sc.pslot[i] = -1;
-        return false;
-    }
-    sc.pslot[i] = (int32_t)h;
-    sc.prank[i] = rank;
-    atomicMax(&sc.tfirst[h], INT32_MAX - (int32_t)i);
-    return true;
-}
-
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;  // an entry the row table had no slot for
 
-// List entry i: a scatter's (home row, cache block) pair; a gather's entry
-// in the row table, or, when it is not grouping, a slice of its own.
+// List entry i: a scatter's (home row, cache block) pair, also a grouping
+// gather's (its row table comes next); a gather's slice of its own when it
+// does not group.
 template <bool GATHER>
 __device__ inline void place(const SelectArgs& a, const Pair& p, int64_t i) {
-    if (!GATHER) {
+    if (!GATHER || a.group) {
         a.sc.pairs[i] = p;
-    } else if (a.group) {
-        a.sc.pairs[i] = p;
-        if (!table_enter(a.sc, p.row, i)) atomicAdd(&a.state->bad_entries, 1ull);
     } else {
         Slice q;
         q.row = p.row;
@@ -334,84 +297,17 @@ __global__ __launch_bounds__(kSelThreads) void k_select_fill(SelectArgs a) {
                      (int64_t)*a.sc.total + a.sc.row_base_h[r]);
 }
 
-// Slices of the list entries start .. start+count-1 (one request's part),
-// by the whole wave: each row's first entry takes slices for all of the
-// row's entries, kSliceDests cache blocks each, from the counters of its
-// part (one allocation per 64 entries, so slices keep the requests' order),
-// and records where the row's cache blocks start. off: where the part's
-// slices and cache blocks begin.
-__device__ inline void group_part(const CopyScratch& sc, int64_t start, int32_t count, int64_t off,
-                                  unsigned long long* nsl_ctr, unsigned long long* nd_ctr, int lane) {
-    for (int32_t w0 = 0; w0 < count; w0 += kWave) {
-        const int64_t i = start + w0 + lane;
-        int32_t h = 0, nsl = 0, n = 0, row = 0;
-        bool owner = false;
-        if (w0 + lane < count) {
-            h = ld_agent(&sc.pslot[i]);
-            owner = h >= 0 && INT32_MAX - ld_agent(&sc.tfirst[h]) == (int32_t)i;
-            if (owner) {
-                const unsigned long long k = ld_agent(&sc.tkey[h]);
-                n = (int32_t)(k & 0xFFFFFFFFull);
-                row = (int32_t)(k >> 32) - 1;
-                nsl = (n + kSliceDests - 1) / kSliceDests;
-            }
-        }
-        int32_t s_nsl = nsl, s_n = n;  // inclusive scans over the wave
-        for (int d = 1; d < kWave; d <<= 1) {
-            const int32_t x = __shfl_up(s_nsl, d, kWave), y = __shfl_up(s_n, d, kWave);
-            if (lane >= d) {
-                s_nsl += x;
-                s_n += y;
-            }
-        }
-        unsigned long long sb = 0, db = 0;
-        if (lane == kWave - 1) {
-            if (s_nsl) sb = atomicAdd(nsl_ctr, (unsigned long long)s_nsl);
-            if (s_n) db = atomicAdd(nd_ctr, (unsigned long long)s_n);
-        }
-        sb = shfl_u64(sb, kWave - 1);
-        db = shfl_u64(db, kWave - 1);
-        if (owner) {
-            const int64_t my_sb = off + (int64_t)sb + (s_nsl - nsl);
-            const int64_t my_db = off + (int64_t)db + (s_n - n);
-            sc.tbase[h] = (int32_t)my_db;
-            for (int j = 0; j < nsl; ++j) {
-                const int32_t left = n - j * kSliceDests;
-                Slice q;
-                q.row = row;
-                q.base = (int32_t)(my_db + j * kSliceDests);
-                q.n = left < kSliceDests ? left : kSliceDests;
-                q.pad = 0;
-                sc.slices[my_sb + j] = q;
-            }
-        }
-    }
-}
-
 // List entry i's cache block into its row's cache-block list; the row's
-// first entry then empties the row's table slot, so the table is empty again
-// when the call ends (only this step still reads the slot, and only its
-// base; a cleared first entry is never taken for another entry's).
+// rank-0 entry then empties the row's table slot, so the table is empty
+// again when the call ends (this step reads only the slot's base, which
+// stays).
 __device__ inline void place_dest(const CopyScratch& sc, int64_t i) {
     const int32_t h = ld_agent(&sc.pslot[i]);
     if (h < 0) return;  // an entry the table had no slot for
     const int32_t rank = ld_agent(&sc.prank[i]);
     const int32_t cb = ld_agent(&sc.pairs[i].cb);
     sc.dests[ld_agent(&sc.tbase[h]) + rank] = cb;
-    if (INT32_MAX - ld_agent(&sc.tfirst[h]) == (int32_t)i) {
-        __hip_atomic_store(&sc.tkey[h], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&sc.tfirst[h], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-}
-
-__global__ __launch_bounds__(kSelThreads) void k_group_fill(SelectArgs a) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t r = (int64_t)blockIdx.x * kSelWaves + threadIdx.x / kWave;
-    if (r >= a.R) return;
-    const int64_t total = (int64_t)*a.sc.total;
-    group_part(a.sc, a.sc.row_base[r], a.sc.row_cnt[r], 0, a.sc.nslices, a.sc.ndests, lane);
-    group_part(a.sc, total + a.sc.row_base_h[r], a.sc.row_cnt_h[r], total, a.sc.nslices_h,
-               a.sc.ndests_h, lane);
+    if (rank == 0) __hip_atomic_store(&sc.tkey[h], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __global__ __launch_bounds__(kSelThreads) void k_group_dests(SelectArgs a) {
@@ -454,16 +350,16 @@ __device__ inline uint32_t lds_enter(unsigned long long* tw, uint32_t slots, int
     return kNoSlot;
 }
 
-template <bool GATHER>
+template <bool GATHER, bool GROUP>
 __global__ __launch_bounds__(kSmallThreads) void k_select_small(SelectArgs a) {
     __shared__ int32_t wc[kSmallCounts], wch[kSmallCounts];  // per (k, wave); then their bases
     __shared__ int32_t total_dev, total_host;
     __shared__ unsigned long long alloc[2];  // per part: slices << 32 | cache blocks
-    __shared__ unsigned long long tw[GATHER ? kSmallSlots : 1];
+    __shared__ unsigned long long tw[GROUP ? kSmallSlots : 1];  // only a grouping call holds it
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const int t = threadIdx.x;
     const unsigned long long count = a.state->count;
-    const bool group = GATHER && a.group;
+    constexpr bool group = GATHER && GROUP;
     const int32_t E = a.R * a.max_blocks;  // the host's condition: E <= kSmallMaxEntries
     uint32_t slots = 2u * (uint32_t)E;
     if (slots < 64) slots = 64;
@@ -610,6 +506,143 @@ __global__ __launch_bounds__(kSmallThreads) void k_select_small(SelectArgs a) {
         *a.sc.nslices_h = alloc[1] >> 32;
         *a.sc.ndests = alloc[0] & 0xFFFFFFFFull;
         *a.sc.ndests_h = alloc[1] & 0xFFFFFFFFull;
+    }
+}
+
+// A gather of several requests with more slots than one workgroup takes:
+// the list's entries grouped by row in chunks of kGroupChunk entries, one
+// workgroup each. The entries of one row in a chunk are first combined in
+// an LDS table, so that the row takes one device-scope add per chunk, not
+// one per entry: adds on one word are serialised across the device, and
+// rows that thousands of requests share made them the longest step.
+constexpr int kGroupThreads = 1024;
+constexpr int kGroupPer = 2;                             // entries per thread
+constexpr int kGroupChunk = kGroupThreads * kGroupPer;  // entries per workgroup
+constexpr uint32_t kGroupSlots = 2 * kGroupChunk;       // LDS table of a chunk
+
+// Reserve n ranks of `row` in the call's row table ((row + 1) << 32 |
+// entries so far, 0 empty): its slot and the first of the n ranks. The
+// table holds at least twice as many slots as entries and every call leaves
+// it empty, so a slot is always found; the probe still stops after one pass.
+__device__ inline bool table_add(const CopyScratch& sc, int32_t row, uint32_t n, int32_t* slot,
+                                 int32_t* first) {
+    const unsigned long long want = (unsigned long long)(uint32_t)(row + 1) << 32;
+    uint64_t h = mix64((uint64_t)(uint32_t)row) & sc.table_mask;
+    for (uint64_t probe = 0; probe <= sc.table_mask; ++probe, h = (h + 1) & sc.table_mask) {
+        unsigned long long k = ld_agent(&sc.tkey[h]);
+        if (k == 0) {
+            k = atomicCAS(&sc.tkey[h], 0ull, want | n);
+            if (k == 0) {
+                *slot = (int32_t)h;
+                *first = 0;
+                return true;
+            }
+        }
+        if ((k & 0xFFFFFFFF00000000ull) == want) {
+            *slot = (int32_t)h;
+            *first = (int32_t)(atomicAdd(&sc.tkey[h], (unsigned long long)n) & 0xFFFFFFFFull);
+            return true;
+        }
+    }
+    return false;
+}
+
+// Each list entry's row-table slot and rank (slot -1: none found, counted
+// as bad). Ranks of one row are unique over the call: a chunk reserves a
+// run of them and hands them out in LDS order.
+__global__ __launch_bounds__(kGroupThreads) void k_group_enter(SelectArgs a) {
+    __shared__ unsigned long long tw[kGroupSlots];  // (row + 1) << 32 | the chunk's entries
+    __shared__ int32_t gslot[kGroupSlots], gfirst[kGroupSlots];
+    const int64_t all = (int64_t)*a.sc.total + (int64_t)*a.sc.total_h;
+    const int64_t c0 = (int64_t)blockIdx.x * kGroupChunk;
+    if (c0 >= all) return;  // the whole workgroup
+    const int t = threadIdx.x;
+    for (uint32_t h = t; h < kGroupSlots; h += kGroupThreads) tw[h] = 0ull;
+    __syncthreads();
+    uint32_t e[kGroupPer];
+#pragma unroll
+    for (int k = 0; k < kGroupPer; ++k) {
+        const int64_t i = c0 + t + k * kGroupThreads;
+        e[k] = kNoSlot;
+        if (i < all) {
+            e[k] = lds_enter(tw, kGroupSlots, a.sc.pairs[i].row);
+            if (e[k] == kNoSlot) atomicAdd(&a.state->bad_entries, 1ull);
+        }
+    }
+    __syncthreads();
+    for (uint32_t h = t; h < kGroupSlots; h += kGroupThreads) {
+        const unsigned long long w = tw[h];
+        if (w == 0) continue;
+        int32_t slot = -1, first = 0;
+        if (!table_add(a.sc, (int32_t)(w >> 32) - 1, (uint32_t)(w & 0xFFFFFFFFull), &slot, &first))
+            atomicAdd(&a.state->bad_entries, w & 0xFFFFFFFFull);
+        gslot[h] = slot;
+        gfirst[h] = first;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kGroupPer; ++k) {
+        const int64_t i = c0 + t + k * kGroupThreads;
+        if (i >= all) continue;
+        const int32_t slot = e[k] == kNoSlot ? -1 : gslot[e[k] & 0xFFFFu];
+        a.sc.pslot[i] = slot;
+        if (slot >= 0) a.sc.prank[i] = gfirst[e[k] & 0xFFFFu] + (int32_t)(e[k] >> 16);
+    }
+}
+
+// Descriptors of the chunk's rows: each row's rank-0 entry takes slices for
+// all of the row's entries (kSliceDests cache blocks each) and records where
+// the row's cache blocks start; the chunk takes its slices and cache blocks
+// from its part's counters with one device-scope add each.
+__global__ __launch_bounds__(kGroupThreads) void k_group_slices(SelectArgs a) {
+    __shared__ unsigned long long alloc[2], gs[2], gd[2];  // per part: slices << 32 | cache blocks
+    const int64_t total = (int64_t)*a.sc.total;
+    const int64_t all = total + (int64_t)*a.sc.total_h;
+    const int64_t c0 = (int64_t)blockIdx.x * kGroupChunk;
+    if (c0 >= all) return;  // the whole workgroup
+    const int t = threadIdx.x;
+    if (t < 2) alloc[t] = 0ull;
+    __syncthreads();
+    int32_t h[kGroupPer], n[kGroupPer], row[kGroupPer];
+    unsigned long long got[kGroupPer];
+#pragma unroll
+    for (int k = 0; k < kGroupPer; ++k) {
+        const int64_t i = c0 + t + k * kGroupThreads;
+        n[k] = 0;
+        if (i >= all) continue;
+        h[k] = a.sc.pslot[i];
+        if (h[k] < 0 || a.sc.prank[i] != 0) continue;
+        const unsigned long long w = a.sc.tkey[h[k]];
+        n[k] = (int32_t)(w & 0xFFFFFFFFull);
+        row[k] = (int32_t)(w >> 32) - 1;
+        const int32_t nsl = (n[k] + kSliceDests - 1) / kSliceDests;
+        got[k] = atomicAdd(&alloc[i >= total ? 1 : 0], (unsigned long long)nsl << 32 | (uint32_t)n[k]);
+    }
+    __syncthreads();
+    if (t < 2 && alloc[t]) {
+        gs[t] = atomicAdd(t ? a.sc.nslices_h : a.sc.nslices, alloc[t] >> 32);
+        gd[t] = atomicAdd(t ? a.sc.ndests_h : a.sc.ndests, alloc[t] & 0xFFFFFFFFull);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kGroupPer; ++k) {
+        if (!n[k]) continue;
+        const int64_t i = c0 + t + k * kGroupThreads;
+        const int part = i >= total ? 1 : 0;
+        const int64_t off = part ? total : 0;
+        const int64_t sb = off + (int64_t)(gs[part] + (got[k] >> 32));
+        const int64_t db = off + (int64_t)(gd[part] + (got[k] & 0xFFFFFFFFull));
+        a.sc.tbase[h[k]] = (int32_t)db;
+        const int32_t nsl = (n[k] + kSliceDests - 1) / kSliceDests;
+        for (int j = 0; j < nsl; ++j) {
+            const int32_t left = n[k] - j * kSliceDests;
+            Slice q;
+            q.row = row[k];
+            q.base = (int32_t)(db + j * kSliceDests);
+            q.n = left < kSliceDests ? left : kSliceDests;
+            q.pad = 0;
+            a.sc.slices[sb + j] = q;
+        }
     }
 }
 
@@ -821,7 +854,10 @@ hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, 
     SelectArgs a{ids, m, created, bt, R, max_blocks, cache_blocks, p.state, sc, p.tier,
                  GATHER && R >= 2 ? 1 : 0};
     if ((int64_t)R * max_blocks <= kSmallMaxEntries) {
-        hipLaunchKernelGGL(k_select_small<GATHER>, dim3(1), dim3(kSmallThreads), 0, s, a);
+        if (a.group)
+            hipLaunchKernelGGL((k_select_small<GATHER, true>), dim3(1), dim3(kSmallThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((k_select_small<GATHER, false>), dim3(1), dim3(kSmallThreads), 0, s, a);
         return hipGetLastError();
     }
     const unsigned grid = (unsigned)((R + kSelWaves - 1) / kSelWaves);
@@ -832,9 +868,12 @@ hipError_t select(const CopyPlan& p, const CopyScratch& sc, const int32_t* ids, 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_select_fill<GATHER>, dim3(grid), dim3(kSelThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess || !a.group) return e;
-    hipLaunchKernelGGL(k_group_fill, dim3(grid), dim3(kSelThreads), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t entries = (int64_t)R * max_blocks;
+    const unsigned chunks = (unsigned)((entries + kGroupChunk - 1) / kGroupChunk);
+    hipLaunchKernelGGL(k_group_enter, dim3(chunks), dim3(kGroupThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_group_slices, dim3(chunks), dim3(kGroupThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     int64_t dgrid = (entries + kSelThreads - 1) / kSelThreads;
     if (dgrid > 4096) dgrid = 4096;
     hipLaunchKernelGGL(k_group_dests, dim3((unsigned)dgrid), dim3(kSelThreads), 0, s, a);
@@ -933,7 +972,7 @@ size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t copy_scratch_bytes(int32_t R, int32_t max_blocks, uint64_t table_cap) {
     const size_t E = (size_t)R * max_blocks, Rs = (size_t)R;
-    return up256(table_cap * 8) + 2 * up256(table_cap * 4) + up256(E * sizeof(Pair)) +
+    return up256(table_cap * 8) + up256(table_cap * 4) + up256(E * sizeof(Pair)) +
            up256(E * sizeof(Slice)) + 3 * up256(E * 4) + 2 * up256(Rs * 4) + 2 * up256(Rs * 8) + 256;
 }
 
@@ -947,7 +986,6 @@ void copy_scratch_carve(void* base, int32_t R, int32_t max_blocks, uint64_t tabl
         return r;
     };
     out->tkey = reinterpret_cast<unsigned long long*>(take(table_cap * 8));
-    out->tfirst = reinterpret_cast<int32_t*>(take(table_cap * 4));
     out->tbase = reinterpret_cast<int32_t*>(take(table_cap * 4));
     out->table_mask = copy_table_slots(R, max_blocks) - 1;
     out->pairs = reinterpret_cast<Pair*>(take(E * sizeof(Pair)));

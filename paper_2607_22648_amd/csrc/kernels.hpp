@@ -130,7 +130,6 @@ constexpr int kSliceDests = 16;
 // every call leaves empty, and a call uses its first table_mask + 1.
 struct CopyScratch {
     unsigned long long* tkey;    // [table_cap] (row + 1) << 32 | entries so far; 0: empty
-    int32_t* tfirst;             // [table_cap] INT32_MAX - first list position of the row
     int32_t* tbase;              // [table_cap] where the row's cache blocks start in dests
     uint64_t table_mask;
     Pair* pairs;                 // [R * max_blocks]
