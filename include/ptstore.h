@@ -500,7 +500,7 @@ int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64
  * default the smallest divisor of 2 * num_layers that leaves at most 64
  * units per block); threads: workgroup size, 64..1024, a multiple of 64
  * (default 1024); grid: workgroups of the copy kernels (by default a
- * gather launches one per possible unit, up to 2048 times the workgroups
+ * gather launches one per possible unit, up to 512 times the workgroups
  * the device holds at once, and a scatter 16 times the workgroups the
  * device holds, looping; a grid once set replaces both until set again).
  * For tuning sweeps; results never depend on it. */

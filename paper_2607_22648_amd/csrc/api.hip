@@ -208,14 +208,18 @@ CopyPlan copy_plan(ptstore_t* s) {
     p.grid = s->grid;
     // in rounds of the workgroups the device holds at once (2048 threads per
     // compute unit): a gather launches one workgroup per possible unit, up to
-    // 2048 rounds, past which a workgroup takes a second unit. Where many
-    // entries miss, this saves the launch of workgroups that find nothing to
-    // do (6 % on the stream at the 8B shape, where 38 % of the possible units
-    // are empty); lower caps cost the trie up to 6 %. A scatter, whose units
-    // are sparse, launches 16 rounds that loop (4 rounds: 7 % slower on a
-    // large scatter; 128 rounds: 45 % slower on a small one).
+    // 512 rounds, past which a workgroup takes further units a grid apart.
+    // The host cannot know how many units a call has: entries that miss, and
+    // entries that share a row with others, leave possible units empty, and
+    // each empty workgroup still costs its launch (about 0.8 ns). On the
+    // trie's 8,192 walks, whose 517,672 entries read 70,570 rows (184,474
+    // units of 1,048,576 possible), 512 rounds copy in 7.46 ms against 8.11
+    // at 2,048 rounds and 7.42 with exactly one workgroup per unit; on the 8B
+    // shape (759,808 units) 12.38 against 12.47 and 12.21. A scatter, whose units are
+    // sparse, launches 16 rounds that loop (4 rounds: 7 % slower on a large
+    // scatter; 128 rounds: 45 % slower on a small one).
     const int resident = s->cus * (2048 / s->threads);
-    p.gather_grid = resident * 2048;
+    p.gather_grid = resident * 512;
     p.loop_grid = resident * 16;
     // host-tier rows move over the host link whatever the grid: a quarter of
     // the compute units carry one workgroup each, the rest stay free

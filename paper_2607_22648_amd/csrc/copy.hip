@@ -19,20 +19,29 @@
 // (offset, size) segments in one request (Section 4.1, RDMA-aware
 // consolidation):
 //   select  count the blocks each request must move (wave per request), scan
-//           the counts, then write a dense descriptor list of (id, cache
-//           block) pairs, compacted with a wave ballot (three kernels; one
+//           the counts, then write a dense list of (row, cache block)
+//           entries, compacted with a wave ballot (three kernels; one
 //           workgroup does all three for a small batch). Entries with an id
 //           or cache block out of range are dropped here and counted.
+//   group   (a gather of several requests) the entries are grouped by the
+//           row they read: a row table in the scratch (in LDS for a small
+//           batch) counts each row's entries, and each row gets slices of
+//           up to kSliceDests of its cache blocks. A row that many requests
+//           share is then read from memory once per slice, not once per
+//           request. A scatter, and a gather of one request (whose blocks
+//           are distinct), keep one slice per entry.
 //   copy    workgroups walk (descriptor, group of chunks) units; the number
 //           of units is read on the device, so no host round trip separates
 //           the parts. Threads move 16-byte vectors with non-temporal loads
-//           and stores (the stream is touched once).
+//           and stores (the stream is touched once); a gather writes each
+//           vector it reads to every cache block of its slice.
 // Only blocks that are really copied cost work, however sparse they are in
 // the [request][block] arrays (a few created blocks per insert, half the
 // requests missing the store). The default copy shape gives each
 // 1024-thread workgroup one chunk per unit (two vectors per thread for a
-// 32 KiB chunk). The copies are pure HBM streaming: no MFMA, and LDS only for
-// the per-layer kernel's table of layer bases.
+// 32 KiB chunk). The copies are pure HBM streaming: no MFMA. LDS holds the
+// row tables of the grouping step and the per-layer kernel's table of layer
+// bases.
 #include "kernels.hpp"
 
 namespace ptsd {
@@ -668,7 +677,7 @@ struct CopyArgs {
 
 // The (descriptor, chunk group) units are visited grid-stride. The host
 // picks the grid: a gather launches one workgroup per possible unit, up to
-// 2048 times what the device holds at once, so the dense front of the list
+// 512 times what the device holds at once, so the dense front of the list
 // runs in hardware dispatch order (neighbouring workgroups copy neighbouring
 // chunks; past the cap a workgroup also takes the unit one grid further on,
 // and workgroups past the end exit at once); a scatter, whose created blocks
