@@ -703,6 +703,19 @@ __global__ __launch_bounds__(1024) void k_copy_pairs(CopyArgs a) {
     }
 }
 
+// A slice's cache blocks, one per lane (lane k holds the k-th; a slice has
+// at most kSliceDests <= kWave of them), loaded once per unit. The copy
+// loops take them with readlane: read from memory inside the store loop,
+// each would be a vector load (the stores might alias the list, as far as
+// the compiler knows) waiting for every store issued before it.
+static_assert(kSliceDests <= kWave, "a slice's cache blocks must fit one per lane");
+__device__ inline int32_t slice_dests(const CopyArgs& a, const Slice& q) {
+    const int lane = threadIdx.x & (kWave - 1);
+    // lanes past the last cache block read it again: no branch, so the load
+    // is issued together with the row's first vectors
+    return a.dests[q.base + min(lane, max(q.n - 1, 0))];
+}
+
 // Gather, uniform slabs: a unit is (slice, group of chunks). Each chunk of
 // the slice's row is read once, two vectors per thread in flight, and
 // written to each of the slice's cache blocks: a row that several requests
@@ -716,6 +729,7 @@ __global__ __launch_bounds__(1024) void k_copy_slices(CopyArgs a) {
         const unsigned long long d = unit / (unsigned)a.groups;
         const int g = (int)(unit - d * (unsigned)a.groups);
         const Slice q = slices[d];
+        const int32_t lane_cb = slice_dests(a, q);
         const int c0 = a.c_lo + g * a.chunks_per_group;
         const int c1 = min(c0 + a.chunks_per_group, a.c_hi);
         const uint8_t* blk = q.row < a.dev_rows ? a.pool + (int64_t)q.row * a.block_bytes
@@ -723,14 +737,20 @@ __global__ __launch_bounds__(1024) void k_copy_slices(CopyArgs a) {
         for (int c = c0; c < c1; ++c) {
             const v4u* src = reinterpret_cast<const v4u*>(blk + (int64_t)c * a.chunk_bytes);
             uint8_t* plane = a.cache + (int64_t)c * a.cache_blocks * a.chunk_bytes;
-            for (int i = threadIdx.x; i < n16; i += 2 * nt) {
-                const bool two = i + nt < n16;
-                const v4u x = ld_nt(src + i);
-                v4u y;
-                if (two) y = ld_nt(src + i + nt);
+            // loops over uniform bounds, so that every lane is active at the
+            // readlane (it reads a lane's register whatever the exec mask)
+            for (int i0 = 0; i0 < n16; i0 += 2 * nt) {
+                const int i = i0 + (int)threadIdx.x;
+                const bool one = i < n16, two = i + nt < n16;
+                // both loads unconditional (a thread past the chunk's end
+                // re-reads its last vector): with no branch between them
+                // they are issued together with the cache-block load
+                const v4u x = ld_nt(src + min(i, n16 - 1));
+                const v4u y = ld_nt(src + min(i + nt, n16 - 1));
                 for (int k = 0; k < q.n; ++k) {
-                    v4u* dst = reinterpret_cast<v4u*>(plane + (int64_t)a.dests[q.base + k] * a.chunk_bytes);
-                    st_nt(dst + i, x);
+                    const int32_t cb = __builtin_amdgcn_readlane(lane_cb, k);
+                    v4u* dst = reinterpret_cast<v4u*>(plane + (int64_t)cb * a.chunk_bytes);
+                    if (one) st_nt(dst + i, x);
                     if (two) st_nt(dst + i + nt, y);
                 }
             }
@@ -790,12 +810,12 @@ __global__ __launch_bounds__(1024) void k_copy_spans(CopyArgs a) {
         const unsigned long long d = unit / spans;
         const int64_t s0 = b0 + (int64_t)(unit - d * spans) * kSpanBytes;
         const int64_t s1 = min(s0 + (int64_t)kSpanBytes, b1);
-        int32_t row, n = 1, base = 0, cb0 = 0;
+        int32_t row, n = 1, cb0 = 0, lane_cb = 0;
         if (GATHER) {
             const Slice q = a.slices[first + d];
             row = q.row;
             n = q.n;
-            base = q.base;
+            lane_cb = slice_dests(a, q);
         } else {
             const Pair p = a.pairs[first + d];
             row = p.row;
@@ -803,24 +823,29 @@ __global__ __launch_bounds__(1024) void k_copy_spans(CopyArgs a) {
         }
         uint8_t* blk = row < a.dev_rows ? a.pool + (int64_t)row * a.block_bytes
                                         : a.host + (int64_t)(row - a.dev_rows) * a.block_bytes;
-        // two vectors per thread in flight: both loaded before either is stored
+        // two vectors per thread in flight: both loaded before either is
+        // stored. The loop runs over uniform bounds, so that every lane is
+        // active at the readlane (it reads a lane's register whatever the
+        // exec mask).
         int li = 0;
-        for (int64_t o = s0 + 16 * (int64_t)threadIdx.x; o < s1; o += 2 * step) {
-            const bool two = o + step < s1;
-            li = slab_from(lb, li, nl, o);
+        for (int64_t o0 = s0; o0 < s1; o0 += 2 * step) {
+            const int64_t o = o0 + 16 * (int64_t)threadIdx.x;
+            const bool one = o < s1, two = o + step < s1;
+            if (one) li = slab_from(lb, li, nl, o);
             const int li1 = two ? slab_from(lb, li, nl, o + step) : li;
             v4u* pv0 = reinterpret_cast<v4u*>(blk + o);
             v4u* pv1 = reinterpret_cast<v4u*>(blk + o + step);
             if (GATHER) {
-                const v4u x0 = ld_nt(pv0);
-                v4u x1;
-                if (two) x1 = ld_nt(pv1);
+                // unconditional loads (past the span's end a thread re-reads
+                // its last vector), issued together
+                const v4u x0 = ld_nt(reinterpret_cast<const v4u*>(blk + min(o, s1 - 16)));
+                const v4u x1 = ld_nt(reinterpret_cast<const v4u*>(blk + min(o + step, s1 - 16)));
                 for (int k = 0; k < n; ++k) {
-                    const int32_t cb = a.dests[base + k];
-                    st_nt(span_cache(a, lb, li, o, cb), x0);
+                    const int32_t cb = __builtin_amdgcn_readlane(lane_cb, k);
+                    if (one) st_nt(span_cache(a, lb, li, o, cb), x0);
                     if (two) st_nt(span_cache(a, lb, li1, o + step, cb), x1);
                 }
-            } else {
+            } else if (one) {
                 const v4u x0 = ld_nt(span_cache(a, lb, li, o, cb0));
                 v4u x1;
                 if (two) x1 = ld_nt(span_cache(a, lb, li1, o + step, cb0));

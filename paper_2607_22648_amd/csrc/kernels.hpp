@@ -111,8 +111,9 @@ constexpr int kMaxVarLayers = 1024;
 
 
 // A block a gather reads once, and the cache blocks it writes it to:
-// dests[base .. base + n), 1 <= n <= kSliceDests.
-struct Slice {
+// dests[base .. base + n), 1 <= n <= kSliceDests. 16-byte aligned, so that a
+// kernel reads one with a single load.
+struct alignas(16) Slice {
     int32_t row;
     int32_t base;
     int32_t n;
