@@ -343,8 +343,16 @@ def store_kernels_only(a):
                          f"{lo['lookups_per_s_kernel']:,.0f} lookups/s at the kernel")
         if "roofline" in tb and not tb.get("kernel_ms_per_round"):
             rf = tb["roofline"]
-            lines.append(f"- gather: {rf['avg_launch_ms']} ms per launch over {rf['launches']} "
-                         f"timed launches ({rf['achieved']} GB/s)")
+            if "avg_launch_ms" in rf:
+                lines.append(f"- gather: {rf['avg_launch_ms']} ms per launch over {rf['launches']} "
+                             f"timed launches ({rf['achieved']} GB/s)")
+            else:  # bound by the host link: bytes per step over the time the link carries them
+                lines.append(f"- {rf['kernel']}: {rf['achieved']} {rf['unit']} over the {rf['bound']} "
+                             f"({rf['frac']} of {rf['peak']} {rf['unit']})")
+            ga = tb.get("gather_all_launches")
+            if ga:
+                lines.append(f"- every gather launch, host-tier and device rows: {ga['avg_launch_ms']} ms "
+                             f"per launch over {ga['launches']} launches")
     for spec in a.window:
         name, first, count, avg = dispatch_window(a.trace, spec)
         lines += ["", f"`{name}` dispatches {first}-{first + count - 1} (start order) in the trace: "
