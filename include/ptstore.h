@@ -498,7 +498,9 @@ int ptstore_kernel_times(ptstore_t *store, int32_t kind, double *total_ms, int64
 /* Launch shape of the copy kernels (gather and scatter); 0 keeps a field's
  * current value. chunks_per_group: (layer, K|V) chunks one unit moves (by
  * default the smallest divisor of 2 * num_layers that leaves at most 64
- * units per block); threads: workgroup size, 64..1024, a multiple of 64
+ * units per block, and a gather of a layer range of at most 4 chunks per
+ * block moves the whole range as one unit; once set here, it applies to
+ * every copy); threads: workgroup size, 64..1024, a multiple of 64
  * (default 1024); grid: workgroups of the copy kernels (by default a
  * gather launches one per possible unit, up to 512 times the workgroups
  * the device holds at once, and a scatter 16 times the workgroups the
