@@ -232,3 +232,39 @@ def test_variable_slabs_beyond_the_gather_grid_cap():
     t.check_pool()
     t.lookup_gather(toks, offs, maxb, block_table_identity(R, maxb), R * maxb)
     t.close()
+
+
+@pytest.mark.parametrize("prepared", [False, True])
+def test_narrow_layer_ranges_with_shared_rows(prepared):
+    """A layer range of at most 4 chunks per block (one or two layers) moves
+    as one copy unit per descriptor, a wider one as the store's own units:
+    ranges of 1, 2 and 3 layers at every start, through a gather per range
+    or one prepared list, with many requests sharing rows (slices of several
+    cache blocks), against the oracle's range gathers into one cache."""
+    rng = np.random.default_rng(31 + prepared)
+    t = Twin(7, 2, 8, 2, 96)  # uniform: 14 chunks per block, one chunk per unit
+    atoms = _fill(t, rng)
+    # 40 requests drawn from a few atoms share most of their blocks
+    toks, offs = random_block_batch(rng, 40, atoms, 6, tail_p=0.3)
+    R = len(offs) - 1
+    (m, ids), (rm, rids) = t.lookup(toks, offs, 6)
+    bt = block_table_identity(R, 6)
+    n = R * 6 * t.shape.block_bytes
+    dst = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")
+    rdst = np.full(n, 0xA5, dtype=np.uint8)
+    if prepared:
+        t.gpu.gather_prepare(ids, m, to_dev(bt), dst)
+    L = t.shape.layers
+    for width in (1, 2, 3):
+        for l0 in range(0, L - width + 1):
+            rng_ = (l0, l0 + width)
+            if prepared:
+                t.gpu.gather_prepared(dst, rng_)
+            else:
+                t.gpu.gather(ids, m, to_dev(bt), dst, layers=rng_)
+            t.ref.gather(rids, rm, bt, rdst, R * 6, layers=rng_)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(host(dst), rdst, err_msg=f"layers {rng_}")
+    rows = host(ids)[np.arange(6)[None, :] < host(m)[:, None]]
+    assert np.bincount(rows).max() > 1  # some rows have several cache blocks
+    t.close()
