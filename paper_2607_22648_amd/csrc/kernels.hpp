@@ -119,7 +119,7 @@ struct alignas(16) Slice {
     int32_t n;
     int32_t pad;
 };
-constexpr int kSliceDests = 16;
+constexpr int kSliceDests = 64;  // one per lane of a wave
 
 // Descriptor list of one gather / scatter call: the blocks whose row is in
 // device memory first (*total of them), then those whose row is in the host

@@ -32,8 +32,8 @@ request size (32, 64 or 128 bytes; a write request is 64 bytes if counted as
 such, else 32), checked against the probes' known bytes as well. Traffic
 is compared with the algorithmic bytes summed over every gather dispatch of
 the run (the JSON line's ``gather_all``). The record carries the SHA-256 of
-the copy kernel's source; bench.py reports the traffic only while that
-source is unchanged.
+the copy kernels' code (csrc/copy.hip and csrc/kernels.hpp); bench.py
+reports the traffic only while that code is unchanged.
 """
 from __future__ import annotations
 
@@ -48,19 +48,27 @@ from collections import defaultdict
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 COPY_SRC = os.path.join(HERE, "csrc", "copy.hip")
+COPY_HDR = os.path.join(HERE, "csrc", "kernels.hpp")  # the copy kernels' shared types and constants
 GATHER = "k_copy_slices("
 SCATTER = "k_copy_pairs("
 PLAIN_COPY = "__amd_rocclr_copyBuffer"
 
 
-def copy_source_sha() -> str:
-    """SHA-256 of the copy kernels' code in csrc/copy.hip: comments dropped and
-    whitespace runs collapsed, so that editing a comment does not void the
-    counter records taken on that code."""
-    src = open(COPY_SRC).read()
+def _code(path: str) -> str:
+    """A source file with comments dropped and whitespace runs collapsed."""
+    src = open(path).read()
     src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
     src = re.sub(r"//[^\n]*", " ", src)
-    return hashlib.sha256(" ".join(src.split()).encode()).hexdigest()
+    return " ".join(src.split())
+
+
+def copy_source_sha() -> str:
+    """SHA-256 of the copy kernels' code: csrc/copy.hip and the header of
+    their shared types and constants (csrc/kernels.hpp), comments dropped and
+    whitespace runs collapsed, so that editing a comment does not void the
+    counter records taken on that code."""
+    code = _code(COPY_SRC) + "\n" + _code(COPY_HDR)
+    return hashlib.sha256(code.encode()).hexdigest()
 
 
 def _one(pattern: str) -> str:
@@ -255,7 +263,7 @@ def gather_traffic(a):
     lines += [f"| traffic, all gather dispatches (scaled) | {traffic_total / 1e9:.3f} GB |",
               f"| algorithmic bytes, all gather dispatches | {algo_total / 1e9:.3f} GB |",
               f"| traffic / algorithmic | {ratio:.4f} |"] + lines_req + [
-              "", f"Copy kernel code SHA-256 (csrc/copy.hip without comments and whitespace): `{rec['copy_code_sha256']}`."]
+              "", f"Copy kernel code SHA-256 (csrc/copy.hip and csrc/kernels.hpp without comments and whitespace): `{rec['copy_code_sha256']}`."]
     with open(os.path.join(a.out, f"{a.name}_hbm_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(rec))

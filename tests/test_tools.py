@@ -159,6 +159,13 @@ def test_copy_code_hash_ignores_comments_only(tmp_path, monkeypatch):
         keys[name] = ps.copy_source_sha()
     assert keys["comment"] == base and keys["block comment"] == base and keys["spacing"] == base
     assert keys["code"] != base
+    monkeypatch.undo()
+    hdr = open(ps.COPY_HDR).read()
+    f = tmp_path / "kernels.hpp"
+    f.write_text(hdr.replace("kSliceDests = 64", "kSliceDests = 32", 1))
+    monkeypatch.setattr(ps, "COPY_HDR", str(f))
+    assert ps.copy_source_sha() != base  # the copy kernels' constants are part of the key
+    monkeypatch.undo()
     import bench
     monkeypatch.setattr(ps, "COPY_SRC", str(tmp_path / "code.hip"))
     assert bench.recorded_traffic("llama8b", 1e9) is None
