@@ -39,8 +39,12 @@ def _grow(t, rng, atoms, R, maxb, seed):
     t.scatter_random(ids, cr, rids, rcr, block_table_identity(Ri, maxb), seed=seed)
 
 
-@pytest.mark.parametrize("chunks", [None, [32, 96, 16]])
-def test_captured_lookup_gather_replays(chunks):
+@pytest.mark.parametrize("chunks,R,maxb", [(None, 16, 8), ([32, 96, 16], 16, 8), (None, 160, 64)])
+def test_captured_lookup_gather_replays(chunks, R, maxb):
+    """16 x 8 entries take the one-workgroup list build; 160 x 64 (past its
+    8,192 entries) the multi-kernel one, whose device-wide row table every
+    replay must find empty and leave empty. Requests drawn from 5 atoms share
+    their first blocks, so rows have several cache blocks."""
     rng = np.random.default_rng(41)
     bt_ = 4
     if chunks is None:
@@ -48,7 +52,6 @@ def test_captured_lookup_gather_replays(chunks):
     else:
         t = Twin(len(chunks), 1, 1, bt_, 2000, layer_chunk_bytes=chunks)
     atoms = _atoms(rng, 5, bt_, 200)
-    R, maxb = 16, 8
     _grow(t, rng, atoms, 8, maxb, seed=1)
     toks, offs = random_block_batch(rng, R, atoms, maxb + 2, tail_p=0.3)
     tt, oo = to_dev(toks), to_dev(offs)
