@@ -137,6 +137,39 @@ def test_profile_summary_dispatch_window(tmp_path):
     assert p.returncode != 0 and "holds 6 dispatches" in p.stderr  # a slice past the end is refused
 
 
+def test_profile_summary_trace_bench_lines(tmp_path):
+    """The trace summary quotes the bench line of the same run: a gather's
+    average launch against the HBM, or, for the tiered store, the host link's
+    rate and the average over every gather launch."""
+    gather = "void ptsd::(anonymous namespace)::k_copy_slices(ptsd::(anonymous namespace)::CopyArgs)"
+    tr = tmp_path / "trace"
+    _write_trace(str(tr), [(gather, 4, 12_500_000, 90.0)])
+    out = tmp_path / "profiles"
+    lines = {
+        "hbm": {"value": 10.0, "unit": "requests/s", "ms_per_step": 25.0,
+                "roofline": {"bound": "hbm", "kernel": "k_copy_slices (gather)", "achieved": 6500.0,
+                             "peak": 8000.0, "unit": "GB/s", "frac": 0.8125, "avg_launch_ms": 12.5,
+                             "launches": 40}},
+        "link": {"value": 89.0, "unit": "requests/s", "ms_per_step": 719.0,
+                 "roofline": {"bound": "host link", "kernel": "k_copy_slices (gather, host-tier rows)",
+                              "achieved": 56.0, "peak": 64.0, "unit": "GB/s", "frac": 0.875},
+                 "gather_all_launches": {"avg_launch_ms": 21.9, "launches": 128}},
+    }
+    for name, line in lines.items():
+        b = tmp_path / f"{name}.json"
+        b.write_text("[bench] log line\n" + json.dumps(line) + "\n")
+        p = subprocess.run([sys.executable, "-m", "paper_2607_22648_amd.profile_summary", "--trace", str(tr),
+                            "--trace-bench", str(b), "--out", str(out), "--name", name, "--cmd", "cmd"],
+                           capture_output=True, text=True, cwd=ROOT, timeout=120)
+        assert p.returncode == 0, p.stderr
+    text = (out / "hbm_kernel_trace.md").read_text()
+    assert "`k_copy_slices` | 4 | 12500.00" in text
+    assert "- gather: 12.5 ms per launch over 40 timed launches (6500.0 GB/s)" in text
+    text = (out / "link_kernel_trace.md").read_text()
+    assert "56.0 GB/s over the host link (0.875 of 64.0 GB/s)" in text
+    assert "21.9 ms per launch over 128 launches" in text
+
+
 def test_copy_code_hash_ignores_comments_only(tmp_path, monkeypatch):
     """The counter records are keyed to the copy kernels' code: editing a
     comment or the spacing keeps the key, changing code changes it, and
