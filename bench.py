@@ -49,7 +49,9 @@ FLUSH_BYTES = 1 << 30
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: 100 for the llama8b fused load, about 2.5 s of "
+                         "copies, 20 for the other workloads)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama8b",
                     choices=["llama8b", "tiny", "llama70b_shard", "trie", "stream", "stream_evict",
@@ -66,7 +68,10 @@ def parse():
                     help="llama70b_full: 'streams' looks all requests up, then loads those read "
                          "from the host tier on one stream and the rest on another (two caches); "
                          "'serial' runs one lookup+gather per request on one stream")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.steps is None:
+        args.steps = 100 if args.config == "llama8b" and not args.per_layer else 20
+    return args
 
 
 def log(*a):
